@@ -1,0 +1,102 @@
+"""Lanczos and stochastic Lanczos quadrature (oracle, float64).
+
+Section 4 states the symmetric Lanczos recurrence
+    beta_{k+1} q_{k+1} = H q_k - alpha_k q_k - beta_k q_{k-1},  alpha_k = q_k^T H q_k,
+whose coefficients form the tridiagonal T_m; SLQ approximates v^T f(H) v by
+e_1^T f(T_m) e_1, i.e. a Gauss quadrature with nodes the eigenvalues of T_m and
+weights the squared first components of its eigenvectors.  Appendix C adds
+reorthogonalisation against a sliding window of r stored vectors (one dot and
+one AXPY per stored vector); section 7.1 uses full reorthogonalisation at every
+iteration; section 7 (GPT-OSS run) uses none.
+
+Readings taken where the text is loose:
+* coefficient order: the standard (Paige) order of section 4 - subtract
+  beta_k q_{k-1}, form alpha_k, subtract alpha_k q_k, reorthogonalise, then
+  beta_{k+1} = ||w|| (Appendix C's "beta_t = ||w||" before the subtraction is
+  taken as a typesetting slip);
+* FULL reorthogonalisation: one modified Gram-Schmidt sweep over q_1..q_k;
+  WINDOW r: the same sweep over the r most recent vectors q_{k-r+1}..q_k;
+* breakdown: stop when beta_{k+1} <= tol * max_j |alpha_j| (tol 1e-12);
+* outputs: alpha[0..s-1] and beta[0..s-1] = beta_2..beta_{s+1}, the last one
+  being the residual norm (not part of T_s).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+NONE, FULL, WINDOW = 0, 1, 2
+
+
+def lanczos(hvp, q1: np.ndarray, m: int, reorth: int = FULL, window: int = 0,
+            tol: float = 1e-12):
+    """Run m Lanczos steps from unit vector q1.  Returns (alpha, beta, Q)."""
+    q = np.asarray(q1, dtype=np.float64).copy()
+    q /= np.linalg.norm(q)
+    q_prev = np.zeros_like(q)
+    beta_k = 0.0
+    alphas, betas, basis = [], [], [q.copy()]
+    for k in range(m):
+        w = hvp(q) - beta_k * q_prev
+        alpha = float(w @ q)
+        w = w - alpha * q
+        if reorth == FULL:
+            sel = basis
+        elif reorth == WINDOW:
+            sel = basis[-window:] if window > 0 else []
+        else:
+            sel = []
+        for qj in sel:
+            w = w - float(w @ qj) * qj
+        beta = float(np.linalg.norm(w))
+        alphas.append(alpha)
+        betas.append(beta)
+        if beta <= tol * max(abs(a) for a in alphas):
+            break
+        q_prev, q = q, w / beta
+        beta_k = beta
+        basis.append(q.copy())
+    return np.array(alphas), np.array(betas), basis
+
+
+def tridiag(alpha, beta) -> np.ndarray:
+    """Dense T_s from alpha[0..s-1] and the off-diagonals beta[0..s-2]."""
+    s = len(alpha)
+    T = np.diag(np.asarray(alpha, dtype=np.float64))
+    for i in range(s - 1):
+        T[i, i + 1] = T[i + 1, i] = beta[i]
+    return T
+
+
+def ritz(alpha, beta):
+    """Gauss quadrature of T: nodes (Ritz values) and weights (U_1i)^2 (section 4)."""
+    T = tridiag(alpha, beta)
+    lam, U = np.linalg.eigh(T)
+    return lam, U[0, :] ** 2
+
+
+def slq(hvp, probes, m: int, reorth: int = FULL, window: int = 0):
+    """SLQ over unit probes: per-probe nodes, weights, and tr(H) ~ P mean alpha_1."""
+    nodes, weights, alpha1, steps = [], [], [], []
+    P = None
+    for z in probes:
+        P = z.size
+        a, b, _ = lanczos(hvp, z, m, reorth, window)
+        lam, tau = ritz(a, b)
+        nodes.append(lam)
+        weights.append(tau)
+        alpha1.append(a[0])
+        steps.append(len(a))
+    trace = P * float(np.mean(alpha1))
+    return nodes, weights, trace, steps
+
+
+def density(nodes, weights, grid: np.ndarray, sigma: float) -> np.ndarray:
+    """Gaussian-broadened density (1/s) sum_j sum_i tau_i delta(lambda - lambda_i).
+
+    The paper does not state its display kernel; this is for plotting only.
+    """
+    out = np.zeros_like(grid, dtype=np.float64)
+    for lam, tau in zip(nodes, weights):
+        for l, t in zip(lam, tau):
+            out += t * np.exp(-0.5 * ((grid - l) / sigma) ** 2) / (sigma * np.sqrt(2 * np.pi))
+    return out / len(nodes)

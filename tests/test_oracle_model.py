@@ -1,0 +1,128 @@
+"""Pins for the oracle's LM loss and hand-written gradient (CPU, float64)."""
+import math
+
+import numpy as np
+import pytest
+
+import synth
+from synth.workloads import WORKLOADS
+from oracle import model as M
+from tests import micro, torch_ref
+
+
+def _cfg(name):
+    return micro.cfg_of(WORKLOADS[name])
+
+
+def test_param_counts_closed_form():
+    # GPT-2 family with F = 4d: P = V d + S d + L (12 d^2 + 13 d) + 2 d
+    for name in ["tiny-gpt2-fp32", "small-gpt2-fp32", "gpt2-medium-bf16"]:
+        w = WORKLOADS[name]
+        d, V, S, L = w["d_model"], w["vocab"], w["max_seq"], w["n_layers"]
+        assert w["d_ff"] == 4 * d
+        assert M.num_params(_cfg(name)) == V * d + S * d + L * (12 * d * d + 13 * d) + 2 * d
+    # Llama family: P = 2 V d + L (2 d + d (H + 2 Hkv) dh + H dh d + 3 d F) + d
+    for name in ["llama-1.3b-bf16", "llama3-8b-bf16"]:
+        w = WORKLOADS[name]
+        d, V, L, F = w["d_model"], w["vocab"], w["n_layers"], w["d_ff"]
+        H, Hkv = w["n_heads"], w["n_kv_heads"]
+        dh = d // H
+        assert M.num_params(_cfg(name)) == 2 * V * d + L * (2 * d + d * (H + 2 * Hkv) * dh + H * dh * d + 3 * d * F) + d
+    # the stated sizes of the five workloads (~110k, ~25M, ~350M, 1.3B, 8B)
+    assert M.num_params(_cfg("tiny-gpt2-fp32")) == 120576
+    assert M.num_params(_cfg("small-gpt2-fp32")) == 23371776
+    assert M.num_params(_cfg("gpt2-medium-bf16")) == 336128000
+    assert M.num_params(_cfg("llama-1.3b-bf16")) == 1364297728
+    assert M.num_params(_cfg("llama3-8b-bf16")) == 8030261248
+
+
+def test_layout_contiguous_and_layer_blocks():
+    for fam in ["gpt2", "llama"]:
+        cfg = micro.cfg_of(micro.MICRO[fam])
+        lay = M.layout(cfg)
+        off = 0
+        for e in lay:
+            assert e.offset == off
+            off += e.numel
+        # each layer's entries form one contiguous block
+        for l in range(cfg.n_layers):
+            ents = [e for e in lay if e.layer == l]
+            for a, b in zip(ents, ents[1:]):
+                assert b.offset == a.offset + a.numel
+
+
+@pytest.mark.parametrize("fam", ["gpt2", "llama"])
+def test_zero_weights_loss_is_log_vocab(fam):
+    cfg = micro.cfg_of(micro.MICRO[fam])
+    P = M.num_params(cfg)
+    theta = np.zeros(P)
+    for e in M.layout(cfg):
+        if e.kind == M.GAIN:
+            theta[e.offset:e.offset + e.numel] = 1.0
+    tok = synth.tokens(3, 2, 8, cfg.vocab)
+    L, g = M.loss_and_grad(cfg, theta, tok)
+    assert abs(L - math.log(cfg.vocab)) < 1e-14
+
+
+@pytest.mark.parametrize("fam", ["gpt2", "llama"])
+def test_gradient_against_loss_differences(fam):
+    cfg, theta, tok = micro.inputs(micro.MICRO[fam])
+    _, g = M.loss_and_grad(cfg, theta, tok)
+    rng = np.random.default_rng(0)
+    h = 1e-5
+    # several coordinates of every layout entry
+    for e in M.layout(cfg):
+        for i in rng.choice(e.numel, size=min(3, e.numel), replace=False):
+            j = e.offset + int(i)
+            tp, tm = theta.copy(), theta.copy()
+            tp[j] += h
+            tm[j] -= h
+            num = (M.loss(cfg, tp, tok) - M.loss(cfg, tm, tok)) / (2 * h)
+            assert abs(num - g[j]) <= 1e-7 * max(1.0, abs(g[j])), (e.name, j, num, g[j])
+
+
+@pytest.mark.parametrize("fam", ["gpt2", "llama"])
+def test_gradient_against_autograd(fam):
+    cfg, theta, tok = micro.inputs(micro.MICRO[fam])
+    assert torch_ref.num_params(micro.MICRO[fam]) == M.num_params(cfg)
+    L, g = M.loss_and_grad(cfg, theta, tok)
+    import torch
+    Lt = torch_ref.loss(micro.MICRO[fam], torch.tensor(theta), tok).item()
+    gt = torch_ref.grad(micro.MICRO[fam], theta, tok)
+    assert abs(L - Lt) < 1e-12
+    assert np.linalg.norm(g - gt) <= 1e-11 * np.linalg.norm(gt)
+
+
+def test_softmax_regression_head_hessian_closed_form():
+    """0-layer Llama model: logits = f W^T with f = RMSNorm(E[x]) fixed w.r.t. W.
+
+    The head block of the Hessian is (1/N) sum_t (diag p_t - p_t p_t^T) (x) f_t f_t^T,
+    so for v supported on the head, (Hv)_head = (1/N) sum_t (diag p_t - p_t p_t^T)(V_h f_t) f_t^T.
+    """
+    fields = dict(micro.MICRO["llama"], n_layers=0)
+    cfg, theta, tok = micro.inputs(fields)
+    lay = {e.name: e for e in M.layout(cfg)}
+    hd = lay["head"]
+    from oracle import hvp as O
+    rng = np.random.default_rng(1)
+    v = np.zeros_like(theta)
+    Vh = rng.standard_normal(hd.shape)
+    v[hd.offset:hd.offset + hd.numel] = Vh.reshape(-1)
+    hv = O.lm_hvp(cfg, theta, v, 1e-4, tok)
+    # closed form
+    W = M.unflatten(cfg, theta)
+    x = W["embed"][tok]
+    f = x / np.sqrt((x * x).mean(-1, keepdims=True) + cfg.norm_eps) * W["normf.g"]
+    f = f[:, :-1].reshape(-1, cfg.d_model)
+    z = f @ W["head"].T
+    p = np.exp(z - z.max(-1, keepdims=True))
+    p /= p.sum(-1, keepdims=True)
+    N = f.shape[0]
+    u = f @ Vh.T                                  # (V_h f_t) for every t
+    r = p * u - p * (p * u).sum(-1, keepdims=True)  # (diag p - p p^T) u
+    want = r.T @ f / N
+    got = hv[hd.offset:hd.offset + hd.numel].reshape(hd.shape)
+    assert np.linalg.norm(got - want) <= 1e-7 * np.linalg.norm(want)
+    # nothing outside the head block is touched by curvature from the head alone
+    # except through the embedding/normf coupling, which is real; check the
+    # head block only
