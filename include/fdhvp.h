@@ -1,0 +1,178 @@
+/*
+ * fdhvp.h - finite-difference Hessian-vector products, Lanczos and stochastic
+ * Lanczos quadrature for decoder-only language-model losses on AMD MI355X
+ * (gfx950).  C ABI: plain pointers and sizes, no framework types.
+ *
+ * The operation (section 3.1, Eq. grad-fd-hvp; Algorithm 1): for parameters
+ * theta, a direction v and a step eps,
+ *     Hv ~= (grad L(theta + eps v) - grad L(theta - eps v)) / (2 eps),
+ * where L is the mean next-token cross-entropy of the model over one token
+ * batch.  Lanczos (section 4; Appendix C) drives it to build the tridiagonal
+ * T_m = (alpha, beta); SLQ (section 4) turns T_m into Gauss quadrature nodes
+ * (Ritz values) and weights.
+ *
+ * Conventions shared by every call
+ *  - Ownership: the caller owns every buffer.  Device pointers: parameters,
+ *    directions, outputs, tokens and the workspace.  Host pointers: alpha,
+ *    beta, nodes, weights, statistics.  The library never allocates device
+ *    memory; it carves all scratch from the workspace given to
+ *    fdh_set_workspace.
+ *  - Parameter vector: one flat array in the order reported by
+ *    fdh_param_layout (per-layer blocks contiguous).  Element type float32
+ *    (dtype FDH_F32) or bfloat16 bit patterns, uint16 (FDH_BF16).  Directions
+ *    v and products Hv are always float32 of length fdh_num_params().
+ *  - Tokens: int32 [B, S] row-major, values in [0, vocab).
+ *  - Streams: all device work is enqueued on the stream given to fdh_create,
+ *    in call order.  fdh_hvp returns without waiting.  Calls that return host
+ *    results (lanczos, slq_density, block_stats, last_losses) wait for the
+ *    stream before returning.
+ *  - Errors: every call returns an fdh_status; negative values are errors and
+ *    leave outputs unspecified; fdh_last_error gives a message.  No call
+ *    throws.  One context per host thread.
+ *  - theta is never written: the perturbed points are formed on the fly.
+ */
+#ifndef FDHVP_H
+#define FDHVP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FDH_API_VERSION 1
+
+typedef enum fdh_status {
+  FDH_OK = 0,
+  FDH_BREAKDOWN = 1,          /* warning: Lanczos stopped early, see steps_done */
+  FDH_ERR_INVALID_ARG = -1,   /* null pointer, bad size/shape, eps <= 0 or not finite, m < 1 */
+  FDH_ERR_WORKSPACE = -2,     /* no workspace, or smaller than fdh_workspace_bytes */
+  FDH_ERR_HIP = -3,           /* a HIP runtime call failed */
+  FDH_ERR_NONFINITE = -4,     /* NaN/Inf found in an input direction or in a product */
+  FDH_ERR_STATE = -5,         /* call order (e.g. lanczos before bind) */
+  FDH_ERR_UNSUPPORTED = -6    /* configuration outside what the kernels support */
+} fdh_status;
+
+typedef enum fdh_family {
+  FDH_FAMILY_GPT2 = 0,        /* LayerNorm, learned positions, GELU(tanh) MLP, biases, tied head */
+  FDH_FAMILY_LLAMA = 1,       /* RMSNorm, RoPE, SwiGLU MLP, GQA, no biases, untied head */
+  FDH_FAMILY_QUAD_DIAG = 2    /* L(theta) = 1/2 sum_i d_i theta_i^2 (test operator, Hv = d*v) */
+} fdh_family;
+
+typedef enum fdh_dtype { FDH_F32 = 0, FDH_BF16 = 1 } fdh_dtype;
+typedef enum fdh_reorth { FDH_REORTH_NONE = 0, FDH_REORTH_FULL = 1, FDH_REORTH_WINDOW = 2 } fdh_reorth;
+typedef enum fdh_token_dist { FDH_TOKENS_UNIFORM = 0, FDH_TOKENS_ZIPF = 1 } fdh_token_dist;
+typedef enum fdh_vec_kind { FDH_VEC_RADEMACHER = 0, FDH_VEC_GAUSSIAN = 1 } fdh_vec_kind;
+typedef enum fdh_param_kind { FDH_PARAM_MATRIX = 0, FDH_PARAM_GAIN = 1, FDH_PARAM_BIAS = 2 } fdh_param_kind;
+
+/* Model description.  For FDH_FAMILY_QUAD_DIAG only quad_n and dtype are read. */
+typedef struct fdh_model_config {
+  int32_t family;       /* fdh_family */
+  int32_t n_layers;
+  int32_t d_model;
+  int32_t n_heads;
+  int32_t n_kv_heads;   /* must divide n_heads */
+  int32_t d_ff;
+  int32_t vocab;
+  int32_t max_seq;      /* learned-position rows (GPT-2) and upper bound on S */
+  int32_t dtype;        /* fdh_dtype of the parameter vector and of the GEMM operands */
+  float norm_eps;       /* LayerNorm / RMSNorm epsilon */
+  float rope_base;      /* RoPE base (Llama family) */
+  int32_t reserved;
+  int64_t quad_n;       /* QUAD_DIAG dimension */
+} fdh_model_config;
+
+typedef struct fdh_lanczos_opts {
+  int32_t reorth;       /* fdh_reorth */
+  int32_t window;       /* WINDOW: number of most recent Lanczos vectors kept (>= 1) */
+  int32_t basis_dtype;  /* fdh_dtype of the stored Krylov basis */
+  float breakdown_tol;  /* stop when beta_{k+1} <= tol * max_j |alpha_j|; 0 selects 1e-5 */
+} fdh_lanczos_opts;
+
+typedef struct fdh_block {
+  char name[48];        /* e.g. "h3.wqkv" */
+  int64_t offset;       /* element offset in the flat vector */
+  int64_t numel;
+  int64_t rows, cols;   /* matrix shape (cols = 1 for vectors) */
+  int32_t layer;        /* transformer layer, -1 for embeddings / final norm / head */
+  int32_t kind;         /* fdh_param_kind */
+} fdh_block;
+
+typedef struct fdh_ctx fdh_ctx;
+
+/* Create a context for one model on the current HIP device; hip_stream is a
+ * hipStream_t (NULL = default stream).  *out receives the context. */
+fdh_status fdh_create(const fdh_model_config* cfg, void* hip_stream, fdh_ctx** out);
+void fdh_destroy(fdh_ctx* ctx);
+int32_t fdh_api_version(void);
+
+/* Number of parameters P (the length of theta, v and Hv). */
+int64_t fdh_num_params(const fdh_ctx* ctx);
+
+/* Parameter layout: up to cap entries into out; *n receives the total count. */
+fdh_status fdh_param_layout(const fdh_ctx* ctx, fdh_block* out, int32_t cap, int32_t* n);
+
+/* Workspace needed for token batches up to [B, S] and Lanczos runs up to m steps
+ * with options o (o may be NULL and m 0 when only fdh_hvp is used). */
+fdh_status fdh_workspace_bytes(const fdh_ctx* ctx, int32_t B, int32_t S, int32_t m,
+                               const fdh_lanczos_opts* o, size_t* bytes);
+/* Hand the library a device buffer of at least the queried size, 256-byte aligned.
+ * The caller keeps ownership and must keep it alive while the context uses it. */
+fdh_status fdh_set_workspace(fdh_ctx* ctx, void* dev, size_t bytes, int32_t B, int32_t S,
+                             int32_t m, const fdh_lanczos_opts* o);
+
+/* Synthetic inputs (SplitMix64 counter generator, see DESIGN notes in the
+ * source): theta with N(0, 0.02) matrices, unit gains, zero biases (bf16 by
+ * round-to-nearest-even); tokens uniform or Zipf(1.1); unit vectors. */
+fdh_status fdh_init_params(fdh_ctx* ctx, void* params_dev, uint64_t seed);
+fdh_status fdh_make_tokens(fdh_ctx* ctx, int32_t* tokens_dev, int32_t B, int32_t S,
+                           uint64_t seed, int32_t dist);
+fdh_status fdh_random_vector(fdh_ctx* ctx, float* out_dev, uint64_t seed, int32_t kind);
+
+/* QUAD_DIAG only: the diagonal d (float32, length P, device, caller-owned). */
+fdh_status fdh_set_quad_diag(fdh_ctx* ctx, const float* diag_dev);
+
+/* Hv ~= (grad L(theta + eps v) - grad L(theta - eps v)) / (2 eps) on one batch
+ * (section 3.1; Algorithm 1 with a single batch).  params: P elements of the
+ * context dtype; v, hv: float32 [P]; tokens int32 [B, S] (ignored for QUAD_DIAG).
+ * hv must not alias params or v. */
+fdh_status fdh_hvp(fdh_ctx* ctx, const void* params_dev, const float* v_dev, double eps,
+                   const int32_t* tokens_dev, int32_t B, int32_t S, float* hv_dev);
+
+/* Loss values L(theta + eps v), L(theta - eps v) of the most recent fdh_hvp. */
+fdh_status fdh_last_losses(fdh_ctx* ctx, double* loss_plus, double* loss_minus);
+
+/* Fix the operator used by fdh_lanczos / fdh_slq_density. The pointers are
+ * kept (not copied) and must stay valid. */
+fdh_status fdh_bind(fdh_ctx* ctx, const void* params_dev, const int32_t* tokens_dev,
+                    int32_t B, int32_t S, double eps);
+
+/* m Lanczos steps (section 4) from the Rademacher probe z/sqrt(P) drawn from
+ * probe_seed.  alpha_host[m], beta_host[m] receive alpha_1..alpha_s and
+ * beta_2..beta_{s+1} (the last is the residual norm), s = *steps_done <= m;
+ * entries past s are zero.  Returns FDH_BREAKDOWN when s < m. */
+fdh_status fdh_lanczos(fdh_ctx* ctx, int32_t m, uint64_t probe_seed, const fdh_lanczos_opts* o,
+                       double* alpha_host, double* beta_host, int32_t* steps_done);
+
+/* SLQ (section 4): for probe j = 0..probes-1, Lanczos from seed + j, then the
+ * eigen-decomposition of T_s: nodes_host[j*m + i] = lambda_i, weights_host[j*m+i]
+ * = (U_1i)^2 (zero-padded past steps_done[j]); *trace_est = P * mean_j alpha_1. */
+fdh_status fdh_slq_density(fdh_ctx* ctx, int32_t probes, int32_t m, uint64_t seed,
+                           const fdh_lanczos_opts* o, double* nodes_host, double* weights_host,
+                           int32_t* steps_done, double* trace_est);
+
+/* Per transformer layer b (section 6): out_host[3b..3b+2] = ||a_b||^2, ||b_b||^2,
+ * <a_b, b_b> over the parameters of layer b; a, b float32 [P] on device. */
+fdh_status fdh_block_stats(fdh_ctx* ctx, const float* a_dev, const float* b_dev, double* out_host);
+
+/* Number of transformer layers (blocks for fdh_block_stats). */
+int32_t fdh_num_blocks(const fdh_ctx* ctx);
+
+/* Message for the most recent error on this context (never NULL). */
+const char* fdh_last_error(const fdh_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FDHVP_H */

@@ -1,0 +1,33 @@
+/*
+ * fdhvp_testing.h - testing hooks of libfdhvp (not needed to use the library).
+ *
+ * They expose internal kernels on caller-owned device buffers so that the test
+ * suite can check each one in isolation against a plain host computation.
+ */
+#ifndef FDHVP_TESTING_H
+#define FDHVP_TESTING_H
+
+#include "fdhvp.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* The internal batched MFMA GEMM:
+ *   C[z] = alpha * (A[z] B[z]^T + A2[z] B2[z]^T)        (second pair optional)
+ * dtype: FDH_F32 (fp32 operands, v_mfma_f32_32x32x2_f32) or FDH_BF16 (uint16
+ * bfloat16 operands, v_mfma_f32_32x32x16_bf16, fp32 accumulation).
+ * A is [batch][M][K] when a_kmajor, else [batch][K][M]; B is [batch][N][K] when
+ * b_kmajor, else [batch][K][N]; A2/B2 (may be NULL together) share the layouts.
+ * C is float32 [batch][M][N], overwritten.  causal: 0 none, 1 skip output tiles
+ * above the diagonal, 2 contract only k <= m, 3 only k >= m.  Enqueued on
+ * hip_stream; returns without waiting.  K, and M/N of MN-major operands, must
+ * be multiples of 8 (bf16) or 4 (fp32). */
+fdh_status fdh_testing_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t batch, int32_t a_kmajor,
+                            int32_t b_kmajor, const void* A, const void* B, const void* A2, const void* B2,
+                            float* C, int32_t causal, float alpha, void* hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FDHVP_TESTING_H */

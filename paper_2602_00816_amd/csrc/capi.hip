@@ -1,0 +1,236 @@
+// C ABI (include/fdhvp.h): argument validation and dispatch to the engine.
+// No exception crosses this boundary.
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "engine.h"
+
+struct fdh_ctx {
+  fdh::Engine* eng = nullptr;
+  std::string err;
+};
+
+namespace {
+
+fdh_status guard(fdh_ctx* c, int rc) {
+  if (rc < 0 && c && c->eng) c->err = c->eng->err;
+  return (fdh_status)rc;
+}
+
+template <typename F>
+fdh_status run(fdh_ctx* c, F&& f) {
+  if (!c || !c->eng) return FDH_ERR_INVALID_ARG;
+  try {
+    return guard(c, f(*c->eng));
+  } catch (const std::bad_alloc&) {
+    c->err = "host allocation failed";
+    return FDH_ERR_INVALID_ARG;
+  } catch (...) {
+    c->err = "unexpected host exception";
+    return FDH_ERR_INVALID_ARG;
+  }
+}
+
+const char* validate(const fdh_model_config* cfg) {
+  if (!cfg) return "null config";
+  if (cfg->dtype != FDH_F32 && cfg->dtype != FDH_BF16) return "dtype must be FDH_F32 or FDH_BF16";
+  if (cfg->family == FDH_FAMILY_QUAD_DIAG) return cfg->quad_n > 0 ? nullptr : "quad_n must be positive";
+  if (cfg->family != FDH_FAMILY_GPT2 && cfg->family != FDH_FAMILY_LLAMA) return "unknown family";
+  if (cfg->n_layers < 0 || cfg->d_model < 1 || cfg->n_heads < 1 || cfg->n_kv_heads < 1 || cfg->d_ff < 1 ||
+      cfg->vocab < 2 || cfg->max_seq < 2)
+    return "non-positive model size";
+  if (cfg->d_model % cfg->n_heads) return "n_heads must divide d_model";
+  if (cfg->n_heads % cfg->n_kv_heads) return "n_kv_heads must divide n_heads";
+  if (cfg->family == FDH_FAMILY_GPT2 && cfg->n_kv_heads != cfg->n_heads) return "GPT-2 family has n_kv_heads == n_heads";
+  const int dh = cfg->d_model / cfg->n_heads;
+  if (dh % 8 || cfg->d_model % 8 || cfg->d_ff % 8 || cfg->vocab % 8) return "d_model, head_dim, d_ff, vocab must be multiples of 8";
+  if (cfg->vocab >= (1 << 18)) return "vocab must be < 2^18";
+  if (!(cfg->norm_eps > 0.f)) return "norm_eps must be positive";
+  if (cfg->family == FDH_FAMILY_LLAMA && !(cfg->rope_base > 1.f)) return "rope_base must be > 1";
+  return nullptr;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t fdh_api_version(void) { return FDH_API_VERSION; }
+
+fdh_status fdh_create(const fdh_model_config* cfg, void* hip_stream, fdh_ctx** out) {
+  if (!out) return FDH_ERR_INVALID_ARG;
+  *out = nullptr;
+  if (validate(cfg)) return FDH_ERR_INVALID_ARG;
+  fdh_ctx* c = new (std::nothrow) fdh_ctx;
+  if (!c) return FDH_ERR_INVALID_ARG;
+  try {
+    c->eng = new fdh::Engine(*cfg, (hipStream_t)hip_stream);
+  } catch (...) {
+    delete c;
+    return FDH_ERR_INVALID_ARG;
+  }
+  *out = c;
+  return FDH_OK;
+}
+
+void fdh_destroy(fdh_ctx* ctx) {
+  if (!ctx) return;
+  delete ctx->eng;
+  delete ctx;
+}
+
+int64_t fdh_num_params(const fdh_ctx* ctx) { return (ctx && ctx->eng) ? ctx->eng->P : -1; }
+
+int32_t fdh_num_blocks(const fdh_ctx* ctx) { return (ctx && ctx->eng) ? ctx->eng->L : -1; }
+
+fdh_status fdh_param_layout(const fdh_ctx* ctx, fdh_block* out, int32_t cap, int32_t* n) {
+  if (!ctx || !ctx->eng || !n || cap < 0 || (cap > 0 && !out)) return FDH_ERR_INVALID_ARG;
+  const auto& E = ctx->eng->entries;
+  *n = (int32_t)E.size();
+  for (int32_t i = 0; i < cap && i < (int32_t)E.size(); ++i) {
+    std::memset(&out[i], 0, sizeof(fdh_block));
+    std::strncpy(out[i].name, E[i].name.c_str(), sizeof(out[i].name) - 1);
+    out[i].offset = E[i].off;
+    out[i].numel = E[i].numel;
+    out[i].rows = E[i].rows;
+    out[i].cols = E[i].cols;
+    out[i].layer = E[i].layer;
+    out[i].kind = E[i].kind;
+  }
+  return FDH_OK;
+}
+
+fdh_status fdh_workspace_bytes(const fdh_ctx* ctx, int32_t B, int32_t S, int32_t m, const fdh_lanczos_opts* o,
+                               size_t* bytes) {
+  if (!ctx || !ctx->eng || !bytes || B < 0 || S < 0 || m < 0 || (m > 0 && !o)) return FDH_ERR_INVALID_ARG;
+  *bytes = ctx->eng->plan(B, S, m, o, false);
+  return FDH_OK;
+}
+
+fdh_status fdh_set_workspace(fdh_ctx* ctx, void* dev, size_t bytes, int32_t B, int32_t S, int32_t m,
+                             const fdh_lanczos_opts* o) {
+  return run(ctx, [&](fdh::Engine& e) -> int {
+    if (!dev || B < 0 || S < 0 || m < 0 || (m > 0 && !o)) { e.err = "bad workspace arguments"; return FDH_ERR_INVALID_ARG; }
+    if ((reinterpret_cast<uintptr_t>(dev) & 255) != 0) { e.err = "workspace must be 256-byte aligned"; return FDH_ERR_WORKSPACE; }
+    const size_t need = e.plan(B, S, m, o, false);
+    if (bytes < need) { e.err = "workspace smaller than fdh_workspace_bytes"; return FDH_ERR_WORKSPACE; }
+    e.plan(B, S, m, o, true);
+    e.ws = (char*)dev;
+    e.ws_bytes = bytes;
+    return FDH_OK;
+  });
+}
+
+fdh_status fdh_init_params(fdh_ctx* ctx, void* params_dev, uint64_t seed) {
+  return run(ctx, [&](fdh::Engine& e) { return e.init_params(params_dev, seed); });
+}
+
+fdh_status fdh_make_tokens(fdh_ctx* ctx, int32_t* tokens_dev, int32_t B, int32_t S, uint64_t seed, int32_t dist) {
+  return run(ctx, [&](fdh::Engine& e) { return e.make_tokens(tokens_dev, B, S, seed, dist); });
+}
+
+fdh_status fdh_random_vector(fdh_ctx* ctx, float* out_dev, uint64_t seed, int32_t kind) {
+  return run(ctx, [&](fdh::Engine& e) { return e.random_vector(out_dev, seed, kind); });
+}
+
+fdh_status fdh_set_quad_diag(fdh_ctx* ctx, const float* diag_dev) {
+  return run(ctx, [&](fdh::Engine& e) -> int {
+    if (!e.quad) { e.err = "not a QUAD_DIAG context"; return FDH_ERR_STATE; }
+    if (!diag_dev) { e.err = "null diagonal"; return FDH_ERR_INVALID_ARG; }
+    e.quad_diag = diag_dev;
+    return FDH_OK;
+  });
+}
+
+fdh_status fdh_hvp(fdh_ctx* ctx, const void* params_dev, const float* v_dev, double eps, const int32_t* tokens_dev,
+                   int32_t B, int32_t S, float* hv_dev) {
+  return run(ctx, [&](fdh::Engine& e) { return e.hvp(params_dev, v_dev, eps, tokens_dev, B, S, hv_dev); });
+}
+
+fdh_status fdh_last_losses(fdh_ctx* ctx, double* loss_plus, double* loss_minus) {
+  return run(ctx, [&](fdh::Engine& e) { return e.last_losses(loss_plus, loss_minus); });
+}
+
+fdh_status fdh_bind(fdh_ctx* ctx, const void* params_dev, const int32_t* tokens_dev, int32_t B, int32_t S, double eps) {
+  return run(ctx, [&](fdh::Engine& e) -> int {
+    if (!params_dev || (!e.quad && !tokens_dev)) { e.err = "null pointer"; return FDH_ERR_INVALID_ARG; }
+    if (!(eps > 0.0) || !(eps < 1e300)) { e.err = "eps must be positive and finite"; return FDH_ERR_INVALID_ARG; }
+    if (!e.quad && (B < 1 || S < 2)) { e.err = "need B >= 1 and S >= 2"; return FDH_ERR_INVALID_ARG; }
+    e.b_params = params_dev;
+    e.b_tokens = tokens_dev;
+    e.b_B = B;
+    e.b_S = S;
+    e.b_eps = eps;
+    e.bound = true;
+    return FDH_OK;
+  });
+}
+
+fdh_status fdh_lanczos(fdh_ctx* ctx, int32_t m, uint64_t probe_seed, const fdh_lanczos_opts* o, double* alpha_host,
+                       double* beta_host, int32_t* steps_done) {
+  return run(ctx, [&](fdh::Engine& e) -> int {
+    if (!o) { e.err = "null options"; return FDH_ERR_INVALID_ARG; }
+    int s = 0;
+    int rc = e.lanczos(m, probe_seed, *o, alpha_host, beta_host, &s);
+    if (steps_done) *steps_done = s;
+    return rc;
+  });
+}
+
+fdh_status fdh_slq_density(fdh_ctx* ctx, int32_t probes, int32_t m, uint64_t seed, const fdh_lanczos_opts* o,
+                           double* nodes_host, double* weights_host, int32_t* steps_done, double* trace_est) {
+  return run(ctx, [&](fdh::Engine& e) -> int {
+    if (!o) { e.err = "null options"; return FDH_ERR_INVALID_ARG; }
+    return e.slq(probes, m, seed, *o, nodes_host, weights_host, steps_done, trace_est);
+  });
+}
+
+fdh_status fdh_block_stats(fdh_ctx* ctx, const float* a_dev, const float* b_dev, double* out_host) {
+  return run(ctx, [&](fdh::Engine& e) { return e.block_stats(a_dev, b_dev, out_host); });
+}
+
+const char* fdh_last_error(const fdh_ctx* ctx) {
+  if (!ctx) return "null context";
+  return ctx->err.c_str();
+}
+
+}  // extern "C"
+
+// ---- testing hooks (include/fdhvp_testing.h) ----
+#include "../../include/fdhvp_testing.h"
+
+extern "C" fdh_status fdh_testing_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t batch, int32_t a_kmajor,
+                                       int32_t b_kmajor, const void* A, const void* B, const void* A2, const void* B2,
+                                       float* C, int32_t causal, float alpha, void* hip_stream) {
+  if (!A || !B || !C || (!A2) != (!B2) || M < 0 || N < 0 || K < 0 || batch < 1 || causal < 0 || causal > 3)
+    return FDH_ERR_INVALID_ARG;
+  fdh::GemmArgs g;
+  g.M = M; g.N = N; g.K = K; g.nbatch = batch; g.inner_count = 1;
+  g.npairs = A2 ? 2 : 1;
+  const void* As[2] = {A, A2};
+  const void* Bs[2] = {B, B2};
+  for (int p = 0; p < g.npairs; ++p) {
+    g.A[p].ptr = As[p];
+    g.A[p].s_row = a_kmajor ? K : 1;
+    g.A[p].s_k = a_kmajor ? 1 : M;
+    g.A[p].s_outer = (int64_t)M * K;
+    g.B[p].ptr = Bs[p];
+    g.B[p].s_row = b_kmajor ? K : 1;
+    g.B[p].s_k = b_kmajor ? 1 : N;
+    g.B[p].s_outer = (int64_t)N * K;
+  }
+  g.C = C; g.ldc = N; g.c_outer = (int64_t)M * N;
+  g.alpha = alpha;
+  g.causal = causal;
+  hipError_t r;
+  if (dtype == FDH_BF16) {
+    if (fdh::gemm_check<fdh::bf16_t>(g)) return FDH_ERR_UNSUPPORTED;
+    r = fdh::gemm<fdh::bf16_t>(g, (hipStream_t)hip_stream);
+  } else if (dtype == FDH_F32) {
+    if (fdh::gemm_check<float>(g)) return FDH_ERR_UNSUPPORTED;
+    r = fdh::gemm<float>(g, (hipStream_t)hip_stream);
+  } else {
+    return FDH_ERR_INVALID_ARG;
+  }
+  return r == hipSuccess ? FDH_OK : FDH_ERR_HIP;
+}

@@ -1,0 +1,89 @@
+// Host-side engine: parameter layout, workspace plan, the lockstep HVP and the
+// Lanczos / SLQ drivers.
+#pragma once
+#include <string>
+#include <vector>
+
+#include "../../include/fdhvp.h"
+#include "kernels.h"
+
+namespace fdh {
+
+struct ParamRef {
+  int64_t off = -1;
+  int64_t rows = 0, cols = 0;
+  bool valid() const { return off >= 0; }
+};
+
+struct LayerRefs {
+  ParamRef n1g, n1b, wqkv, bqkv, wo, bo, n2g, n2b, w1, b1, w2, b2;
+};
+
+struct Entry {
+  std::string name;
+  int64_t off, numel, rows, cols;
+  int layer, kind;
+};
+
+struct Span {  // carve of the workspace
+  size_t off = 0, bytes = 0;
+};
+
+class Engine {
+ public:
+  explicit Engine(const fdh_model_config& cfg, hipStream_t stream);
+
+  // configuration
+  fdh_model_config cfg;
+  hipStream_t stream;
+  bool gpt2 = false, llama = false, quad = false, bf16 = false;
+  int L = 0, d = 0, Hq = 0, Hk = 0, dh = 0, F = 0, V = 0, Smax = 0, qkvd = 0;
+  int64_t P = 0;
+  std::vector<Entry> entries;
+  std::vector<LayerRefs> layers;
+  ParamRef wte, wpe, head, nfg, nfb;
+  std::string err;
+
+  // workspace
+  char* ws = nullptr;
+  size_t ws_bytes = 0;
+  int planB = 0, planS = 0, planM = 0;
+  fdh_lanczos_opts planO{};
+  size_t plan(int B, int S, int m, const fdh_lanczos_opts* o, bool carve);
+
+  // operator binding for Lanczos
+  const void* b_params = nullptr;
+  const int32_t* b_tokens = nullptr;
+  int b_B = 0, b_S = 0;
+  double b_eps = 0.0;
+  bool bound = false;
+  const float* quad_diag = nullptr;
+
+  // entry points (return fdh_status)
+  int hvp(const void* params, const float* v, double eps, const int32_t* tok, int B, int S, float* hv);
+  int last_losses(double* lp, double* lm);
+  int lanczos(int m, uint64_t seed, const fdh_lanczos_opts& o, double* alpha, double* beta, int* steps);
+  int slq(int probes, int m, uint64_t seed, const fdh_lanczos_opts& o, double* nodes, double* weights, int* steps,
+          double* trace);
+  int init_params(void* params, uint64_t seed);
+  int make_tokens(int32_t* tok, int B, int S, uint64_t seed, int dist);
+  int random_vector(float* out, uint64_t seed, int kind);
+  int block_stats(const float* a, const float* b, double* out);
+
+ private:
+  template <typename T> int hvp_t(const T* th, const float* v, double eps, const int32_t* tok, int B, int S, float* hv);
+  template <typename B> int lanczos_t(int m, uint64_t seed, const fdh_lanczos_opts& o, double* alpha, double* beta, int* steps);
+  template <typename T> void* wsp(const Span& s) const { return (void*)(ws + s.off); }
+
+  // workspace spans
+  struct LayerSpans {
+    Span x_in_m, x_in_d, a_m, a_d, qkv_m, qkv_d, P_m, P_d, o_m, o_d, xmid_m, xmid_d, b_m, b_d, u_m, u_d, z_m, z_d;
+  };
+  std::vector<LayerSpans> ls;
+  Span xL_m, xL_d, f_m, f_d, lo, qkvf_m, qkvf_d, sc_m, sc_d, log_m, log_d, dlog_m, dlog_d, rowloss, losses;
+  Span dx0_m, dx0_d, dx1_m, dx1_d, dxo_m, dxo_d, dz_m, dz_d, dgu_m, dgu_d, dudf, db_m, db_d, gpart, do_m, do_d, dS_m, dS_d;
+  Span dqkv_m, dqkv_d, dqkvo_m, dqkvo_d, gqa_m, gqa_d, da_m, da_d, colpart, keys, rope, cdf, gpartial, bpart, bout;
+  Span lz_w, lz_q, lz_qp, lz_basis, lz_alpha, lz_beta, lz_coef, lz_partial, lz_flag, lz_maxabs;
+};
+
+}  // namespace fdh

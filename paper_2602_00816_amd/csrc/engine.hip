@@ -1,0 +1,830 @@
+// Host engine: layout, workspace plan, lockstep FD-HVP, Lanczos and SLQ.
+//
+// The FD-HVP (section 3.1, Eq. grad-fd-hvp; Algorithm 1 with one batch) needs
+// the gradients at theta + eps v and theta - eps v.  Both gradient passes run
+// at once: every activation and every upstream gradient is held as its mean m
+// and half difference d over the two points.  A linear layer y = x W^T with
+// W = theta +- eps v then splits exactly into
+//     y.m = x.m theta^T                      (+ x.d (eps v)^T, O(eps^2), below the rounding of y.m: not formed)
+//     y.d = x.d theta^T + x.m (eps v)^T
+// and the weight gradient needs only its half difference
+//     (g+ - g-)/2 = dy.m^T x.d + dy.d^T x.m,   so   Hv_W = (dy.m^T x.d + dy.d^T x.m) / eps.
+// Every non-linear step (norms, softmax, GELU/SwiGLU, cross-entropy) is
+// evaluated at both points in fp64 inside its kernel.  theta is never written.
+#include "engine.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+
+namespace fdh {
+
+#define CK(x)                                                                     \
+  do {                                                                            \
+    hipError_t e_ = (x);                                                          \
+    if (e_ != hipSuccess) {                                                       \
+      err = std::string(#x) + ": " + hipGetErrorString(e_);                       \
+      return FDH_ERR_HIP;                                                         \
+    }                                                                             \
+  } while (0)
+
+namespace {
+
+GemmOperand kmaj(const void* p, int64_t ld) {
+  GemmOperand o;
+  o.ptr = p;
+  o.s_row = ld;
+  o.s_k = 1;
+  return o;
+}
+GemmOperand mnmaj(const void* p, int64_t ld) {
+  GemmOperand o;
+  o.ptr = p;
+  o.s_row = 1;
+  o.s_k = ld;
+  return o;
+}
+
+constexpr size_t ALIGN = 256;
+
+}  // namespace
+
+Engine::Engine(const fdh_model_config& c, hipStream_t s) : cfg(c), stream(s) {
+  quad = cfg.family == FDH_FAMILY_QUAD_DIAG;
+  gpt2 = cfg.family == FDH_FAMILY_GPT2;
+  llama = cfg.family == FDH_FAMILY_LLAMA;
+  bf16 = cfg.dtype == FDH_BF16;
+  if (quad) {
+    P = cfg.quad_n;
+    entries.push_back({"theta", 0, P, P, 1, -1, FDH_PARAM_MATRIX});
+    return;
+  }
+  L = cfg.n_layers;
+  d = cfg.d_model;
+  Hq = cfg.n_heads;
+  Hk = cfg.n_kv_heads;
+  dh = d / Hq;
+  F = cfg.d_ff;
+  V = cfg.vocab;
+  Smax = cfg.max_seq;
+  qkvd = (Hq + 2 * Hk) * dh;
+  int64_t off = 0;
+  auto add = [&](const std::string& name, int64_t rows, int64_t cols, int layer, int kind) {
+    ParamRef r;
+    r.off = off;
+    r.rows = rows;
+    r.cols = cols;
+    entries.push_back({name, off, rows * cols, rows, cols, layer, kind});
+    off += rows * cols;
+    return r;
+  };
+  layers.resize(L);
+  if (gpt2) {
+    wte = add("wte", V, d, -1, FDH_PARAM_MATRIX);
+    wpe = add("wpe", Smax, d, -1, FDH_PARAM_MATRIX);
+    for (int l = 0; l < L; ++l) {
+      const std::string p = "h" + std::to_string(l) + ".";
+      LayerRefs& R = layers[l];
+      R.n1g = add(p + "ln1.g", d, 1, l, FDH_PARAM_GAIN);
+      R.n1b = add(p + "ln1.b", d, 1, l, FDH_PARAM_BIAS);
+      R.wqkv = add(p + "wqkv", 3 * d, d, l, FDH_PARAM_MATRIX);
+      R.bqkv = add(p + "bqkv", 3 * d, 1, l, FDH_PARAM_BIAS);
+      R.wo = add(p + "wo", d, d, l, FDH_PARAM_MATRIX);
+      R.bo = add(p + "bo", d, 1, l, FDH_PARAM_BIAS);
+      R.n2g = add(p + "ln2.g", d, 1, l, FDH_PARAM_GAIN);
+      R.n2b = add(p + "ln2.b", d, 1, l, FDH_PARAM_BIAS);
+      R.w1 = add(p + "w1", F, d, l, FDH_PARAM_MATRIX);
+      R.b1 = add(p + "b1", F, 1, l, FDH_PARAM_BIAS);
+      R.w2 = add(p + "w2", d, F, l, FDH_PARAM_MATRIX);
+      R.b2 = add(p + "b2", d, 1, l, FDH_PARAM_BIAS);
+    }
+    nfg = add("lnf.g", d, 1, -1, FDH_PARAM_GAIN);
+    nfb = add("lnf.b", d, 1, -1, FDH_PARAM_BIAS);
+    head = wte;
+  } else {
+    wte = add("embed", V, d, -1, FDH_PARAM_MATRIX);
+    for (int l = 0; l < L; ++l) {
+      const std::string p = "h" + std::to_string(l) + ".";
+      LayerRefs& R = layers[l];
+      R.n1g = add(p + "norm1.g", d, 1, l, FDH_PARAM_GAIN);
+      R.wqkv = add(p + "wqkv", qkvd, d, l, FDH_PARAM_MATRIX);
+      R.wo = add(p + "wo", d, Hq * dh, l, FDH_PARAM_MATRIX);
+      R.n2g = add(p + "norm2.g", d, 1, l, FDH_PARAM_GAIN);
+      R.w1 = add(p + "wgu", 2 * F, d, l, FDH_PARAM_MATRIX);
+      R.w2 = add(p + "wd", d, F, l, FDH_PARAM_MATRIX);
+    }
+    nfg = add("normf.g", d, 1, -1, FDH_PARAM_GAIN);
+    head = add("head", V, d, -1, FDH_PARAM_MATRIX);
+  }
+  P = off;
+}
+
+// ---------------------------------------------------------------------------
+// workspace plan
+// ---------------------------------------------------------------------------
+size_t Engine::plan(int B, int S, int m, const fdh_lanczos_opts* o, bool carve) {
+  size_t cur = 0;
+  auto take = [&](Span& s, size_t bytes) {
+    s.off = cur;
+    s.bytes = bytes;
+    cur += (bytes + ALIGN - 1) / ALIGN * ALIGN;
+  };
+  Span dummy;
+  const size_t ob = bf16 ? 2 : 4;
+  if (!quad) {
+    const size_t T_ = (size_t)B * S;
+    const size_t td = T_ * d, tq = T_ * qkvd, ta = T_ * (size_t)Hq * dh;
+    const size_t tu = T_ * (size_t)(gpt2 ? F : 2 * F), tz = T_ * F;
+    const size_t pp = (size_t)B * Hq * S * S;
+    ls.assign(L, LayerSpans{});
+    for (int l = 0; l < L; ++l) {
+      LayerSpans& s = ls[l];
+      take(s.x_in_m, td * 4); take(s.x_in_d, td * 4);
+      take(s.a_m, td * ob); take(s.a_d, td * ob);
+      take(s.qkv_m, tq * ob); take(s.qkv_d, tq * ob);
+      take(s.P_m, pp * ob); take(s.P_d, pp * ob);
+      take(s.o_m, ta * ob); take(s.o_d, ta * ob);
+      take(s.xmid_m, td * 4); take(s.xmid_d, td * 4);
+      take(s.b_m, td * ob); take(s.b_d, td * ob);
+      take(s.u_m, tu * 4); take(s.u_d, tu * 4);
+      take(s.z_m, tz * ob); take(s.z_d, tz * ob);
+    }
+    take(xL_m, td * 4); take(xL_d, td * 4);
+    take(f_m, td * ob); take(f_d, td * ob);
+    take(lo, (size_t)P * ob);
+    take(qkvf_m, tq * 4); take(qkvf_d, tq * 4);
+    take(sc_m, pp * 4); take(sc_d, pp * 4);
+    take(log_m, T_ * V * 4); take(log_d, T_ * V * 4);
+    take(dlog_m, T_ * V * ob); take(dlog_d, T_ * V * ob);
+    take(rowloss, 2 * T_ * 8);
+    take(losses, 2 * 8);
+    take(dx0_m, td * 4); take(dx0_d, td * 4);
+    take(dx1_m, td * 4); take(dx1_d, td * 4);
+    take(dxo_m, td * ob); take(dxo_d, td * ob);
+    take(dz_m, tz * 4); take(dz_d, tz * 4);
+    take(dgu_m, tu * ob); take(dgu_d, tu * ob);
+    take(dudf, gpt2 ? tz * 4 : 0);
+    take(db_m, td * 4); take(db_d, td * 4);
+    take(gpart, td * 4);
+    take(do_m, ta * ob); take(do_d, ta * ob);
+    take(dS_m, pp * ob); take(dS_d, pp * ob);
+    take(dqkv_m, tq * 4); take(dqkv_d, tq * 4);
+    take(dqkvo_m, tq * ob); take(dqkvo_d, tq * ob);
+    take(gqa_m, Hq != Hk ? ta * 4 : 0); take(gqa_d, Hq != Hk ? ta * 4 : 0);
+    take(da_m, td * 4); take(da_d, td * 4);
+    const size_t maxc = std::max<size_t>({(size_t)qkvd, (size_t)F, (size_t)d, (size_t)1});
+    take(colpart, 64 * maxc * 8);
+    take(keys, T_ * 4);
+    take(rope, (size_t)Smax * dh * 8);
+    take(cdf, (size_t)V * 8);
+  }
+  take(gpartial, 1024 * 8);
+  take(bpart, 256 * 3 * 8);
+  take(bout, (size_t)std::max(L, 1) * 3 * 8);
+  // Lanczos
+  if (m > 0) {
+    const int reorth = o ? o->reorth : FDH_REORTH_NONE;
+    const int bdt = o ? o->basis_dtype : FDH_F32;
+    int cap = 0;
+    if (reorth == FDH_REORTH_FULL) cap = m;
+    else if (reorth == FDH_REORTH_WINDOW) cap = std::min(m, o->window);
+    take(lz_w, (size_t)P * 4);
+    take(lz_q, (size_t)P * 4);
+    take(lz_qp, (size_t)P * 4);
+    take(lz_basis, (size_t)cap * P * (bdt == FDH_BF16 ? 2 : 4));
+    take(lz_alpha, (size_t)m * 8);
+    take(lz_beta, (size_t)m * 8);
+    take(lz_coef, 3 * 128 * 8);
+    take(lz_partial, (size_t)RED_BLOCKS * (cap + 2) * 8);
+    take(lz_flag, 2 * 4);
+    take(lz_maxabs, 8);
+  }
+  (void)dummy;
+  if (carve) {
+    planB = B;
+    planS = S;
+    planM = m;
+    if (o) planO = *o;
+  }
+  return cur;
+}
+
+// ---------------------------------------------------------------------------
+// GEMM plumbing
+// ---------------------------------------------------------------------------
+template <typename T>
+static int run_gemm(Engine& e, GemmArgs& g) {
+  const char* msg = gemm_check<T>(g);
+  if (msg) {
+    e.err = msg;
+    return FDH_ERR_UNSUPPORTED;
+  }
+  hipError_t r = gemm<T>(g, e.stream);
+  if (r != hipSuccess) {
+    e.err = std::string("gemm launch: ") + hipGetErrorString(r);
+    return FDH_ERR_HIP;
+  }
+  return FDH_OK;
+}
+
+#define RG(T, g)                       \
+  do {                                 \
+    int rc_ = run_gemm<T>(*this, g);   \
+    if (rc_ != FDH_OK) return rc_;     \
+  } while (0)
+
+// ---------------------------------------------------------------------------
+// lockstep FD-HVP
+// ---------------------------------------------------------------------------
+template <typename T>
+int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, int B, int S, float* hv) {
+  hipStream_t st = stream;
+  const int T_ = B * S;
+  const float feps = (float)eps;
+  const float inv_eps = (float)(1.0 / eps);
+  const bool ln = gpt2;
+  const float neps = cfg.norm_eps;
+  const int G = Hq / Hk;
+  const float att_scale = (float)(1.0 / std::sqrt((double)dh));
+  auto F32 = [&](const Span& s) { return (float*)(ws + s.off); };
+  auto OP = [&](const Span& s) { return (T*)(ws + s.off); };
+  T* lo = OP(this->lo);
+  const int64_t pp_stride = (int64_t)S * S;  // per (b,h) matrix
+
+  // perturbation operand: lo = eps * v in the operand type
+  CK(launch_scale_cast<T>(lo, v, eps, P, st));
+  if (llama) CK(launch_rope_table((double*)(ws + rope.off), S, dh, (double)cfg.rope_base, st));
+
+  // ---- linear helpers ----
+  auto lin_fwd = [&](const T* Xm, const T* Xd, int K, const ParamRef& W, const ParamRef& bias, float* Ym, float* Yd,
+                     const float* Rm, const float* Rd, int N) -> int {
+    GemmArgs g;
+    g.M = T_; g.N = N; g.K = K;
+    g.A[0] = kmaj(Xm, K);
+    g.B[0] = kmaj(th + W.off, K);
+    g.C = Ym; g.ldc = N;
+    g.resid = Rm;
+    if (bias.valid()) g.bias_theta = th + bias.off;
+    RG(T, g);
+    GemmArgs h;
+    h.M = T_; h.N = N; h.K = K; h.npairs = 2;
+    h.A[0] = kmaj(Xd, K); h.B[0] = kmaj(th + W.off, K);
+    h.A[1] = kmaj(Xm, K); h.B[1] = kmaj(lo + W.off, K);
+    h.C = Yd; h.ldc = N;
+    h.resid = Rd;
+    if (bias.valid()) { h.bias_v = v + bias.off; h.bias_v_scale = feps; }
+    RG(T, h);
+    return FDH_OK;
+  };
+  // dX = dY W ; W [N, K]
+  auto lin_dgrad = [&](const T* dYm, const T* dYd, int N, const ParamRef& W, int K, void* dXm, void* dXd, int out) -> int {
+    GemmArgs g;
+    g.M = T_; g.N = K; g.K = N;
+    g.A[0] = kmaj(dYm, N);
+    g.B[0] = mnmaj(th + W.off, K);
+    g.C = dXm; g.ldc = K; g.out_type = out;
+    RG(T, g);
+    GemmArgs h;
+    h.M = T_; h.N = K; h.K = N; h.npairs = 2;
+    h.A[0] = kmaj(dYd, N); h.B[0] = mnmaj(th + W.off, K);
+    h.A[1] = kmaj(dYm, N); h.B[1] = mnmaj(lo + W.off, K);
+    h.C = dXd; h.ldc = K; h.out_type = out;
+    RG(T, h);
+    return FDH_OK;
+  };
+  // Hv_W = (dY.m^T X.d + dY.d^T X.m) / eps
+  auto lin_wgrad = [&](const T* dYm, const T* dYd, int N, const T* Xm, const T* Xd, int K, const ParamRef& W) -> int {
+    GemmArgs g;
+    g.M = N; g.N = K; g.K = T_; g.npairs = 2;
+    g.A[0] = mnmaj(dYm, N); g.B[0] = mnmaj(Xd, K);
+    g.A[1] = mnmaj(dYd, N); g.B[1] = mnmaj(Xm, K);
+    g.C = hv + W.off; g.ldc = K; g.alpha = inv_eps;
+    RG(T, g);
+    return FDH_OK;
+  };
+  auto colsum_hv = [&](const float* X, int C, int64_t ld, const ParamRef& R) -> int {
+    CK(launch_colsum(hv + R.off, X, T_, C, ld, 1.0 / eps, false, (double*)(ws + colpart.off), st));
+    return FDH_OK;
+  };
+  // fp32 pair -> operand pair (aliases in fp32 mode)
+  auto as_op = [&](const float* m, const float* dd, const Span& om, const Span& od, int64_t n, T** rm, T** rd) -> int {
+    if (!bf16) {
+      *rm = (T*)m;
+      *rd = (T*)dd;
+      return FDH_OK;
+    }
+    PairT<T> o{OP(om), OP(od)};
+    CK(launch_cast_pair<T>(o, m, dd, n, st));
+    *rm = o.m;
+    *rd = o.d;
+    return FDH_OK;
+  };
+#define RC(x)                     \
+  do {                            \
+    int rc_ = (x);                \
+    if (rc_ != FDH_OK) return rc_; \
+  } while (0)
+
+  // ================= forward =================
+  {
+    PairF x0{F32(ls.empty() ? xL_m : ls[0].x_in_m), F32(ls.empty() ? xL_d : ls[0].x_in_d)};
+    CK(launch_embed_fwd<T>(x0, tok, T_, S, d, V, th + wte.off, v + wte.off, gpt2 ? th + wpe.off : nullptr,
+                           gpt2 ? v + wpe.off : nullptr, eps, st));
+  }
+  for (int l = 0; l < L; ++l) {
+    const LayerRefs& R = layers[l];
+    LayerSpans& s = ls[l];
+    const float* xm = F32(s.x_in_m);
+    const float* xd = F32(s.x_in_d);
+    // norm 1
+    CK(launch_norm_fwd<T>(PairT<T>{OP(s.a_m), OP(s.a_d)}, xm, xd, T_, d, ln, th + R.n1g.off, v + R.n1g.off,
+                          ln ? th + R.n1b.off : nullptr, ln ? v + R.n1b.off : nullptr, eps, neps, st));
+    // qkv projection
+    RC(lin_fwd(OP(s.a_m), OP(s.a_d), d, R.wqkv, R.bqkv, F32(qkvf_m), F32(qkvf_d), nullptr, nullptr, qkvd));
+    CK(launch_qkv_post<T>(PairT<T>{OP(s.qkv_m), OP(s.qkv_d)}, F32(qkvf_m), F32(qkvf_d), T_, S, Hq, Hk, dh,
+                          (const double*)(ws + rope.off), llama, st));
+    // scores S = q k^T / sqrt(dh), causal
+    {
+      const T* qm = OP(s.qkv_m);
+      const T* qd = OP(s.qkv_d);
+      GemmOperand Aq_m = kmaj(qm, qkvd), Aq_d = kmaj(qd, qkvd);
+      GemmOperand Bk_m = kmaj(qm + Hq * dh, qkvd), Bk_d = kmaj(qd + Hq * dh, qkvd);
+      for (GemmOperand* o : {&Aq_m, &Aq_d}) { o->s_outer = (int64_t)S * qkvd; o->s_inner = dh; }
+      for (GemmOperand* o : {&Bk_m, &Bk_d}) { o->s_outer = (int64_t)S * qkvd; o->s_inner = dh; o->inner_div = G; }
+      GemmArgs g;
+      g.M = S; g.N = S; g.K = dh; g.nbatch = B * Hq; g.inner_count = Hq;
+      g.A[0] = Aq_m; g.B[0] = Bk_m;
+      g.C = F32(sc_m); g.ldc = S; g.c_outer = (int64_t)Hq * pp_stride; g.c_inner = pp_stride;
+      g.alpha = att_scale; g.causal = CAUSAL_SKIP_UPPER;
+      RG(T, g);
+      GemmArgs h = g;
+      h.npairs = 2;
+      h.A[0] = Aq_m; h.B[0] = Bk_d;
+      h.A[1] = Aq_d; h.B[1] = Bk_m;
+      h.C = F32(sc_d);
+      RG(T, h);
+    }
+    CK(launch_attn_softmax<T>(PairT<T>{OP(s.P_m), OP(s.P_d)}, F32(sc_m), F32(sc_d), B * Hq * S, S, st));
+    // o = P v
+    {
+      const T* vm = OP(s.qkv_m) + (Hq + Hk) * dh;
+      const T* vd = OP(s.qkv_d) + (Hq + Hk) * dh;
+      GemmOperand Ap_m = kmaj(OP(s.P_m), S), Ap_d = kmaj(OP(s.P_d), S);
+      for (GemmOperand* o : {&Ap_m, &Ap_d}) { o->s_outer = (int64_t)Hq * pp_stride; o->s_inner = pp_stride; }
+      GemmOperand Bv_m = mnmaj(vm, qkvd), Bv_d = mnmaj(vd, qkvd);
+      for (GemmOperand* o : {&Bv_m, &Bv_d}) { o->s_outer = (int64_t)S * qkvd; o->s_inner = dh; o->inner_div = G; }
+      GemmArgs g;
+      g.M = S; g.N = dh; g.K = S; g.nbatch = B * Hq; g.inner_count = Hq;
+      g.A[0] = Ap_m; g.B[0] = Bv_m;
+      g.C = OP(s.o_m); g.ldc = (int64_t)Hq * dh; g.c_outer = (int64_t)S * Hq * dh; g.c_inner = dh;
+      g.out_type = OUT_OP; g.causal = CAUSAL_K_LE_M;
+      RG(T, g);
+      GemmArgs h = g;
+      h.npairs = 2;
+      h.A[0] = Ap_m; h.B[0] = Bv_d;
+      h.A[1] = Ap_d; h.B[1] = Bv_m;
+      h.C = OP(s.o_d);
+      RG(T, h);
+    }
+    // output projection + residual
+    RC(lin_fwd(OP(s.o_m), OP(s.o_d), Hq * dh, R.wo, R.bo, F32(s.xmid_m), F32(s.xmid_d), xm, xd, d));
+    // norm 2
+    CK(launch_norm_fwd<T>(PairT<T>{OP(s.b_m), OP(s.b_d)}, F32(s.xmid_m), F32(s.xmid_d), T_, d, ln, th + R.n2g.off,
+                          v + R.n2g.off, ln ? th + R.n2b.off : nullptr, ln ? v + R.n2b.off : nullptr, eps, neps, st));
+    // MLP
+    const int nu = gpt2 ? F : 2 * F;
+    RC(lin_fwd(OP(s.b_m), OP(s.b_d), d, R.w1, R.b1, F32(s.u_m), F32(s.u_d), nullptr, nullptr, nu));
+    if (gpt2) CK(launch_gelu_fwd<T>(PairT<T>{OP(s.z_m), OP(s.z_d)}, F32(s.u_m), F32(s.u_d), (int64_t)T_ * F, st));
+    else CK(launch_swiglu_fwd<T>(PairT<T>{OP(s.z_m), OP(s.z_d)}, F32(s.u_m), F32(s.u_d), T_, F, st));
+    float* nxm = (l + 1 < L) ? F32(ls[l + 1].x_in_m) : F32(xL_m);
+    float* nxd = (l + 1 < L) ? F32(ls[l + 1].x_in_d) : F32(xL_d);
+    RC(lin_fwd(OP(s.z_m), OP(s.z_d), F, R.w2, R.b2, nxm, nxd, F32(s.xmid_m), F32(s.xmid_d), d));
+  }
+  // final norm + head + cross-entropy
+  CK(launch_norm_fwd<T>(PairT<T>{OP(f_m), OP(f_d)}, F32(xL_m), F32(xL_d), T_, d, ln, th + nfg.off, v + nfg.off,
+                        ln ? th + nfb.off : nullptr, ln ? v + nfb.off : nullptr, eps, neps, st));
+  RC(lin_fwd(OP(f_m), OP(f_d), d, head, ParamRef{}, F32(log_m), F32(log_d), nullptr, nullptr, V));
+  const double inv_n = 1.0 / ((double)B * (S - 1));
+  CK(launch_ce<T>(PairT<T>{OP(dlog_m), OP(dlog_d)}, (double*)(ws + rowloss.off), F32(log_m), F32(log_d), tok, T_, S, V,
+                  inv_n, st));
+  CK(launch_loss_sum((double*)(ws + losses.off), (const double*)(ws + rowloss.off), T_, st));
+
+  // ================= backward =================
+  // head
+  RC(lin_wgrad(OP(dlog_m), OP(dlog_d), V, OP(f_m), OP(f_d), d, head));
+  RC(lin_dgrad(OP(dlog_m), OP(dlog_d), V, head, d, F32(db_m), F32(db_d), OUT_F32));
+  float* dxm = F32(dx0_m);
+  float* dxd = F32(dx0_d);
+  float* dym = F32(dx1_m);
+  float* dyd = F32(dx1_d);
+  CK(launch_norm_bwd<T>(PairF{dxm, dxd}, nullptr, nullptr, F32(xL_m), F32(xL_d), F32(db_m), F32(db_d), T_, d, ln,
+                        th + nfg.off, v + nfg.off, eps, neps, F32(gpart), st));
+  RC(colsum_hv(F32(gpart), d, d, nfg));
+  if (ln) RC(colsum_hv(F32(db_d), d, d, nfb));
+
+  for (int l = L - 1; l >= 0; --l) {
+    const LayerRefs& R = layers[l];
+    LayerSpans& s = ls[l];
+    // ---- MLP ----  (dx = gradient w.r.t. layer output)
+    T *gom, *god;
+    RC(as_op(dxm, dxd, dxo_m, dxo_d, (int64_t)T_ * d, &gom, &god));
+    if (gpt2) RC(colsum_hv(dxd, d, d, R.b2));
+    RC(lin_wgrad(gom, god, d, OP(s.z_m), OP(s.z_d), F, R.w2));
+    RC(lin_dgrad(gom, god, d, R.w2, F, F32(dz_m), F32(dz_d), OUT_F32));
+    const int nu = gpt2 ? F : 2 * F;
+    if (gpt2) {
+      CK(launch_gelu_bwd<T>(PairT<T>{OP(dgu_m), OP(dgu_d)}, F32(dudf), F32(s.u_m), F32(s.u_d), F32(dz_m), F32(dz_d),
+                            (int64_t)T_ * F, st));
+      RC(colsum_hv(F32(dudf), F, F, R.b1));
+    } else {
+      CK(launch_swiglu_bwd<T>(PairT<T>{OP(dgu_m), OP(dgu_d)}, F32(s.u_m), F32(s.u_d), F32(dz_m), F32(dz_d), T_, F, st));
+    }
+    RC(lin_wgrad(OP(dgu_m), OP(dgu_d), nu, OP(s.b_m), OP(s.b_d), d, R.w1));
+    RC(lin_dgrad(OP(dgu_m), OP(dgu_d), nu, R.w1, d, F32(db_m), F32(db_d), OUT_F32));
+    // norm 2 backward, residual: dy = dx + norm2'(db)
+    CK(launch_norm_bwd<T>(PairF{dym, dyd}, dxm, dxd, F32(s.xmid_m), F32(s.xmid_d), F32(db_m), F32(db_d), T_, d, ln,
+                          th + R.n2g.off, v + R.n2g.off, eps, neps, F32(gpart), st));
+    RC(colsum_hv(F32(gpart), d, d, R.n2g));
+    if (ln) RC(colsum_hv(F32(db_d), d, d, R.n2b));
+    std::swap(dxm, dym);
+    std::swap(dxd, dyd);
+    // ---- attention ----  (dx = gradient w.r.t. x_mid)
+    RC(as_op(dxm, dxd, dxo_m, dxo_d, (int64_t)T_ * d, &gom, &god));
+    if (gpt2) RC(colsum_hv(dxd, d, d, R.bo));
+    RC(lin_wgrad(gom, god, d, OP(s.o_m), OP(s.o_d), Hq * dh, R.wo));
+    RC(lin_dgrad(gom, god, d, R.wo, Hq * dh, OP(do_m), OP(do_d), OUT_OP));
+    const T* qm = OP(s.qkv_m);
+    const T* qd = OP(s.qkv_d);
+    // dP = do v^T
+    {
+      GemmOperand Ao_m = kmaj(OP(do_m), (int64_t)Hq * dh), Ao_d = kmaj(OP(do_d), (int64_t)Hq * dh);
+      for (GemmOperand* o : {&Ao_m, &Ao_d}) { o->s_outer = (int64_t)S * Hq * dh; o->s_inner = dh; }
+      GemmOperand Bv_m = kmaj(qm + (Hq + Hk) * dh, qkvd), Bv_d = kmaj(qd + (Hq + Hk) * dh, qkvd);
+      for (GemmOperand* o : {&Bv_m, &Bv_d}) { o->s_outer = (int64_t)S * qkvd; o->s_inner = dh; o->inner_div = G; }
+      GemmArgs g;
+      g.M = S; g.N = S; g.K = dh; g.nbatch = B * Hq; g.inner_count = Hq;
+      g.A[0] = Ao_m; g.B[0] = Bv_m;
+      g.C = F32(sc_m); g.ldc = S; g.c_outer = (int64_t)Hq * pp_stride; g.c_inner = pp_stride;
+      g.causal = CAUSAL_SKIP_UPPER;
+      RG(T, g);
+      GemmArgs h = g;
+      h.npairs = 2;
+      h.A[0] = Ao_m; h.B[0] = Bv_d;
+      h.A[1] = Ao_d; h.B[1] = Bv_m;
+      h.C = F32(sc_d);
+      RG(T, h);
+    }
+    CK(launch_attn_dsoftmax<T>(PairT<T>{OP(dS_m), OP(dS_d)}, OP(s.P_m), OP(s.P_d), F32(sc_m), F32(sc_d), B * Hq * S, S, st));
+    // dv = P^T do ; dq = dS k / sqrt(dh) ; dk = dS^T q / sqrt(dh)
+    {
+      float* gm = F32(dqkv_m);
+      float* gd = F32(dqkv_d);
+      const bool grp = G > 1;
+      // helpers for the per-(b,h) outputs
+      auto out_into = [&](GemmArgs& g, bool to_tmp) {
+        if (to_tmp) {
+          g.ldc = (int64_t)Hq * dh; g.c_outer = (int64_t)S * Hq * dh; g.c_inner = dh;
+        } else {
+          g.ldc = qkvd; g.c_outer = (int64_t)S * qkvd; g.c_inner = dh;
+        }
+      };
+      // dv
+      GemmOperand At_m = mnmaj(OP(s.P_m), S), At_d = mnmaj(OP(s.P_d), S);
+      for (GemmOperand* o : {&At_m, &At_d}) { o->s_outer = (int64_t)Hq * pp_stride; o->s_inner = pp_stride; }
+      GemmOperand Bo_m = mnmaj(OP(do_m), (int64_t)Hq * dh), Bo_d = mnmaj(OP(do_d), (int64_t)Hq * dh);
+      for (GemmOperand* o : {&Bo_m, &Bo_d}) { o->s_outer = (int64_t)S * Hq * dh; o->s_inner = dh; }
+      const int voff = (Hq + Hk) * dh, koff = Hq * dh;
+      {
+        GemmArgs g;
+        g.M = S; g.N = dh; g.K = S; g.nbatch = B * Hq; g.inner_count = Hq; g.causal = CAUSAL_K_GE_M;
+        g.A[0] = At_m; g.B[0] = Bo_m;
+        out_into(g, grp);
+        g.C = grp ? F32(gqa_m) : gm + voff;
+        RG(T, g);
+        GemmArgs h = g;
+        h.npairs = 2;
+        h.A[0] = At_m; h.B[0] = Bo_d;
+        h.A[1] = At_d; h.B[1] = Bo_m;
+        h.C = grp ? F32(gqa_d) : gd + voff;
+        RG(T, h);
+        if (grp) {
+          CK(launch_group_sum(gm + voff, qkvd, F32(gqa_m), T_, Hk, G, dh, st));
+          CK(launch_group_sum(gd + voff, qkvd, F32(gqa_d), T_, Hk, G, dh, st));
+        }
+      }
+      // dq
+      {
+        GemmOperand As_m = kmaj(OP(dS_m), S), As_d = kmaj(OP(dS_d), S);
+        for (GemmOperand* o : {&As_m, &As_d}) { o->s_outer = (int64_t)Hq * pp_stride; o->s_inner = pp_stride; }
+        GemmOperand Bk_m = mnmaj(qm + koff, qkvd), Bk_d = mnmaj(qd + koff, qkvd);
+        for (GemmOperand* o : {&Bk_m, &Bk_d}) { o->s_outer = (int64_t)S * qkvd; o->s_inner = dh; o->inner_div = G; }
+        GemmArgs g;
+        g.M = S; g.N = dh; g.K = S; g.nbatch = B * Hq; g.inner_count = Hq; g.causal = CAUSAL_K_LE_M;
+        g.alpha = att_scale;
+        g.A[0] = As_m; g.B[0] = Bk_m;
+        out_into(g, false);
+        g.C = gm;
+        RG(T, g);
+        GemmArgs h = g;
+        h.npairs = 2;
+        h.A[0] = As_m; h.B[0] = Bk_d;
+        h.A[1] = As_d; h.B[1] = Bk_m;
+        h.C = gd;
+        RG(T, h);
+      }
+      // dk
+      {
+        GemmOperand Ast_m = mnmaj(OP(dS_m), S), Ast_d = mnmaj(OP(dS_d), S);
+        for (GemmOperand* o : {&Ast_m, &Ast_d}) { o->s_outer = (int64_t)Hq * pp_stride; o->s_inner = pp_stride; }
+        GemmOperand Bq_m = mnmaj(qm, qkvd), Bq_d = mnmaj(qd, qkvd);
+        for (GemmOperand* o : {&Bq_m, &Bq_d}) { o->s_outer = (int64_t)S * qkvd; o->s_inner = dh; }
+        GemmArgs g;
+        g.M = S; g.N = dh; g.K = S; g.nbatch = B * Hq; g.inner_count = Hq; g.causal = CAUSAL_K_GE_M;
+        g.alpha = att_scale;
+        g.A[0] = Ast_m; g.B[0] = Bq_m;
+        out_into(g, grp);
+        g.C = grp ? F32(gqa_m) : gm + koff;
+        RG(T, g);
+        GemmArgs h = g;
+        h.npairs = 2;
+        h.A[0] = Ast_m; h.B[0] = Bq_d;
+        h.A[1] = Ast_d; h.B[1] = Bq_m;
+        h.C = grp ? F32(gqa_d) : gd + koff;
+        RG(T, h);
+        if (grp) {
+          CK(launch_group_sum(gm + koff, qkvd, F32(gqa_m), T_, Hk, G, dh, st));
+          CK(launch_group_sum(gd + koff, qkvd, F32(gqa_d), T_, Hk, G, dh, st));
+        }
+      }
+      if (gpt2) RC(colsum_hv(gd, qkvd, qkvd, R.bqkv));
+      CK(launch_qkv_bwd_post<T>(PairT<T>{OP(dqkvo_m), OP(dqkvo_d)}, gm, gd, T_, S, Hq, Hk, dh,
+                                (const double*)(ws + rope.off), llama, st));
+    }
+    RC(lin_wgrad(OP(dqkvo_m), OP(dqkvo_d), qkvd, OP(s.a_m), OP(s.a_d), d, R.wqkv));
+    RC(lin_dgrad(OP(dqkvo_m), OP(dqkvo_d), qkvd, R.wqkv, d, F32(da_m), F32(da_d), OUT_F32));
+    CK(launch_norm_bwd<T>(PairF{dym, dyd}, dxm, dxd, F32(s.x_in_m), F32(s.x_in_d), F32(da_m), F32(da_d), T_, d, ln,
+                          th + R.n1g.off, v + R.n1g.off, eps, neps, F32(gpart), st));
+    RC(colsum_hv(F32(gpart), d, d, R.n1g));
+    if (ln) RC(colsum_hv(F32(da_d), d, d, R.n1b));
+    std::swap(dxm, dym);
+    std::swap(dxd, dyd);
+  }
+  // embeddings (difference channel of the gradient w.r.t. the embedding output)
+  CK(launch_token_sort((uint32_t*)(ws + keys.off), tok, T_, V, st));
+  if (!gpt2) CK(launch_fill_f32(hv + wte.off, (int64_t)V * d, 0.f, st));
+  CK(launch_embed_bwd(hv + wte.off, (const uint32_t*)(ws + keys.off), dxd, T_, d, 1.0 / eps, gpt2, st));
+  if (gpt2) {
+    CK(launch_pos_bwd(hv + wpe.off, dxd, B, S, d, 1.0 / eps, st));
+    if (Smax > S) CK(launch_fill_f32(hv + wpe.off + (int64_t)S * d, (int64_t)(Smax - S) * d, 0.f, st));
+  }
+  (void)dxm;
+  return FDH_OK;
+#undef RC
+}
+
+int Engine::hvp(const void* params, const float* v, double eps, const int32_t* tok, int B, int S, float* hv) {
+  if (!params || !v || !hv) { err = "null pointer"; return FDH_ERR_INVALID_ARG; }
+  if (!(eps > 0.0) || !std::isfinite(eps)) { err = "eps must be positive and finite"; return FDH_ERR_INVALID_ARG; }
+  if ((const void*)hv == params || (const void*)hv == (const void*)v) { err = "hv aliases an input"; return FDH_ERR_INVALID_ARG; }
+  if (quad) {
+    if (!quad_diag) { err = "QUAD_DIAG: call fdh_set_quad_diag first"; return FDH_ERR_STATE; }
+    if (bf16) CK(launch_quad_diag_hvp<bf16_t>((const bf16_t*)params, quad_diag, v, eps, hv, P, stream));
+    else CK(launch_quad_diag_hvp<float>((const float*)params, quad_diag, v, eps, hv, P, stream));
+    return FDH_OK;
+  }
+  if (!tok) { err = "null tokens"; return FDH_ERR_INVALID_ARG; }
+  if (B < 1 || S < 2) { err = "need B >= 1 and S >= 2"; return FDH_ERR_INVALID_ARG; }
+  if (!ws) { err = "no workspace"; return FDH_ERR_WORKSPACE; }
+  if (B > planB || S > planS || S > Smax) { err = "batch larger than the workspace plan (or S > max_seq)"; return FDH_ERR_WORKSPACE; }
+  if ((int64_t)B * S > 16384) { err = "B*S must be <= 16384"; return FDH_ERR_UNSUPPORTED; }
+  if (S > 4096) { err = "S must be <= 4096"; return FDH_ERR_UNSUPPORTED; }
+  if (S % 8 || dh % 8) { err = "S and head_dim must be multiples of 8"; return FDH_ERR_UNSUPPORTED; }
+  if (bf16) return hvp_t<bf16_t>((const bf16_t*)params, v, eps, tok, B, S, hv);
+  return hvp_t<float>((const float*)params, v, eps, tok, B, S, hv);
+}
+
+int Engine::last_losses(double* lp, double* lm) {
+  if (quad || !ws) { err = "no losses for this context"; return FDH_ERR_STATE; }
+  double h[2];
+  CK(hipMemcpyAsync(h, ws + losses.off, 16, hipMemcpyDeviceToHost, stream));
+  CK(hipStreamSynchronize(stream));
+  if (lp) *lp = h[0];
+  if (lm) *lm = h[1];
+  return FDH_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Lanczos (section 4; Appendix C) with device-resident scalars
+// ---------------------------------------------------------------------------
+template <typename Bt>
+int Engine::lanczos_t(int m, uint64_t seed, const fdh_lanczos_opts& o, double* alpha, double* beta, int* steps) {
+  hipStream_t st = stream;
+  float* w = (float*)(ws + lz_w.off);
+  float* q = (float*)(ws + lz_q.off);
+  float* qp = (float*)(ws + lz_qp.off);
+  Bt* basis = (Bt*)(ws + lz_basis.off);
+  LanczosDev D;
+  D.alpha = (double*)(ws + lz_alpha.off);
+  D.beta = (double*)(ws + lz_beta.off);
+  D.coef = (double*)(ws + lz_coef.off);
+  D.partial = (double*)(ws + lz_partial.off);
+  D.flag = (int*)(ws + lz_flag.off);
+  D.maxabs = (double*)(ws + lz_maxabs.off);
+  const int cap = o.reorth == FDH_REORTH_FULL ? m : (o.reorth == FDH_REORTH_WINDOW ? std::min(m, o.window) : 0);
+  const double tol = o.breakdown_tol > 0.f ? (double)o.breakdown_tol : 1e-5;
+
+  CK(launch_fill_f64(D.alpha, m, 0.0, st));
+  CK(launch_fill_f64(D.beta, m, 0.0, st));
+  CK(launch_fill_f64(D.maxabs, 1, 0.0, st));
+  CK(launch_fill_f32((float*)D.flag, 2, 0.f, st));
+  CK(launch_fill_f32(qp, P, 0.f, st));
+  CK(launch_rademacher(q, P, seed, st));
+  if (cap > 0) CK(launch_scale_cast<Bt>(basis, q, 1.0, P, st));  // slot 0 = q_1
+
+  for (int k = 0; k < m; ++k) {
+    int rc = hvp(b_params, q, b_eps, b_tokens, b_B, b_S, w);
+    if (rc != FDH_OK) return rc;
+    CK(launch_lanczos_alpha(w, q, qp, D, k, P, st));
+    const int nv = std::min(k + 1, cap);
+    CK(launch_lanczos_b<Bt>(w, q, basis, nv, D, k, P, st));
+    if (nv > 0) {
+      CK(launch_lanczos_cgs<Bt>(w, basis, nv, D, 0, false, k, P, st));
+      CK(launch_lanczos_cgs<Bt>(w, basis, nv, D, 1, true, k, P, st));
+    }
+    Bt* row = nullptr;
+    if (cap > 0 && k + 1 < m) row = basis + (int64_t)((k + 1) % cap) * P;
+    CK(launch_lanczos_normalise<Bt>(w, qp, row, D, k, tol, P, st));
+    std::swap(q, qp);
+  }
+  std::vector<double> a(m), b(m);
+  int flag[2];
+  CK(hipMemcpyAsync(a.data(), D.alpha, m * 8, hipMemcpyDeviceToHost, st));
+  CK(hipMemcpyAsync(b.data(), D.beta, m * 8, hipMemcpyDeviceToHost, st));
+  CK(hipMemcpyAsync(flag, D.flag, 8, hipMemcpyDeviceToHost, st));
+  CK(hipStreamSynchronize(st));
+  const int s = flag[0] ? flag[0] : m;
+  for (int k = 0; k < m; ++k) {
+    alpha[k] = k < s ? a[k] : 0.0;
+    beta[k] = k < s ? b[k] : 0.0;
+  }
+  *steps = s;
+  for (int k = 0; k < s; ++k)
+    if (!std::isfinite(a[k]) || !std::isfinite(b[k])) { err = "non-finite Lanczos coefficient"; return FDH_ERR_NONFINITE; }
+  return s < m ? FDH_BREAKDOWN : FDH_OK;
+}
+
+int Engine::lanczos(int m, uint64_t seed, const fdh_lanczos_opts& o, double* alpha, double* beta, int* steps) {
+  if (!bound) { err = "call fdh_bind first"; return FDH_ERR_STATE; }
+  if (m < 1 || !alpha || !beta || !steps) { err = "bad lanczos arguments"; return FDH_ERR_INVALID_ARG; }
+  if (o.reorth < 0 || o.reorth > 2 || (o.reorth == FDH_REORTH_WINDOW && o.window < 1)) { err = "bad reorth options"; return FDH_ERR_INVALID_ARG; }
+  if (!ws || m > planM || o.reorth != planO.reorth || o.basis_dtype != planO.basis_dtype ||
+      (o.reorth == FDH_REORTH_WINDOW && std::min(m, o.window) > std::min(planM, planO.window))) {
+    err = "Lanczos options or m exceed the workspace plan";
+    return FDH_ERR_WORKSPACE;
+  }
+  if (m > 128) { err = "m must be <= 128"; return FDH_ERR_UNSUPPORTED; }
+  if (o.basis_dtype == FDH_BF16) return lanczos_t<bf16_t>(m, seed, o, alpha, beta, steps);
+  return lanczos_t<float>(m, seed, o, alpha, beta, steps);
+}
+
+// Eigen-decomposition of the symmetric tridiagonal T (order n <= 128) by the
+// cyclic Jacobi method (Golub and Van Loan, Matrix Computations, section 8.5):
+// plane rotations annihilate each off-diagonal entry in turn until the
+// off-diagonal mass vanishes.  On return dd holds the eigenvalues and column i
+// of z (row-major n x n) the eigenvector of dd[i].
+static void tridiag_eig(int n, std::vector<double>& dd, const std::vector<double>& e, std::vector<double>& z) {
+  std::vector<double> A((size_t)n * n, 0.0);
+  for (int i = 0; i < n; ++i) A[(size_t)i * n + i] = dd[i];
+  for (int i = 0; i + 1 < n; ++i) A[(size_t)i * n + i + 1] = A[(size_t)(i + 1) * n + i] = e[i];
+  z.assign((size_t)n * n, 0.0);
+  for (int i = 0; i < n; ++i) z[(size_t)i * n + i] = 1.0;
+  double fro = 0.0;
+  for (double x : A) fro += x * x;
+  for (int sweep = 0; sweep < 100; ++sweep) {
+    double off = 0.0;
+    for (int p = 0; p < n; ++p)
+      for (int q = p + 1; q < n; ++q) off += A[(size_t)p * n + q] * A[(size_t)p * n + q];
+    if (off <= 1e-32 * fro || off == 0.0) break;
+    for (int p = 0; p < n; ++p)
+      for (int q = p + 1; q < n; ++q) {
+        const double apq = A[(size_t)p * n + q];
+        if (apq == 0.0) continue;
+        const double tau = (A[(size_t)q * n + q] - A[(size_t)p * n + p]) / (2.0 * apq);
+        const double t = (tau >= 0 ? 1.0 : -1.0) / (std::fabs(tau) + std::sqrt(1.0 + tau * tau));
+        const double c = 1.0 / std::sqrt(1.0 + t * t), s = t * c;
+        for (int k = 0; k < n; ++k) {  // A <- A J  (columns p, q)
+          const double akp = A[(size_t)k * n + p], akq = A[(size_t)k * n + q];
+          A[(size_t)k * n + p] = c * akp - s * akq;
+          A[(size_t)k * n + q] = s * akp + c * akq;
+        }
+        for (int k = 0; k < n; ++k) {  // A <- J^T A  (rows p, q)
+          const double apk = A[(size_t)p * n + k], aqk = A[(size_t)q * n + k];
+          A[(size_t)p * n + k] = c * apk - s * aqk;
+          A[(size_t)q * n + k] = s * apk + c * aqk;
+        }
+        for (int k = 0; k < n; ++k) {  // z <- z J
+          const double zkp = z[(size_t)k * n + p], zkq = z[(size_t)k * n + q];
+          z[(size_t)k * n + p] = c * zkp - s * zkq;
+          z[(size_t)k * n + q] = s * zkp + c * zkq;
+        }
+      }
+  }
+  for (int i = 0; i < n; ++i) dd[i] = A[(size_t)i * n + i];
+}
+
+int Engine::slq(int probes, int m, uint64_t seed, const fdh_lanczos_opts& o, double* nodes, double* weights, int* steps,
+                double* trace) {
+  if (probes < 1 || !nodes || !weights || !steps) { err = "bad slq arguments"; return FDH_ERR_INVALID_ARG; }
+  std::vector<double> a(m), b(m);
+  double sum_a1 = 0.0;
+  int status = FDH_OK;
+  for (int j = 0; j < probes; ++j) {
+    int s = 0;
+    int rc = lanczos(m, seed + (uint64_t)j, o, a.data(), b.data(), &s);
+    if (rc < 0) return rc;
+    if (rc == FDH_BREAKDOWN) status = FDH_BREAKDOWN;
+    steps[j] = s;
+    sum_a1 += a[0];
+    std::vector<double> dd(a.begin(), a.begin() + s), e(b.begin(), b.begin() + std::max(0, s - 1)), z;
+    tridiag_eig(s, dd, e, z);
+    // sort ascending with the first eigenvector components
+    std::vector<int> idx(s);
+    for (int i = 0; i < s; ++i) idx[i] = i;
+    std::sort(idx.begin(), idx.end(), [&](int x, int y) { return dd[x] < dd[y]; });
+    for (int i = 0; i < m; ++i) {
+      nodes[(size_t)j * m + i] = i < s ? dd[idx[i]] : 0.0;
+      weights[(size_t)j * m + i] = i < s ? z[(size_t)0 * s + idx[i]] * z[(size_t)0 * s + idx[i]] : 0.0;
+    }
+  }
+  if (trace) *trace = (double)P * sum_a1 / probes;
+  return status;
+}
+
+// ---------------------------------------------------------------------------
+// synthetic inputs and block statistics
+// ---------------------------------------------------------------------------
+int Engine::init_params(void* params, uint64_t seed) {
+  if (!params) { err = "null params"; return FDH_ERR_INVALID_ARG; }
+  for (const Entry& e : entries) {
+    const int kind = quad ? FDH_PARAM_MATRIX : e.kind;
+    if (bf16) CK(launch_init_range<bf16_t>((bf16_t*)params, e.off, e.numel, kind, seed, 0.02, stream));
+    else CK(launch_init_range<float>((float*)params, e.off, e.numel, kind, seed, 0.02, stream));
+  }
+  return FDH_OK;
+}
+
+int Engine::make_tokens(int32_t* tok, int B, int S, uint64_t seed, int dist) {
+  if (quad || !tok || B < 1 || S < 1) { err = "bad token arguments"; return FDH_ERR_INVALID_ARG; }
+  const int64_t n = (int64_t)B * S;
+  if (dist == FDH_TOKENS_UNIFORM) {
+    CK(launch_tokens_uniform(tok, n, seed, V, stream));
+    return FDH_OK;
+  }
+  if (dist != FDH_TOKENS_ZIPF) { err = "unknown token distribution"; return FDH_ERR_INVALID_ARG; }
+  if (!ws) { err = "Zipf tokens need the workspace"; return FDH_ERR_WORKSPACE; }
+  std::vector<double> c(V);
+  double acc = 0.0;
+  for (int k = 0; k < V; ++k) {
+    acc += std::pow((double)(k + 1), -1.1);
+    c[k] = acc;
+  }
+  for (int k = 0; k < V; ++k) c[k] /= acc;
+  CK(hipMemcpyAsync(ws + cdf.off, c.data(), (size_t)V * 8, hipMemcpyHostToDevice, stream));
+  CK(launch_tokens_zipf(tok, n, seed, (const double*)(ws + cdf.off), V, stream));
+  CK(hipStreamSynchronize(stream));  // the host cdf buffer goes out of scope
+  return FDH_OK;
+}
+
+int Engine::random_vector(float* out, uint64_t seed, int kind) {
+  if (!out) { err = "null output"; return FDH_ERR_INVALID_ARG; }
+  if (kind == FDH_VEC_RADEMACHER) {
+    CK(launch_rademacher(out, P, seed, stream));
+    return FDH_OK;
+  }
+  if (kind != FDH_VEC_GAUSSIAN) { err = "unknown vector kind"; return FDH_ERR_INVALID_ARG; }
+  if (!ws) { err = "Gaussian vectors need the workspace"; return FDH_ERR_WORKSPACE; }
+  CK(launch_gaussian_unit(out, (double*)(ws + gpartial.off), P, seed, stream));
+  return FDH_OK;
+}
+
+int Engine::block_stats(const float* a, const float* b, double* out) {
+  if (quad || !a || !b || !out) { err = "bad block_stats arguments"; return FDH_ERR_INVALID_ARG; }
+  if (!ws) { err = "no workspace"; return FDH_ERR_WORKSPACE; }
+  std::vector<int64_t> ranges(2 * L);
+  for (int l = 0; l < L; ++l) {
+    int64_t s0 = -1, s1 = -1;
+    for (const Entry& e : entries)
+      if (e.layer == l) {
+        if (s0 < 0) s0 = e.off;
+        s1 = e.off + e.numel;
+      }
+    ranges[2 * l] = s0;
+    ranges[2 * l + 1] = s1;
+  }
+  CK(launch_block_stats(a, b, ranges.data(), L, (double*)(ws + bpart.off), (double*)(ws + bout.off), stream));
+  CK(hipMemcpyAsync(out, ws + bout.off, (size_t)L * 3 * 8, hipMemcpyDeviceToHost, stream));
+  CK(hipStreamSynchronize(stream));
+  return FDH_OK;
+}
+
+}  // namespace fdh

@@ -1,0 +1,131 @@
+// Launchers for the HIP kernels (internal interface between the host engine and
+// the device code).  Every launcher enqueues on the given stream and returns
+// the launch status; none synchronises.
+#pragma once
+#include "common.h"
+#include "gemm.h"
+
+namespace fdh {
+
+// SplitMix64 streams (one per purpose)
+constexpr uint64_t STREAM_PARAMS = 1, STREAM_TOKENS = 2, STREAM_PROBE = 3, STREAM_GAUSS = 4;
+
+// ---- rng.hip ---------------------------------------------------------------
+template <typename T>
+hipError_t launch_init_range(T* theta, int64_t off, int64_t n, int kind, uint64_t seed, double stdv, hipStream_t s);
+hipError_t launch_tokens_uniform(int32_t* tok, int64_t n, uint64_t seed, int V, hipStream_t s);
+hipError_t launch_tokens_zipf(int32_t* tok, int64_t n, uint64_t seed, const double* cdf, int V, hipStream_t s);
+hipError_t launch_rademacher(float* out, int64_t n, uint64_t seed, hipStream_t s);
+hipError_t launch_gaussian_unit(float* out, double* partial1024, int64_t n, uint64_t seed, hipStream_t s);
+
+// ---- vec.hip ---------------------------------------------------------------
+constexpr int RED_BLOCKS = 1024;   // fixed grid of the deterministic reductions
+
+hipError_t launch_fill_f32(float* p, int64_t n, float v, hipStream_t s);
+hipError_t launch_fill_f64(double* p, int64_t n, double v, hipStream_t s);
+// lo[i] = T(eps * v[i])
+template <typename T>
+hipError_t launch_scale_cast(T* lo, const float* v, double eps, int64_t n, hipStream_t s);
+// QUAD_DIAG: hv = (d (theta + eps v) - d (theta - eps v)) / (2 eps), both points in fp64
+template <typename T>
+hipError_t launch_quad_diag_hvp(const T* theta, const float* d, const float* v, double eps, float* hv, int64_t n, hipStream_t s);
+
+// Lanczos state kept in device memory (fp64 scalars)
+struct LanczosDev {
+  double* alpha;     // [m]
+  double* beta;      // [m]  beta[k] = beta_{k+2} in 1-based notation (residual after step k)
+  double* coef;      // [2 * cap] reorthogonalisation coefficients (two CGS passes)
+  double* partial;   // [RED_BLOCKS * (cap + 2)]
+  int* flag;         // [2]: [0] = breakdown step + 1 (0 = none), [1] = spare
+  double* maxabs;    // [1]  max_j |alpha_j| so far
+};
+
+// Step A:  w <- w - beta_k q_prev;  alpha_k = <w, q>  (beta_k = beta[k-1], 0 for k = 0)
+hipError_t launch_lanczos_alpha(float* w, const float* q, const float* qprev, LanczosDev st, int k, int64_t n, hipStream_t s);
+// Step B:  w <- w - alpha_k q; then either ||w||^2 (no reorth) or coef[0..nv) = Q^T w
+template <typename B>
+hipError_t launch_lanczos_b(float* w, const float* q, const B* basis, int nv, LanczosDev st, int k, int64_t n, hipStream_t s);
+// CGS correction: w <- w - sum_j coef[pass][j] Q_j ; then coef[pass+1] = Q^T w (if another pass) or ||w||^2
+template <typename B>
+hipError_t launch_lanczos_cgs(float* w, const B* basis, int nv, LanczosDev st, int pass, bool last, int k, int64_t n, hipStream_t s);
+// Normalise: beta_{k+1} = ||w|| (from the last reduction); breakdown test;
+// q_next = w / beta; basis slot row written.  tol relative to max |alpha|.
+template <typename B>
+hipError_t launch_lanczos_normalise(const float* w, float* qnext, B* basis_row, LanczosDev st, int k, double tol, int64_t n, hipStream_t s);
+
+// Per-block sums over ranges: out[b*3 + {0,1,2}] = ||a_b||^2, ||b_b||^2, <a_b, b_b>
+hipError_t launch_block_stats(const float* a, const float* b, const int64_t* ranges, int nblk, double* partial, double* out, hipStream_t s);
+
+// ---- lm.hip ----------------------------------------------------------------
+// All "pair" tensors are two buffers: m (mean of the two points) and d (half difference).
+struct PairF { float* m; float* d; };
+template <typename T> struct PairT { T* m; T* d; };
+
+template <typename T>
+hipError_t launch_cast_pair(PairT<T> out, const float* m, const float* d, int64_t n, hipStream_t s);
+
+// x = E[tok] (+ Pos[s]);  m = theta rows, d = eps * v rows
+template <typename T>
+hipError_t launch_embed_fwd(PairF x, const int32_t* tok, int T_, int S, int dmodel, int V,
+                            const T* th_e, const float* v_e, const T* th_p, const float* v_p, double eps, hipStream_t s);
+
+// Norm forward at both points: y = norm(x; g +- eps vg, b +- eps vb)
+template <typename T>
+hipError_t launch_norm_fwd(PairT<T> y, const float* xm, const float* xd, int rows, int dmodel, bool layernorm,
+                           const T* th_g, const float* v_g, const T* th_b, const float* v_b, double eps, float norm_eps, hipStream_t s);
+// Norm backward at both points: dx_out = dx_res + d/dx, gpart[t][j] = half difference of dy * xhat
+template <typename T>
+hipError_t launch_norm_bwd(PairF dx_out, const float* dres_m, const float* dres_d, const float* xm, const float* xd,
+                           const float* dym, const float* dyd, int rows, int dmodel, bool layernorm,
+                           const T* th_g, const float* v_g, double eps, float norm_eps, float* gpart, hipStream_t s);
+
+// out[j] = scale * sum_t X[t*ld + j] (deterministic); accumulate adds to out.  partial: [64 * C]
+hipError_t launch_colsum(float* out, const float* X, int rows, int C, int64_t ld, double scale, bool accumulate,
+                         double* partial, hipStream_t s);
+
+// RoPE (Llama) or plain cast (GPT-2) of q,k,v columns into operand type
+template <typename T>
+hipError_t launch_qkv_post(PairT<T> out, const float* qm, const float* qd, int T_, int S, int Hq, int Hk, int dh,
+                           const double* rope_cs, bool rope, hipStream_t s);
+// backward RoPE on dq/dk columns (fp32, in place) + cast of dq,dk,dv into operand type
+template <typename T>
+hipError_t launch_qkv_bwd_post(PairT<T> out, float* gm, float* gd, int T_, int S, int Hq, int Hk, int dh,
+                               const double* rope_cs, bool rope, hipStream_t s);
+// rope table: cs[s*dh + 2i] = cos(s * base^(-2i/dh)), cs[s*dh + 2i + 1] = sin(...)
+hipError_t launch_rope_table(double* cs, int S, int dh, double base, hipStream_t s);
+
+// causal softmax at both points: rows of S scores (fp32 pairs, already scaled) -> P (operand type)
+template <typename T>
+hipError_t launch_attn_softmax(PairT<T> P, const float* Sm, const float* Sd, int nrows_total, int S, hipStream_t s);
+// dS = P (dP - rowsum(P dP)) at both points
+template <typename T>
+hipError_t launch_attn_dsoftmax(PairT<T> dS, const T* Pm, const T* Pd, const float* dPm, const float* dPd,
+                                int nrows_total, int S, hipStream_t s);
+// GQA: sum groups of G consecutive query-head gradients into KV heads
+hipError_t launch_group_sum(float* out, int64_t out_ld, const float* in, int T_, int Hk, int G, int dh, hipStream_t s);
+
+// activations at both points
+template <typename T>
+hipError_t launch_gelu_fwd(PairT<T> z, const float* um, const float* ud, int64_t n, hipStream_t s);
+template <typename T>
+hipError_t launch_gelu_bwd(PairT<T> du, float* dud_f32, const float* um, const float* ud, const float* dzm, const float* dzd,
+                           int64_t n, hipStream_t s);
+template <typename T>
+hipError_t launch_swiglu_fwd(PairT<T> z, const float* gum, const float* gud, int rows, int F, hipStream_t s);
+template <typename T>
+hipError_t launch_swiglu_bwd(PairT<T> dgu, const float* gum, const float* gud, const float* dzm, const float* dzd,
+                             int rows, int F, hipStream_t s);
+
+// cross-entropy at both points: dlogits (operand type) and per-row losses (fp64, [2][T])
+template <typename T>
+hipError_t launch_ce(PairT<T> dl, double* rowloss, const float* lm, const float* ld, const int32_t* tok,
+                     int T_, int S, int V, double inv_n, hipStream_t s);
+hipError_t launch_loss_sum(double* out2, const double* rowloss, int T_, hipStream_t s);
+
+// embedding backward (difference channel only): deterministic sort + segment sums
+hipError_t launch_token_sort(uint32_t* keys, const int32_t* tok, int T_, int V, hipStream_t s);
+hipError_t launch_embed_bwd(float* hv_e, const uint32_t* keys, const float* dxd, int T_, int dmodel, double inv_eps,
+                            bool accumulate, hipStream_t s);
+hipError_t launch_pos_bwd(float* hv_p, const float* dxd, int B, int S, int dmodel, double inv_eps, hipStream_t s);
+
+}  // namespace fdh

@@ -1,0 +1,628 @@
+// Transformer kernels for the two gradient passes, run in lockstep.
+//
+// Every activation is carried as a pair of fp32 tensors: m = (x+ + x-)/2 and
+// d = (x+ - x-)/2, where x+ and x- are the activation at theta + eps v and at
+// theta - eps v.  The bilinear contractions run on MFMA (gemm.hip); every
+// other operation here reconstructs the two points x+- = m +- d in fp64,
+// evaluates the operation at each point in fp64, and stores the mean and half
+// difference of the two results.  The half difference therefore keeps full
+// relative precision however small the step eps is.
+#include "kernels.h"
+
+namespace fdh {
+
+namespace {
+
+constexpr int NT = 256;
+
+unsigned grid_for(int64_t n) {
+  int64_t g = (n + NT - 1) / NT;
+  if (g > 262144) g = 262144;
+  if (g < 1) g = 1;
+  return (unsigned)g;
+}
+
+#define GRID_LOOP(i, n) for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < (n); i += (int64_t)gridDim.x * blockDim.x)
+
+template <typename T>
+__device__ inline void put_pair(PairT<T> o, int64_t i, double p, double q) {
+  stf(o.m, i, (float)(0.5 * (p + q)));
+  stf(o.d, i, (float)(0.5 * (p - q)));
+}
+
+template <typename T>
+__global__ void cast_pair_kernel(PairT<T> o, const float* m, const float* d, int64_t n) {
+  GRID_LOOP(i, n) {
+    stf(o.m, i, m[i]);
+    stf(o.d, i, d[i]);
+  }
+}
+
+// ---- embedding ----------------------------------------------------------------
+// token ids outside [0, V) are clamped so that no access leaves the tables
+__device__ inline int clamp_tok(int t, int V) { return t < 0 ? 0 : (t >= V ? V - 1 : t); }
+
+template <typename T>
+__global__ void embed_fwd_kernel(PairF x, const int32_t* tok, int T_, int S, int dm, int V, const T* the, const float* ve,
+                                 const T* thp, const float* vp, double eps) {
+  const int64_t n = (int64_t)T_ * dm;
+  GRID_LOOP(i, n) {
+    const int t = (int)(i / dm), j = (int)(i % dm);
+    const int64_t r = (int64_t)clamp_tok(tok[t], V) * dm + j;
+    double xp = (double)ldf(the, r) + eps * (double)ve[r];
+    double xm = (double)ldf(the, r) - eps * (double)ve[r];
+    if (thp) {
+      const int64_t pr = (int64_t)(t % S) * dm + j;
+      xp += (double)ldf(thp, pr) + eps * (double)vp[pr];
+      xm += (double)ldf(thp, pr) - eps * (double)vp[pr];
+    }
+    x.m[i] = (float)(0.5 * (xp + xm));
+    x.d[i] = (float)(0.5 * (xp - xm));
+  }
+}
+
+// ---- LayerNorm / RMSNorm ---------------------------------------------------------
+// one workgroup per row
+template <typename T>
+__global__ __launch_bounds__(NT) void norm_fwd_kernel(PairT<T> y, const float* xm, const float* xd, int dm, bool ln,
+                                                      const T* thg, const float* vg, const T* thb, const float* vb,
+                                                      double eps, double neps) {
+  __shared__ double sh[NT / 64];
+  const int64_t row = blockIdx.x;
+  const float* rm = xm + row * dm;
+  const float* rd = xd + row * dm;
+  double mup = 0.0, mum = 0.0;
+  if (ln) {
+    double sp = 0.0, sm = 0.0;
+    for (int j = threadIdx.x; j < dm; j += NT) {
+      sp += (double)rm[j] + (double)rd[j];
+      sm += (double)rm[j] - (double)rd[j];
+    }
+    mup = block_sum<NT>(sp, sh) / dm;
+    mum = block_sum<NT>(sm, sh) / dm;
+  }
+  double qp = 0.0, qm = 0.0;
+  for (int j = threadIdx.x; j < dm; j += NT) {
+    const double a = (double)rm[j] + (double)rd[j] - mup;
+    const double b = (double)rm[j] - (double)rd[j] - mum;
+    qp += a * a;
+    qm += b * b;
+  }
+  const double rp = 1.0 / sqrt(block_sum<NT>(qp, sh) / dm + neps);
+  const double rmi = 1.0 / sqrt(block_sum<NT>(qm, sh) / dm + neps);
+  for (int j = threadIdx.x; j < dm; j += NT) {
+    const double g = ldf(thg, j), dg = eps * (double)vg[j];
+    double op = ((double)rm[j] + (double)rd[j] - mup) * rp * (g + dg);
+    double om = ((double)rm[j] - (double)rd[j] - mum) * rmi * (g - dg);
+    if (thb) {
+      const double b = ldf(thb, j), db = eps * (double)vb[j];
+      op += b + db;
+      om += b - db;
+    }
+    put_pair(y, row * dm + j, op, om);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(NT) void norm_bwd_kernel(PairF dx, const float* dresm, const float* dresd,
+                                                      const float* xm, const float* xd, const float* dym,
+                                                      const float* dyd, int dm, bool ln, const T* thg,
+                                                      const float* vg, double eps, double neps, float* gpart) {
+  __shared__ double sh[NT / 64];
+  const int64_t row = blockIdx.x;
+  const int64_t o = row * dm;
+  double mup = 0.0, mum = 0.0;
+  if (ln) {
+    double sp = 0.0, sm = 0.0;
+    for (int j = threadIdx.x; j < dm; j += NT) {
+      sp += (double)xm[o + j] + (double)xd[o + j];
+      sm += (double)xm[o + j] - (double)xd[o + j];
+    }
+    mup = block_sum<NT>(sp, sh) / dm;
+    mum = block_sum<NT>(sm, sh) / dm;
+  }
+  double qp = 0.0, qm = 0.0;
+  for (int j = threadIdx.x; j < dm; j += NT) {
+    const double a = (double)xm[o + j] + (double)xd[o + j] - mup;
+    const double b = (double)xm[o + j] - (double)xd[o + j] - mum;
+    qp += a * a;
+    qm += b * b;
+  }
+  const double rp = 1.0 / sqrt(block_sum<NT>(qp, sh) / dm + neps);
+  const double rmi = 1.0 / sqrt(block_sum<NT>(qm, sh) / dm + neps);
+  // means of dxhat and dxhat * xhat at both points
+  double s1p = 0.0, s1m = 0.0, s2p = 0.0, s2m = 0.0;
+  for (int j = threadIdx.x; j < dm; j += NT) {
+    const double g = ldf(thg, j), dg = eps * (double)vg[j];
+    const double xhp = ((double)xm[o + j] + (double)xd[o + j] - mup) * rp;
+    const double xhm = ((double)xm[o + j] - (double)xd[o + j] - mum) * rmi;
+    const double dhp = ((double)dym[o + j] + (double)dyd[o + j]) * (g + dg);
+    const double dhm = ((double)dym[o + j] - (double)dyd[o + j]) * (g - dg);
+    s1p += dhp;
+    s1m += dhm;
+    s2p += dhp * xhp;
+    s2m += dhm * xhm;
+  }
+  const double a1p = ln ? block_sum<NT>(s1p, sh) / dm : 0.0;
+  const double a1m = ln ? block_sum<NT>(s1m, sh) / dm : 0.0;
+  const double a2p = block_sum<NT>(s2p, sh) / dm;
+  const double a2m = block_sum<NT>(s2m, sh) / dm;
+  for (int j = threadIdx.x; j < dm; j += NT) {
+    const double g = ldf(thg, j), dg = eps * (double)vg[j];
+    const double xhp = ((double)xm[o + j] + (double)xd[o + j] - mup) * rp;
+    const double xhm = ((double)xm[o + j] - (double)xd[o + j] - mum) * rmi;
+    const double dyp = (double)dym[o + j] + (double)dyd[o + j];
+    const double dymi = (double)dym[o + j] - (double)dyd[o + j];
+    const double dhp = dyp * (g + dg), dhm = dymi * (g - dg);
+    const double dxp = rp * (dhp - a1p - xhp * a2p);
+    const double dxm = rmi * (dhm - a1m - xhm * a2m);
+    const double rm0 = dresm ? (double)dresm[o + j] : 0.0;
+    const double rd0 = dresd ? (double)dresd[o + j] : 0.0;
+    dx.m[o + j] = (float)(rm0 + 0.5 * (dxp + dxm));
+    dx.d[o + j] = (float)(rd0 + 0.5 * (dxp - dxm));
+    gpart[o + j] = (float)(0.5 * (dyp * xhp - dymi * xhm));
+  }
+}
+
+// ---- column sums ---------------------------------------------------------------
+constexpr int COLSUM_CHUNKS = 64;
+__global__ void colsum_stage1(double* partial, const float* X, int rows, int C, int64_t ld) {
+  const int j = blockIdx.x * NT + threadIdx.x;
+  if (j >= C) return;
+  const int c = blockIdx.y;
+  const int per = (rows + COLSUM_CHUNKS - 1) / COLSUM_CHUNKS;
+  const int r0 = c * per, r1 = min(rows, r0 + per);
+  double s = 0.0;
+  for (int r = r0; r < r1; ++r) s += (double)X[(int64_t)r * ld + j];
+  partial[(int64_t)c * C + j] = s;
+}
+__global__ void colsum_stage2(float* out, const double* partial, int C, double scale, bool acc) {
+  const int j = blockIdx.x * NT + threadIdx.x;
+  if (j >= C) return;
+  double s = 0.0;
+  for (int c = 0; c < COLSUM_CHUNKS; ++c) s += partial[(int64_t)c * C + j];
+  s *= scale;
+  out[j] = acc ? (float)((double)out[j] + s) : (float)s;
+}
+
+// ---- RoPE ----------------------------------------------------------------------
+__global__ void rope_table_kernel(double* cs, int S, int dh, double base) {
+  const int half = dh / 2;
+  GRID_LOOP(i, (int64_t)S * half) {
+    const int s = (int)(i / half), f = (int)(i % half);
+    const double inv = pow(base, -(double)(2 * f) / (double)dh);
+    const double ang = (double)s * inv;
+    cs[(int64_t)s * dh + 2 * f] = cos(ang);
+    cs[(int64_t)s * dh + 2 * f + 1] = sin(ang);
+  }
+}
+
+// forward: q/k columns rotated (rotate-half), v columns copied; one channel per call
+template <typename T>
+__global__ void qkv_post_kernel(T* out, const float* in, int T_, int S, int ncols, int qk_cols, int dh,
+                                const double* cs, bool rope, bool inverse) {
+  const int64_t n = (int64_t)T_ * ncols;
+  const int half = dh / 2;
+  GRID_LOOP(i, n) {
+    const int t = (int)(i / ncols), c = (int)(i % ncols);
+    double x = in[i];
+    if (rope && c < qk_cols) {
+      const int hi = c % dh;
+      const int f = hi % half;
+      const double co = cs[(int64_t)(t % S) * dh + 2 * f], si = cs[(int64_t)(t % S) * dh + 2 * f + 1];
+      const double sgn = inverse ? -1.0 : 1.0;
+      if (hi < half) x = x * co - sgn * (double)in[i + half] * si;
+      else x = x * co + sgn * (double)in[i - half] * si;
+    }
+    stf(out, i, (float)x);
+  }
+}
+
+// ---- causal softmax and its backward, both points ---------------------------------------
+constexpr int MAXE = 16;  // row elements per thread (rows up to 4096)
+
+template <typename T>
+__global__ __launch_bounds__(NT) void attn_softmax_kernel(PairT<T> P, const float* Sm, const float* Sd, int S) {
+  __shared__ double sh[NT / 64];
+  const int64_t r = blockIdx.x;
+  const int i = (int)(r % S);
+  const int64_t base = r * (int64_t)S;
+  const int len = i + 1;
+  double ep[MAXE], em[MAXE];
+  double mx = -1e300;
+#pragma unroll
+  for (int e = 0; e < MAXE; ++e) {
+    const int j = threadIdx.x + e * NT;
+    if (j < len) mx = fmax(mx, (double)Sm[base + j]);
+  }
+  mx = block_max<NT>(mx, sh);
+  double zp = 0.0, zm = 0.0;
+#pragma unroll
+  for (int e = 0; e < MAXE; ++e) {
+    const int j = threadIdx.x + e * NT;
+    ep[e] = em[e] = 0.0;
+    if (j < len) {
+      const double a = (double)Sm[base + j] - mx, b = (double)Sd[base + j];
+      ep[e] = exp(a + b);
+      em[e] = exp(a - b);
+      zp += ep[e];
+      zm += em[e];
+    }
+  }
+  zp = block_sum<NT>(zp, sh);
+  zm = block_sum<NT>(zm, sh);
+  const double izp = 1.0 / zp, izm = 1.0 / zm;
+#pragma unroll
+  for (int e = 0; e < MAXE; ++e) {
+    const int j = threadIdx.x + e * NT;
+    if (j < S) put_pair(P, base + j, ep[e] * izp, em[e] * izm);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(NT) void attn_dsoftmax_kernel(PairT<T> dS, const T* Pm, const T* Pd, const float* dPm,
+                                                           const float* dPd, int S) {
+  __shared__ double sh[NT / 64];
+  const int64_t r = blockIdx.x;
+  const int i = (int)(r % S);
+  const int64_t base = r * (int64_t)S;
+  const int len = i + 1;
+  double dp = 0.0, dm = 0.0;
+#pragma unroll
+  for (int e = 0; e < MAXE; ++e) {
+    const int j = threadIdx.x + e * NT;
+    if (j < len) {
+      const double pm = ldf(Pm, base + j), pd = ldf(Pd, base + j);
+      const double gm = dPm[base + j], gd = dPd[base + j];
+      dp += (pm + pd) * (gm + gd);
+      dm += (pm - pd) * (gm - gd);
+    }
+  }
+  dp = block_sum<NT>(dp, sh);
+  dm = block_sum<NT>(dm, sh);
+#pragma unroll
+  for (int e = 0; e < MAXE; ++e) {
+    const int j = threadIdx.x + e * NT;
+    if (j < S) {
+      double sp = 0.0, sn = 0.0;
+      if (j < len) {
+        const double pm = ldf(Pm, base + j), pd = ldf(Pd, base + j);
+        const double gm = dPm[base + j], gd = dPd[base + j];
+        sp = (pm + pd) * (gm + gd - dp);
+        sn = (pm - pd) * (gm - gd - dm);
+      }
+      put_pair(dS, base + j, sp, sn);
+    }
+  }
+}
+
+__global__ void group_sum_kernel(float* out, int64_t out_ld, const float* in, int T_, int Hk, int G, int dh) {
+  const int64_t n = (int64_t)T_ * Hk * dh;
+  GRID_LOOP(i, n) {
+    const int t = (int)(i / (Hk * dh)), c = (int)(i % (Hk * dh));
+    const int kh = c / dh, e = c % dh;
+    double s = 0.0;
+    for (int g = 0; g < G; ++g) s += in[(int64_t)t * (Hk * G * dh) + (int64_t)(kh * G + g) * dh + e];
+    out[(int64_t)t * out_ld + c] = (float)s;
+  }
+}
+
+// ---- activations ------------------------------------------------------------------
+__device__ inline double gelu_t(double u) {
+  const double k = 0.7978845608028654, a = 0.044715;
+  return 0.5 * u * (1.0 + tanh(k * (u + a * u * u * u)));
+}
+__device__ inline double gelu_t_grad(double u) {
+  const double k = 0.7978845608028654, a = 0.044715;
+  const double t = tanh(k * (u + a * u * u * u));
+  return 0.5 * (1.0 + t) + 0.5 * u * (1.0 - t * t) * k * (1.0 + 3.0 * a * u * u);
+}
+__device__ inline double sigm(double x) { return 1.0 / (1.0 + exp(-x)); }
+
+template <typename T>
+__global__ void gelu_fwd_kernel(PairT<T> z, const float* um, const float* ud, int64_t n) {
+  GRID_LOOP(i, n) {
+    const double up = (double)um[i] + (double)ud[i], un = (double)um[i] - (double)ud[i];
+    put_pair(z, i, gelu_t(up), gelu_t(un));
+  }
+}
+template <typename T>
+__global__ void gelu_bwd_kernel(PairT<T> du, float* dudf, const float* um, const float* ud, const float* dzm,
+                                const float* dzd, int64_t n) {
+  GRID_LOOP(i, n) {
+    const double up = (double)um[i] + (double)ud[i], un = (double)um[i] - (double)ud[i];
+    const double gp = ((double)dzm[i] + (double)dzd[i]) * gelu_t_grad(up);
+    const double gn = ((double)dzm[i] - (double)dzd[i]) * gelu_t_grad(un);
+    put_pair(du, i, gp, gn);
+    if (dudf) dudf[i] = (float)(0.5 * (gp - gn));
+  }
+}
+template <typename T>
+__global__ void swiglu_fwd_kernel(PairT<T> z, const float* gum, const float* gud, int rows, int F) {
+  const int64_t n = (int64_t)rows * F;
+  GRID_LOOP(i, n) {
+    const int64_t t = i / F, c = i % F;
+    const int64_t ig = t * 2 * F + c, iu = ig + F;
+    const double gp = (double)gum[ig] + (double)gud[ig], gn = (double)gum[ig] - (double)gud[ig];
+    const double vp = (double)gum[iu] + (double)gud[iu], vn = (double)gum[iu] - (double)gud[iu];
+    put_pair(z, i, gp * sigm(gp) * vp, gn * sigm(gn) * vn);
+  }
+}
+template <typename T>
+__global__ void swiglu_bwd_kernel(PairT<T> dgu, const float* gum, const float* gud, const float* dzm, const float* dzd,
+                                  int rows, int F) {
+  const int64_t n = (int64_t)rows * F;
+  GRID_LOOP(i, n) {
+    const int64_t t = i / F, c = i % F;
+    const int64_t ig = t * 2 * F + c, iu = ig + F;
+    const double gp = (double)gum[ig] + (double)gud[ig], gn = (double)gum[ig] - (double)gud[ig];
+    const double vp = (double)gum[iu] + (double)gud[iu], vn = (double)gum[iu] - (double)gud[iu];
+    const double zp = (double)dzm[i] + (double)dzd[i], zn = (double)dzm[i] - (double)dzd[i];
+    const double sp = sigm(gp), sn = sigm(gn);
+    put_pair(dgu, ig, zp * vp * sp * (1.0 + gp * (1.0 - sp)), zn * vn * sn * (1.0 + gn * (1.0 - sn)));
+    put_pair(dgu, iu, zp * gp * sp, zn * gn * sn);
+  }
+}
+
+// ---- cross-entropy, both points -------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(NT) void ce_kernel(PairT<T> dl, double* rowloss, const float* lm, const float* ld,
+                                                const int32_t* tok, int T_, int S, int V, double inv_n) {
+  __shared__ double sh[NT / 64];
+  const int64_t t = blockIdx.x;
+  const int64_t o = t * (int64_t)V;
+  const bool has_target = (t % S) != (S - 1);
+  if (!has_target) {
+    for (int j = threadIdx.x; j < V; j += NT) put_pair(dl, o + j, 0.0, 0.0);
+    if (threadIdx.x == 0) { rowloss[t] = 0.0; rowloss[T_ + t] = 0.0; }
+    return;
+  }
+  const int y = clamp_tok(tok[t + 1], V);
+  double mx = -1e300;
+  for (int j = threadIdx.x; j < V; j += NT) mx = fmax(mx, (double)lm[o + j]);
+  mx = block_max<NT>(mx, sh);
+  double zp = 0.0, zm = 0.0;
+  for (int j = threadIdx.x; j < V; j += NT) {
+    const double a = (double)lm[o + j] - mx, b = (double)ld[o + j];
+    zp += exp(a + b);
+    zm += exp(a - b);
+  }
+  zp = block_sum<NT>(zp, sh);
+  zm = block_sum<NT>(zm, sh);
+  const double izp = 1.0 / zp, izm = 1.0 / zm;
+  for (int j = threadIdx.x; j < V; j += NT) {
+    const double a = (double)lm[o + j] - mx, b = (double)ld[o + j];
+    double pp = exp(a + b) * izp, pn = exp(a - b) * izm;
+    if (j == y) { pp -= 1.0; pn -= 1.0; }
+    put_pair(dl, o + j, pp * inv_n, pn * inv_n);
+  }
+  if (threadIdx.x == 0) {
+    const double a = (double)lm[o + y] - mx, b = (double)ld[o + y];
+    rowloss[t] = (log(zp) - (a + b)) * inv_n;
+    rowloss[T_ + t] = (log(zm) - (a - b)) * inv_n;
+  }
+}
+
+__global__ void loss_sum_kernel(double* out2, const double* rowloss, int T_) {
+  __shared__ double sh[NT / 64];
+  double a = 0.0, b = 0.0;
+  // fixed assignment of rows to threads, fixed reduction tree
+  for (int t = threadIdx.x; t < T_; t += NT) { a += rowloss[t]; b += rowloss[T_ + t]; }
+  a = block_sum<NT>(a, sh);
+  b = block_sum<NT>(b, sh);
+  if (threadIdx.x == 0) { out2[0] = a; out2[1] = b; }
+}
+
+// ---- embedding backward --------------------------------------------------------------
+constexpr int SORT_N = 16384;  // keys = token << 14 | position, positions < 2^14
+__global__ __launch_bounds__(1024) void token_sort_kernel(uint32_t* keys, const int32_t* tok, int T_, int V) {
+  __shared__ uint32_t k[SORT_N];
+  int n2 = 1;
+  while (n2 < T_) n2 <<= 1;
+  for (int i = threadIdx.x; i < n2; i += 1024)
+    k[i] = (i < T_) ? (((uint32_t)clamp_tok(tok[i], V) << 14) | (uint32_t)i) : 0xFFFFFFFFu;
+  __syncthreads();
+  for (int size = 2; size <= n2; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int i = threadIdx.x; i < n2; i += 1024) {
+        const int p = i ^ stride;
+        if (p > i) {
+          const bool up = (i & size) == 0;
+          const uint32_t a = k[i], b = k[p];
+          if ((a > b) == up) { k[i] = b; k[p] = a; }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  for (int i = threadIdx.x; i < T_; i += 1024) keys[i] = k[i];
+}
+
+// one workgroup per sorted position; only segment starts work
+__global__ void embed_bwd_kernel(float* hv, const uint32_t* keys, const float* dxd, int T_, int dm, double inv_eps,
+                                 bool acc) {
+  const int j = blockIdx.x;
+  const uint32_t tk = keys[j] >> 14;
+  if (j > 0 && (keys[j - 1] >> 14) == tk) return;
+  int e = j + 1;
+  while (e < T_ && (keys[e] >> 14) == tk) ++e;
+  for (int c = threadIdx.x; c < dm; c += NT) {
+    double s = 0.0;
+    for (int q = j; q < e; ++q) s += (double)dxd[(int64_t)(keys[q] & 0x3FFFu) * dm + c];
+    const int64_t idx = (int64_t)tk * dm + c;
+    hv[idx] = acc ? (float)((double)hv[idx] + s * inv_eps) : (float)(s * inv_eps);
+  }
+}
+
+__global__ void pos_bwd_kernel(float* hv, const float* dxd, int B, int S, int dm, double inv_eps) {
+  const int64_t n = (int64_t)S * dm;
+  GRID_LOOP(i, n) {
+    const int s = (int)(i / dm), c = (int)(i % dm);
+    double a = 0.0;
+    for (int b = 0; b < B; ++b) a += (double)dxd[((int64_t)b * S + s) * dm + c];
+    hv[i] = (float)(a * inv_eps);
+  }
+}
+
+}  // namespace
+
+// ================================ launchers ==============================================
+template <typename T>
+hipError_t launch_cast_pair(PairT<T> out, const float* m, const float* d, int64_t n, hipStream_t s) {
+  hipLaunchKernelGGL(cast_pair_kernel<T>, dim3(grid_for(n)), dim3(NT), 0, s, out, m, d, n);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_embed_fwd(PairF x, const int32_t* tok, int T_, int S, int dm, int V, const T* the, const float* ve,
+                            const T* thp, const float* vp, double eps, hipStream_t s) {
+  hipLaunchKernelGGL(embed_fwd_kernel<T>, dim3(grid_for((int64_t)T_ * dm)), dim3(NT), 0, s, x, tok, T_, S, dm, V, the,
+                     ve, thp, vp, eps);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_norm_fwd(PairT<T> y, const float* xm, const float* xd, int rows, int dm, bool ln, const T* thg,
+                           const float* vg, const T* thb, const float* vb, double eps, float neps, hipStream_t s) {
+  hipLaunchKernelGGL(norm_fwd_kernel<T>, dim3(rows), dim3(NT), 0, s, y, xm, xd, dm, ln, thg, vg, thb, vb, eps, (double)neps);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_norm_bwd(PairF dx, const float* dresm, const float* dresd, const float* xm, const float* xd,
+                           const float* dym, const float* dyd, int rows, int dm, bool ln, const T* thg,
+                           const float* vg, double eps, float neps, float* gpart, hipStream_t s) {
+  hipLaunchKernelGGL(norm_bwd_kernel<T>, dim3(rows), dim3(NT), 0, s, dx, dresm, dresd, xm, xd, dym, dyd, dm, ln, thg,
+                     vg, eps, (double)neps, gpart);
+  return hipGetLastError();
+}
+
+hipError_t launch_colsum(float* out, const float* X, int rows, int C, int64_t ld, double scale, bool acc, double* partial,
+                         hipStream_t s) {
+  hipLaunchKernelGGL(colsum_stage1, dim3(ceil_div(C, NT), COLSUM_CHUNKS), dim3(NT), 0, s, partial, X, rows, C, ld);
+  hipLaunchKernelGGL(colsum_stage2, dim3(ceil_div(C, NT)), dim3(NT), 0, s, out, (const double*)partial, C, scale, acc);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_table(double* cs, int S, int dh, double base, hipStream_t s) {
+  hipLaunchKernelGGL(rope_table_kernel, dim3(grid_for((int64_t)S * dh / 2)), dim3(NT), 0, s, cs, S, dh, base);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_qkv_post(PairT<T> out, const float* qm, const float* qd, int T_, int S, int Hq, int Hk, int dh,
+                           const double* cs, bool rope, hipStream_t s) {
+  const int ncols = (Hq + 2 * Hk) * dh, qk = (Hq + Hk) * dh;
+  const unsigned g = grid_for((int64_t)T_ * ncols);
+  hipLaunchKernelGGL(qkv_post_kernel<T>, dim3(g), dim3(NT), 0, s, out.m, qm, T_, S, ncols, qk, dh, cs, rope, false);
+  hipLaunchKernelGGL(qkv_post_kernel<T>, dim3(g), dim3(NT), 0, s, out.d, qd, T_, S, ncols, qk, dh, cs, rope, false);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_qkv_bwd_post(PairT<T> out, float* gm, float* gd, int T_, int S, int Hq, int Hk, int dh,
+                               const double* cs, bool rope, hipStream_t s) {
+  const int ncols = (Hq + 2 * Hk) * dh, qk = (Hq + Hk) * dh;
+  const unsigned g = grid_for((int64_t)T_ * ncols);
+  hipLaunchKernelGGL(qkv_post_kernel<T>, dim3(g), dim3(NT), 0, s, out.m, (const float*)gm, T_, S, ncols, qk, dh, cs, rope, true);
+  hipLaunchKernelGGL(qkv_post_kernel<T>, dim3(g), dim3(NT), 0, s, out.d, (const float*)gd, T_, S, ncols, qk, dh, cs, rope, true);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_attn_softmax(PairT<T> P, const float* Sm, const float* Sd, int nrows, int S, hipStream_t s) {
+  if (S > MAXE * NT) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(attn_softmax_kernel<T>, dim3(nrows), dim3(NT), 0, s, P, Sm, Sd, S);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_attn_dsoftmax(PairT<T> dS, const T* Pm, const T* Pd, const float* dPm, const float* dPd, int nrows,
+                                int S, hipStream_t s) {
+  if (S > MAXE * NT) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(attn_dsoftmax_kernel<T>, dim3(nrows), dim3(NT), 0, s, dS, Pm, Pd, dPm, dPd, S);
+  return hipGetLastError();
+}
+
+hipError_t launch_group_sum(float* out, int64_t out_ld, const float* in, int T_, int Hk, int G, int dh, hipStream_t s) {
+  hipLaunchKernelGGL(group_sum_kernel, dim3(grid_for((int64_t)T_ * Hk * dh)), dim3(NT), 0, s, out, out_ld, in, T_, Hk, G, dh);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_gelu_fwd(PairT<T> z, const float* um, const float* ud, int64_t n, hipStream_t s) {
+  hipLaunchKernelGGL(gelu_fwd_kernel<T>, dim3(grid_for(n)), dim3(NT), 0, s, z, um, ud, n);
+  return hipGetLastError();
+}
+template <typename T>
+hipError_t launch_gelu_bwd(PairT<T> du, float* dudf, const float* um, const float* ud, const float* dzm, const float* dzd,
+                           int64_t n, hipStream_t s) {
+  hipLaunchKernelGGL(gelu_bwd_kernel<T>, dim3(grid_for(n)), dim3(NT), 0, s, du, dudf, um, ud, dzm, dzd, n);
+  return hipGetLastError();
+}
+template <typename T>
+hipError_t launch_swiglu_fwd(PairT<T> z, const float* gum, const float* gud, int rows, int F, hipStream_t s) {
+  hipLaunchKernelGGL(swiglu_fwd_kernel<T>, dim3(grid_for((int64_t)rows * F)), dim3(NT), 0, s, z, gum, gud, rows, F);
+  return hipGetLastError();
+}
+template <typename T>
+hipError_t launch_swiglu_bwd(PairT<T> dgu, const float* gum, const float* gud, const float* dzm, const float* dzd, int rows,
+                             int F, hipStream_t s) {
+  hipLaunchKernelGGL(swiglu_bwd_kernel<T>, dim3(grid_for((int64_t)rows * F)), dim3(NT), 0, s, dgu, gum, gud, dzm, dzd, rows, F);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_ce(PairT<T> dl, double* rowloss, const float* lm, const float* ld, const int32_t* tok, int T_, int S,
+                     int V, double inv_n, hipStream_t s) {
+  hipLaunchKernelGGL(ce_kernel<T>, dim3(T_), dim3(NT), 0, s, dl, rowloss, lm, ld, tok, T_, S, V, inv_n);
+  return hipGetLastError();
+}
+hipError_t launch_loss_sum(double* out2, const double* rowloss, int T_, hipStream_t s) {
+  hipLaunchKernelGGL(loss_sum_kernel, dim3(1), dim3(NT), 0, s, out2, rowloss, T_);
+  return hipGetLastError();
+}
+
+hipError_t launch_token_sort(uint32_t* keys, const int32_t* tok, int T_, int V, hipStream_t s) {
+  if (T_ > SORT_N) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(token_sort_kernel, dim3(1), dim3(1024), 0, s, keys, tok, T_, V);
+  return hipGetLastError();
+}
+hipError_t launch_embed_bwd(float* hv, const uint32_t* keys, const float* dxd, int T_, int dm, double inv_eps, bool acc,
+                            hipStream_t s) {
+  hipLaunchKernelGGL(embed_bwd_kernel, dim3(T_), dim3(NT), 0, s, hv, keys, dxd, T_, dm, inv_eps, acc);
+  return hipGetLastError();
+}
+hipError_t launch_pos_bwd(float* hv, const float* dxd, int B, int S, int dm, double inv_eps, hipStream_t s) {
+  hipLaunchKernelGGL(pos_bwd_kernel, dim3(grid_for((int64_t)S * dm)), dim3(NT), 0, s, hv, dxd, B, S, dm, inv_eps);
+  return hipGetLastError();
+}
+
+#define INST_T(T)                                                                                                     \
+  template hipError_t launch_cast_pair<T>(PairT<T>, const float*, const float*, int64_t, hipStream_t);                 \
+  template hipError_t launch_embed_fwd<T>(PairF, const int32_t*, int, int, int, int, const T*, const float*, const T*, \
+                                          const float*, double, hipStream_t);                                          \
+  template hipError_t launch_norm_fwd<T>(PairT<T>, const float*, const float*, int, int, bool, const T*, const float*, \
+                                         const T*, const float*, double, float, hipStream_t);                          \
+  template hipError_t launch_norm_bwd<T>(PairF, const float*, const float*, const float*, const float*, const float*,  \
+                                         const float*, int, int, bool, const T*, const float*, double, float, float*,  \
+                                         hipStream_t);                                                                 \
+  template hipError_t launch_qkv_post<T>(PairT<T>, const float*, const float*, int, int, int, int, int, const double*, \
+                                         bool, hipStream_t);                                                           \
+  template hipError_t launch_qkv_bwd_post<T>(PairT<T>, float*, float*, int, int, int, int, int, const double*, bool,   \
+                                             hipStream_t);                                                             \
+  template hipError_t launch_attn_softmax<T>(PairT<T>, const float*, const float*, int, int, hipStream_t);             \
+  template hipError_t launch_attn_dsoftmax<T>(PairT<T>, const T*, const T*, const float*, const float*, int, int,      \
+                                              hipStream_t);                                                            \
+  template hipError_t launch_gelu_fwd<T>(PairT<T>, const float*, const float*, int64_t, hipStream_t);                  \
+  template hipError_t launch_gelu_bwd<T>(PairT<T>, float*, const float*, const float*, const float*, const float*,     \
+                                         int64_t, hipStream_t);                                                        \
+  template hipError_t launch_swiglu_fwd<T>(PairT<T>, const float*, const float*, int, int, hipStream_t);               \
+  template hipError_t launch_swiglu_bwd<T>(PairT<T>, const float*, const float*, const float*, const float*, int, int, \
+                                           hipStream_t);                                                               \
+  template hipError_t launch_ce<T>(PairT<T>, double*, const float*, const float*, const int32_t*, int, int, int,       \
+                                   double, hipStream_t);
+INST_T(float)
+INST_T(bf16_t)
+
+}  // namespace fdh

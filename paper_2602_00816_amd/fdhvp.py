@@ -1,0 +1,272 @@
+"""Python binding of libfdhvp (include/fdhvp.h): argument marshalling only.
+
+Every computation runs in the HIP library; PyTorch supplies device memory and
+the current stream.  Loading fails loudly when the library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libfdhvp.so")
+
+# enums (include/fdhvp.h)
+OK, BREAKDOWN = 0, 1
+ERR = {-1: "INVALID_ARG", -2: "WORKSPACE", -3: "HIP", -4: "NONFINITE", -5: "STATE", -6: "UNSUPPORTED"}
+FAMILY = {"gpt2": 0, "llama": 1, "quad_diag": 2}
+DTYPE = {"f32": 0, "bf16": 1}
+REORTH = {"none": 0, "full": 1, "window": 2}
+TOKENS = {"uniform": 0, "zipf": 1}
+VEC = {"rademacher": 0, "gaussian": 1}
+
+
+class FdhError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"fdhvp error {ERR.get(status, status)}: {msg}")
+        self.status = status
+
+
+class ModelConfig(C.Structure):
+    _fields_ = [("family", C.c_int32), ("n_layers", C.c_int32), ("d_model", C.c_int32),
+                ("n_heads", C.c_int32), ("n_kv_heads", C.c_int32), ("d_ff", C.c_int32),
+                ("vocab", C.c_int32), ("max_seq", C.c_int32), ("dtype", C.c_int32),
+                ("norm_eps", C.c_float), ("rope_base", C.c_float), ("reserved", C.c_int32),
+                ("quad_n", C.c_int64)]
+
+
+class LanczosOpts(C.Structure):
+    _fields_ = [("reorth", C.c_int32), ("window", C.c_int32), ("basis_dtype", C.c_int32),
+                ("breakdown_tol", C.c_float)]
+
+
+class Block(C.Structure):
+    _fields_ = [("name", C.c_char * 48), ("offset", C.c_int64), ("numel", C.c_int64),
+                ("rows", C.c_int64), ("cols", C.c_int64), ("layer", C.c_int32), ("kind", C.c_int32)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded shared library (raises if it is missing)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2602_00816_amd.build`")
+    L = C.CDLL(LIB_PATH)
+    vp, i32, i64, u64, f64 = C.c_void_p, C.c_int32, C.c_int64, C.c_uint64, C.c_double
+    pd, pi = C.POINTER(C.c_double), C.POINTER(C.c_int32)
+    sig = {
+        "fdh_api_version": (i32, []),
+        "fdh_create": (i32, [C.POINTER(ModelConfig), vp, C.POINTER(vp)]),
+        "fdh_destroy": (None, [vp]),
+        "fdh_num_params": (i64, [vp]),
+        "fdh_num_blocks": (i32, [vp]),
+        "fdh_param_layout": (i32, [vp, C.POINTER(Block), i32, pi]),
+        "fdh_workspace_bytes": (i32, [vp, i32, i32, i32, C.POINTER(LanczosOpts), C.POINTER(C.c_size_t)]),
+        "fdh_set_workspace": (i32, [vp, vp, C.c_size_t, i32, i32, i32, C.POINTER(LanczosOpts)]),
+        "fdh_init_params": (i32, [vp, vp, u64]),
+        "fdh_make_tokens": (i32, [vp, vp, i32, i32, u64, i32]),
+        "fdh_random_vector": (i32, [vp, vp, u64, i32]),
+        "fdh_set_quad_diag": (i32, [vp, vp]),
+        "fdh_hvp": (i32, [vp, vp, vp, f64, vp, i32, i32, vp]),
+        "fdh_last_losses": (i32, [vp, pd, pd]),
+        "fdh_bind": (i32, [vp, vp, vp, i32, i32, f64]),
+        "fdh_lanczos": (i32, [vp, i32, u64, C.POINTER(LanczosOpts), pd, pd, pi]),
+        "fdh_slq_density": (i32, [vp, i32, i32, u64, C.POINTER(LanczosOpts), pd, pd, pi, pd]),
+        "fdh_block_stats": (i32, [vp, vp, vp, pd]),
+        "fdh_last_error": (C.c_char_p, [vp]),
+        "fdh_testing_gemm": (i32, [i32, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, i32, C.c_float, vp]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(L, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = L
+    return L
+
+
+def _ptr(t) -> int:
+    return 0 if t is None else int(t.data_ptr())
+
+
+def _stream():
+    import torch
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def opts(reorth="full", window=0, basis="f32", tol=0.0) -> LanczosOpts:
+    return LanczosOpts(REORTH[reorth], int(window), DTYPE[basis], float(tol))
+
+
+@dataclass
+class Entry:
+    name: str
+    offset: int
+    numel: int
+    rows: int
+    cols: int
+    layer: int
+    kind: int
+
+
+class Model:
+    """One fdh_ctx: a model (or the quadratic test operator) on the current GPU."""
+
+    def __init__(self, family: str, n_layers=0, d_model=0, n_heads=1, n_kv_heads=0, d_ff=0, vocab=0,
+                 max_seq=0, dtype="f32", norm_eps=1e-5, rope_base=10000.0, quad_n=0, stream=None):
+        self._L = lib()
+        self.cfg = ModelConfig(FAMILY[family], n_layers, d_model, n_heads, n_kv_heads or n_heads, d_ff, vocab,
+                               max_seq, DTYPE[dtype], norm_eps, rope_base, 0, quad_n)
+        self.family, self.dtype = family, dtype
+        h = C.c_void_p()
+        st = self._L.fdh_create(C.byref(self.cfg), stream if stream is not None else C.c_void_p(0), C.byref(h))
+        if st != OK:
+            raise FdhError(st, "fdh_create rejected the configuration")
+        self._h = h
+        self._ws = None
+        self._keep = []
+
+    @classmethod
+    def from_workload(cls, w: dict, stream=None):
+        return cls(w["family"], w["n_layers"], w["d_model"], w["n_heads"], w["n_kv_heads"], w["d_ff"],
+                   w["vocab"], w["max_seq"], w["dtype"], rope_base=w["rope_base"], stream=stream)
+
+    def close(self):
+        if getattr(self, "_h", None):
+            self._L.fdh_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _check(self, st: int, what: str) -> int:
+        if st < 0:
+            msg = self._L.fdh_last_error(self._h)
+            raise FdhError(st, f"{what}: {msg.decode() if msg else ''}")
+        return st
+
+    # ---- description ----
+    @property
+    def num_params(self) -> int:
+        return int(self._L.fdh_num_params(self._h))
+
+    @property
+    def num_blocks(self) -> int:
+        return int(self._L.fdh_num_blocks(self._h))
+
+    def layout(self) -> list[Entry]:
+        n = C.c_int32()
+        self._check(self._L.fdh_param_layout(self._h, None, 0, C.byref(n)), "fdh_param_layout")
+        arr = (Block * n.value)()
+        self._check(self._L.fdh_param_layout(self._h, arr, n.value, C.byref(n)), "fdh_param_layout")
+        return [Entry(b.name.decode(), b.offset, b.numel, b.rows, b.cols, b.layer, b.kind) for b in arr]
+
+    def workspace_bytes(self, B=0, S=0, m=0, o: LanczosOpts | None = None) -> int:
+        out = C.c_size_t()
+        self._check(self._L.fdh_workspace_bytes(self._h, B, S, m, C.byref(o) if o else None, C.byref(out)),
+                    "fdh_workspace_bytes")
+        return int(out.value)
+
+    # ---- memory ----
+    def set_workspace(self, B=0, S=0, m=0, o: LanczosOpts | None = None):
+        import torch
+        n = self.workspace_bytes(B, S, m, o)
+        self._ws = None
+        buf = torch.empty(max(n, 256) + 256, dtype=torch.uint8, device="cuda")
+        base = buf.data_ptr()
+        off = (-base) % 256
+        self._ws = buf
+        self._check(self._L.fdh_set_workspace(self._h, C.c_void_p(base + off), n, B, S, m,
+                                              C.byref(o) if o else None), "fdh_set_workspace")
+        return n
+
+    def empty_params(self):
+        import torch
+        dt = torch.float32 if self.dtype == "f32" else torch.uint16 if hasattr(torch, "uint16") else torch.int16
+        if self.dtype == "bf16":
+            dt = torch.bfloat16
+        return torch.empty(self.num_params, dtype=dt, device="cuda")
+
+    def init_params(self, seed: int):
+        p = self.empty_params()
+        self._check(self._L.fdh_init_params(self._h, _ptr(p), seed), "fdh_init_params")
+        return p
+
+    def make_tokens(self, B: int, S: int, seed: int, dist="uniform"):
+        import torch
+        t = torch.empty((B, S), dtype=torch.int32, device="cuda")
+        self._check(self._L.fdh_make_tokens(self._h, _ptr(t), B, S, seed, TOKENS[dist]), "fdh_make_tokens")
+        return t
+
+    def random_vector(self, seed: int, kind="rademacher"):
+        import torch
+        v = torch.empty(self.num_params, dtype=torch.float32, device="cuda")
+        self._check(self._L.fdh_random_vector(self._h, _ptr(v), seed, VEC[kind]), "fdh_random_vector")
+        return v
+
+    def set_quad_diag(self, diag):
+        self._keep.append(diag)
+        self._check(self._L.fdh_set_quad_diag(self._h, _ptr(diag)), "fdh_set_quad_diag")
+
+    # ---- the hot path ----
+    def hvp(self, params, v, eps: float, tokens=None, out=None):
+        """Hv (float32 [P]) of the FD-HVP at step eps; enqueued on the context stream."""
+        import torch
+        if out is None:
+            out = torch.empty(self.num_params, dtype=torch.float32, device="cuda")
+        B, S = (tokens.shape if tokens is not None else (0, 0))
+        self._check(self._L.fdh_hvp(self._h, _ptr(params), _ptr(v), float(eps), _ptr(tokens), B, S, _ptr(out)),
+                    "fdh_hvp")
+        return out
+
+    def last_losses(self):
+        lp, lm = C.c_double(), C.c_double()
+        self._check(self._L.fdh_last_losses(self._h, C.byref(lp), C.byref(lm)), "fdh_last_losses")
+        return lp.value, lm.value
+
+    def bind(self, params, tokens, eps: float):
+        B, S = (tokens.shape if tokens is not None else (0, 0))
+        self._keep = [params, tokens]
+        self._check(self._L.fdh_bind(self._h, _ptr(params), _ptr(tokens), B, S, float(eps)), "fdh_bind")
+
+    def lanczos(self, m: int, probe_seed: int, o: LanczosOpts):
+        a = np.zeros(m)
+        b = np.zeros(m)
+        s = C.c_int32()
+        st = self._check(self._L.fdh_lanczos(self._h, m, probe_seed, C.byref(o),
+                                             a.ctypes.data_as(C.POINTER(C.c_double)),
+                                             b.ctypes.data_as(C.POINTER(C.c_double)), C.byref(s)), "fdh_lanczos")
+        return a, b, int(s.value), st
+
+    def slq_density(self, probes: int, m: int, seed: int, o: LanczosOpts):
+        nodes = np.zeros((probes, m))
+        weights = np.zeros((probes, m))
+        steps = np.zeros(probes, dtype=np.int32)
+        tr = C.c_double()
+        st = self._check(self._L.fdh_slq_density(
+            self._h, probes, m, seed, C.byref(o), nodes.ctypes.data_as(C.POINTER(C.c_double)),
+            weights.ctypes.data_as(C.POINTER(C.c_double)), steps.ctypes.data_as(C.POINTER(C.c_int32)),
+            C.byref(tr)), "fdh_slq_density")
+        return nodes, weights, steps, tr.value, st
+
+    def block_stats(self, a, b):
+        out = np.zeros((max(self.num_blocks, 0), 3))
+        self._check(self._L.fdh_block_stats(self._h, _ptr(a), _ptr(b), out.ctypes.data_as(C.POINTER(C.c_double))),
+                    "fdh_block_stats")
+        return out
+
+
+def testing_gemm(dtype: str, M, N, K, batch, a_kmajor, b_kmajor, A, B, A2, B2, Cout, causal=0, alpha=1.0):
+    st = lib().fdh_testing_gemm(DTYPE[dtype], M, N, K, batch, int(a_kmajor), int(b_kmajor), _ptr(A), _ptr(B),
+                                _ptr(A2), _ptr(B2), _ptr(Cout), causal, float(alpha), _stream())
+    if st != OK:
+        raise FdhError(st, "fdh_testing_gemm")
