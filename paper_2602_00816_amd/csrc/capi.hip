@@ -234,3 +234,37 @@ extern "C" fdh_status fdh_testing_gemm(int32_t dtype, int32_t M, int32_t N, int3
   }
   return r == hipSuccess ? FDH_OK : FDH_ERR_HIP;
 }
+
+extern "C" fdh_status fdh_testing_timing(fdh_ctx* ctx, int32_t enable) {
+  return run(ctx, [&](fdh::Engine& e) -> int {
+    if (e.timing.on) {
+      hipError_t r = e.timing.harvest(e.stream);
+      if (r != hipSuccess) { e.err = "timing harvest"; return FDH_ERR_HIP; }
+    }
+    e.timing.on = enable != 0;
+    e.timing.reset();
+    return FDH_OK;
+  });
+}
+
+extern "C" fdh_status fdh_testing_timing_read(fdh_ctx* ctx, double* out16) {
+  return run(ctx, [&](fdh::Engine& e) -> int {
+    if (!out16) { e.err = "null output"; return FDH_ERR_INVALID_ARG; }
+    hipError_t r = e.timing.harvest(e.stream);
+    if (r != hipSuccess) { e.err = "timing harvest"; return FDH_ERR_HIP; }
+    for (int c = 0; c < fdh::Timing::NCAT; ++c) {
+      out16[4 * c + 0] = e.timing.count[c];
+      out16[4 * c + 1] = e.timing.ms[c];
+      out16[4 * c + 2] = e.timing.flops[c];
+      out16[4 * c + 3] = e.timing.bytes[c];
+    }
+    e.timing.reset();
+    return FDH_OK;
+  });
+}
+
+extern "C" fdh_status fdh_testing_copy(void* dst, const void* src, size_t bytes, void* hip_stream) {
+  if (!dst || !src || (bytes & 15) || (reinterpret_cast<uintptr_t>(dst) & 15) || (reinterpret_cast<uintptr_t>(src) & 15))
+    return FDH_ERR_INVALID_ARG;
+  return fdh::launch_copy16(dst, src, bytes, (hipStream_t)hip_stream) == hipSuccess ? FDH_OK : FDH_ERR_HIP;
+}

@@ -29,6 +29,25 @@ struct Span {  // carve of the workspace
   size_t off = 0, bytes = 0;
 };
 
+// Optional per-launch timing with HIP events on the context stream (testing
+// hook used by the benchmark).  Categories: 0 GEMM, 1 Lanczos vector kernels.
+struct Timing {
+  static constexpr int NCAT = 4;
+  static constexpr size_t POOL = 8192;
+  bool on = false;
+  std::vector<hipEvent_t> ev;
+  size_t used = 0;
+  struct Rec { int cat, e0; double flops, bytes; };
+  std::vector<Rec> recs;
+  double ms[NCAT] = {}, flops[NCAT] = {}, bytes[NCAT] = {};
+  double count[NCAT] = {};
+  hipError_t begin(hipStream_t s, int* e0);
+  hipError_t end(hipStream_t s, int cat, int e0, double fl, double by);
+  hipError_t harvest(hipStream_t s);
+  void reset() { for (int i = 0; i < NCAT; ++i) ms[i] = flops[i] = bytes[i] = count[i] = 0.0; }
+  ~Timing();
+};
+
 class Engine {
  public:
   explicit Engine(const fdh_model_config& cfg, hipStream_t stream);
@@ -58,6 +77,7 @@ class Engine {
   double b_eps = 0.0;
   bool bound = false;
   const float* quad_diag = nullptr;
+  Timing timing;
 
   // entry points (return fdh_status)
   int hvp(const void* params, const float* v, double eps, const int32_t* tok, int B, int S, float* hv);

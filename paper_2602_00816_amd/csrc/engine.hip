@@ -210,6 +210,67 @@ size_t Engine::plan(int B, int S, int m, const fdh_lanczos_opts* o, bool carve) 
 }
 
 // ---------------------------------------------------------------------------
+// launch timing (testing hook)
+// ---------------------------------------------------------------------------
+hipError_t Timing::begin(hipStream_t s, int* e0) {
+  if (ev.empty()) {
+    ev.resize(POOL);
+    for (auto& x : ev) {
+      hipError_t r = hipEventCreate(&x);
+      if (r != hipSuccess) return r;
+    }
+  }
+  if (used + 2 > ev.size()) {
+    hipError_t r = harvest(s);
+    if (r != hipSuccess) return r;
+  }
+  *e0 = (int)used;
+  used += 2;
+  return hipEventRecord(ev[*e0], s);
+}
+
+hipError_t Timing::end(hipStream_t s, int cat, int e0, double fl, double by) {
+  recs.push_back({cat, e0, fl, by});
+  return hipEventRecord(ev[e0 + 1], s);
+}
+
+hipError_t Timing::harvest(hipStream_t s) {
+  hipError_t r = hipStreamSynchronize(s);
+  if (r != hipSuccess) return r;
+  for (const Rec& x : recs) {
+    float t = 0.f;
+    r = hipEventElapsedTime(&t, ev[x.e0], ev[x.e0 + 1]);
+    if (r != hipSuccess) return r;
+    ms[x.cat] += t;
+    flops[x.cat] += x.flops;
+    bytes[x.cat] += x.bytes;
+    count[x.cat] += 1.0;
+  }
+  recs.clear();
+  used = 0;
+  return hipSuccess;
+}
+
+Timing::~Timing() {
+  for (auto& x : ev) (void)hipEventDestroy(x);
+}
+
+// executed (tile-exact, tails clipped) FLOPs of one GEMM call
+static double gemm_flops(const GemmArgs& g) {
+  const int BMt = 128;
+  double f = 0.0;
+  for (int m0 = 0; m0 < g.M; m0 += BMt) {
+    const double rows = std::min(BMt, g.M - m0);
+    double cols = g.N, kk = g.K;
+    if (g.causal == CAUSAL_SKIP_UPPER) cols = std::min<double>(g.N, m0 + BMt);
+    if (g.causal == CAUSAL_K_LE_M) kk = std::min<double>(g.K, m0 + BMt);
+    if (g.causal == CAUSAL_K_GE_M) kk = g.K - std::min(m0, g.K);
+    f += 2.0 * rows * cols * kk;
+  }
+  return f * g.npairs * g.nbatch;
+}
+
+// ---------------------------------------------------------------------------
 // GEMM plumbing
 // ---------------------------------------------------------------------------
 template <typename T>
@@ -219,10 +280,19 @@ static int run_gemm(Engine& e, GemmArgs& g) {
     e.err = msg;
     return FDH_ERR_UNSUPPORTED;
   }
+  int e0 = 0;
+  if (e.timing.on) {
+    hipError_t r = e.timing.begin(e.stream, &e0);
+    if (r != hipSuccess) { e.err = "timing event"; return FDH_ERR_HIP; }
+  }
   hipError_t r = gemm<T>(g, e.stream);
   if (r != hipSuccess) {
     e.err = std::string("gemm launch: ") + hipGetErrorString(r);
     return FDH_ERR_HIP;
+  }
+  if (e.timing.on) {
+    r = e.timing.end(e.stream, 0, e0, gemm_flops(g), 0.0);
+    if (r != hipSuccess) { e.err = "timing event"; return FDH_ERR_HIP; }
   }
   return FDH_OK;
 }
@@ -641,21 +711,36 @@ int Engine::lanczos_t(int m, uint64_t seed, const fdh_lanczos_opts& o, double* a
   CK(launch_rademacher(q, P, seed, st));
   if (cap > 0) CK(launch_scale_cast<Bt>(basis, q, 1.0, P, st));  // slot 0 = q_1
 
+  const double bb = sizeof(Bt), Pd = (double)P;
+  // one timed vector launch (algorithmic bytes: each operand touched once)
+  auto timed = [&](double bytes, auto&& launch) -> int {
+    int e0 = 0;
+    if (timing.on) CK(timing.begin(st, &e0));
+    CK(launch());
+    if (timing.on) CK(timing.end(st, 1, e0, 0.0, bytes));
+    return FDH_OK;
+  };
+#define TV(bytes, call)                                 \
+  do {                                                  \
+    int rc_ = timed((bytes), [&]() { return (call); }); \
+    if (rc_ != FDH_OK) return rc_;                      \
+  } while (0)
   for (int k = 0; k < m; ++k) {
     int rc = hvp(b_params, q, b_eps, b_tokens, b_B, b_S, w);
     if (rc != FDH_OK) return rc;
-    CK(launch_lanczos_alpha(w, q, qp, D, k, P, st));
+    TV(16.0 * Pd, launch_lanczos_alpha(w, q, qp, D, k, P, st));
     const int nv = std::min(k + 1, cap);
-    CK(launch_lanczos_b<Bt>(w, q, basis, nv, D, k, P, st));
+    TV((12.0 + nv * bb) * Pd, launch_lanczos_b<Bt>(w, q, basis, nv, D, k, P, st));
     if (nv > 0) {
-      CK(launch_lanczos_cgs<Bt>(w, basis, nv, D, 0, false, k, P, st));
-      CK(launch_lanczos_cgs<Bt>(w, basis, nv, D, 1, true, k, P, st));
+      TV((8.0 + nv * bb) * Pd, launch_lanczos_cgs<Bt>(w, basis, nv, D, 0, false, k, P, st));
+      TV((8.0 + nv * bb) * Pd, launch_lanczos_cgs<Bt>(w, basis, nv, D, 1, true, k, P, st));
     }
     Bt* row = nullptr;
     if (cap > 0 && k + 1 < m) row = basis + (int64_t)((k + 1) % cap) * P;
-    CK(launch_lanczos_normalise<Bt>(w, qp, row, D, k, tol, P, st));
+    TV((8.0 + (row ? bb : 0.0)) * Pd, launch_lanczos_normalise<Bt>(w, qp, row, D, k, tol, P, st));
     std::swap(q, qp);
   }
+#undef TV
   std::vector<double> a(m), b(m);
   int flag[2];
   CK(hipMemcpyAsync(a.data(), D.alpha, m * 8, hipMemcpyDeviceToHost, st));

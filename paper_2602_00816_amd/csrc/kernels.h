@@ -22,6 +22,7 @@ hipError_t launch_gaussian_unit(float* out, double* partial1024, int64_t n, uint
 constexpr int RED_BLOCKS = 1024;   // fixed grid of the deterministic reductions
 
 hipError_t launch_fill_f32(float* p, int64_t n, float v, hipStream_t s);
+hipError_t launch_copy16(void* dst, const void* src, size_t bytes, hipStream_t s);
 hipError_t launch_fill_f64(double* p, int64_t n, double v, hipStream_t s);
 // lo[i] = T(eps * v[i])
 template <typename T>

@@ -184,6 +184,20 @@ hipError_t launch_fill_f32(float* p, int64_t n, float v, hipStream_t s) {
   hipLaunchKernelGGL(fill_f32_kernel, dim3(grid_for(n)), dim3(NT), 0, s, p, n, v);
   return hipGetLastError();
 }
+namespace {
+__global__ void copy16_kernel(uint4* dst, const uint4* src, int64_t n) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    dst[i] = src[i];
+}
+}  // namespace
+
+hipError_t launch_copy16(void* dst, const void* src, size_t bytes, hipStream_t s) {
+  const int64_t n = (int64_t)(bytes / 16);
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(copy16_kernel, dim3(grid_for(n)), dim3(NT), 0, s, (uint4*)dst, (const uint4*)src, n);
+  return hipGetLastError();
+}
+
 hipError_t launch_fill_f64(double* p, int64_t n, double v, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(fill_f64_kernel, dim3(grid_for(n)), dim3(NT), 0, s, p, n, v);

@@ -82,6 +82,9 @@ def lib():
         "fdh_block_stats": (i32, [vp, vp, vp, pd]),
         "fdh_last_error": (C.c_char_p, [vp]),
         "fdh_testing_gemm": (i32, [i32, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, i32, C.c_float, vp]),
+        "fdh_testing_timing": (i32, [vp, i32]),
+        "fdh_testing_timing_read": (i32, [vp, pd]),
+        "fdh_testing_copy": (i32, [vp, vp, C.c_size_t, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -258,11 +261,28 @@ class Model:
             C.byref(tr)), "fdh_slq_density")
         return nodes, weights, steps, tr.value, st
 
+    def timing(self, enable: bool):
+        self._check(self._L.fdh_testing_timing(self._h, int(enable)), "fdh_testing_timing")
+
+    def timing_read(self) -> dict:
+        out = np.zeros(16)
+        self._check(self._L.fdh_testing_timing_read(self._h, out.ctypes.data_as(C.POINTER(C.c_double))),
+                    "fdh_testing_timing_read")
+        cats = ["gemm", "lanczos", "c2", "c3"]
+        return {c: dict(launches=out[4 * i], ms=out[4 * i + 1], flops=out[4 * i + 2], bytes=out[4 * i + 3])
+                for i, c in enumerate(cats)}
+
     def block_stats(self, a, b):
         out = np.zeros((max(self.num_blocks, 0), 3))
         self._check(self._L.fdh_block_stats(self._h, _ptr(a), _ptr(b), out.ctypes.data_as(C.POINTER(C.c_double))),
                     "fdh_block_stats")
         return out
+
+
+def testing_copy(dst, src, nbytes: int):
+    st = lib().fdh_testing_copy(_ptr(dst), _ptr(src), int(nbytes), _stream())
+    if st != OK:
+        raise FdhError(st, "fdh_testing_copy")
 
 
 def testing_gemm(dtype: str, M, N, K, batch, a_kmajor, b_kmajor, A, B, A2, B2, Cout, causal=0, alpha=1.0):
