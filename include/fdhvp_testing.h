@@ -20,12 +20,13 @@ extern "C" {
  * A is [batch][M][K] when a_kmajor, else [batch][K][M]; B is [batch][N][K] when
  * b_kmajor, else [batch][K][N]; A2/B2 (may be NULL together) share the layouts.
  * C is float32 [batch][M][N], overwritten.  causal: 0 none, 1 skip output tiles
- * above the diagonal, 2 contract only k <= m, 3 only k >= m.  Enqueued on
- * hip_stream; returns without waiting.  K, and M/N of MN-major operands, must
- * be multiples of 8 (bf16) or 4 (fp32). */
+ * above the diagonal, 2 contract only k <= m, 3 only k >= m.  tile selects
+ * the bf16 kernel variant (0 automatic, 1 128x128, 2 256x256, 3 256x128).
+ * Enqueued on hip_stream; returns without waiting.  K, and M/N of MN-major
+ * operands, must be multiples of 8 (bf16) or 4 (fp32). */
 fdh_status fdh_testing_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t batch, int32_t a_kmajor,
                             int32_t b_kmajor, const void* A, const void* B, const void* A2, const void* B2,
-                            float* C, int32_t causal, float alpha, void* hip_stream);
+                            float* C, int32_t causal, float alpha, int32_t tile, void* hip_stream);
 
 /* Per-launch timing with HIP events recorded on the context stream around every
  * GEMM launch (category 0) and every Lanczos vector launch (category 1).

@@ -201,10 +201,12 @@ const char* fdh_last_error(const fdh_ctx* ctx) {
 
 extern "C" fdh_status fdh_testing_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t batch, int32_t a_kmajor,
                                        int32_t b_kmajor, const void* A, const void* B, const void* A2, const void* B2,
-                                       float* C, int32_t causal, float alpha, void* hip_stream) {
-  if (!A || !B || !C || (!A2) != (!B2) || M < 0 || N < 0 || K < 0 || batch < 1 || causal < 0 || causal > 3)
+                                       float* C, int32_t causal, float alpha, int32_t tile, void* hip_stream) {
+  if (!A || !B || !C || (!A2) != (!B2) || M < 0 || N < 0 || K < 0 || batch < 1 || causal < 0 || causal > 3 ||
+      tile < 0 || tile > 3)
     return FDH_ERR_INVALID_ARG;
   fdh::GemmArgs g;
+  g.tile = tile;
   g.M = M; g.N = N; g.K = K; g.nbatch = batch; g.inner_count = 1;
   g.npairs = A2 ? 2 : 1;
   const void* As[2] = {A, A2};

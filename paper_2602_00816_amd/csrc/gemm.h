@@ -38,6 +38,7 @@ struct GemmArgs {
   float bias_v_scale = 1.f;
   const float* resid = nullptr;           // fp32, same indexing as C, added (OUT_F32 only)
   int causal = CAUSAL_NONE;
+  int tile = 0;                           // 0 automatic; bf16 only: 1 128x128, 2 256x256, 3 256x128
 };
 
 // T = float (fp32 MFMA) or bf16_t (bf16 MFMA, fp32 accumulation)

@@ -1,13 +1,18 @@
-// Batched MFMA GEMM for gfx950.
+// Batched MFMA GEMM for gfx950:  C[z] = alpha * sum_p A_p[z] B_p[z]^T (+ epilogue).
 //
-// One workgroup of 256 threads (4 wavefronts of 64) computes a 128x128 tile of
-// C.  Each wavefront owns a 64x64 quarter as 2x2 blocks of 32x32 MFMA
-// accumulators (v_mfma_f32_32x32x16_bf16 for bf16 operands,
-// v_mfma_f32_32x32x2_f32 for fp32 operands).  A and B tiles are staged in LDS
-// in K-contiguous rows; operands that are stored MN-major in HBM are
-// transposed while being written to LDS, so the MFMA fragment reads are always
-// single 16-byte (bf16) or 4-byte (fp32) LDS reads.  Global loads are 16-byte
-// vectors, prefetched into registers one K-tile ahead.
+// Two kernels:
+//  * gemm_kernel  - 128x128 workgroup tile, 4 wavefronts of 64x64 (2x2 blocks
+//    of 32x32 MFMA accumulators), fp32 (v_mfma_f32_32x32x2_f32) or bf16
+//    (v_mfma_f32_32x32x16_bf16) operands; used for fp32 and for small bf16
+//    problems.
+//  * gemm_bf16_big - bf16 only, 256x256 (8 wavefronts) or 256x128 (4
+//    wavefronts) workgroup tiles; every wavefront owns 128x64 as 4x2 blocks of
+//    32x32, so one A fragment read from LDS feeds two MFMAs and one B fragment
+//    four.  K tile 64, LDS double-buffered, one barrier per K tile.
+// Both stage A and B in LDS as K-contiguous rows.  Operands stored MN-major in
+// HBM are transposed on their way into LDS, so the MFMA fragment reads are
+// always single 16-byte LDS reads.  Global loads are 16-byte vectors,
+// prefetched into registers one K tile ahead.
 #include "gemm.h"
 
 namespace fdh {
@@ -37,8 +42,11 @@ __device__ inline int64_t batch_off(int z, int inner_count, int64_t s_outer, int
   return (int64_t)(z / inner_count) * s_outer + (int64_t)((z % inner_count) / div) * s_inner;
 }
 
-// Load the VEC-element vector number `i` (0..1) of this thread for a tile
-// starting at (row0, k0).  Returns zeros outside [0,rows) x [0,K).
+// ===========================================================================
+// 128x128 kernel
+// ===========================================================================
+// Load the 16-byte vector number `vid` of a tile starting at (row0, k0).
+// Returns zeros outside [0,rows) x [0,K).
 template <typename T, bool KMAJ>
 __device__ inline Vec16 load_vec(const T* base, int64_t s_row, int64_t s_k, int rows, int K,
                                  int row0, int k0, int vid) {
@@ -119,6 +127,33 @@ __device__ inline void mma_tile<float>(const float* sA, const float* sB, f32x16_
   }
 }
 
+// shared epilogue: accumulator block (i, j) of a wavefront whose 32x32 block
+// origin is (rb, cb); lane layout of the 32x32 MFMA output
+template <typename T>
+__device__ inline void store_block(const GemmArgs& a, const f32x16_t& acc, int64_t coff, int rb, int cb, int lane) {
+  const int col = cb + (lane & 31);
+  if (col >= a.N) return;
+  float badd = 0.f;
+  if (a.bias_theta) badd += a.bias_theta_scale * ldf(reinterpret_cast<const T*>(a.bias_theta), col);
+  if (a.bias_v) badd += a.bias_v_scale * a.bias_v[col];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int row = rb + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+    if (row < a.M) {
+      const int64_t idx = coff + (int64_t)row * a.ldc + col;
+      float x = a.alpha * acc[r] + badd;
+      if (a.out_type == OUT_F32) {
+        float* C = reinterpret_cast<float*>(a.C);
+        if (a.resid) x += a.resid[idx];
+        if (a.beta != 0.f) x += a.beta * C[idx];
+        C[idx] = x;
+      } else {
+        stf(reinterpret_cast<T*>(a.C), idx, x);
+      }
+    }
+  }
+}
+
 template <typename T, bool AK, bool BKM>
 __global__ __launch_bounds__(NT) void gemm_kernel(GemmArgs a) {
   constexpr int KT = Tr<T>::KT, LD = KT + Tr<T>::PAD;
@@ -174,33 +209,210 @@ __global__ __launch_bounds__(NT) void gemm_kernel(GemmArgs a) {
     }
   }
 
-  // epilogue
   const int64_t coff = batch_off(z, a.inner_count, a.c_outer, a.c_inner, a.c_div);
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int col = n0 + wn * 64 + j * 32 + (lane & 31);
-      if (col >= a.N) continue;
-      float badd = 0.f;
-      if (a.bias_theta) badd += a.bias_theta_scale * ldf(reinterpret_cast<const T*>(a.bias_theta), col);
-      if (a.bias_v) badd += a.bias_v_scale * a.bias_v[col];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm * 64 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-        if (row >= a.M) continue;
-        const int64_t idx = coff + (int64_t)row * a.ldc + col;
-        float x = a.alpha * acc[i][j][r] + badd;
-        if (a.out_type == OUT_F32) {
-          float* C = reinterpret_cast<float*>(a.C);
-          if (a.resid) x += a.resid[idx];
-          if (a.beta != 0.f) x += a.beta * C[idx];
-          C[idx] = x;
-        } else {
-          stf(reinterpret_cast<T*>(a.C), idx, x);
+    for (int j = 0; j < 2; ++j)
+      store_block<T>(a, acc[i][j], coff, m0 + wm * 64 + i * 32, n0 + wn * 64 + j * 32, lane);
+}
+
+// ===========================================================================
+// bf16 kernel with large tiles: BM x BN workgroup tile, WM x WN wavefronts,
+// each wavefront 128 x 64 (4 x 2 blocks of 32x32).
+// ===========================================================================
+// LDS holds each tile row as 64 bf16 = 128 bytes (8 chunks of 16 bytes) with
+// the chunk index XOR-swizzled by bits 0-2 and 3-5 of the row: the 16-byte
+// MFMA fragment reads (8 consecutive rows, one chunk), the 16-byte K-major
+// stores (one row, 8 chunks) and the 8-byte transposed stores (rows 8 apart,
+// one chunk) all spread over the 32 LDS banks.
+constexpr int KT2 = 64, LD2 = KT2;
+__device__ inline int swz(int row, int chunk) { return row * LD2 + ((chunk ^ (row & 7) ^ ((row >> 3) & 7)) << 3); }
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+// One R x KT2 tile.  K-major: R*8 vectors of 8 consecutive k; MN-major:
+// 2R bundles of 4 consecutive k x 8 consecutive rows, transposed in registers
+// into 8-byte LDS rows.  NTH threads share the work.
+template <int R, bool KMAJ, int NTH>
+struct TileLoader {
+  static constexpr int UNITS = KMAJ ? R * 8 : 2 * R;        // vectors or bundles
+  static constexpr int PER = (UNITS + NTH - 1) / NTH;       // units per thread
+  static constexpr int NV = KMAJ ? PER : 4 * PER;           // 16-byte registers per thread
+  u32x4 v[NV];
+
+  __device__ inline void load(const bf16_t* base, int64_t s_row, int64_t s_k, int rows, int kmax, int row0, int k0,
+                              int tid) {
+#pragma clang loop unroll(full)
+    for (int u = 0; u < PER; ++u) {
+      const int id = tid + u * NTH;
+      if (KMAJ) {
+        const int r = id >> 3, kk = (id & 7) * 8;
+        const int gr = row0 + r, gk = k0 + kk;
+        u32x4 x = {0u, 0u, 0u, 0u};
+        if (id < UNITS && gr < rows && gk < kmax) x = *reinterpret_cast<const u32x4*>(base + (int64_t)gr * s_row + gk);
+        v[u] = x;
+      } else {
+        const int rg = id % (R / 8), kq = id / (R / 8);
+        const int gr = row0 + rg * 8;
+#pragma clang loop unroll(full)
+        for (int j = 0; j < 4; ++j) {
+          const int gk = k0 + kq * 4 + j;
+          u32x4 x = {0u, 0u, 0u, 0u};
+          if (id < UNITS && gr < rows && gk < kmax) x = *reinterpret_cast<const u32x4*>(base + (int64_t)gk * s_k + gr);
+          v[4 * u + j] = x;
         }
       }
     }
+  }
+
+  __device__ inline void store(bf16_t* s, int tid) const {
+#pragma clang loop unroll(full)
+    for (int u = 0; u < PER; ++u) {
+      const int id = tid + u * NTH;
+      if (id >= UNITS) continue;
+      if (KMAJ) {
+        const int r = id >> 3, kk = (id & 7) * 8;
+        *reinterpret_cast<u32x4*>(s + swz(r, kk >> 3)) = v[u];
+      } else {
+        const int rg = id % (R / 8), kq = id / (R / 8);
+        const u32x4* w = &v[4 * u];
+#pragma clang loop unroll(full)
+        for (int q = 0; q < 4; ++q) {
+          // rows 2q (low halves) and 2q+1 (high halves) of the four k vectors
+          uint2 ev, od;
+          ev.x = (w[0][q] & 0xFFFFu) | (w[1][q] << 16);
+          ev.y = (w[2][q] & 0xFFFFu) | (w[3][q] << 16);
+          od.x = (w[0][q] >> 16) | (w[1][q] & 0xFFFF0000u);
+          od.y = (w[2][q] >> 16) | (w[3][q] & 0xFFFF0000u);
+          *reinterpret_cast<uint2*>(s + swz(rg * 8 + 2 * q, kq >> 1) + (kq & 1) * 4) = ev;
+          *reinterpret_cast<uint2*>(s + swz(rg * 8 + 2 * q + 1, kq >> 1) + (kq & 1) * 4) = od;
+        }
+      }
+    }
+  }
+};
+
+template <int BM_, int BN_, int WM, int WN, bool AK, bool BKM>
+__global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_big(GemmArgs a) {
+  constexpr int NTH = 64 * WM * WN;
+  constexpr int IM = BM_ / (32 * WM), JN = BN_ / (32 * WN);
+  __shared__ __attribute__((aligned(16))) bf16_t sA[2][BM_ * LD2];
+  __shared__ __attribute__((aligned(16))) bf16_t sB[2][BN_ * LD2];
+
+  // XCD-aware tile order.  Workgroups are handed to the 8 XCDs round-robin
+  // in launch order; renumber so that each XCD receives one contiguous run of
+  // tiles, and walk tiles in groups of 8 row panels so that the workgroups
+  // resident on one XCD share A and B panels in that XCD's L2.
+  const int gx = gridDim.x, gy = gridDim.y;
+  const int nb = gx * gy * gridDim.z;
+  int lin = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
+  const int per = nb / 8;
+  if (lin < per * 8) lin = (lin % 8) * per + lin / 8;
+  const int tiles = gx * gy;
+  const int z = lin / tiles;
+  const int tl = lin % tiles;
+  constexpr int GM = 8;
+  const int gsize = GM * gx;
+  const int first_m = (tl / gsize) * GM;
+  const int gm_rows = min(gy - first_m, GM);
+  const int tm = first_m + (tl % gsize) % gm_rows;
+  const int tn = (tl % gsize) / gm_rows;
+  const int m0 = tm * BM_, n0 = tn * BN_;
+  if (a.causal == CAUSAL_SKIP_UPPER && n0 > m0 + BM_ - 1) return;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+
+  int kmin = 0, kmax = a.K;
+  if (a.causal == CAUSAL_K_LE_M) kmax = min(a.K, m0 + BM_);
+  if (a.causal == CAUSAL_K_GE_M) kmin = (min(m0, a.K) / KT2) * KT2;
+
+  f32x16_t acc[IM][JN];
+#pragma clang loop unroll(full)
+  for (int i = 0; i < IM; ++i)
+#pragma clang loop unroll(full)
+    for (int j = 0; j < JN; ++j)
+#pragma clang loop unroll(full)
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  TileLoader<BM_, AK, NTH> la;
+  TileLoader<BN_, BKM, NTH> lb;
+  const int nkt = (kmax > kmin) ? (kmax - kmin + KT2 - 1) / KT2 : 0;
+  const int total = nkt * a.npairs;
+
+  // operand bases of both pairs (pair p covers K tiles p*nkt .. p*nkt + nkt - 1)
+  const bf16_t* pa0 = reinterpret_cast<const bf16_t*>(a.A[0].ptr) +
+                      batch_off(z, a.inner_count, a.A[0].s_outer, a.A[0].s_inner, a.A[0].inner_div);
+  const bf16_t* pb0 = reinterpret_cast<const bf16_t*>(a.B[0].ptr) +
+                      batch_off(z, a.inner_count, a.B[0].s_outer, a.B[0].s_inner, a.B[0].inner_div);
+  const bf16_t* pa1 = pa0;
+  const bf16_t* pb1 = pb0;
+  if (a.npairs > 1) {
+    pa1 = reinterpret_cast<const bf16_t*>(a.A[1].ptr) +
+          batch_off(z, a.inner_count, a.A[1].s_outer, a.A[1].s_inner, a.A[1].inner_div);
+    pb1 = reinterpret_cast<const bf16_t*>(a.B[1].ptr) +
+          batch_off(z, a.inner_count, a.B[1].s_outer, a.B[1].s_inner, a.B[1].inner_div);
+  }
+  const int64_t asr0 = a.A[0].s_row, ask0 = a.A[0].s_k, bsr0 = a.B[0].s_row, bsk0 = a.B[0].s_k;
+  const int64_t asr1 = a.A[1].s_row, ask1 = a.A[1].s_k, bsr1 = a.B[1].s_row, bsk1 = a.B[1].s_k;
+
+  if (total > 0) {
+    la.load(pa0, asr0, ask0, a.M, kmax, m0, kmin, tid);
+    lb.load(pb0, bsr0, bsk0, a.N, kmax, n0, kmin, tid);
+    la.store(sA[0], tid);
+    lb.store(sB[0], tid);
+    __syncthreads();
+  }
+  for (int t = 0; t < total; ++t) {
+    const int cur = t & 1;
+    if (t + 1 < total) {
+      const int t1 = t + 1;
+      const bool second = t1 >= nkt;
+      const int k0 = kmin + (second ? t1 - nkt : t1) * KT2;
+      la.load(second ? pa1 : pa0, second ? asr1 : asr0, second ? ask1 : ask0, a.M, kmax, m0, k0, tid);
+      lb.load(second ? pb1 : pb0, second ? bsr1 : bsr0, second ? bsk1 : bsk0, a.N, kmax, n0, k0, tid);
+    }
+    const bf16_t* cA = sA[cur];
+    const bf16_t* cB = sB[cur];
+#pragma clang loop unroll(full)
+    for (int kk = 0; kk < KT2; kk += 16) {
+      bf16x8_t af[IM], bfr[JN];
+#pragma clang loop unroll(full)
+      for (int i = 0; i < IM; ++i)
+        af[i] = *reinterpret_cast<const bf16x8_t*>(cA + swz(wm * (BM_ / WM) + i * 32 + (lane & 31), (kk >> 3) + (lane >> 5)));
+#pragma clang loop unroll(full)
+      for (int j = 0; j < JN; ++j)
+        bfr[j] = *reinterpret_cast<const bf16x8_t*>(cB + swz(wn * (BN_ / WN) + j * 32 + (lane & 31), (kk >> 3) + (lane >> 5)));
+#pragma clang loop unroll(full)
+      for (int i = 0; i < IM; ++i)
+#pragma clang loop unroll(full)
+        for (int j = 0; j < JN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    }
+    if (t + 1 < total) {
+      la.store(sA[cur ^ 1], tid);
+      lb.store(sB[cur ^ 1], tid);
+    }
+    __syncthreads();
+  }
+
+  const int64_t coff = batch_off(z, a.inner_count, a.c_outer, a.c_inner, a.c_div);
+#pragma clang loop unroll(full)
+  for (int i = 0; i < IM; ++i)
+#pragma clang loop unroll(full)
+    for (int j = 0; j < JN; ++j)
+      store_block<bf16_t>(a, acc[i][j], coff, m0 + wm * (BM_ / WM) + i * 32, n0 + wn * (BN_ / WN) + j * 32, lane);
+}
+
+template <int BM_, int BN_, int WM, int WN>
+void launch_big(const GemmArgs& a, hipStream_t stream) {
+  dim3 grid(ceil_div(a.N, BN_), ceil_div(a.M, BM_), a.nbatch);
+  dim3 block(64 * WM * WN);
+  const bool ak = a.A[0].s_k == 1, bk = a.B[0].s_k == 1;
+  if (ak && bk) hipLaunchKernelGGL((gemm_bf16_big<BM_, BN_, WM, WN, true, true>), grid, block, 0, stream, a);
+  else if (ak && !bk) hipLaunchKernelGGL((gemm_bf16_big<BM_, BN_, WM, WN, true, false>), grid, block, 0, stream, a);
+  else if (!ak && bk) hipLaunchKernelGGL((gemm_bf16_big<BM_, BN_, WM, WN, false, true>), grid, block, 0, stream, a);
+  else hipLaunchKernelGGL((gemm_bf16_big<BM_, BN_, WM, WN, false, false>), grid, block, 0, stream, a);
 }
 
 }  // namespace
@@ -235,13 +447,25 @@ const char* gemm_check(const GemmArgs& a) {
       }
     }
   }
-  if (a.causal != CAUSAL_NONE && a.M > a.N && a.causal == CAUSAL_SKIP_UPPER) return "gemm: causal skip needs M <= N";
+  if (a.causal == CAUSAL_SKIP_UPPER && a.M > a.N) return "gemm: causal skip needs M <= N";
+  if (a.tile < 0 || a.tile > 3) return "gemm: bad tile";
   return nullptr;
 }
 
 template <typename T>
 hipError_t gemm(const GemmArgs& a, hipStream_t stream) {
   if (a.M == 0 || a.N == 0) return hipSuccess;
+  if constexpr (sizeof(T) == 2) {
+    int tile = a.tile;
+    if (tile == 0 && a.M >= 256) {
+      const int64_t t256 = (int64_t)ceil_div(a.M, 256) * ceil_div(a.N, 256) * a.nbatch;
+      const int64_t t128 = (int64_t)ceil_div(a.M, 256) * ceil_div(a.N, 128) * a.nbatch;
+      if (a.N > 128 && t256 >= 192) tile = 2;
+      else if (t128 >= 64) tile = 3;
+    }
+    if (tile == 2) { launch_big<256, 256, 2, 4>(a, stream); return hipGetLastError(); }
+    if (tile == 3) { launch_big<256, 128, 2, 2>(a, stream); return hipGetLastError(); }
+  }
   dim3 grid(ceil_div(a.N, BN), ceil_div(a.M, BM), a.nbatch);
   const bool ak = a.A[0].s_k == 1, bk = a.B[0].s_k == 1;
   if (ak && bk) hipLaunchKernelGGL((gemm_kernel<T, true, true>), grid, dim3(NT), 0, stream, a);

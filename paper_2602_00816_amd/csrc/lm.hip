@@ -296,6 +296,101 @@ __global__ __launch_bounds__(NT) void attn_dsoftmax_kernel(PairT<T> dS, const T*
   }
 }
 
+// Wavefront-per-row versions (4 rows per workgroup).  Row i of a causal score
+// matrix has i+1 live entries; entries i < j < roundup(i+1, 256) are written
+// as zeros, because the MFMA tiles that contract over a row read exactly up
+// to that boundary; entries beyond it are never read and not written.
+// The softmax keeps, per live entry, a = exp(Sm - c) cosh(Sd) and
+// b = exp(Sm - c) sinh(Sd) (both with full relative precision, computed from
+// the two fp64 exponentials), so that e+- = a +- b and
+//   P.m = (a Zm - b Zd) / (Z+ Z-),  P.d = (b Zm - a Zd) / (Z+ Z-),
+// with Zm, Zd the mean and half difference of Z+ = sum e+, Z- = sum e-.
+__device__ inline int zero_end(int i, int S) { return min(S, ((i + 256) / 256) * 256); }
+
+template <typename T, int PER>
+__global__ __launch_bounds__(256) void attn_softmax_w(PairT<T> P, const float* Sm, const float* Sd, int nrows, int S) {
+  const int lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= nrows) return;
+  const int i = (int)(r % S);
+  const int64_t base = r * (int64_t)S;
+  const int len = i + 1;
+  float av[PER], bv[PER];
+  double mx = -1e300;
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    const int j = lane + 64 * e;
+    if (j < len) mx = fmax(mx, (double)Sm[base + j]);
+  }
+  mx = wave_max(mx);
+  double zp = 0.0, zm = 0.0;
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    const int j = lane + 64 * e;
+    av[e] = bv[e] = 0.f;
+    if (j < len) {
+      const double a = (double)Sm[base + j] - mx, b = (double)Sd[base + j];
+      const double ep = exp(a + b), em = exp(a - b);
+      zp += ep;
+      zm += em;
+      av[e] = (float)(0.5 * (ep + em));
+      bv[e] = (float)(0.5 * (ep - em));
+    }
+  }
+  zp = wave_sum(zp);
+  zm = wave_sum(zm);
+  const double Zm = 0.5 * (zp + zm), Zd = 0.5 * (zp - zm), inv = 1.0 / (zp * zm);
+  const int ze = zero_end(i, S);
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    const int j = lane + 64 * e;
+    if (j < ze) {
+      const double a = av[e], b = bv[e];
+      stf(P.m, base + j, (float)((a * Zm - b * Zd) * inv));
+      stf(P.d, base + j, (float)((b * Zm - a * Zd) * inv));
+    }
+  }
+}
+
+template <typename T, int PER>
+__global__ __launch_bounds__(256) void attn_dsoftmax_w(PairT<T> dS, const T* Pm, const T* Pd, const float* dPm,
+                                                       const float* dPd, int nrows, int S) {
+  const int lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= nrows) return;
+  const int i = (int)(r % S);
+  const int64_t base = r * (int64_t)S;
+  const int len = i + 1;
+  double dp = 0.0, dm = 0.0;
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    const int j = lane + 64 * e;
+    if (j < len) {
+      const double pm = ldf(Pm, base + j), pd = ldf(Pd, base + j);
+      const double gm = dPm[base + j], gd = dPd[base + j];
+      dp += (pm + pd) * (gm + gd);
+      dm += (pm - pd) * (gm - gd);
+    }
+  }
+  dp = wave_sum(dp);
+  dm = wave_sum(dm);
+  const int ze = zero_end(i, S);
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    const int j = lane + 64 * e;
+    if (j < ze) {
+      double sp = 0.0, sn = 0.0;
+      if (j < len) {
+        const double pm = ldf(Pm, base + j), pd = ldf(Pd, base + j);
+        const double gm = dPm[base + j], gd = dPd[base + j];
+        sp = (pm + pd) * (gm + gd - dp);
+        sn = (pm - pd) * (gm - gd - dm);
+      }
+      put_pair(dS, base + j, sp, sn);
+    }
+  }
+}
+
 __global__ void group_sum_kernel(float* out, int64_t out_ld, const float* in, int T_, int Hk, int G, int dh) {
   const int64_t n = (int64_t)T_ * Hk * dh;
   GRID_LOOP(i, n) {
@@ -531,16 +626,24 @@ hipError_t launch_qkv_bwd_post(PairT<T> out, float* gm, float* gd, int T_, int S
 
 template <typename T>
 hipError_t launch_attn_softmax(PairT<T> P, const float* Sm, const float* Sd, int nrows, int S, hipStream_t s) {
-  if (S > MAXE * NT) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(attn_softmax_kernel<T>, dim3(nrows), dim3(NT), 0, s, P, Sm, Sd, S);
+  if (S > 4096) return hipErrorInvalidValue;
+  const dim3 g(ceil_div(nrows, 4)), b(256);
+  if (S <= 512) hipLaunchKernelGGL((attn_softmax_w<T, 8>), g, b, 0, s, P, Sm, Sd, nrows, S);
+  else if (S <= 1024) hipLaunchKernelGGL((attn_softmax_w<T, 16>), g, b, 0, s, P, Sm, Sd, nrows, S);
+  else if (S <= 2048) hipLaunchKernelGGL((attn_softmax_w<T, 32>), g, b, 0, s, P, Sm, Sd, nrows, S);
+  else hipLaunchKernelGGL((attn_softmax_w<T, 64>), g, b, 0, s, P, Sm, Sd, nrows, S);
   return hipGetLastError();
 }
 
 template <typename T>
 hipError_t launch_attn_dsoftmax(PairT<T> dS, const T* Pm, const T* Pd, const float* dPm, const float* dPd, int nrows,
                                 int S, hipStream_t s) {
-  if (S > MAXE * NT) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(attn_dsoftmax_kernel<T>, dim3(nrows), dim3(NT), 0, s, dS, Pm, Pd, dPm, dPd, S);
+  if (S > 4096) return hipErrorInvalidValue;
+  const dim3 g(ceil_div(nrows, 4)), b(256);
+  if (S <= 512) hipLaunchKernelGGL((attn_dsoftmax_w<T, 8>), g, b, 0, s, dS, Pm, Pd, dPm, dPd, nrows, S);
+  else if (S <= 1024) hipLaunchKernelGGL((attn_dsoftmax_w<T, 16>), g, b, 0, s, dS, Pm, Pd, dPm, dPd, nrows, S);
+  else if (S <= 2048) hipLaunchKernelGGL((attn_dsoftmax_w<T, 32>), g, b, 0, s, dS, Pm, Pd, dPm, dPd, nrows, S);
+  else hipLaunchKernelGGL((attn_dsoftmax_w<T, 64>), g, b, 0, s, dS, Pm, Pd, dPm, dPd, nrows, S);
   return hipGetLastError();
 }
 

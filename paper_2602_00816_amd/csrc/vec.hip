@@ -71,6 +71,130 @@ __global__ void lz_alpha_kernel(float* w, const float* q, const float* qprev, co
   if (threadIdx.x == 0) partial[blockIdx.x] = acc;
 }
 
+// 4-element groups: float4 for fp32 vectors, 4 basis entries (8 or 16 bytes)
+struct F4 { float x[4]; };
+__device__ inline F4 ld4(const float* p, int64_t i) {
+  const float4 v = *reinterpret_cast<const float4*>(p + i);
+  return F4{{v.x, v.y, v.z, v.w}};
+}
+__device__ inline void st4(float* p, int64_t i, const F4& f) {
+  *reinterpret_cast<float4*>(p + i) = make_float4(f.x[0], f.x[1], f.x[2], f.x[3]);
+}
+__device__ inline F4 ld4(const bf16_t* p, int64_t i) {
+  const uint2 u = *reinterpret_cast<const uint2*>(p + i);
+  return F4{{bf16_to_f32((bf16_t)(u.x & 0xFFFF)), bf16_to_f32((bf16_t)(u.x >> 16)), bf16_to_f32((bf16_t)(u.y & 0xFFFF)),
+             bf16_to_f32((bf16_t)(u.y >> 16))}};
+}
+__device__ inline void st4(bf16_t* p, int64_t i, const F4& f) {
+  uint2 u;
+  u.x = (uint32_t)f32_to_bf16(f.x[0]) | ((uint32_t)f32_to_bf16(f.x[1]) << 16);
+  u.y = (uint32_t)f32_to_bf16(f.x[2]) | ((uint32_t)f32_to_bf16(f.x[3]) << 16);
+  *reinterpret_cast<uint2*>(p + i) = u;
+}
+
+// Vectorised pass (n % 4 == 0): each thread owns groups of 4 consecutive
+// elements of its workgroup's chunk.  Same arithmetic as lz_pass_kernel.
+template <typename B>
+__global__ __launch_bounds__(NT) void lz_pass4_kernel(float* w, const float* x, const double* a_src, const double* c_src,
+                                                      int nv_upd, const B* basis, int nv_proj, int64_t n,
+                                                      double* partial) {
+  __shared__ double sh[NT / 64];
+  __shared__ double cs[128];
+  const int64_t ch = red_chunk(n);
+  const int64_t s0 = blockIdx.x * ch, s1 = min(n, s0 + ch);
+  const double a = a_src ? *a_src : 0.0;
+  for (int j = threadIdx.x; j < nv_upd; j += NT) cs[j] = c_src[j];
+  __syncthreads();
+  if (x || nv_upd > 0) {
+    for (int64_t i = s0 + 4 * threadIdx.x; i < s1; i += 4 * NT) {
+      F4 wv = ld4(w, i);
+      double acc4[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc4[e] = wv.x[e];
+      if (x) {
+        const F4 xv = ld4(x, i);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc4[e] -= a * (double)xv.x[e];
+      }
+      for (int j = 0; j < nv_upd; ++j) {
+        const F4 q = ld4(basis, (int64_t)j * n + i);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc4[e] -= cs[j] * (double)q.x[e];
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) wv.x[e] = (float)acc4[e];
+      st4(w, i, wv);
+    }
+  }
+  if (nv_proj == 0) {
+    double acc = 0.0;
+    for (int64_t i = s0 + 4 * threadIdx.x; i < s1; i += 4 * NT) {
+      const F4 wv = ld4(w, i);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc += (double)wv.x[e] * (double)wv.x[e];
+    }
+    acc = block_sum<NT>(acc, sh);
+    if (threadIdx.x == 0) partial[blockIdx.x] = acc;
+    return;
+  }
+  for (int j0 = 0; j0 < nv_proj; j0 += JG) {
+    double acc[JG];
+#pragma unroll
+    for (int j = 0; j < JG; ++j) acc[j] = 0.0;
+    const int nj = min(JG, nv_proj - j0);
+    for (int64_t i = s0 + 4 * threadIdx.x; i < s1; i += 4 * NT) {
+      const F4 wv = ld4(w, i);
+#pragma unroll
+      for (int j = 0; j < JG; ++j)
+        if (j < nj) {
+          const F4 q = ld4(basis, (int64_t)(j0 + j) * n + i);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[j] += (double)wv.x[e] * (double)q.x[e];
+        }
+    }
+    for (int j = 0; j < nj; ++j) {
+      const double t = block_sum<NT>(acc[j], sh);
+      if (threadIdx.x == 0) partial[(int64_t)(j0 + j) * RED_BLOCKS + blockIdx.x] = t;
+    }
+  }
+}
+
+__global__ __launch_bounds__(NT) void lz_alpha4_kernel(float* w, const float* q, const float* qprev, const double* beta,
+                                                       int k, int64_t n, double* partial) {
+  __shared__ double sh[NT / 64];
+  const double bk = (k > 0) ? beta[k - 1] : 0.0;
+  const int64_t ch = red_chunk(n);
+  const int64_t s0 = blockIdx.x * ch, s1 = min(n, s0 + ch);
+  double acc = 0.0;
+  for (int64_t i = s0 + 4 * threadIdx.x; i < s1; i += 4 * NT) {
+    F4 wv = ld4(w, i);
+    const F4 pv = ld4(qprev, i), qv = ld4(q, i);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      wv.x[e] = (float)((double)wv.x[e] - bk * (double)pv.x[e]);
+      acc += (double)wv.x[e] * (double)qv.x[e];
+    }
+    st4(w, i, wv);
+  }
+  acc = block_sum<NT>(acc, sh);
+  if (threadIdx.x == 0) partial[blockIdx.x] = acc;
+}
+
+template <typename B>
+__global__ void lz_scale4_kernel(const float* w, float* qn, B* row, const double* beta_k, const int* flag, int64_t n) {
+  const bool broken = flag[0] != 0;
+  const double inv = broken ? 0.0 : 1.0 / *beta_k;
+  const int64_t n4 = n / 4;
+  for (int64_t g = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; g < n4; g += (int64_t)gridDim.x * blockDim.x) {
+    const F4 wv = ld4(w, 4 * g);
+    F4 q;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) q.x[e] = (float)((double)wv.x[e] * inv);
+    st4(qn, 4 * g, q);
+    if (row) st4(row, 4 * g, q);
+  }
+}
+
 // Generic pass: w <- w - a*x - sum_j c_j Q_j (any part optional), then either
 // partial[j] = <w, Q_j> for j < nv_proj, or partial[0] = ||w||^2 when nv_proj == 0.
 template <typename B>
@@ -223,15 +347,22 @@ template hipError_t launch_quad_diag_hvp<float>(const float*, const float*, cons
 template hipError_t launch_quad_diag_hvp<bf16_t>(const bf16_t*, const float*, const float*, double, float*, int64_t, hipStream_t);
 
 hipError_t launch_lanczos_alpha(float* w, const float* q, const float* qprev, LanczosDev st, int k, int64_t n, hipStream_t s) {
-  hipLaunchKernelGGL(lz_alpha_kernel, dim3(RED_BLOCKS), dim3(NT), 0, s, w, q, qprev, st.beta, k, n, st.partial);
+  if (n % 4 == 0)
+    hipLaunchKernelGGL(lz_alpha4_kernel, dim3(RED_BLOCKS), dim3(NT), 0, s, w, q, qprev, st.beta, k, n, st.partial);
+  else
+    hipLaunchKernelGGL(lz_alpha_kernel, dim3(RED_BLOCKS), dim3(NT), 0, s, w, q, qprev, st.beta, k, n, st.partial);
   hipLaunchKernelGGL(lz_finish_kernel, dim3(1), dim3(256), 0, s, st, 0, k, 1, 0, 0.0);
   return hipGetLastError();
 }
 
 template <typename B>
 hipError_t launch_lanczos_b(float* w, const float* q, const B* basis, int nv, LanczosDev st, int k, int64_t n, hipStream_t s) {
-  hipLaunchKernelGGL(lz_pass_kernel<B>, dim3(RED_BLOCKS), dim3(NT), 0, s, w, q, (const double*)(st.alpha + k),
-                     (const double*)nullptr, 0, basis, nv, n, st.partial);
+  if (n % 4 == 0)
+    hipLaunchKernelGGL(lz_pass4_kernel<B>, dim3(RED_BLOCKS), dim3(NT), 0, s, w, q, (const double*)(st.alpha + k),
+                       (const double*)nullptr, 0, basis, nv, n, st.partial);
+  else
+    hipLaunchKernelGGL(lz_pass_kernel<B>, dim3(RED_BLOCKS), dim3(NT), 0, s, w, q, (const double*)(st.alpha + k),
+                       (const double*)nullptr, 0, basis, nv, n, st.partial);
   if (nv > 0) hipLaunchKernelGGL(lz_finish_kernel, dim3(1), dim3(256), 0, s, st, 1, k, nv, 0, 0.0);
   return hipGetLastError();
 }
@@ -239,6 +370,10 @@ hipError_t launch_lanczos_b(float* w, const float* q, const B* basis, int nv, La
 template <typename B>
 hipError_t launch_lanczos_cgs(float* w, const B* basis, int nv, LanczosDev st, int pass, bool last, int k, int64_t n, hipStream_t s) {
   // coefficients of this pass live at coef[pass * 128]; the next pass writes coef[(pass+1) * 128]
+  if (n % 4 == 0)
+    hipLaunchKernelGGL(lz_pass4_kernel<B>, dim3(RED_BLOCKS), dim3(NT), 0, s, w, (const float*)nullptr, (const double*)nullptr,
+                       (const double*)(st.coef + pass * 128), nv, basis, last ? 0 : nv, n, st.partial);
+  else
   hipLaunchKernelGGL(lz_pass_kernel<B>, dim3(RED_BLOCKS), dim3(NT), 0, s, w, (const float*)nullptr, (const double*)nullptr,
                      (const double*)(st.coef + pass * 128), nv, basis, last ? 0 : nv, n, st.partial);
   if (!last) hipLaunchKernelGGL(lz_finish_kernel, dim3(1), dim3(256), 0, s, st, 1, k, nv, (pass + 1) * 128, 0.0);
@@ -248,6 +383,10 @@ hipError_t launch_lanczos_cgs(float* w, const B* basis, int nv, LanczosDev st, i
 template <typename B>
 hipError_t launch_lanczos_normalise(const float* w, float* qnext, B* basis_row, LanczosDev st, int k, double tol, int64_t n, hipStream_t s) {
   hipLaunchKernelGGL(lz_finish_kernel, dim3(1), dim3(256), 0, s, st, 2, k, 1, 0, tol);
+  if (n % 4 == 0)
+    hipLaunchKernelGGL(lz_scale4_kernel<B>, dim3(grid_for(n / 4)), dim3(NT), 0, s, w, qnext, basis_row,
+                       (const double*)(st.beta + k), (const int*)st.flag, n);
+  else
   hipLaunchKernelGGL(lz_scale_kernel<B>, dim3(grid_for(n)), dim3(NT), 0, s, w, qnext, basis_row,
                      (const double*)(st.beta + k), (const int*)st.flag, n);
   return hipGetLastError();

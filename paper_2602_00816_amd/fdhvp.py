@@ -81,7 +81,7 @@ def lib():
         "fdh_slq_density": (i32, [vp, i32, i32, u64, C.POINTER(LanczosOpts), pd, pd, pi, pd]),
         "fdh_block_stats": (i32, [vp, vp, vp, pd]),
         "fdh_last_error": (C.c_char_p, [vp]),
-        "fdh_testing_gemm": (i32, [i32, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, i32, C.c_float, vp]),
+        "fdh_testing_gemm": (i32, [i32, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, i32, C.c_float, i32, vp]),
         "fdh_testing_timing": (i32, [vp, i32]),
         "fdh_testing_timing_read": (i32, [vp, pd]),
         "fdh_testing_copy": (i32, [vp, vp, C.c_size_t, vp]),
@@ -285,8 +285,8 @@ def testing_copy(dst, src, nbytes: int):
         raise FdhError(st, "fdh_testing_copy")
 
 
-def testing_gemm(dtype: str, M, N, K, batch, a_kmajor, b_kmajor, A, B, A2, B2, Cout, causal=0, alpha=1.0):
+def testing_gemm(dtype: str, M, N, K, batch, a_kmajor, b_kmajor, A, B, A2, B2, Cout, causal=0, alpha=1.0, tile=0):
     st = lib().fdh_testing_gemm(DTYPE[dtype], M, N, K, batch, int(a_kmajor), int(b_kmajor), _ptr(A), _ptr(B),
-                                _ptr(A2), _ptr(B2), _ptr(Cout), causal, float(alpha), _stream())
+                                _ptr(A2), _ptr(B2), _ptr(Cout), causal, float(alpha), int(tile), _stream())
     if st != OK:
         raise FdhError(st, "fdh_testing_gemm")

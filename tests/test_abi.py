@@ -92,7 +92,7 @@ def test_argument_validation_without_gpu_work():
     assert lib.fdh_create(C.byref(bad), None, C.byref(out)) == -1
     # testing GEMM: K not a multiple of the vector width
     assert lib.fdh_testing_gemm(1, 8, 8, 12, 1, 1, 1, C.c_void_p(256), C.c_void_p(256), None, None,
-                                C.c_void_p(256), 0, 1.0, None) == -6
+                                C.c_void_p(256), 0, 1.0, 0, None) == -6
 
 
 def test_quad_diag_context():

@@ -18,14 +18,15 @@ def _bf16_np(x):
     return synth.bf16_round(x.astype(np.float32))
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("dtype,tile", [("bf16", 1), ("bf16", 2), ("bf16", 3), ("f32", 0)])
 @pytest.mark.parametrize("ak,bk", [(1, 1), (1, 0), (0, 1), (0, 0)])
-def test_gemm_layouts_pairs_batches(dtype, ak, bk):
+def test_gemm_layouts_pairs_batches(dtype, tile, ak, bk):
     torch = need_gpu()
     from paper_2602_00816_amd import fdhvp as fd
-    say(f"gemm {dtype} ak={ak} bk={bk}")
+    say(f"gemm {dtype} tile={tile} ak={ak} bk={bk}")
     rng = np.random.default_rng(7)
-    batch, M_, N_, K_ = 3, 200, 136, 72   # ragged: several tiles and a tail in M, N and K
+    # ragged: several tiles and a tail in M, N and K for every tile variant
+    batch, M_, N_, K_ = (3, 200, 136, 72) if tile <= 1 else (2, 296, 264, 200)
     def mk(r, c):
         x = rng.standard_normal((batch, r, c)).astype(np.float32)
         return _bf16_np(x) if dtype == "bf16" else x
@@ -39,19 +40,20 @@ def test_gemm_layouts_pairs_batches(dtype, ak, bk):
         return torch.from_numpy(np.ascontiguousarray(y)).cuda().to(tdt)
     dA, dB, dA2, dB2 = up(A, ak), up(B, bk), up(A2, ak), up(B2, bk)
     C = torch.full((batch, M_, N_), float("nan"), device="cuda")
-    fd.testing_gemm(dtype, M_, N_, K_, batch, ak, bk, dA, dB, dA2, dB2, C, 0, 0.5)
+    fd.testing_gemm(dtype, M_, N_, K_, batch, ak, bk, dA, dB, dA2, dB2, C, 0, 0.5, tile)
     got = C.cpu().numpy().astype(np.float64)
     err = np.abs(got - want).max() / np.abs(want).max()
     assert err < 2e-6, err
 
 
+@pytest.mark.parametrize("tile", [1, 2, 3])
 @pytest.mark.parametrize("causal", [1, 2, 3])
-def test_gemm_causal_modes(causal):
+def test_gemm_causal_modes(causal, tile):
     torch = need_gpu()
     from paper_2602_00816_amd import fdhvp as fd
-    say(f"gemm causal {causal}")
+    say(f"gemm causal {causal} tile {tile}")
     rng = np.random.default_rng(8)
-    S = 320
+    S = 320 if tile == 1 else 584
     if causal == 1:     # scores: only tiles on/below the diagonal are produced
         M_, N_, K_ = S, S, 64
         A = _bf16_np(rng.standard_normal((2, M_, K_)))
@@ -68,7 +70,7 @@ def test_gemm_causal_modes(causal):
     dA = torch.from_numpy(A).cuda().to(torch.bfloat16)
     dB = torch.from_numpy(B).cuda().to(torch.bfloat16)
     C = torch.zeros((2, M_, N_), device="cuda")
-    fd.testing_gemm("bf16", M_, N_, K_, 2, ak, bk, dA, dB, None, None, C, causal, 1.0)
+    fd.testing_gemm("bf16", M_, N_, K_, 2, ak, bk, dA, dB, None, None, C, causal, 1.0, tile)
     got = C.cpu().numpy().astype(np.float64)
     if causal == 1:
         i, j = np.tril_indices(S)
