@@ -50,6 +50,23 @@ def alg_flops_per_hvp(w: dict) -> float:
     return 2.0 * (6.0 * n_mm * T + 3.0 * a_fwd)
 
 
+def committed_gemm_traffic(workload: str):
+    """HBM bytes per step of the GEMM launches, from the committed counter
+    summary, or None when the GEMM source changed after the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"gemm_{workload}.md")
+    src = os.path.join(ROOT, "paper_2602_00816_amd", "csrc", "gemm.hip")
+    try:
+        txt = open(path).read()
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    except OSError:
+        return None
+    vals = dict(l.split(": ", 1) for l in txt.splitlines() if l.startswith(("traffic_bytes_per_step:", "gemm_source_sha256:")))
+    if vals.get("gemm_source_sha256", "").strip() != sha:
+        return None
+    return float(vals["traffic_bytes_per_step"])
+
+
 def cpu_baseline(w: dict, budget_s: float = 20.0) -> dict:
     """The fp64 oracle's HVP on a bounded slice of the workload, scaled by FLOPs."""
     from oracle import hvp as OH
@@ -85,7 +102,10 @@ def main():
     ap.add_argument("--workload", default="llama-1.3b-bf16")
     ap.add_argument("--hvp-reps", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run one plain 1 GiB device copy first (reference for hardware byte counters)")
     args = ap.parse_args()
+    args.hvp_reps = max(1, args.hvp_reps)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
               "(the sharded design is described, not built).", file=sys.stderr)
@@ -109,6 +129,13 @@ def main():
     mod.bind(params, tok, eps)
     torch.cuda.synchronize()
     print(f"[bench] {args.workload}: P={mod.num_params} workspace={ws / 1e9:.1f} GB", file=sys.stderr, flush=True)
+    if args.copy_calibration:
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        fd.testing_copy(dst, src, 1 << 30)
+        torch.cuda.synchronize()
+        del src, dst
+        print("[bench] copy calibration: 1 GiB copied", file=sys.stderr, flush=True)
 
     for i in range(W):
         mod.hvp(params, v, eps, tok, out=hv)
@@ -169,9 +196,9 @@ def main():
         "lanczos_vec_ms_per_step": tm["lanczos"]["ms"] / K,
         "lanczos_vec_hbm_GBps": lz_gbps,
         "lanczos_vec_hbm_frac": (lz_gbps / PEAK_HBM_GBPS) if lz_gbps else None,
-        "roofline": {"bound": "mfma", "kernel": "gemm_kernel (all launches of one step)",
+        "roofline": {"bound": "mfma", "kernel": "bf16 MFMA GEMM (all launches of one step)",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
-                     "traffic": None},
+                     "traffic": committed_gemm_traffic(args.workload)},
     }
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
