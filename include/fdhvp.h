@@ -166,6 +166,16 @@ fdh_status fdh_slq_density(fdh_ctx* ctx, int32_t probes, int32_t m, uint64_t see
  * <a_b, b_b> over the parameters of layer b; a, b float32 [P] on device. */
 fdh_status fdh_block_stats(fdh_ctx* ctx, const float* a_dev, const float* b_dev, double* out_host);
 
+/* Block-diagonal hypothesis test (section 6, Exp I) on the bound operator:
+ * h = H v, and for every transformer layer b, h_b = H v^(b) where v^(b) is v
+ * with all entries outside layer b set to zero (not renormalised).  For each b,
+ * stats_host[4b + 0] = ||h^(b) - h_b^(b)||, [4b + 1] = that over ||h^(b)||,
+ * [4b + 2] = cosine of h^(b) and h_b^(b), [4b + 3] = ||h^(b)||, all restricted
+ * to the parameters of layer b.  Runs L + 1 FD-HVPs; v: float32 [P] on device.
+ * Needs fdh_bind and a workspace planned with m >= 1 (its Lanczos vectors are
+ * used as scratch).  Waits for the stream. */
+fdh_status fdh_block_diagonal(fdh_ctx* ctx, const float* v_dev, double* stats_host);
+
 /* Number of transformer layers (blocks for fdh_block_stats). */
 int32_t fdh_num_blocks(const fdh_ctx* ctx);
 

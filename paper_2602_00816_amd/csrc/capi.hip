@@ -189,6 +189,10 @@ fdh_status fdh_block_stats(fdh_ctx* ctx, const float* a_dev, const float* b_dev,
   return run(ctx, [&](fdh::Engine& e) { return e.block_stats(a_dev, b_dev, out_host); });
 }
 
+fdh_status fdh_block_diagonal(fdh_ctx* ctx, const float* v_dev, double* stats_host) {
+  return run(ctx, [&](fdh::Engine& e) { return e.block_diagonal(v_dev, stats_host); });
+}
+
 const char* fdh_last_error(const fdh_ctx* ctx) {
   if (!ctx) return "null context";
   return ctx->err.c_str();

@@ -89,6 +89,8 @@ class Engine {
   int make_tokens(int32_t* tok, int B, int S, uint64_t seed, int dist);
   int random_vector(float* out, uint64_t seed, int kind);
   int block_stats(const float* a, const float* b, double* out);
+  int block_diagonal(const float* v, double* out);
+  std::vector<int64_t> layer_ranges() const;
 
  private:
   template <typename T> int hvp_t(const T* th, const float* v, double eps, const int32_t* tok, int B, int S, float* hv);

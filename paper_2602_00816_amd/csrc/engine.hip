@@ -179,8 +179,8 @@ size_t Engine::plan(int B, int S, int m, const fdh_lanczos_opts* o, bool carve) 
     take(cdf, (size_t)V * 8);
   }
   take(gpartial, 1024 * 8);
-  take(bpart, 256 * 3 * 8);
-  take(bout, (size_t)std::max(L, 1) * 3 * 8);
+  take(bpart, 256 * 4 * 8);
+  take(bout, (size_t)std::max(L, 1) * 4 * 8);
   // Lanczos
   if (m > 0) {
     const int reorth = o ? o->reorth : FDH_REORTH_NONE;
@@ -892,9 +892,7 @@ int Engine::random_vector(float* out, uint64_t seed, int kind) {
   return FDH_OK;
 }
 
-int Engine::block_stats(const float* a, const float* b, double* out) {
-  if (quad || !a || !b || !out) { err = "bad block_stats arguments"; return FDH_ERR_INVALID_ARG; }
-  if (!ws) { err = "no workspace"; return FDH_ERR_WORKSPACE; }
+std::vector<int64_t> Engine::layer_ranges() const {
   std::vector<int64_t> ranges(2 * L);
   for (int l = 0; l < L; ++l) {
     int64_t s0 = -1, s1 = -1;
@@ -906,9 +904,48 @@ int Engine::block_stats(const float* a, const float* b, double* out) {
     ranges[2 * l] = s0;
     ranges[2 * l + 1] = s1;
   }
+  return ranges;
+}
+
+int Engine::block_stats(const float* a, const float* b, double* out) {
+  if (quad || !a || !b || !out) { err = "bad block_stats arguments"; return FDH_ERR_INVALID_ARG; }
+  if (!ws) { err = "no workspace"; return FDH_ERR_WORKSPACE; }
+  std::vector<int64_t> ranges = layer_ranges();
+  std::vector<double> h((size_t)L * 4);
   CK(launch_block_stats(a, b, ranges.data(), L, (double*)(ws + bpart.off), (double*)(ws + bout.off), stream));
-  CK(hipMemcpyAsync(out, ws + bout.off, (size_t)L * 3 * 8, hipMemcpyDeviceToHost, stream));
+  CK(hipMemcpyAsync(h.data(), ws + bout.off, (size_t)L * 4 * 8, hipMemcpyDeviceToHost, stream));
   CK(hipStreamSynchronize(stream));
+  for (int l = 0; l < L; ++l)
+    for (int c = 0; c < 3; ++c) out[3 * l + c] = h[4 * l + c];
+  return FDH_OK;
+}
+
+// Exp I (section 6): h = H v, and per layer b, h_b = H v^(b) with v masked to
+// layer b (not renormalised); statistics of h^(b) against h_b^(b).
+int Engine::block_diagonal(const float* v, double* out) {
+  if (quad || !v || !out) { err = "bad block_diagonal arguments"; return FDH_ERR_INVALID_ARG; }
+  if (!bound) { err = "call fdh_bind first"; return FDH_ERR_STATE; }
+  if (!ws || planM < 1) { err = "block_diagonal needs a workspace planned with m >= 1"; return FDH_ERR_WORKSPACE; }
+  float* h = (float*)(ws + lz_w.off);
+  float* vb = (float*)(ws + lz_q.off);
+  float* hb = (float*)(ws + lz_qp.off);
+  int rc = hvp(b_params, v, b_eps, b_tokens, b_B, b_S, h);
+  if (rc != FDH_OK) return rc;
+  std::vector<int64_t> ranges = layer_ranges();
+  std::vector<double> s4(4);
+  for (int l = 0; l < L; ++l) {
+    CK(launch_mask_range(vb, v, ranges[2 * l], ranges[2 * l + 1], P, stream));
+    rc = hvp(b_params, vb, b_eps, b_tokens, b_B, b_S, hb);
+    if (rc != FDH_OK) return rc;
+    CK(launch_block_stats(h, hb, &ranges[2 * l], 1, (double*)(ws + bpart.off), (double*)(ws + bout.off), stream));
+    CK(hipMemcpyAsync(s4.data(), ws + bout.off, 32, hipMemcpyDeviceToHost, stream));
+    CK(hipStreamSynchronize(stream));
+    const double na = std::sqrt(s4[0]), nb = std::sqrt(s4[1]), dif = std::sqrt(s4[3]);
+    out[4 * l + 0] = dif;
+    out[4 * l + 1] = na > 0 ? dif / na : 0.0;
+    out[4 * l + 2] = (na > 0 && nb > 0) ? s4[2] / (na * nb) : 0.0;
+    out[4 * l + 3] = na;
+  }
   return FDH_OK;
 }
 

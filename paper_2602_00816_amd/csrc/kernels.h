@@ -54,8 +54,11 @@ hipError_t launch_lanczos_cgs(float* w, const B* basis, int nv, LanczosDev st, i
 template <typename B>
 hipError_t launch_lanczos_normalise(const float* w, float* qnext, B* basis_row, LanczosDev st, int k, double tol, int64_t n, hipStream_t s);
 
-// Per-block sums over ranges: out[b*3 + {0,1,2}] = ||a_b||^2, ||b_b||^2, <a_b, b_b>
+// Per-block sums over host ranges [nblk][2]:
+// out[b*4 + {0,1,2,3}] = ||a_b||^2, ||b_b||^2, <a_b, b_b>, ||a_b - b_b||^2
 hipError_t launch_block_stats(const float* a, const float* b, const int64_t* ranges, int nblk, double* partial, double* out, hipStream_t s);
+// out = v on [s0, s1), 0 elsewhere (length n)
+hipError_t launch_mask_range(float* out, const float* v, int64_t s0, int64_t s1, int64_t n, hipStream_t s);
 
 // ---- lm.hip ----------------------------------------------------------------
 // All "pair" tensors are two buffers: m (mean of the two points) and d (half difference).

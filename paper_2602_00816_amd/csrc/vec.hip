@@ -274,31 +274,40 @@ __global__ void lz_scale_kernel(const float* w, float* qn, B* row, const double*
   }
 }
 
+// sums over [s0, s1): ||a||^2, ||b||^2, <a, b>, ||a - b||^2
 __global__ void range_dots_kernel(const float* a, const float* b, int64_t s0, int64_t s1, double* partial) {
   __shared__ double sh[NT / 64];
-  double aa = 0.0, bb = 0.0, ab = 0.0;
+  double aa = 0.0, bb = 0.0, ab = 0.0, dd = 0.0;
   for (int64_t i = s0 + blockIdx.x * (int64_t)NT + threadIdx.x; i < s1; i += (int64_t)gridDim.x * NT) {
     const double x = a[i], y = b[i];
     aa += x * x;
     bb += y * y;
     ab += x * y;
+    dd += (x - y) * (x - y);
   }
   aa = block_sum<NT>(aa, sh);
   bb = block_sum<NT>(bb, sh);
   ab = block_sum<NT>(ab, sh);
+  dd = block_sum<NT>(dd, sh);
   if (threadIdx.x == 0) {
-    partial[blockIdx.x * 3 + 0] = aa;
-    partial[blockIdx.x * 3 + 1] = bb;
-    partial[blockIdx.x * 3 + 2] = ab;
+    partial[blockIdx.x * 4 + 0] = aa;
+    partial[blockIdx.x * 4 + 1] = bb;
+    partial[blockIdx.x * 4 + 2] = ab;
+    partial[blockIdx.x * 4 + 3] = dd;
   }
 }
 
 __global__ void range_dots_finish(const double* partial, int nb, double* out) {
   const int c = threadIdx.x;
-  if (c >= 3) return;
+  if (c >= 4) return;
   double s = 0.0;
-  for (int b = 0; b < nb; ++b) s += partial[b * 3 + c];
+  for (int b = 0; b < nb; ++b) s += partial[b * 4 + c];
   out[c] = s;
+}
+
+__global__ void mask_range_kernel(float* out, const float* v, int64_t s0, int64_t s1, int64_t n) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    out[i] = (i >= s0 && i < s1) ? v[i] : 0.f;
 }
 
 }  // namespace
@@ -400,11 +409,16 @@ INST_LZ(float)
 INST_LZ(bf16_t)
 
 hipError_t launch_block_stats(const float* a, const float* b, const int64_t* ranges, int nblk, double* partial, double* out, hipStream_t s) {
-  // ranges: host array [nblk][2]; partial: device [256 * 3]; out: device [nblk * 3]
+  // ranges: host array [nblk][2]; partial: device [256 * 4]; out: device [nblk * 4]
   for (int i = 0; i < nblk; ++i) {
     hipLaunchKernelGGL(range_dots_kernel, dim3(256), dim3(NT), 0, s, a, b, ranges[2 * i], ranges[2 * i + 1], partial);
-    hipLaunchKernelGGL(range_dots_finish, dim3(1), dim3(64), 0, s, (const double*)partial, 256, out + 3 * i);
+    hipLaunchKernelGGL(range_dots_finish, dim3(1), dim3(64), 0, s, (const double*)partial, 256, out + 4 * i);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_mask_range(float* out, const float* v, int64_t s0, int64_t s1, int64_t n, hipStream_t s) {
+  hipLaunchKernelGGL(mask_range_kernel, dim3(grid_for(n)), dim3(NT), 0, s, out, v, s0, s1, n);
   return hipGetLastError();
 }
 

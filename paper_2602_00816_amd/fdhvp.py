@@ -80,6 +80,7 @@ def lib():
         "fdh_lanczos": (i32, [vp, i32, u64, C.POINTER(LanczosOpts), pd, pd, pi]),
         "fdh_slq_density": (i32, [vp, i32, i32, u64, C.POINTER(LanczosOpts), pd, pd, pi, pd]),
         "fdh_block_stats": (i32, [vp, vp, vp, pd]),
+        "fdh_block_diagonal": (i32, [vp, vp, pd]),
         "fdh_last_error": (C.c_char_p, [vp]),
         "fdh_testing_gemm": (i32, [i32, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, i32, C.c_float, i32, vp]),
         "fdh_testing_timing": (i32, [vp, i32]),
@@ -271,6 +272,13 @@ class Model:
         cats = ["gemm", "lanczos", "c2", "c3"]
         return {c: dict(launches=out[4 * i], ms=out[4 * i + 1], flops=out[4 * i + 2], bytes=out[4 * i + 3])
                 for i, c in enumerate(cats)}
+
+    def block_diagonal(self, v):
+        """Exp I statistics per layer: columns abs diff, relative error, cosine, ||(Hv)^(b)||."""
+        out = np.zeros((max(self.num_blocks, 0), 4))
+        self._check(self._L.fdh_block_diagonal(self._h, _ptr(v), out.ctypes.data_as(C.POINTER(C.c_double))),
+                    "fdh_block_diagonal")
+        return out
 
     def block_stats(self, a, b):
         out = np.zeros((max(self.num_blocks, 0), 3))
