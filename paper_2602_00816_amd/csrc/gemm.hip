@@ -15,6 +15,8 @@
 // prefetched into registers one K tile ahead.
 #include "gemm.h"
 
+#include <type_traits>
+
 namespace fdh {
 
 namespace {
@@ -404,6 +406,224 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_big(GemmArgs a) {
       store_block<bf16_t>(a, acc[i][j], coff, m0 + wm * (BM_ / WM) + i * 32, n0 + wn * (BN_ / WN) + j * 32, lane);
 }
 
+// ===========================================================================
+// bf16 kernel fed by direct global->LDS loads (global_load_lds_dwordx4).
+//
+// A 4-stage LDS ring of K = 32 slices: the loads for slice t + 3 are issued
+// right after the barrier that opens slice t, so three slices (~3 us of MFMA
+// work) cover the memory latency, and no VGPR holds prefetched data.  Each
+// load instruction writes 64 lanes x 16 bytes contiguously in LDS (lane l at
+// +16 l), so the global address of each lane is chosen to match the swizzled
+// LDS position it lands in.
+//   K-major tile (rows x 32 k): 64-byte rows, 16-byte chunk c of row r stored
+//     at chunk c ^ ((r >> 1) & 3); MFMA fragments are single 16-byte reads.
+//   MN-major tile (32 k x rows): rows of `rows` elements along m/n, chunk c of
+//     k-row k stored at c ^ (2 (k & 7)); MFMA fragments are two transposing
+//     reads (ds_read_b64_tr_b16), each giving a lane 4 consecutive k of its
+//     m/n column.
+// Every layout is free of LDS bank conflicts for its reads and writes.
+// Requires K, kmin, kmax multiples of 32; rows past M/N are clamped to valid
+// memory (they only feed discarded outputs).
+// ===========================================================================
+constexpr int KT3 = 32, NS3 = 4;
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16_t;
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+__device__ inline int kswz(int row, int c) { return row * KT3 + ((c ^ ((row >> 1) & 3)) << 3); }        // elements
+template <int R>
+__device__ inline int mswz(int k, int m) { return k * R + ((((m >> 3) ^ ((k & 7) << 1))) << 3) + (m & 7); }  // elements
+
+// issue this wave's DMA instructions for one operand tile
+template <int R, bool KMAJ, int NW>
+__device__ inline void dma_tile(bf16_t* lds_tile, const bf16_t* base, int64_t s_row, int64_t s_k, int rows, int row0,
+                                int k0, int wave, int lane) {
+  constexpr int NI = R * KT3 * 2 / 1024;  // 1 KB instructions per tile
+#pragma clang loop unroll(full)
+  for (int u = 0; u < NI / NW; ++u) {
+    const int q = wave + u * NW;
+    const bf16_t* g;
+    if (KMAJ) {
+      const int r = q * 16 + (lane >> 2);                       // 16 rows of 64 B per instruction
+      const int c = (lane & 3) ^ ((r >> 1) & 3);
+      const int gr = min(row0 + r, rows - 1);
+      g = base + (int64_t)gr * s_row + k0 + 8 * c;
+    } else {
+      constexpr int RPI = 1024 / (R * 2);                       // k-rows per instruction
+      constexpr int CPR = R / 8;                                // chunks per k-row
+      const int k = q * RPI + lane / CPR;
+      const int c = (lane % CPR) ^ ((k & 7) << 1);
+      const int gm = min(row0 + 8 * c, rows - 8);
+      g = base + (int64_t)(k0 + k) * s_k + gm;
+    }
+    // Issued as inline assembly so that the compiler does not track it: its
+    // own tracking cannot tell the ring stages apart and would wait for every
+    // outstanding load before each LDS read.  Completion is waited for
+    // explicitly (wait_vm) before the barrier that publishes a stage.
+    const uint32_t ldsaddr = (uint32_t)(uintptr_t)(lds_void_t*)(lds_tile + q * 512);
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, off"
+        :
+        : "s"(__builtin_amdgcn_readfirstlane(ldsaddr)), "v"(g)
+        : "memory", "m0");
+  }
+}
+
+template <int R, bool KMAJ>
+__device__ inline bf16x8_t frag(const bf16_t* t, int r0, int kk, int lane) {
+  if (KMAJ) {
+    return *reinterpret_cast<const bf16x8_t*>(t + kswz(r0 + (lane & 31), (kk >> 3) + (lane >> 5)));
+  } else {
+    const int g = lane >> 4, r = lane & 15;
+    const int mb = r0 + 16 * (g & 1) + 4 * (r & 3);
+    const int kb = kk + 8 * (g >> 1) + (r >> 2);
+    const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(t + mswz<R>(kb, mb)));
+    const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(t + mswz<R>(kb + 4, mb)));
+    typedef short v8i16 __attribute__((ext_vector_type(8)));
+    const v8i16 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return __builtin_bit_cast(bf16x8_t, v);
+  }
+}
+
+template <int N>
+__device__ inline void wait_vm() {
+  // s_waitcnt with vmcnt = N (bits 3:0 and 15:14), expcnt and lgkmcnt left at their maxima
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+template <int BN_, bool AK, bool BKM>
+__global__ __launch_bounds__(64 * 2 * (BN_ / 64)) void gemm_bf16_dma(GemmArgs a) {
+  constexpr int BM_ = 256, WM = 2, WN = BN_ / 64, NW = WM * WN;
+  constexpr int IM = 4, JN = 2;
+  constexpr int ASZ = BM_ * KT3, BSZ = BN_ * KT3;              // elements per stage
+  constexpr int PERT = (BM_ + BN_) * KT3 * 2 / 1024 / NW;      // DMA instructions per wave per tile
+  // one LDS object per stage: with compile-time stage indices the compiler
+  // waits, before an LDS read, only for the DMA into that same stage
+  __shared__ __attribute__((aligned(1024))) bf16_t st0[ASZ + BSZ];
+  __shared__ __attribute__((aligned(1024))) bf16_t st1[ASZ + BSZ];
+  __shared__ __attribute__((aligned(1024))) bf16_t st2[ASZ + BSZ];
+  __shared__ __attribute__((aligned(1024))) bf16_t st3[ASZ + BSZ];
+
+  const int gx = gridDim.x, gy = gridDim.y;
+  const int nb = gx * gy * gridDim.z;
+  int lin = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
+  const int per = nb / 8;
+  if (lin < per * 8) lin = (lin % 8) * per + lin / 8;
+  const int tiles = gx * gy;
+  const int z = lin / tiles;
+  const int tl = lin % tiles;
+  constexpr int GM = 8;
+  const int gsize = GM * gx;
+  const int first_m = (tl / gsize) * GM;
+  const int gm_rows = min(gy - first_m, GM);
+  const int tm = first_m + (tl % gsize) % gm_rows;
+  const int tn = (tl % gsize) / gm_rows;
+  const int m0 = tm * BM_, n0 = tn * BN_;
+  if (a.causal == CAUSAL_SKIP_UPPER && n0 > m0 + BM_ - 1) return;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WN, wn = wave % WN;
+
+  int kmin = 0, kmax = a.K;
+  if (a.causal == CAUSAL_K_LE_M) kmax = min(a.K, m0 + BM_);
+  if (a.causal == CAUSAL_K_GE_M) kmin = (min(m0, a.K) / KT3) * KT3;
+  const int nkt = (kmax > kmin) ? (kmax - kmin) / KT3 : 0;
+  const int total = nkt * a.npairs;
+
+  const bf16_t* pa[2];
+  const bf16_t* pb[2];
+#pragma clang loop unroll(full)
+  for (int p = 0; p < 2; ++p) {
+    const int pp = p < a.npairs ? p : 0;
+    pa[p] = reinterpret_cast<const bf16_t*>(a.A[pp].ptr) +
+            batch_off(z, a.inner_count, a.A[pp].s_outer, a.A[pp].s_inner, a.A[pp].inner_div);
+    pb[p] = reinterpret_cast<const bf16_t*>(a.B[pp].ptr) +
+            batch_off(z, a.inner_count, a.B[pp].s_outer, a.B[pp].s_inner, a.B[pp].inner_div);
+  }
+
+  auto stage = [&](auto s) -> bf16_t* {
+    constexpr int S = decltype(s)::value;
+    if constexpr (S == 0) return st0;
+    else if constexpr (S == 1) return st1;
+    else if constexpr (S == 2) return st2;
+    else return st3;
+  };
+  auto issue = [&](int t, bf16_t* st) {
+    const int p = t >= nkt ? 1 : 0;
+    const int k0 = kmin + (t - p * nkt) * KT3;
+    dma_tile<BM_, AK, NW>(st, p ? pa[1] : pa[0], a.A[p].s_row, a.A[p].s_k, a.M, m0, k0, wave, lane);
+    dma_tile<BN_, BKM, NW>(st + ASZ, p ? pb[1] : pb[0], a.B[p].s_row, a.B[p].s_k, a.N, n0, k0, wave, lane);
+  };
+
+  f32x16_t acc[IM][JN];
+#pragma clang loop unroll(full)
+  for (int i = 0; i < IM; ++i)
+#pragma clang loop unroll(full)
+    for (int j = 0; j < JN; ++j)
+#pragma clang loop unroll(full)
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  // one K slice on stage S (compile time): wait for this wave's loads of the
+  // slice (later slices stay in flight), barrier, refill the stage freed by
+  // the previous slice, then 2 x IM x JN MFMAs
+  auto step = [&](auto s, int t) {
+    constexpr int S = decltype(s)::value;
+    const int ahead = min(NS3 - 2, total - 1 - t);
+    if (ahead >= 2) wait_vm<2 * PERT>();
+    else if (ahead == 1) wait_vm<PERT>();
+    else wait_vm<0>();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");  // keep the stage's LDS reads after the barrier
+    if (t + NS3 - 1 < total) issue(t + NS3 - 1, stage(std::integral_constant<int, (S + NS3 - 1) % NS3>{}));
+    const bf16_t* cA = stage(s);
+    const bf16_t* cB = cA + ASZ;
+#pragma clang loop unroll(full)
+    for (int kk = 0; kk < KT3; kk += 16) {
+      bf16x8_t af[IM], bfr[JN];
+#pragma clang loop unroll(full)
+      for (int i = 0; i < IM; ++i) af[i] = frag<BM_, AK>(cA, wm * 128 + i * 32, kk, lane);
+#pragma clang loop unroll(full)
+      for (int j = 0; j < JN; ++j) bfr[j] = frag<BN_, BKM>(cB, wn * 64 + j * 32, kk, lane);
+#pragma clang loop unroll(full)
+      for (int i = 0; i < IM; ++i)
+#pragma clang loop unroll(full)
+        for (int j = 0; j < JN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    }
+  };
+
+  if (total > 0) issue(0, st0);
+  if (total > 1) issue(1, st1);
+  if (total > 2) issue(2, st2);
+  for (int t0 = 0; t0 < total; t0 += NS3) {
+    step(std::integral_constant<int, 0>{}, t0);
+    if (t0 + 1 < total) step(std::integral_constant<int, 1>{}, t0 + 1);
+    if (t0 + 2 < total) step(std::integral_constant<int, 2>{}, t0 + 2);
+    if (t0 + 3 < total) step(std::integral_constant<int, 3>{}, t0 + 3);
+  }
+
+  const int64_t coff = batch_off(z, a.inner_count, a.c_outer, a.c_inner, a.c_div);
+#pragma clang loop unroll(full)
+  for (int i = 0; i < IM; ++i)
+#pragma clang loop unroll(full)
+    for (int j = 0; j < JN; ++j)
+      store_block<bf16_t>(a, acc[i][j], coff, m0 + wm * 128 + i * 32, n0 + wn * 64 + j * 32, lane);
+}
+
+template <int BN_>
+void launch_dma(const GemmArgs& a, hipStream_t stream) {
+  dim3 grid(ceil_div(a.N, BN_), ceil_div(a.M, 256), a.nbatch);
+  dim3 block(64 * 2 * (BN_ / 64));
+  const bool ak = a.A[0].s_k == 1, bk = a.B[0].s_k == 1;
+  if (ak && bk) hipLaunchKernelGGL((gemm_bf16_dma<BN_, true, true>), grid, block, 0, stream, a);
+  else if (ak && !bk) hipLaunchKernelGGL((gemm_bf16_dma<BN_, true, false>), grid, block, 0, stream, a);
+  else if (!ak && bk) hipLaunchKernelGGL((gemm_bf16_dma<BN_, false, true>), grid, block, 0, stream, a);
+  else hipLaunchKernelGGL((gemm_bf16_dma<BN_, false, false>), grid, block, 0, stream, a);
+}
+
 template <int BM_, int BN_, int WM, int WN>
 void launch_big(const GemmArgs& a, hipStream_t stream) {
   dim3 grid(ceil_div(a.N, BN_), ceil_div(a.M, BM_), a.nbatch);
@@ -448,7 +668,8 @@ const char* gemm_check(const GemmArgs& a) {
     }
   }
   if (a.causal == CAUSAL_SKIP_UPPER && a.M > a.N) return "gemm: causal skip needs M <= N";
-  if (a.tile < 0 || a.tile > 3) return "gemm: bad tile";
+  if (a.tile < 0 || a.tile > 5) return "gemm: bad tile";
+  if (a.tile >= 4 && (a.K % 32 || a.M < 8 || a.N < 8)) return "gemm: the DMA kernel needs K % 32 == 0";
   return nullptr;
 }
 
@@ -460,11 +681,14 @@ hipError_t gemm(const GemmArgs& a, hipStream_t stream) {
     if (tile == 0 && a.M >= 256) {
       const int64_t t256 = (int64_t)ceil_div(a.M, 256) * ceil_div(a.N, 256) * a.nbatch;
       const int64_t t128 = (int64_t)ceil_div(a.M, 256) * ceil_div(a.N, 128) * a.nbatch;
-      if (a.N > 128 && t256 >= 192) tile = 2;
-      else if (t128 >= 64) tile = 3;
+      const bool dma = a.K % KT3 == 0;
+      if (a.N > 128 && t256 >= 192) tile = dma ? 4 : 2;
+      else if (t128 >= 64) tile = dma ? 5 : 3;
     }
     if (tile == 2) { launch_big<256, 256, 2, 4>(a, stream); return hipGetLastError(); }
     if (tile == 3) { launch_big<256, 128, 2, 2>(a, stream); return hipGetLastError(); }
+    if (tile == 4) { launch_dma<256>(a, stream); return hipGetLastError(); }
+    if (tile == 5) { launch_dma<128>(a, stream); return hipGetLastError(); }
   }
   dim3 grid(ceil_div(a.N, BN), ceil_div(a.M, BM), a.nbatch);
   const bool ak = a.A[0].s_k == 1, bk = a.B[0].s_k == 1;

@@ -197,6 +197,38 @@ __global__ void rope_table_kernel(double* cs, int S, int dh, double base) {
   }
 }
 
+// Vectorised form: grid.y = token, each thread 4 consecutive columns (all
+// column offsets, and dh/2, are multiples of 4).  Same arithmetic as below.
+template <typename T>
+__global__ void qkv_post4_kernel(T* out, const float* in, int S, int ncols, int qk_cols, int dh, const double* cs,
+                                 bool rope, bool inverse) {
+  const int t = blockIdx.y;
+  const int c = 4 * (blockIdx.x * blockDim.x + threadIdx.x);
+  if (c >= ncols) return;
+  const int64_t o = (int64_t)t * ncols + c;
+  const float4 x4 = *reinterpret_cast<const float4*>(in + o);
+  float x[4] = {x4.x, x4.y, x4.z, x4.w};
+  float r[4] = {x[0], x[1], x[2], x[3]};
+  if (rope && c < qk_cols) {
+    const int half = dh / 2;
+    const int hi = c % dh;
+    const bool lo_half = hi < half;
+    const float4 y4 = *reinterpret_cast<const float4*>(in + o + (lo_half ? half : -half));
+    const float y[4] = {y4.x, y4.y, y4.z, y4.w};
+    const double sgn = inverse ? -1.0 : 1.0;
+    const double* row = cs + (int64_t)(t % S) * dh;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int f = (hi + e) % half;
+      const double co = row[2 * f], si = row[2 * f + 1];
+      r[e] = lo_half ? (float)((double)x[e] * co - sgn * (double)y[e] * si)
+                     : (float)((double)x[e] * co + sgn * (double)y[e] * si);
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) stf(out, o + e, r[e]);
+}
+
 // forward: q/k columns rotated (rotate-half), v columns copied; one channel per call
 template <typename T>
 __global__ void qkv_post_kernel(T* out, const float* in, int T_, int S, int ncols, int qk_cols, int dh,
@@ -300,11 +332,13 @@ __global__ __launch_bounds__(NT) void attn_dsoftmax_kernel(PairT<T> dS, const T*
 // matrix has i+1 live entries; entries i < j < roundup(i+1, 256) are written
 // as zeros, because the MFMA tiles that contract over a row read exactly up
 // to that boundary; entries beyond it are never read and not written.
-// The softmax keeps, per live entry, a = exp(Sm - c) cosh(Sd) and
-// b = exp(Sm - c) sinh(Sd) (both with full relative precision, computed from
-// the two fp64 exponentials), so that e+- = a +- b and
+// The softmax at both points uses exp(Sm - c +- Sd) = exp(Sm - c) (cosh Sd +- sinh Sd):
+// per live entry a = exp(Sm - c) cosh(Sd) and b = exp(Sm - c) sinh(Sd), both
+// with full relative precision however small Sd is, so that e+- = a +- b and
 //   P.m = (a Zm - b Zd) / (Z+ Z-),  P.d = (b Zm - a Zd) / (Z+ Z-),
-// with Zm, Zd the mean and half difference of Z+ = sum e+, Z- = sum e-.
+// with Zm = sum a and Zd = sum b (fp64 sums) the mean and half difference of
+// Z+- = sum e+-.  exp(Sm - c) is formed in fp32: its rounding is common to the
+// two points.
 __device__ inline int zero_end(int i, int S) { return min(S, ((i + 256) / 256) * 256); }
 
 template <typename T, int PER>
@@ -316,30 +350,33 @@ __global__ __launch_bounds__(256) void attn_softmax_w(PairT<T> P, const float* S
   const int64_t base = r * (int64_t)S;
   const int len = i + 1;
   float av[PER], bv[PER];
-  double mx = -1e300;
+  float mx = -3.0e38f;
 #pragma unroll
   for (int e = 0; e < PER; ++e) {
     const int j = lane + 64 * e;
-    if (j < len) mx = fmax(mx, (double)Sm[base + j]);
+    av[e] = (j < len) ? Sm[base + j] : -3.0e38f;
+    bv[e] = (j < len) ? Sd[base + j] : 0.f;
+    mx = fmaxf(mx, av[e]);
   }
   mx = wave_max(mx);
-  double zp = 0.0, zm = 0.0;
+  double Zm = 0.0, Zd = 0.0;
 #pragma unroll
   for (int e = 0; e < PER; ++e) {
     const int j = lane + 64 * e;
-    av[e] = bv[e] = 0.f;
     if (j < len) {
-      const double a = (double)Sm[base + j] - mx, b = (double)Sd[base + j];
-      const double ep = exp(a + b), em = exp(a - b);
-      zp += ep;
-      zm += em;
-      av[e] = (float)(0.5 * (ep + em));
-      bv[e] = (float)(0.5 * (ep - em));
+      const float ea = expf(av[e] - mx);
+      const float b = bv[e];
+      av[e] = ea * coshf(b);
+      bv[e] = ea * sinhf(b);
+      Zm += (double)av[e];
+      Zd += (double)bv[e];
+    } else {
+      av[e] = bv[e] = 0.f;
     }
   }
-  zp = wave_sum(zp);
-  zm = wave_sum(zm);
-  const double Zm = 0.5 * (zp + zm), Zd = 0.5 * (zp - zm), inv = 1.0 / (zp * zm);
+  Zm = wave_sum(Zm);
+  Zd = wave_sum(Zd);
+  const double inv = 1.0 / ((Zm + Zd) * (Zm - Zd));
   const int ze = zero_end(i, S);
 #pragma unroll
   for (int e = 0; e < PER; ++e) {
@@ -609,8 +646,10 @@ hipError_t launch_qkv_post(PairT<T> out, const float* qm, const float* qd, int T
                            const double* cs, bool rope, hipStream_t s) {
   const int ncols = (Hq + 2 * Hk) * dh, qk = (Hq + Hk) * dh;
   const unsigned g = grid_for((int64_t)T_ * ncols);
-  hipLaunchKernelGGL(qkv_post_kernel<T>, dim3(g), dim3(NT), 0, s, out.m, qm, T_, S, ncols, qk, dh, cs, rope, false);
-  hipLaunchKernelGGL(qkv_post_kernel<T>, dim3(g), dim3(NT), 0, s, out.d, qd, T_, S, ncols, qk, dh, cs, rope, false);
+  (void)g;
+  const dim3 g4(ceil_div(ncols / 4, NT), T_);
+  hipLaunchKernelGGL(qkv_post4_kernel<T>, g4, dim3(NT), 0, s, out.m, qm, S, ncols, qk, dh, cs, rope, false);
+  hipLaunchKernelGGL(qkv_post4_kernel<T>, g4, dim3(NT), 0, s, out.d, qd, S, ncols, qk, dh, cs, rope, false);
   return hipGetLastError();
 }
 
@@ -619,8 +658,10 @@ hipError_t launch_qkv_bwd_post(PairT<T> out, float* gm, float* gd, int T_, int S
                                const double* cs, bool rope, hipStream_t s) {
   const int ncols = (Hq + 2 * Hk) * dh, qk = (Hq + Hk) * dh;
   const unsigned g = grid_for((int64_t)T_ * ncols);
-  hipLaunchKernelGGL(qkv_post_kernel<T>, dim3(g), dim3(NT), 0, s, out.m, (const float*)gm, T_, S, ncols, qk, dh, cs, rope, true);
-  hipLaunchKernelGGL(qkv_post_kernel<T>, dim3(g), dim3(NT), 0, s, out.d, (const float*)gd, T_, S, ncols, qk, dh, cs, rope, true);
+  (void)g;
+  const dim3 g4(ceil_div(ncols / 4, NT), T_);
+  hipLaunchKernelGGL(qkv_post4_kernel<T>, g4, dim3(NT), 0, s, out.m, (const float*)gm, S, ncols, qk, dh, cs, rope, true);
+  hipLaunchKernelGGL(qkv_post4_kernel<T>, g4, dim3(NT), 0, s, out.d, (const float*)gd, S, ncols, qk, dh, cs, rope, true);
   return hipGetLastError();
 }
 
