@@ -416,12 +416,14 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_big(GemmArgs a) {
 // +16 l), so the global address of each lane is chosen to match the swizzled
 // LDS position it lands in.
 //   K-major tile (rows x 32 k): 64-byte rows, 16-byte chunk c of row r stored
-//     at chunk c ^ ((r >> 1) & 3); MFMA fragments are single 16-byte reads.
+//     at chunk c ^ ((r >> 2) & 3); MFMA fragments are single 16-byte reads.
 //   MN-major tile (32 k x rows): rows of `rows` elements along m/n, chunk c of
-//     k-row k stored at c ^ (2 (k & 7)); MFMA fragments are two transposing
+//     k-row k stored at c ^ (4 (k & 3)); MFMA fragments are two transposing
 //     reads (ds_read_b64_tr_b16), each giving a lane 4 consecutive k of its
 //     m/n column.
-// Every layout is free of LDS bank conflicts for its reads and writes.
+// The LDS has 64 banks of 4 bytes and serves a 16-byte read for 16 lanes, an
+// 8-byte read for 32 lanes per clock; in both layouts those lanes hit 64
+// distinct banks, and the DMA writes are contiguous.
 // Requires K, kmin, kmax multiples of 32; rows past M/N are clamped to valid
 // memory (they only feed discarded outputs).
 // ===========================================================================
@@ -430,9 +432,9 @@ typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16_t;
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-__device__ inline int kswz(int row, int c) { return row * KT3 + ((c ^ ((row >> 1) & 3)) << 3); }        // elements
+__device__ inline int kswz(int row, int c) { return row * KT3 + ((c ^ ((row >> 2) & 3)) << 3); }        // elements
 template <int R>
-__device__ inline int mswz(int k, int m) { return k * R + ((((m >> 3) ^ ((k & 7) << 1))) << 3) + (m & 7); }  // elements
+__device__ inline int mswz(int k, int m) { return k * R + ((((m >> 3) ^ (4 * (k & 3)))) << 3) + (m & 7); }  // elements
 
 // issue this wave's DMA instructions for one operand tile
 template <int R, bool KMAJ, int NW>
@@ -445,14 +447,14 @@ __device__ inline void dma_tile(bf16_t* lds_tile, const bf16_t* base, int64_t s_
     const bf16_t* g;
     if (KMAJ) {
       const int r = q * 16 + (lane >> 2);                       // 16 rows of 64 B per instruction
-      const int c = (lane & 3) ^ ((r >> 1) & 3);
+      const int c = (lane & 3) ^ ((r >> 2) & 3);
       const int gr = min(row0 + r, rows - 1);
       g = base + (int64_t)gr * s_row + k0 + 8 * c;
     } else {
       constexpr int RPI = 1024 / (R * 2);                       // k-rows per instruction
       constexpr int CPR = R / 8;                                // chunks per k-row
       const int k = q * RPI + lane / CPR;
-      const int c = (lane % CPR) ^ ((k & 7) << 1);
+      const int c = (lane % CPR) ^ (4 * (k & 3));
       const int gm = min(row0 + 8 * c, rows - 8);
       g = base + (int64_t)(k0 + k) * s_k + gm;
     }
@@ -493,10 +495,11 @@ __device__ inline void wait_vm() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-template <int BN_, bool AK, bool BKM>
-__global__ __launch_bounds__(64 * 2 * (BN_ / 64)) void gemm_bf16_dma(GemmArgs a) {
-  constexpr int BM_ = 256, WM = 2, WN = BN_ / 64, NW = WM * WN;
-  constexpr int IM = 4, JN = 2;
+template <int BN_, int WN, bool AK, bool BKM>
+__global__ __launch_bounds__(64 * 2 * WN) void gemm_bf16_dma(GemmArgs a) {
+  constexpr int BM_ = 256, WM = 2, NW = WM * WN;
+  constexpr int WTN = BN_ / WN;                 // wavefront tile: 128 x WTN
+  constexpr int IM = 4, JN = WTN / 32;
   constexpr int ASZ = BM_ * KT3, BSZ = BN_ * KT3;              // elements per stage
   constexpr int PERT = (BM_ + BN_) * KT3 * 2 / 1024 / NW;      // DMA instructions per wave per tile
   // one LDS object per stage: with compile-time stage indices the compiler
@@ -586,7 +589,7 @@ __global__ __launch_bounds__(64 * 2 * (BN_ / 64)) void gemm_bf16_dma(GemmArgs a)
 #pragma clang loop unroll(full)
       for (int i = 0; i < IM; ++i) af[i] = frag<BM_, AK>(cA, wm * 128 + i * 32, kk, lane);
 #pragma clang loop unroll(full)
-      for (int j = 0; j < JN; ++j) bfr[j] = frag<BN_, BKM>(cB, wn * 64 + j * 32, kk, lane);
+      for (int j = 0; j < JN; ++j) bfr[j] = frag<BN_, BKM>(cB, wn * WTN + j * 32, kk, lane);
 #pragma clang loop unroll(full)
       for (int i = 0; i < IM; ++i)
 #pragma clang loop unroll(full)
@@ -610,18 +613,412 @@ __global__ __launch_bounds__(64 * 2 * (BN_ / 64)) void gemm_bf16_dma(GemmArgs a)
   for (int i = 0; i < IM; ++i)
 #pragma clang loop unroll(full)
     for (int j = 0; j < JN; ++j)
-      store_block<bf16_t>(a, acc[i][j], coff, m0 + wm * 128 + i * 32, n0 + wn * 64 + j * 32, lane);
+      store_block<bf16_t>(a, acc[i][j], coff, m0 + wm * 128 + i * 32, n0 + wn * WTN + j * 32, lane);
 }
 
-template <int BN_>
+// ===========================================================================
+// bf16 GEMM, 256 x 256 block tile, four wavefronts of 128 x 128 each (one per
+// SIMD), on the same DMA-fed LDS ring and LDS layouts as gemm_bf16_dma.  With
+// 128 x 128 per wavefront every fragment read from LDS feeds four MFMAs
+// instead of two or three, which halves LDS read traffic per FLOP.  With a
+// single wavefront per SIMD nothing else hides LDS latency, so each wavefront
+// keeps two fragment register sets and its instruction order is fixed by
+// scheduling barriers: a K slice is two half slices of 16 k; while the 16
+// MFMAs of one half run, the fragments of the next half are read and, after
+// the ring barrier, the refill of the freed stage is issued.  Refills past the
+// last slice reload the last slice into the free stage (never read), so every
+// slice issues the same number of loads and the vmcnt waits are constants.
+// ===========================================================================
+template <bool AK, bool BKM>
+__global__ __launch_bounds__(256) void gemm_bf16_w4(GemmArgs a) {
+  constexpr int BM_ = 256, BN_ = 256, NW = 4, IM = 4, JN = 4;
+  constexpr int ASZ = BM_ * KT3, BSZ = BN_ * KT3;
+  constexpr int NU = BM_ * KT3 * 2 / 1024 / NW;   // 1 KB loads per operand per wavefront per slice
+  constexpr int PERT = 2 * NU;                    // loads per wavefront per slice
+  __shared__ __attribute__((aligned(1024))) bf16_t st0[ASZ + BSZ];
+  __shared__ __attribute__((aligned(1024))) bf16_t st1[ASZ + BSZ];
+  __shared__ __attribute__((aligned(1024))) bf16_t st2[ASZ + BSZ];
+  __shared__ __attribute__((aligned(1024))) bf16_t st3[ASZ + BSZ];
+
+  const int gx = gridDim.x, gy = gridDim.y;
+  const int nb = gx * gy * gridDim.z;
+  int lin = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
+  const int per = nb / 8;
+  if (lin < per * 8) lin = (lin % 8) * per + lin / 8;
+  const int tiles = gx * gy;
+  const int z = lin / tiles;
+  const int tl = lin % tiles;
+  constexpr int GM = 8;
+  const int gsize = GM * gx;
+  const int first_m = (tl / gsize) * GM;
+  const int gm_rows = min(gy - first_m, GM);
+  const int tm = first_m + (tl % gsize) % gm_rows;
+  const int tn = (tl % gsize) / gm_rows;
+  const int m0 = tm * BM_, n0 = tn * BN_;
+  if (a.causal == CAUSAL_SKIP_UPPER && n0 > m0 + BM_ - 1) return;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+
+  int kmin = 0, kmax = a.K;
+  if (a.causal == CAUSAL_K_LE_M) kmax = min(a.K, m0 + BM_);
+  if (a.causal == CAUSAL_K_GE_M) kmin = (min(m0, a.K) / KT3) * KT3;
+  const int nkt = (kmax > kmin) ? (kmax - kmin) / KT3 : 0;
+  const int total = nkt * a.npairs;
+
+  // per-lane source offsets (elements) of this wavefront's loads, both pairs
+  const bf16_t* baseA[2];
+  const bf16_t* baseB[2];
+  int64_t offA[2][NU], offB[2][NU], skA[2], skB[2];
+#pragma clang loop unroll(full)
+  for (int p = 0; p < 2; ++p) {
+    const int pp = p < a.npairs ? p : 0;
+    const GemmOperand& A = a.A[pp];
+    const GemmOperand& B = a.B[pp];
+    baseA[p] = reinterpret_cast<const bf16_t*>(A.ptr) + batch_off(z, a.inner_count, A.s_outer, A.s_inner, A.inner_div);
+    baseB[p] = reinterpret_cast<const bf16_t*>(B.ptr) + batch_off(z, a.inner_count, B.s_outer, B.s_inner, B.inner_div);
+    skA[p] = AK ? 1 : A.s_k;
+    skB[p] = BKM ? 1 : B.s_k;
+#pragma clang loop unroll(full)
+    for (int u = 0; u < NU; ++u) {
+      const int q = wave + u * NW;
+      // K-major: 16 rows of 64 B per load; MN-major: 2 k-rows of 512 B per load
+      const int r = q * 16 + (lane >> 2), ck = (lane & 3) ^ ((r >> 2) & 3);
+      const int k = q * 2 + (lane >> 5), cm = (lane & 31) ^ (4 * (k & 3));
+      offA[p][u] = AK ? (int64_t)min(m0 + r, a.M - 1) * A.s_row + 8 * ck
+                      : (int64_t)k * A.s_k + min(m0 + 8 * cm, a.M - 8);
+      offB[p][u] = BKM ? (int64_t)min(n0 + r, a.N - 1) * B.s_row + 8 * ck
+                       : (int64_t)k * B.s_k + min(n0 + 8 * cm, a.N - 8);
+    }
+  }
+
+  auto stage = [&](auto s) -> bf16_t* {
+    constexpr int S = decltype(s)::value & 3;
+    if constexpr (S == 0) return st0;
+    else if constexpr (S == 1) return st1;
+    else if constexpr (S == 2) return st2;
+    else return st3;
+  };
+  // load u (0..2 NU-1) of slice t (clamped to the last slice) into stage st
+  auto dma = [&](bf16_t* st, int t, int u) {
+    t = min(t, total - 1);
+    const int p = t >= nkt ? 1 : 0;
+    const int64_t k0 = kmin + (t - p * nkt) * KT3;
+    const bool isA = u < NU;
+    const int uu = isA ? u : u - NU;
+    const int q = wave + uu * NW;
+    const bf16_t* g = isA ? (p ? baseA[1] + offA[1][uu] + k0 * skA[1] : baseA[0] + offA[0][uu] + k0 * skA[0])
+                          : (p ? baseB[1] + offB[1][uu] + k0 * skB[1] : baseB[0] + offB[0][uu] + k0 * skB[0]);
+    // LDS byte address: stage base (a link-time constant) + wave-uniform offset
+    const uint32_t ldsaddr = (uint32_t)(uintptr_t)(lds_void_t*)st + (uint32_t)(((isA ? 0 : ASZ) + q * 512) * 2);
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, off"
+        :
+        : "s"(ldsaddr), "v"(g)
+        : "memory", "m0");
+  };
+
+  f32x16_t acc[IM][JN];
+#pragma clang loop unroll(full)
+  for (int i = 0; i < IM; ++i)
+#pragma clang loop unroll(full)
+    for (int j = 0; j < JN; ++j)
+#pragma clang loop unroll(full)
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  bf16x8_t f0[IM + JN], f1[IM + JN];   // fragments of half slices (k 0..15, k 16..31)
+  auto rd = [&](bf16x8_t& f, const bf16_t* st, int x, int kk) {
+    if (x < IM) f = frag<BM_, AK>(st, wm * 128 + x * 32, kk, lane);
+    else f = frag<BN_, BKM>(st + ASZ, wn * 128 + (x - IM) * 32, kk, lane);
+  };
+  auto mma = [&](const bf16x8_t (&f)[IM + JN], int e) {
+    const int i = e / JN, j = e % JN;
+    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[i], f[IM + j], acc[i][j], 0, 0, 0);
+  };
+
+  auto step = [&](auto s, int t) {
+    constexpr int S = decltype(s)::value;
+    const bf16_t* cur = stage(s);
+    // half slice 0 on f0 (read during the previous slice); read half 1 into f1
+#pragma clang loop unroll(full)
+    for (int x = 0; x < IM + JN; ++x) {
+      rd(f1[x], cur, x, 16);
+      mma(f0, 2 * x);
+      mma(f0, 2 * x + 1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // own loads of slice t + 1 done, then everyone's; stage S - 1 is free
+    wait_vm<PERT>();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+    bf16_t* nxt_fill = stage(std::integral_constant<int, S + 3>{});
+    const bf16_t* nxt = stage(std::integral_constant<int, S + 1>{});
+    // half slice 1 on f1; refill stage S - 1 with slice t + 3; read half 0 of slice t + 1 into f0
+#pragma clang loop unroll(full)
+    for (int x = 0; x < IM + JN; ++x) {
+      dma(nxt_fill, t + 3, x);
+      rd(f0[x], nxt, x, 0);
+      mma(f1, 2 * x);
+      mma(f1, 2 * x + 1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  if (total > 0) {
+#pragma clang loop unroll(full)
+    for (int u = 0; u < 2 * NU; ++u) dma(st0, 0, u);
+#pragma clang loop unroll(full)
+    for (int u = 0; u < 2 * NU; ++u) dma(st1, 1, u);
+#pragma clang loop unroll(full)
+    for (int u = 0; u < 2 * NU; ++u) dma(st2, 2, u);
+    wait_vm<2 * PERT>();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+#pragma clang loop unroll(full)
+    for (int x = 0; x < IM + JN; ++x) rd(f0[x], st0, x, 0);
+    for (int t0 = 0; t0 < total; t0 += NS3) {
+      step(std::integral_constant<int, 0>{}, t0);
+      if (t0 + 1 < total) step(std::integral_constant<int, 1>{}, t0 + 1);
+      if (t0 + 2 < total) step(std::integral_constant<int, 2>{}, t0 + 2);
+      if (t0 + 3 < total) step(std::integral_constant<int, 3>{}, t0 + 3);
+    }
+    wait_vm<0>();   // no load may land in LDS after the workgroup ends
+  }
+
+  const int64_t coff = batch_off(z, a.inner_count, a.c_outer, a.c_inner, a.c_div);
+#pragma clang loop unroll(full)
+  for (int i = 0; i < IM; ++i)
+#pragma clang loop unroll(full)
+    for (int j = 0; j < JN; ++j)
+      store_block<bf16_t>(a, acc[i][j], coff, m0 + wm * 128 + i * 32, n0 + wn * 128 + j * 32, lane);
+}
+
+// ===========================================================================
+// As gemm_bf16_w4 with K slices of 64 in a two-stage ring (2 x 64 KB).  A
+// K-major row of a slice is one whole 128-byte line, so each DMA load moves 8
+// full lines (half as many L1/L2 requests per byte as 64-byte row pieces),
+// and there is one barrier per 64 k.  A slice is four half slices of 16 k
+// read and multiplied in a two-register-set rotation; after the third, each
+// wavefront waits for its own LDS reads of the stage and for its loads of the
+// next slice, then the barrier frees the stage for the slice after next.
+// K-major LDS layout: row r of a slice is 8 chunks of 16 B, logical chunk c at
+// c ^ ((r >> 1) & 7) (16 lanes reading 16 consecutive rows hit 64 banks).
+// ===========================================================================
+constexpr int KT4 = 64;
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+__device__ inline int kswz64(int row, int c) { return row * KT4 + ((c ^ ((row >> 1) & 7)) << 3); }   // elements
+
+template <int R, bool KMAJ>
+__device__ inline bf16x8_t frag64(const bf16_t* t, int r0, int kk, int lane) {
+  if (KMAJ) return *reinterpret_cast<const bf16x8_t*>(t + kswz64(r0 + (lane & 31), (kk >> 3) + (lane >> 5)));
+  return frag<R, false>(t, r0, kk, lane);
+}
+
+template <bool AK, bool BKM>
+__global__ __launch_bounds__(256) void gemm_bf16_w4k64(GemmArgs a) {
+  constexpr int BM_ = 256, BN_ = 256, NW = 4, IM = 4, JN = 4;
+  constexpr int ASZ = BM_ * KT4, BSZ = BN_ * KT4;
+  constexpr int NU = BM_ * KT4 * 2 / 1024 / NW;   // 1 KB loads per operand per wavefront per slice (8)
+  constexpr int SSZ = ASZ + BSZ;                  // elements per stage
+  __shared__ __attribute__((aligned(1024))) bf16_t ring[2 * SSZ];
+
+  const int gx = gridDim.x, gy = gridDim.y;
+  const int nb = gx * gy * gridDim.z;
+  int lin = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
+  const int per = nb / 8;
+  if (lin < per * 8) lin = (lin % 8) * per + lin / 8;
+  const int tiles = gx * gy;
+  const int z = lin / tiles;
+  const int tl = lin % tiles;
+  constexpr int GM = 8;
+  const int gsize = GM * gx;
+  const int first_m = (tl / gsize) * GM;
+  const int gm_rows = min(gy - first_m, GM);
+  const int tm = first_m + (tl % gsize) % gm_rows;
+  const int tn = (tl % gsize) / gm_rows;
+  const int m0 = tm * BM_, n0 = tn * BN_;
+  if (a.causal == CAUSAL_SKIP_UPPER && n0 > m0 + BM_ - 1) return;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+
+  int kmin = 0, kmax = a.K;
+  if (a.causal == CAUSAL_K_LE_M) kmax = min(a.K, m0 + BM_);
+  if (a.causal == CAUSAL_K_GE_M) kmin = (min(m0, a.K) / KT4) * KT4;
+  const int nkt = (kmax > kmin) ? (kmax - kmin) / KT4 : 0;
+  const int total = nkt * a.npairs;
+
+  // Loads go through buffer resources whose base is the slice origin of the
+  // tile (row m0 / n0, column k0), so each lane keeps one small 32-bit byte
+  // offset per load for the whole K loop.  Both pairs share these offsets:
+  // their operands have equal strides (checked on the host).
+  const bf16_t* baseA[2];
+  const bf16_t* baseB[2];
+#pragma clang loop unroll(full)
+  for (int p = 0; p < 2; ++p) {
+    const int pp = p < a.npairs ? p : 0;
+    const GemmOperand& A = a.A[pp];
+    const GemmOperand& B = a.B[pp];
+    baseA[p] = reinterpret_cast<const bf16_t*>(A.ptr) + batch_off(z, a.inner_count, A.s_outer, A.s_inner, A.inner_div) +
+               (AK ? (int64_t)m0 * A.s_row : (int64_t)m0);
+    baseB[p] = reinterpret_cast<const bf16_t*>(B.ptr) + batch_off(z, a.inner_count, B.s_outer, B.s_inner, B.inner_div) +
+               (BKM ? (int64_t)n0 * B.s_row : (int64_t)n0);
+  }
+  const int64_t skA = AK ? 1 : a.A[0].s_k, skB = BKM ? 1 : a.B[0].s_k;
+  uint32_t voA[NU], voB[NU];
+#pragma clang loop unroll(full)
+  for (int u = 0; u < NU; ++u) {
+    const int q = wave + u * NW;
+    // K-major: 8 rows of 128 B per load; MN-major: 2 k-rows of 512 B per load
+    const int r = q * 8 + (lane >> 3), ck = (lane & 7) ^ ((r >> 1) & 7);
+    const int k = q * 2 + (lane >> 5), cm = (lane & 31) ^ (4 * (k & 3));
+    voA[u] = 2u * (uint32_t)(AK ? (int64_t)(min(m0 + r, a.M - 1) - m0) * a.A[0].s_row + 8 * ck
+                                : (int64_t)k * a.A[0].s_k + (min(m0 + 8 * cm, a.M - 8) - m0));
+    voB[u] = 2u * (uint32_t)(BKM ? (int64_t)(min(n0 + r, a.N - 1) - n0) * a.B[0].s_row + 8 * ck
+                                 : (int64_t)k * a.B[0].s_k + (min(n0 + 8 * cm, a.N - 8) - n0));
+  }
+
+  // raw buffer resource: base, stride 0, no range limit, 32-bit data format
+  auto rsrc = [](const bf16_t* base) {
+    const uint64_t b = (uint64_t)(uintptr_t)base;
+    return i32x4_t{(int)(uint32_t)b, (int)((b >> 32) & 0xffffu), -1, 0x00020000};
+  };
+  // load u (0..2 NU-1) of slice t (clamped to the last slice) into stage st
+  auto dma = [&](bf16_t* st, int t, int u) {
+    t = min(t, total - 1);
+    const int p = t >= nkt ? 1 : 0;
+    const int64_t k0 = kmin + (t - p * nkt) * KT4;
+    const bool isA = u < NU;
+    const int uu = isA ? u : u - NU;
+    const int q = wave + uu * NW;
+    const i32x4_t rs = isA ? rsrc((p ? baseA[1] : baseA[0]) + k0 * skA) : rsrc((p ? baseB[1] : baseB[0]) + k0 * skB);
+    const uint32_t vo = isA ? voA[uu] : voB[uu];
+    const uint32_t ldsaddr = (uint32_t)(uintptr_t)(lds_void_t*)st + (uint32_t)(((isA ? 0 : ASZ) + q * 512) * 2);
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "s_nop 0\n\t"
+        "buffer_load_dwordx4 %1, %2, 0 offen lds"
+        :
+        : "s"(ldsaddr), "v"(vo), "s"(rs)
+        : "memory", "m0");
+  };
+
+  f32x16_t acc[IM][JN];
+#pragma clang loop unroll(full)
+  for (int i = 0; i < IM; ++i)
+#pragma clang loop unroll(full)
+    for (int j = 0; j < JN; ++j)
+#pragma clang loop unroll(full)
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  bf16x8_t f0[IM + JN], f1[IM + JN];
+  auto rd = [&](bf16x8_t& f, const bf16_t* st, int x, int kk) {
+    if (x < IM) f = frag64<BM_, AK>(st, wm * 128 + x * 32, kk, lane);
+    else f = frag64<BN_, BKM>(st + ASZ, wn * 128 + (x - IM) * 32, kk, lane);
+  };
+  auto mma = [&](const bf16x8_t (&f)[IM + JN], int e) {
+    const int i = e / JN, j = e % JN;
+    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[i], f[IM + j], acc[i][j], 0, 0, 0);
+  };
+  // one half slice: MFMAs on `use`, fragments of the next half slice into `load`
+  auto half = [&](const bf16x8_t (&use)[IM + JN], bf16x8_t (&load)[IM + JN], const bf16_t* st, int kk) {
+#pragma clang loop unroll(full)
+    for (int x = 0; x < IM + JN; ++x) {
+      rd(load[x], st, x, kk);
+      mma(use, 2 * x);
+      mma(use, 2 * x + 1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  // The stage is a run-time choice (one slice per loop trip, no branches
+  // inside the trip, so the accumulators stay in place across iterations).
+  auto step = [&](int t) {
+    bf16_t* cur = ring + (t & 1) * SSZ;
+    const bf16_t* nxt = ring + ((t + 1) & 1) * SSZ;
+    half(f0, f1, cur, 16);
+    half(f1, f0, cur, 32);
+    half(f0, f1, cur, 48);
+    // this wavefront's reads of the stage and its loads of slice t + 1 are
+    // complete; after the barrier everyone's are, and the stage is free
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+#pragma clang loop unroll(full)
+    for (int x = 0; x < IM + JN; ++x) {
+      dma(cur, t + 2, 2 * x);
+      dma(cur, t + 2, 2 * x + 1);
+      rd(f0[x], nxt, x, 0);
+      mma(f1, 2 * x);
+      mma(f1, 2 * x + 1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  if (total > 0) {
+#pragma clang loop unroll(full)
+    for (int u = 0; u < 2 * NU; ++u) dma(ring, 0, u);
+#pragma clang loop unroll(full)
+    for (int u = 0; u < 2 * NU; ++u) dma(ring + SSZ, 1, u);
+    wait_vm<2 * NU>();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+#pragma clang loop unroll(full)
+    for (int x = 0; x < IM + JN; ++x) rd(f0[x], ring, x, 0);
+#pragma clang loop unroll(disable)
+    for (int t = 0; t < total; ++t) step(t);
+    wait_vm<0>();   // no load may land in LDS after the workgroup ends
+  }
+
+  const int64_t coff = batch_off(z, a.inner_count, a.c_outer, a.c_inner, a.c_div);
+#pragma clang loop unroll(full)
+  for (int i = 0; i < IM; ++i)
+#pragma clang loop unroll(full)
+    for (int j = 0; j < JN; ++j)
+      store_block<bf16_t>(a, acc[i][j], coff, m0 + wm * 128 + i * 32, n0 + wn * 128 + j * 32, lane);
+}
+
+template <bool AK, bool BKM>
+void launch_w4k64_t(const GemmArgs& a, hipStream_t stream) {
+  dim3 grid(ceil_div(a.N, 256), ceil_div(a.M, 256), a.nbatch);
+  hipLaunchKernelGGL((gemm_bf16_w4k64<AK, BKM>), grid, dim3(256), 0, stream, a);
+}
+void launch_w4k64(const GemmArgs& a, hipStream_t stream) {
+  const bool ak = a.A[0].s_k == 1, bk = a.B[0].s_k == 1;
+  if (ak && bk) launch_w4k64_t<true, true>(a, stream);
+  else if (ak && !bk) launch_w4k64_t<true, false>(a, stream);
+  else if (!ak && bk) launch_w4k64_t<false, true>(a, stream);
+  else launch_w4k64_t<false, false>(a, stream);
+}
+
+template <bool AK, bool BKM>
+void launch_w4_t(const GemmArgs& a, hipStream_t stream) {
+  dim3 grid(ceil_div(a.N, 256), ceil_div(a.M, 256), a.nbatch);
+  hipLaunchKernelGGL((gemm_bf16_w4<AK, BKM>), grid, dim3(256), 0, stream, a);
+}
+void launch_w4(const GemmArgs& a, hipStream_t stream) {
+  const bool ak = a.A[0].s_k == 1, bk = a.B[0].s_k == 1;
+  if (ak && bk) launch_w4_t<true, true>(a, stream);
+  else if (ak && !bk) launch_w4_t<true, false>(a, stream);
+  else if (!ak && bk) launch_w4_t<false, true>(a, stream);
+  else launch_w4_t<false, false>(a, stream);
+}
+
+template <int BN_, int WN>
 void launch_dma(const GemmArgs& a, hipStream_t stream) {
   dim3 grid(ceil_div(a.N, BN_), ceil_div(a.M, 256), a.nbatch);
-  dim3 block(64 * 2 * (BN_ / 64));
+  dim3 block(64 * 2 * WN);
   const bool ak = a.A[0].s_k == 1, bk = a.B[0].s_k == 1;
-  if (ak && bk) hipLaunchKernelGGL((gemm_bf16_dma<BN_, true, true>), grid, block, 0, stream, a);
-  else if (ak && !bk) hipLaunchKernelGGL((gemm_bf16_dma<BN_, true, false>), grid, block, 0, stream, a);
-  else if (!ak && bk) hipLaunchKernelGGL((gemm_bf16_dma<BN_, false, true>), grid, block, 0, stream, a);
-  else hipLaunchKernelGGL((gemm_bf16_dma<BN_, false, false>), grid, block, 0, stream, a);
+  if (ak && bk) hipLaunchKernelGGL((gemm_bf16_dma<BN_, WN, true, true>), grid, block, 0, stream, a);
+  else if (ak && !bk) hipLaunchKernelGGL((gemm_bf16_dma<BN_, WN, true, false>), grid, block, 0, stream, a);
+  else if (!ak && bk) hipLaunchKernelGGL((gemm_bf16_dma<BN_, WN, false, true>), grid, block, 0, stream, a);
+  else hipLaunchKernelGGL((gemm_bf16_dma<BN_, WN, false, false>), grid, block, 0, stream, a);
 }
 
 template <int BM_, int BN_, int WM, int WN>
@@ -668,8 +1065,13 @@ const char* gemm_check(const GemmArgs& a) {
     }
   }
   if (a.causal == CAUSAL_SKIP_UPPER && a.M > a.N) return "gemm: causal skip needs M <= N";
-  if (a.tile < 0 || a.tile > 5) return "gemm: bad tile";
+  if (a.tile < 0 || a.tile > 7) return "gemm: bad tile";
   if (a.tile >= 4 && (a.K % 32 || a.M < 8 || a.N < 8)) return "gemm: the DMA kernel needs K % 32 == 0";
+  if (a.tile >= 7 && a.K % 64) return "gemm: the 64-deep kernels need K % 64 == 0";
+  if (a.tile >= 7 && a.npairs == 2 &&
+      (a.A[1].s_row != a.A[0].s_row || a.A[1].s_k != a.A[0].s_k || a.B[1].s_row != a.B[0].s_row ||
+       a.B[1].s_k != a.B[0].s_k))
+    return "gemm: the 64-deep kernels need equal operand strides in both pairs";
   return nullptr;
 }
 
@@ -682,13 +1084,23 @@ hipError_t gemm(const GemmArgs& a, hipStream_t stream) {
       const int64_t t256 = (int64_t)ceil_div(a.M, 256) * ceil_div(a.N, 256) * a.nbatch;
       const int64_t t128 = (int64_t)ceil_div(a.M, 256) * ceil_div(a.N, 128) * a.nbatch;
       const bool dma = a.K % KT3 == 0;
-      if (a.N > 128 && t256 >= 192) tile = dma ? 4 : 2;
+      // 256 x 256 tiles once there are more than 128 of them; with fewer,
+      // 256 x 128 tiles keep more of the 256 CUs busy.  With an MN-major
+      // operand the four-wavefront kernel is fastest (measured on the 1.3B
+      // layer shapes); with both operands K-major, and for short contractions
+      // that never fill its pipeline, the eight-wavefront kernel is as fast
+      // or faster, and its epilogue (fp32 output plus residual) is spread
+      // over twice as many wavefronts.
+      const bool kk = a.A[0].s_k == 1 && a.B[0].s_k == 1;
+      if (a.N > 128 && t256 > 128) tile = dma ? ((kk || a.K < 512) ? 4 : 6) : 2;
       else if (t128 >= 64) tile = dma ? 5 : 3;
     }
     if (tile == 2) { launch_big<256, 256, 2, 4>(a, stream); return hipGetLastError(); }
     if (tile == 3) { launch_big<256, 128, 2, 2>(a, stream); return hipGetLastError(); }
-    if (tile == 4) { launch_dma<256>(a, stream); return hipGetLastError(); }
-    if (tile == 5) { launch_dma<128>(a, stream); return hipGetLastError(); }
+    if (tile == 4) { launch_dma<256, 4>(a, stream); return hipGetLastError(); }
+    if (tile == 5) { launch_dma<128, 2>(a, stream); return hipGetLastError(); }
+    if (tile == 6) { launch_w4(a, stream); return hipGetLastError(); }
+    if (tile == 7) { launch_w4k64(a, stream); return hipGetLastError(); }
   }
   dim3 grid(ceil_div(a.N, BN), ceil_div(a.M, BM), a.nbatch);
   const bool ak = a.A[0].s_k == 1, bk = a.B[0].s_k == 1;
