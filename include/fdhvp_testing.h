@@ -23,7 +23,9 @@ extern "C" {
  * above the diagonal, 2 contract only k <= m, 3 only k >= m.  tile selects
  * the bf16 kernel variant (0 automatic, 1 128x128, 2 256x256, 3 256x128,
  * 4 256x256 and 5 256x128 fed by direct global-to-LDS loads, K % 32 == 0,
- * 6 as 4 with four 128x128 wavefront tiles instead of eight 128x64 ones).
+ * 6 as 4 with four 128x128 wavefront tiles instead of eight 128x64 ones,
+ * 7 as 6 with 64-deep K slices in a two-stage ring, K % 64 == 0 and equal
+ * operand strides in both pairs).
  * Enqueued on hip_stream; returns without waiting.  K, and M/N of MN-major
  * operands, must be multiples of 8 (bf16) or 4 (fp32). */
 fdh_status fdh_testing_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t batch, int32_t a_kmajor,
