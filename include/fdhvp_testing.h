@@ -32,6 +32,13 @@ fdh_status fdh_testing_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, int3
                             int32_t b_kmajor, const void* A, const void* B, const void* A2, const void* B2,
                             float* C, int32_t causal, float alpha, int32_t tile, void* hip_stream);
 
+/* on != 0 makes the next fdh_set_workspace plan the unfused attention path
+ * (score, probability and score-gradient matrices in the workspace, MFMA
+ * GEMMs and row kernels) even where the fused kernels apply (bf16 operands,
+ * head dimension 64 or 128, S a multiple of 128), so that the two paths can
+ * be compared on one model. */
+fdh_status fdh_testing_unfused_attention(fdh_ctx* ctx, int32_t on);
+
 /* Per-launch timing with HIP events recorded on the context stream around every
  * GEMM launch (category 0) and every Lanczos vector launch (category 1).
  * enable != 0 turns it on (and clears the accumulators).  While on, the event

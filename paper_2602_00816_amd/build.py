@@ -21,7 +21,7 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-u
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-I" + os.path.join(os.path.dirname(HERE), "include")]
 
-SOURCES = ["gemm.hip", "rng.hip", "vec.hip", "lm.hip", "engine.hip", "capi.hip"]
+SOURCES = ["gemm.hip", "attn.hip", "rng.hip", "vec.hip", "lm.hip", "engine.hip", "capi.hip"]
 
 
 def _compile(src: str) -> str:

@@ -1,0 +1,704 @@
+// Fused causal attention for the lockstep pair (bf16 operands, fp32
+// accumulation): the forward output and the three input gradients without
+// materialising the S x S score, probability or score-gradient matrices.
+//
+// The two gradient passes at theta +- eps v are carried as m = half sum and
+// d = half difference of the two points' values (section 3.2, central
+// difference of two backward passes).  With logits a = S.m * scale and
+// b = S.d * scale of one query row, the two points' softmaxes are
+// softmax(a + b) and softmax(a - b).  With Zc = sum e^a cosh b and
+// Zs = sum e^a sinh b (row sums), D = Zc^2 - Zs^2, u = Zc / D, w = Zs / D:
+//   P.m = e^a (u cosh b - w sinh b),   P.d = e^a (u sinh b - w cosh b)
+// exactly, and with no difference of nearly equal numbers: the small
+// quantities (b, sinh b, Zs) are carried directly.  The products follow the
+// unfused path term by term (terms of order eps^2 relative are dropped):
+//   O.m  = P.m V.m                 O.d  = P.m V.d + P.d V.m
+//   dP.m = dO.m V.m^T              dP.d = dO.m V.d^T + dO.d V.m^T
+//   dS.m = P.m (dP.m - D.m) + P.d (dP.d - D.d)
+//   dS.d = P.m (dP.d - D.d) + P.d (dP.m - D.m)
+//   with D.m = rowsum(dO.m O.m + dO.d O.d), D.d = rowsum(dO.m O.d + dO.d O.m)
+//   dV.m = P.m^T dO.m              dV.d = P.m^T dO.d + P.d^T dO.m
+//   dQ.m = dS.m K.m                dQ.d = dS.m K.d + dS.d K.m      (x scale)
+//   dK.m = dS.m^T Q.m              dK.d = dS.m^T Q.d + dS.d^T Q.m  (x scale)
+// The forward runs the softmax online over key blocks (running maximum of a,
+// rescaled accumulators of e^a cosh b V.m, e^a sinh b V.m, e^a cosh b V.d)
+// and stores per query row (max a, u, w) for the backward.
+//
+// Three kernels, each with MFMA tiles oriented so that the probability-like
+// accumulator feeds the next MFMA straight from registers: a 32x32 (16x16)
+// accumulator holds, per lane, one column and 16 (4) rows; read in the order
+// the accumulator holds them, its rows are a permutation of the next
+// product's contraction index, and the other operand is read from LDS with
+// the same permutation (transposing LDS reads, ds_read_b64_tr_b16).
+//   flash_fwd   : one workgroup per 128 queries of one head, S^T = K Q^T tiles
+//   flash_bwd_q : one workgroup per 128 queries, dQ^T = K^T dS^T
+//   flash_bwd_kv: one workgroup per 64 keys of one key/value head (all query
+//                 heads of its group), S = Q K^T tiles, dV = P^T dO, dK = dS^T Q
+// K/V (or Q/dO) tiles are streamed into a double-buffered LDS ring by direct
+// global-to-LDS loads.  LDS tiles are [rows][D] with the 16-byte chunk c of
+// row r at c ^ f(r), f a bit reversal of low row bits, which keeps 16-byte
+// row reads and both kinds of transposing reads free of bank conflicts.
+#include "common.h"
+#include "kernels.h"
+
+#include <type_traits>
+
+namespace fdh {
+
+namespace {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16_t;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef short v8i16 __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16_t;
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+constexpr float NEG = -1.0e30f;   // masked logit (exp underflows to 0, no NaN)
+
+// element offset of chunk `chunk` (8 elements) of row `row` in an LDS [rows][D] tile
+template <int D>
+__device__ inline int tswz(int row, int chunk) {
+  int f;
+  if (D == 128) {
+    const int r = row & 15;
+    f = ((r & 1) << 3) | ((r & 2) << 1) | ((r & 4) >> 1) | ((r & 8) >> 3);
+  } else {
+    const int r = (row >> 1) & 7;
+    f = ((r & 1) << 2) | (r & 2) | ((r & 4) >> 2);
+  }
+  return row * D + ((chunk ^ f) << 3);
+}
+
+// 32x32x16 operand with the contraction along D: lane -> row r0 + lane % 32,
+// columns 16 s + 8 (lane / 32) .. + 7
+template <int D>
+__device__ inline bf16x8_t ld_k32(const bf16_t* t, int r0, int s, int lane) {
+  return *reinterpret_cast<const bf16x8_t*>(t + tswz<D>(r0 + (lane & 31), 2 * s + (lane >> 5)));
+}
+// 16x16x32 operand with the contraction along D: lane -> row r0 + lane % 16,
+// columns 32 s + 8 (lane / 16) .. + 7
+template <int D>
+__device__ inline bf16x8_t ld_k16(const bf16_t* t, int r0, int s, int lane) {
+  return *reinterpret_cast<const bf16x8_t*>(t + tswz<D>(r0 + (lane & 15), 4 * s + (lane >> 4)));
+}
+template <int D>
+__device__ inline v4i16 tr4(const bf16_t* t, int row, int col) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(t + tswz<D>(row, col >> 3) + (col & 7)));
+}
+__device__ inline bf16x8_t cat(v4i16 a, v4i16 b) {
+  const v8i16 v = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  return __builtin_bit_cast(bf16x8_t, v);
+}
+// 32x32x16 operand with the contraction along the rows kk .. kk + 15 of the
+// tile, in the row order of a 32x32 accumulator (lane half g: rows
+// kk + 4 g .. + 3 and kk + 8 + 4 g .. + 3), column n0 + lane % 32
+template <int D>
+__device__ inline bf16x8_t ld_t32(const bf16_t* t, int kk, int n0, int lane) {
+  const int g = lane >> 4, i = lane & 15;
+  const int col = n0 + 16 * (g & 1) + 4 * (i & 3);
+  const int lo = kk + 4 * (g >> 1) + (i >> 2);
+  return cat(tr4<D>(t, lo, col), tr4<D>(t, lo + 8, col));
+}
+// 16x16x32 operand with the contraction along rows kk .. kk + 31 in the row
+// order of two stacked 16x16 accumulators (lane quarter g: rows kk + 4 g .. + 3
+// and kk + 16 + 4 g .. + 3), column n0 + lane % 16
+template <int D>
+__device__ inline bf16x8_t ld_t16(const bf16_t* t, int kk, int n0, int lane) {
+  const int g = lane >> 4, i = lane & 15;
+  const int col = n0 + 4 * (i & 3);
+  const int lo = kk + 4 * g + (i >> 2);
+  return cat(tr4<D>(t, lo, col), tr4<D>(t, lo + 16, col));
+}
+
+__device__ inline bf16x8_t pack8(const float* x) {
+  bf16x8_t v;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) v[j] = (__bf16)x[j];
+  return v;
+}
+
+__device__ inline f32x16_t mma32(bf16x8_t a, bf16x8_t b, f32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+__device__ inline f32x4_t mma16(bf16x8_t a, bf16x8_t b, f32x4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// cosh and sinh of a logit difference b.  b is of order eps times a logit
+// derivative; when every |b| of the wavefront is below SERIES_MAX the
+// two-term series is exact to fp32 rounding (dropped terms b^4/120 and b^4/24
+// relative, below 4e-8), otherwise the exponential form is used.
+constexpr float SERIES_MAX = 1.f / 32.f;
+template <bool SERIES>
+__device__ inline void coshsinh(float b, float& c, float& s) {
+  if constexpr (SERIES) {
+    const float b2 = b * b;
+    s = fmaf(b * b2, 1.f / 6.f, b);
+    c = fmaf(b2, 0.5f, 1.f);
+  } else {
+    const float e = __expf(b), ie = __expf(-b);
+    s = 0.5f * (e - ie);
+    c = 0.5f * (e + ie);
+  }
+}
+
+// Issue this wavefront's direct global-to-LDS loads of NTILE tiles of R rows
+// x D bf16: tile i comes from rows src[i] + r * ld and lands swizzled at
+// dst + i * R * D.  Each load moves 1 KB: 64 lanes x 16 bytes, lane l at
+// +16 l in LDS, so each lane fetches the logical chunk that the swizzle puts
+// at that position.  Completion is waited for with vmcnt before the barrier
+// that publishes the tiles.
+template <int D, int R, int NTILE>
+__device__ inline void dma_tiles(bf16_t* dst, const bf16_t* const (&src)[NTILE], int64_t ld, int wave, int lane) {
+  constexpr int CPR = D / 8, RPI = 64 / CPR, IPT = R / RPI, NI = NTILE * IPT;
+  static_assert(IPT % 4 == 0, "each tile's loads must split evenly over four wavefronts");
+#pragma unroll
+  for (int u = 0; u < NI / 4; ++u) {
+    const int tile = 4 * u / IPT;           // compile-time: wave < 4 never crosses a tile
+    const int q = 4 * u % IPT + wave;
+    const int row = q * RPI + lane / CPR, pch = lane % CPR;
+    const int lch = (tswz<D>(row, pch) - row * D) >> 3;   // the swizzle is an involution on chunks
+    const bf16_t* g = src[tile] + (int64_t)row * ld + 8 * lch;
+    const uint32_t la = (uint32_t)(uintptr_t)(lds_void_t*)(dst + tile * R * D + q * 512);
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, off"
+        :
+        : "s"(__builtin_amdgcn_readfirstlane(la)), "v"(g)
+        : "memory", "m0");
+  }
+}
+
+// ---------------------------------------------------------------------------
+// forward
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void flash_fwd_kernel(FlashArgs a) {
+  constexpr int KB = 32, KS = D / 16, NT = D / 32, TILE = KB * D;
+  __shared__ __attribute__((aligned(1024))) bf16_t ring[2][4 * TILE];   // K.m K.d V.m V.d
+
+  const int qb = gridDim.x - 1 - blockIdx.x;   // longest rows first
+  const int bh = blockIdx.y, b = bh / a.Hq, h = bh % a.Hq, kh = h / a.G;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int q0 = qb * 128, qw = q0 + 32 * wave;
+  const int64_t row0 = (int64_t)b * a.S;
+  const int qi = qw + (lane & 31);
+
+  // Q fragments (B operand of S^T = K Q^T), both points' halves
+  bf16x8_t qm[KS], qd[KS];
+  {
+    const int64_t off = (row0 + qi) * a.ld + (int64_t)h * D + 8 * (lane >> 5);
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      qm[s] = *reinterpret_cast<const bf16x8_t*>(a.qkv_m + off + 16 * s);
+      qd[s] = *reinterpret_cast<const bf16x8_t*>(a.qkv_d + off + 16 * s);
+    }
+  }
+  f32x16_t Ac[NT], As[NT], Bc[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) Ac[t][r] = As[t][r] = Bc[t][r] = 0.f;
+  float zc = 0.f, zs = 0.f;
+
+  const int nkb = (q0 + 128) / KB;
+  const int lastw = qw / KB;   // this wavefront's diagonal block
+
+  // Pass 1: the exact row maximum of the logits a (only S.m = K.m Q.m^T, one
+  // product in six), so that the accumulating pass never rescales: an
+  // online rescale of the 192 accumulators inside the loop makes the
+  // compiler keep VGPR copies of them and spill the Q fragments.
+  float mrun = NEG;
+  {
+    auto issue1 = [&](int kb) {
+      const bf16_t* src[1] = {a.qkv_m + (row0 + (int64_t)kb * KB) * a.ld + a.koff + kh * D};
+      dma_tiles<D, KB, 1>(ring[kb & 1], src, a.ld, wave, lane);
+    };
+    issue1(0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    for (int kb = 0; kb < nkb; ++kb) {
+      if (kb + 1 < nkb) issue1(kb + 1);
+      const bf16_t* Km = ring[kb & 1];
+      f32x16_t sm;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sm[r] = 0.f;
+#pragma unroll
+      for (int s = 0; s < KS; ++s) sm = mma32(ld_k32<D>(Km, 0, s, lane), qm[s], sm);
+      const bool diag = kb >= lastw;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = kb * KB + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+        if (!diag || key <= qi) mrun = fmaxf(mrun, sm[r] * a.scale);
+      }
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+    }
+    mrun = fmaxf(mrun, __shfl_xor(mrun, 32, 64));
+  }
+
+  // Pass 2: accumulate with the fixed reference maximum
+  auto issue = [&](int kb) {
+    const int64_t r = row0 + (int64_t)kb * KB;
+    const bf16_t* src[4] = {a.qkv_m + r * a.ld + a.koff + kh * D, a.qkv_d + r * a.ld + a.koff + kh * D,
+                            a.qkv_m + r * a.ld + a.voff + kh * D, a.qkv_d + r * a.ld + a.voff + kh * D};
+    dma_tiles<D, KB, 4>(ring[kb & 1], src, a.ld, wave, lane);
+  };
+  issue(0);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  for (int kb = 0; kb < nkb; ++kb) {
+    if (kb + 1 < nkb) issue(kb + 1);
+    // every wavefront runs every block: past its diagonal all keys are masked
+    // (exact zeros); a branch around the accumulator updates would make the
+    // register allocator shuttle the accumulators through VGPRs each block
+    {
+      const bf16_t* Km = ring[kb & 1];
+      const bf16_t* Kd = Km + TILE;
+      const bf16_t* Vm = Km + 2 * TILE;
+      const bf16_t* Vd = Km + 3 * TILE;
+      f32x16_t sm, sd;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sm[r] = sd[r] = 0.f;
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        const bf16x8_t km = ld_k32<D>(Km, 0, s, lane), kd = ld_k32<D>(Kd, 0, s, lane);
+        sm = mma32(km, qm[s], sm);
+        sd = mma32(km, qd[s], sd);
+        sd = mma32(kd, qm[s], sd);
+      }
+      const bool diag = kb >= lastw;
+      float bmax = 0.f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        sm[r] *= a.scale;
+        sd[r] *= a.scale;
+        bmax = fmaxf(bmax, fabsf(sd[r]));
+      }
+      if (diag) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = kb * KB + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+          if (key > qi) sm[r] = NEG;
+        }
+      }
+      float pc[16], ps[16];
+      auto terms = [&](auto ser) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float e = __expf(sm[r] - mrun);
+          float c, sn;
+          coshsinh<decltype(ser)::value>(sd[r], c, sn);
+          pc[r] = e * c;   // e^a cosh b
+          ps[r] = e * sn;  // e^a sinh b
+          zc += pc[r];
+          zs += ps[r];
+        }
+      };
+      if (!__any(bmax >= SERIES_MAX)) terms(std::true_type{});
+      else terms(std::false_type{});
+#pragma unroll
+      for (int t2 = 0; t2 < 2; ++t2) {
+        const bf16x8_t bc = pack8(pc + 8 * t2), bs = pack8(ps + 8 * t2);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          const bf16x8_t vm = ld_t32<D>(Vm, 16 * t2, 32 * t, lane), vd = ld_t32<D>(Vd, 16 * t2, 32 * t, lane);
+          Ac[t] = mma32(vm, bc, Ac[t]);
+          As[t] = mma32(vm, bs, As[t]);
+          Bc[t] = mma32(vd, bc, Bc[t]);
+        }
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+  }
+
+  zc += __shfl_xor(zc, 32, 64);
+  zs += __shfl_xor(zs, 32, 64);
+  const float den = (zc - zs) * (zc + zs);
+  const float u = zc / den, w = zs / den;
+  const int64_t orow = (row0 + qi) * a.ldo + (int64_t)h * D + 4 * (lane >> 5);
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      uint16_t om[4], od[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = 4 * g + e;
+        om[e] = f32_to_bf16(u * Ac[t][r] - w * As[t][r]);
+        od[e] = f32_to_bf16(u * As[t][r] - w * Ac[t][r] + u * Bc[t][r]);
+      }
+      const int64_t o = orow + 32 * t + 8 * g;
+      *reinterpret_cast<uint2*>(a.o_m + o) = make_uint2(om[0] | ((uint32_t)om[1] << 16), om[2] | ((uint32_t)om[3] << 16));
+      *reinterpret_cast<uint2*>(a.o_d + o) = make_uint2(od[0] | ((uint32_t)od[1] << 16), od[2] | ((uint32_t)od[3] << 16));
+    }
+  if (lane < 32) a.stats[(int64_t)bh * a.S + qi] = make_float4(mrun, u, w, 0.f);
+}
+
+// ---------------------------------------------------------------------------
+// backward: row terms D.m, D.d
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void flash_delta_kernel(FlashArgs a, int nrows) {
+  // 16 lanes per (token, head) row; D / 16 elements per lane
+  constexpr int E = D / 16;
+  const int64_t row = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
+  if (row >= nrows) return;
+  const int sub = threadIdx.x & 15;
+  const int64_t t = row / a.Hq;
+  const int h = (int)(row % a.Hq);
+  const int64_t off = t * a.ldo + (int64_t)h * D + sub * E;
+  float dm = 0.f, dd = 0.f;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const float om = bf16_to_f32(a.o_m[off + e]), od = bf16_to_f32(a.o_d[off + e]);
+    const float gm = bf16_to_f32(a.do_m[off + e]), gd = bf16_to_f32(a.do_d[off + e]);
+    dm += gm * om + gd * od;
+    dd += gm * od + gd * om;
+  }
+#pragma unroll
+  for (int o = 8; o > 0; o >>= 1) {
+    dm += __shfl_xor(dm, o, 64);
+    dd += __shfl_xor(dd, o, 64);
+  }
+  if (sub == 0) {
+    const int b = (int)(t / a.S), i = (int)(t % a.S);
+    a.delta[((int64_t)b * a.Hq + h) * a.S + i] = make_float2(dm, dd);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// backward: dQ
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void flash_bwd_q_kernel(FlashArgs a) {
+  constexpr int KB = 32, KS = D / 16, NT = D / 32, TILE = KB * D;
+  __shared__ __attribute__((aligned(1024))) bf16_t ring[2][4 * TILE];   // K.m K.d V.m V.d
+
+  const int qb = gridDim.x - 1 - blockIdx.x;
+  const int bh = blockIdx.y, b = bh / a.Hq, h = bh % a.Hq, kh = h / a.G;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int q0 = qb * 128, qw = q0 + 32 * wave;
+  const int64_t row0 = (int64_t)b * a.S;
+  const int qi = qw + (lane & 31);
+
+  bf16x8_t qm[KS], qd[KS], gm[KS], gd[KS];   // Q and dO fragments (B operands)
+  {
+    const int64_t off = (row0 + qi) * a.ld + (int64_t)h * D + 8 * (lane >> 5);
+    const int64_t offo = (row0 + qi) * a.ldo + (int64_t)h * D + 8 * (lane >> 5);
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      qm[s] = *reinterpret_cast<const bf16x8_t*>(a.qkv_m + off + 16 * s);
+      qd[s] = *reinterpret_cast<const bf16x8_t*>(a.qkv_d + off + 16 * s);
+      gm[s] = *reinterpret_cast<const bf16x8_t*>(a.do_m + offo + 16 * s);
+      gd[s] = *reinterpret_cast<const bf16x8_t*>(a.do_d + offo + 16 * s);
+    }
+  }
+  const float4 st = a.stats[(int64_t)bh * a.S + qi];
+  const float2 dl = a.delta[(int64_t)bh * a.S + qi];
+  f32x16_t Qm[NT], Qd[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) Qm[t][r] = Qd[t][r] = 0.f;
+
+  const int nkb = (q0 + 128) / KB;
+  const int lastw = qw / KB;
+  auto issue = [&](int kb) {
+    const int64_t r = row0 + (int64_t)kb * KB;
+    const bf16_t* src[4] = {a.qkv_m + r * a.ld + a.koff + kh * D, a.qkv_d + r * a.ld + a.koff + kh * D,
+                            a.qkv_m + r * a.ld + a.voff + kh * D, a.qkv_d + r * a.ld + a.voff + kh * D};
+    dma_tiles<D, KB, 4>(ring[kb & 1], src, a.ld, wave, lane);
+  };
+  issue(0);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  for (int kb = 0; kb < nkb; ++kb) {
+    if (kb + 1 < nkb) issue(kb + 1);
+    {   // every block, masked past the diagonal (see the forward kernel)
+      const bf16_t* Km = ring[kb & 1];
+      const bf16_t* Kd = Km + TILE;
+      const bf16_t* Vm = Km + 2 * TILE;
+      const bf16_t* Vd = Km + 3 * TILE;
+      f32x16_t sm, sd, pm, pd;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sm[r] = sd[r] = pm[r] = pd[r] = 0.f;
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        const bf16x8_t km = ld_k32<D>(Km, 0, s, lane), kd = ld_k32<D>(Kd, 0, s, lane);
+        sm = mma32(km, qm[s], sm);
+        sd = mma32(km, qd[s], sd);
+        sd = mma32(kd, qm[s], sd);
+        const bf16x8_t vm = ld_k32<D>(Vm, 0, s, lane), vd = ld_k32<D>(Vd, 0, s, lane);
+        pm = mma32(vm, gm[s], pm);
+        pd = mma32(vm, gd[s], pd);
+        pd = mma32(vd, gm[s], pd);
+      }
+      const bool diag = kb >= lastw;
+      float bmax = 0.f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        sm[r] *= a.scale;
+        sd[r] *= a.scale;
+        bmax = fmaxf(bmax, fabsf(sd[r]));
+      }
+      if (diag) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = kb * KB + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+          if (key > qi) sm[r] = NEG;
+        }
+      }
+      float gsm[16], gsd[16];
+      auto terms = [&](auto ser) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float e = __expf(sm[r] - st.x);
+          float c, sn;
+          coshsinh<decltype(ser)::value>(sd[r], c, sn);
+          const float Pm = e * (c * st.y - sn * st.z), Pd = e * (sn * st.y - c * st.z);
+          const float xm = pm[r] - dl.x, xd = pd[r] - dl.y;
+          gsm[r] = Pm * xm + Pd * xd;
+          gsd[r] = Pm * xd + Pd * xm;
+        }
+      };
+      if (!__any(bmax >= SERIES_MAX)) terms(std::true_type{});
+      else terms(std::false_type{});
+#pragma unroll
+      for (int t2 = 0; t2 < 2; ++t2) {
+        const bf16x8_t bm = pack8(gsm + 8 * t2), bd = pack8(gsd + 8 * t2);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          const bf16x8_t km = ld_t32<D>(Km, 16 * t2, 32 * t, lane), kd = ld_t32<D>(Kd, 16 * t2, 32 * t, lane);
+          Qm[t] = mma32(km, bm, Qm[t]);
+          Qd[t] = mma32(kd, bm, Qd[t]);
+          Qd[t] = mma32(km, bd, Qd[t]);
+        }
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+  }
+
+  const int64_t grow = (row0 + qi) * a.ldg + (int64_t)h * D + 4 * (lane >> 5);
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int64_t o = grow + 32 * t + 8 * g;
+      *reinterpret_cast<float4*>(a.g_m + o) =
+          make_float4(Qm[t][4 * g] * a.scale, Qm[t][4 * g + 1] * a.scale, Qm[t][4 * g + 2] * a.scale,
+                      Qm[t][4 * g + 3] * a.scale);
+      *reinterpret_cast<float4*>(a.g_d + o) =
+          make_float4(Qd[t][4 * g] * a.scale, Qd[t][4 * g + 1] * a.scale, Qd[t][4 * g + 2] * a.scale,
+                      Qd[t][4 * g + 3] * a.scale);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// backward: dK, dV (summed over the query heads that share the key/value head)
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void flash_bwd_kv_kernel(FlashArgs a) {
+  constexpr int QB = 32, KS = D / 32, NT = D / 16, TILE = QB * D;
+  __shared__ __attribute__((aligned(1024))) bf16_t ring[2][4 * TILE];   // Q.m Q.d dO.m dO.d
+  __shared__ float4 sst[2][QB];                                         // m, u, w, D.m
+  __shared__ __attribute__((aligned(16))) float sdd[2][QB];             // D.d
+
+  const int kblk = blockIdx.x;   // lowest keys (most queries) first
+  const int bkh = blockIdx.y, b = bkh / a.Hk, kh = bkh % a.Hk;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int k0 = kblk * 64, kw = k0 + 16 * wave;
+  const int64_t row0 = (int64_t)b * a.S;
+  const int kj = kw + (lane & 15);
+
+  // K and V fragments of this wavefront's 16 keys (B operands of S = Q K^T, dP = dO V^T)
+  bf16x8_t km[KS], kd[KS], vm[KS], vd[KS];
+  {
+    const int64_t r = (row0 + kj) * a.ld + kh * D + 8 * (lane >> 4);
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      km[s] = *reinterpret_cast<const bf16x8_t*>(a.qkv_m + r + a.koff + 32 * s);
+      kd[s] = *reinterpret_cast<const bf16x8_t*>(a.qkv_d + r + a.koff + 32 * s);
+      vm[s] = *reinterpret_cast<const bf16x8_t*>(a.qkv_m + r + a.voff + 32 * s);
+      vd[s] = *reinterpret_cast<const bf16x8_t*>(a.qkv_d + r + a.voff + 32 * s);
+    }
+  }
+  f32x4_t Vm_[NT], Vd_[NT], Km_[NT], Kd_[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) Vm_[t][r] = Vd_[t][r] = Km_[t][r] = Kd_[t][r] = 0.f;
+
+  const int nqb = (a.S - k0) / QB;   // query blocks from the first key on, per head
+  const int total = nqb * a.G;
+  auto issue = [&](int it) {
+    const int g = it / nqb, qbk = it % nqb;
+    const int h = kh * a.G + g, q0 = k0 + qbk * QB;
+    const int64_t r = row0 + q0;
+    const bf16_t* src[4] = {a.qkv_m + r * a.ld + (int64_t)h * D, a.qkv_d + r * a.ld + (int64_t)h * D,
+                            a.do_m + r * a.ldo + (int64_t)h * D, a.do_d + r * a.ldo + (int64_t)h * D};
+    // the two row strides differ: issue the Q and dO pairs separately
+    const bf16_t* sq[2] = {src[0], src[1]};
+    const bf16_t* so[2] = {src[2], src[3]};
+    dma_tiles<D, QB, 2>(ring[it & 1], sq, a.ld, wave, lane);
+    dma_tiles<D, QB, 2>(ring[it & 1] + 2 * TILE, so, a.ldo, wave, lane);
+  };
+  // row terms of the next block: loaded into registers with its tiles, written
+  // to LDS after this block's compute (the load's wait would otherwise also
+  // wait for the tile loads issued just before it)
+  float4 nst = make_float4(0.f, 0.f, 0.f, 0.f);
+  float ndd = 0.f;
+  auto load_rows = [&](int it) {
+    if (tid < QB) {
+      const int g = it / nqb, qbk = it % nqb;
+      const int64_t si = ((int64_t)b * a.Hq + kh * a.G + g) * a.S + k0 + qbk * QB + tid;
+      const float4 st = a.stats[si];
+      const float2 dl = a.delta[si];
+      nst = make_float4(st.x, st.y, st.z, dl.x);
+      ndd = dl.y;
+    }
+  };
+  auto store_rows = [&](int it) {
+    if (tid < QB) {
+      sst[it & 1][tid] = nst;
+      sdd[it & 1][tid] = ndd;
+    }
+  };
+  load_rows(0);
+  issue(0);
+  __builtin_amdgcn_s_waitcnt(0);
+  store_rows(0);
+  __syncthreads();
+  for (int it = 0; it < total; ++it) {
+    if (it + 1 < total) {
+      load_rows(it + 1);
+      issue(it + 1);
+    }
+    const int q0 = k0 + (it % nqb) * QB;
+    {   // every block; blocks wholly before this wavefront's keys are fully masked
+      const bf16_t* Qm = ring[it & 1];
+      const bf16_t* Qd = Qm + TILE;
+      const bf16_t* Om = Qm + 2 * TILE;
+      const bf16_t* Od = Qm + 3 * TILE;
+      f32x4_t sm[2], sd[2], pm[2], pd[2];
+#pragma unroll
+      for (int qt = 0; qt < 2; ++qt) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sm[qt][r] = sd[qt][r] = pm[qt][r] = pd[qt][r] = 0.f;
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+          const bf16x8_t qa = ld_k16<D>(Qm, 16 * qt, s, lane), qb_ = ld_k16<D>(Qd, 16 * qt, s, lane);
+          sm[qt] = mma16(qa, km[s], sm[qt]);
+          sd[qt] = mma16(qa, kd[s], sd[qt]);
+          sd[qt] = mma16(qb_, km[s], sd[qt]);
+          const bf16x8_t oa = ld_k16<D>(Om, 16 * qt, s, lane), ob = ld_k16<D>(Od, 16 * qt, s, lane);
+          pm[qt] = mma16(oa, vm[s], pm[qt]);
+          pd[qt] = mma16(oa, vd[s], pd[qt]);
+          pd[qt] = mma16(ob, vm[s], pd[qt]);
+        }
+      }
+      const bool diag = q0 < kw + 16;
+      float bmax = 0.f;
+#pragma unroll
+      for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          sm[qt][r] *= a.scale;
+          sd[qt][r] *= a.scale;
+          bmax = fmaxf(bmax, fabsf(sd[qt][r]));
+        }
+      if (diag) {
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (q0 + 16 * qt + 4 * (lane >> 4) + r < kj) sm[qt][r] = NEG;
+      }
+      float Pm[8], Pd[8], gsm[8], gsd[8];   // rows in accumulator order: (qt, r) -> 4 qt + r
+      auto terms = [&](auto ser) {
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) {
+          const float4 ddv = *reinterpret_cast<const float4*>(&sdd[it & 1][16 * qt + 4 * (lane >> 4)]);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float4 st = sst[it & 1][16 * qt + 4 * (lane >> 4) + r];
+            const float dd = r == 0 ? ddv.x : (r == 1 ? ddv.y : (r == 2 ? ddv.z : ddv.w));
+            const float e = __expf(sm[qt][r] - st.x);
+            float c, sn;
+            coshsinh<decltype(ser)::value>(sd[qt][r], c, sn);
+            const float P_m = e * (c * st.y - sn * st.z), P_d = e * (sn * st.y - c * st.z);
+            const float xm = pm[qt][r] - st.w, xd = pd[qt][r] - dd;
+            Pm[4 * qt + r] = P_m;
+            Pd[4 * qt + r] = P_d;
+            gsm[4 * qt + r] = P_m * xm + P_d * xd;
+            gsd[4 * qt + r] = P_m * xd + P_d * xm;
+          }
+        }
+      };
+      if (!__any(bmax >= SERIES_MAX)) terms(std::true_type{});
+      else terms(std::false_type{});
+      const bf16x8_t apm = pack8(Pm), apd = pack8(Pd), asm_ = pack8(gsm), asd = pack8(gsd);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const bf16x8_t om = ld_t16<D>(Om, 0, 16 * t, lane), od = ld_t16<D>(Od, 0, 16 * t, lane);
+        Vm_[t] = mma16(apm, om, Vm_[t]);
+        Vd_[t] = mma16(apm, od, Vd_[t]);
+        Vd_[t] = mma16(apd, om, Vd_[t]);
+        const bf16x8_t qa = ld_t16<D>(Qm, 0, 16 * t, lane), qb_ = ld_t16<D>(Qd, 0, 16 * t, lane);
+        Km_[t] = mma16(asm_, qa, Km_[t]);
+        Kd_[t] = mma16(asm_, qb_, Kd_[t]);
+        Kd_[t] = mma16(asd, qa, Kd_[t]);
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    if (it + 1 < total) store_rows(it + 1);
+    __syncthreads();
+  }
+
+  // accumulator (t, r): key kw + 4 (lane / 16) + r, column 16 t + lane % 16
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t o = (row0 + kw + 4 * (lane >> 4) + r) * a.ldg + kh * D + 16 * t + (lane & 15);
+      a.g_m[o + a.koff] = Km_[t][r] * a.scale;
+      a.g_d[o + a.koff] = Kd_[t][r] * a.scale;
+      a.g_m[o + a.voff] = Vm_[t][r];
+      a.g_d[o + a.voff] = Vd_[t][r];
+    }
+}
+
+}  // namespace
+
+bool flash_supported(int dh, int S) { return (dh == 64 || dh == 128) && S % 128 == 0; }
+
+hipError_t launch_flash_fwd(const FlashArgs& a, int B, hipStream_t s) {
+  dim3 g(a.S / 128, B * a.Hq);
+  if (a.D == 128) hipLaunchKernelGGL(flash_fwd_kernel<128>, g, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(flash_fwd_kernel<64>, g, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_flash_bwd(const FlashArgs& a, int B, hipStream_t s) {
+  const int nrows = B * a.S * a.Hq;
+  dim3 gd((nrows + 15) / 16);
+  if (a.D == 128) hipLaunchKernelGGL(flash_delta_kernel<128>, gd, dim3(256), 0, s, a, nrows);
+  else hipLaunchKernelGGL(flash_delta_kernel<64>, gd, dim3(256), 0, s, a, nrows);
+  dim3 gq(a.S / 128, B * a.Hq);
+  if (a.D == 128) hipLaunchKernelGGL(flash_bwd_q_kernel<128>, gq, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(flash_bwd_q_kernel<64>, gq, dim3(256), 0, s, a);
+  dim3 gk(a.S / 64, B * a.Hk);
+  if (a.D == 128) hipLaunchKernelGGL(flash_bwd_kv_kernel<128>, gk, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(flash_bwd_kv_kernel<64>, gk, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace fdh

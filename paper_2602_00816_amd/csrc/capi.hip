@@ -241,6 +241,13 @@ extern "C" fdh_status fdh_testing_gemm(int32_t dtype, int32_t M, int32_t N, int3
   return r == hipSuccess ? FDH_OK : FDH_ERR_HIP;
 }
 
+extern "C" fdh_status fdh_testing_unfused_attention(fdh_ctx* ctx, int32_t on) {
+  return run(ctx, [&](fdh::Engine& e) -> int {
+    e.force_unfused = on != 0;
+    return FDH_OK;
+  });
+}
+
 extern "C" fdh_status fdh_testing_timing(fdh_ctx* ctx, int32_t enable) {
   return run(ctx, [&](fdh::Engine& e) -> int {
     if (e.timing.on) {

@@ -67,6 +67,10 @@ class Engine {
   char* ws = nullptr;
   size_t ws_bytes = 0;
   int planB = 0, planS = 0, planM = 0;
+  // attention path of the current plan: fused kernels (bf16, head dim 64 or
+  // 128, S a multiple of 128) or score/probability matrices in the workspace
+  bool fused = false;
+  bool force_unfused = false;   // testing: plan the unfused path even where the fused one applies
   fdh_lanczos_opts planO{};
   size_t plan(int B, int S, int m, const fdh_lanczos_opts* o, bool carve);
 
@@ -99,12 +103,12 @@ class Engine {
 
   // workspace spans
   struct LayerSpans {
-    Span x_in_m, x_in_d, a_m, a_d, qkv_m, qkv_d, P_m, P_d, o_m, o_d, xmid_m, xmid_d, b_m, b_d, u_m, u_d, z_m, z_d;
+    Span x_in_m, x_in_d, a_m, a_d, qkv_m, qkv_d, P_m, P_d, st, o_m, o_d, xmid_m, xmid_d, b_m, b_d, u_m, u_d, z_m, z_d;
   };
   std::vector<LayerSpans> ls;
   Span xL_m, xL_d, f_m, f_d, lo, qkvf_m, qkvf_d, sc_m, sc_d, log_m, log_d, dlog_m, dlog_d, rowloss, losses;
   Span dx0_m, dx0_d, dx1_m, dx1_d, dxo_m, dxo_d, dz_m, dz_d, dgu_m, dgu_d, dudf, db_m, db_d, gpart, do_m, do_d, dS_m, dS_d;
-  Span dqkv_m, dqkv_d, dqkvo_m, dqkvo_d, gqa_m, gqa_d, da_m, da_d, colpart, keys, rope, cdf, gpartial, bpart, bout;
+  Span dqkv_m, dqkv_d, dqkvo_m, dqkvo_d, gqa_m, gqa_d, dl, da_m, da_d, colpart, keys, rope, cdf, gpartial, bpart, bout;
   Span lz_w, lz_q, lz_qp, lz_basis, lz_alpha, lz_beta, lz_coef, lz_partial, lz_flag, lz_maxabs;
 };
 

@@ -14,6 +14,7 @@
 #include "engine.h"
 
 #include <algorithm>
+#include <type_traits>
 #include <cmath>
 #include <cstring>
 
@@ -135,7 +136,9 @@ size_t Engine::plan(int B, int S, int m, const fdh_lanczos_opts* o, bool carve) 
     const size_t T_ = (size_t)B * S;
     const size_t td = T_ * d, tq = T_ * qkvd, ta = T_ * (size_t)Hq * dh;
     const size_t tu = T_ * (size_t)(gpt2 ? F : 2 * F), tz = T_ * F;
-    const size_t pp = (size_t)B * Hq * S * S;
+    fused = bf16 && !force_unfused && flash_supported(dh, S);
+    const size_t pp = fused ? 0 : (size_t)B * Hq * S * S;   // score-shaped matrices (unfused path only)
+    const size_t rows = (size_t)B * Hq * S;
     ls.assign(L, LayerSpans{});
     for (int l = 0; l < L; ++l) {
       LayerSpans& s = ls[l];
@@ -143,6 +146,7 @@ size_t Engine::plan(int B, int S, int m, const fdh_lanczos_opts* o, bool carve) 
       take(s.a_m, td * ob); take(s.a_d, td * ob);
       take(s.qkv_m, tq * ob); take(s.qkv_d, tq * ob);
       take(s.P_m, pp * ob); take(s.P_d, pp * ob);
+      take(s.st, fused ? rows * 16 : 0);
       take(s.o_m, ta * ob); take(s.o_d, ta * ob);
       take(s.xmid_m, td * 4); take(s.xmid_d, td * 4);
       take(s.b_m, td * ob); take(s.b_d, td * ob);
@@ -170,7 +174,8 @@ size_t Engine::plan(int B, int S, int m, const fdh_lanczos_opts* o, bool carve) 
     take(dS_m, pp * ob); take(dS_d, pp * ob);
     take(dqkv_m, tq * 4); take(dqkv_d, tq * 4);
     take(dqkvo_m, tq * ob); take(dqkvo_d, tq * ob);
-    take(gqa_m, Hq != Hk ? ta * 4 : 0); take(gqa_d, Hq != Hk ? ta * 4 : 0);
+    take(gqa_m, Hq != Hk && !fused ? ta * 4 : 0); take(gqa_d, Hq != Hk && !fused ? ta * 4 : 0);
+    take(dl, fused ? rows * 8 : 0);
     take(da_m, td * 4); take(da_d, td * 4);
     const size_t maxc = std::max<size_t>({(size_t)qkvd, (size_t)F, (size_t)d, (size_t)1});
     take(colpart, 64 * maxc * 8);
@@ -316,6 +321,16 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, i
   const float neps = cfg.norm_eps;
   const int G = Hq / Hk;
   const float att_scale = (float)(1.0 / std::sqrt((double)dh));
+  // fused attention arguments shared by the forward and backward launches
+  auto flash_args = [&](const T* qm_, const T* qd_, float scale) {
+    FlashArgs fa{};
+    fa.qkv_m = (const bf16_t*)qm_; fa.qkv_d = (const bf16_t*)qd_; fa.ld = qkvd;
+    fa.S = S; fa.Hq = Hq; fa.Hk = Hk; fa.G = G; fa.D = dh;
+    fa.koff = Hq * dh; fa.voff = (Hq + Hk) * dh;
+    fa.scale = scale;
+    fa.ldo = (int64_t)Hq * dh;
+    return fa;
+  };
   auto F32 = [&](const Span& s) { return (float*)(ws + s.off); };
   auto OP = [&](const Span& s) { return (T*)(ws + s.off); };
   T* lo = OP(this->lo);
@@ -413,48 +428,57 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, i
     RC(lin_fwd(OP(s.a_m), OP(s.a_d), d, R.wqkv, R.bqkv, F32(qkvf_m), F32(qkvf_d), nullptr, nullptr, qkvd));
     CK(launch_qkv_post<T>(PairT<T>{OP(s.qkv_m), OP(s.qkv_d)}, F32(qkvf_m), F32(qkvf_d), T_, S, Hq, Hk, dh,
                           (const double*)(ws + rope.off), llama, st));
-    // scores S = q k^T / sqrt(dh), causal
-    {
-      const T* qm = OP(s.qkv_m);
-      const T* qd = OP(s.qkv_d);
-      GemmOperand Aq_m = kmaj(qm, qkvd), Aq_d = kmaj(qd, qkvd);
-      GemmOperand Bk_m = kmaj(qm + Hq * dh, qkvd), Bk_d = kmaj(qd + Hq * dh, qkvd);
-      for (GemmOperand* o : {&Aq_m, &Aq_d}) { o->s_outer = (int64_t)S * qkvd; o->s_inner = dh; }
-      for (GemmOperand* o : {&Bk_m, &Bk_d}) { o->s_outer = (int64_t)S * qkvd; o->s_inner = dh; o->inner_div = G; }
-      GemmArgs g;
-      g.M = S; g.N = S; g.K = dh; g.nbatch = B * Hq; g.inner_count = Hq;
-      g.A[0] = Aq_m; g.B[0] = Bk_m;
-      g.C = F32(sc_m); g.ldc = S; g.c_outer = (int64_t)Hq * pp_stride; g.c_inner = pp_stride;
-      g.alpha = att_scale; g.causal = CAUSAL_SKIP_UPPER;
-      RG(T, g);
-      GemmArgs h = g;
-      h.npairs = 2;
-      h.A[0] = Aq_m; h.B[0] = Bk_d;
-      h.A[1] = Aq_d; h.B[1] = Bk_m;
-      h.C = F32(sc_d);
-      RG(T, h);
-    }
-    CK(launch_attn_softmax<T>(PairT<T>{OP(s.P_m), OP(s.P_d)}, F32(sc_m), F32(sc_d), B * Hq * S, S, st));
-    // o = P v
-    {
-      const T* vm = OP(s.qkv_m) + (Hq + Hk) * dh;
-      const T* vd = OP(s.qkv_d) + (Hq + Hk) * dh;
-      GemmOperand Ap_m = kmaj(OP(s.P_m), S), Ap_d = kmaj(OP(s.P_d), S);
-      for (GemmOperand* o : {&Ap_m, &Ap_d}) { o->s_outer = (int64_t)Hq * pp_stride; o->s_inner = pp_stride; }
-      GemmOperand Bv_m = mnmaj(vm, qkvd), Bv_d = mnmaj(vd, qkvd);
-      for (GemmOperand* o : {&Bv_m, &Bv_d}) { o->s_outer = (int64_t)S * qkvd; o->s_inner = dh; o->inner_div = G; }
-      GemmArgs g;
-      g.M = S; g.N = dh; g.K = S; g.nbatch = B * Hq; g.inner_count = Hq;
-      g.A[0] = Ap_m; g.B[0] = Bv_m;
-      g.C = OP(s.o_m); g.ldc = (int64_t)Hq * dh; g.c_outer = (int64_t)S * Hq * dh; g.c_inner = dh;
-      g.out_type = OUT_OP; g.causal = CAUSAL_K_LE_M;
-      RG(T, g);
-      GemmArgs h = g;
-      h.npairs = 2;
-      h.A[0] = Ap_m; h.B[0] = Bv_d;
-      h.A[1] = Ap_d; h.B[1] = Bv_m;
-      h.C = OP(s.o_d);
-      RG(T, h);
+    if (fused) {
+      if constexpr (std::is_same<T, bf16_t>::value) {
+        FlashArgs fa = flash_args(OP(s.qkv_m), OP(s.qkv_d), att_scale);
+        fa.o_m = OP(s.o_m); fa.o_d = OP(s.o_d);
+        fa.stats = (float4*)(ws + s.st.off);
+        CK(launch_flash_fwd(fa, B, st));
+      }
+    } else {
+      // scores S = q k^T / sqrt(dh), causal
+      {
+        const T* qm = OP(s.qkv_m);
+        const T* qd = OP(s.qkv_d);
+        GemmOperand Aq_m = kmaj(qm, qkvd), Aq_d = kmaj(qd, qkvd);
+        GemmOperand Bk_m = kmaj(qm + Hq * dh, qkvd), Bk_d = kmaj(qd + Hq * dh, qkvd);
+        for (GemmOperand* o : {&Aq_m, &Aq_d}) { o->s_outer = (int64_t)S * qkvd; o->s_inner = dh; }
+        for (GemmOperand* o : {&Bk_m, &Bk_d}) { o->s_outer = (int64_t)S * qkvd; o->s_inner = dh; o->inner_div = G; }
+        GemmArgs g;
+        g.M = S; g.N = S; g.K = dh; g.nbatch = B * Hq; g.inner_count = Hq;
+        g.A[0] = Aq_m; g.B[0] = Bk_m;
+        g.C = F32(sc_m); g.ldc = S; g.c_outer = (int64_t)Hq * pp_stride; g.c_inner = pp_stride;
+        g.alpha = att_scale; g.causal = CAUSAL_SKIP_UPPER;
+        RG(T, g);
+        GemmArgs h = g;
+        h.npairs = 2;
+        h.A[0] = Aq_m; h.B[0] = Bk_d;
+        h.A[1] = Aq_d; h.B[1] = Bk_m;
+        h.C = F32(sc_d);
+        RG(T, h);
+      }
+      CK(launch_attn_softmax<T>(PairT<T>{OP(s.P_m), OP(s.P_d)}, F32(sc_m), F32(sc_d), B * Hq * S, S, st));
+      // o = P v
+      {
+        const T* vm = OP(s.qkv_m) + (Hq + Hk) * dh;
+        const T* vd = OP(s.qkv_d) + (Hq + Hk) * dh;
+        GemmOperand Ap_m = kmaj(OP(s.P_m), S), Ap_d = kmaj(OP(s.P_d), S);
+        for (GemmOperand* o : {&Ap_m, &Ap_d}) { o->s_outer = (int64_t)Hq * pp_stride; o->s_inner = pp_stride; }
+        GemmOperand Bv_m = mnmaj(vm, qkvd), Bv_d = mnmaj(vd, qkvd);
+        for (GemmOperand* o : {&Bv_m, &Bv_d}) { o->s_outer = (int64_t)S * qkvd; o->s_inner = dh; o->inner_div = G; }
+        GemmArgs g;
+        g.M = S; g.N = dh; g.K = S; g.nbatch = B * Hq; g.inner_count = Hq;
+        g.A[0] = Ap_m; g.B[0] = Bv_m;
+        g.C = OP(s.o_m); g.ldc = (int64_t)Hq * dh; g.c_outer = (int64_t)S * Hq * dh; g.c_inner = dh;
+        g.out_type = OUT_OP; g.causal = CAUSAL_K_LE_M;
+        RG(T, g);
+        GemmArgs h = g;
+        h.npairs = 2;
+        h.A[0] = Ap_m; h.B[0] = Bv_d;
+        h.A[1] = Ap_d; h.B[1] = Bv_m;
+        h.C = OP(s.o_d);
+        RG(T, h);
+      }
     }
     // output projection + residual
     RC(lin_fwd(OP(s.o_m), OP(s.o_d), Hq * dh, R.wo, R.bo, F32(s.xmid_m), F32(s.xmid_d), xm, xd, d));
@@ -525,107 +549,121 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, i
     RC(lin_dgrad(gom, god, d, R.wo, Hq * dh, OP(do_m), OP(do_d), OUT_OP));
     const T* qm = OP(s.qkv_m);
     const T* qd = OP(s.qkv_d);
-    // dP = do v^T
-    {
-      GemmOperand Ao_m = kmaj(OP(do_m), (int64_t)Hq * dh), Ao_d = kmaj(OP(do_d), (int64_t)Hq * dh);
-      for (GemmOperand* o : {&Ao_m, &Ao_d}) { o->s_outer = (int64_t)S * Hq * dh; o->s_inner = dh; }
-      GemmOperand Bv_m = kmaj(qm + (Hq + Hk) * dh, qkvd), Bv_d = kmaj(qd + (Hq + Hk) * dh, qkvd);
-      for (GemmOperand* o : {&Bv_m, &Bv_d}) { o->s_outer = (int64_t)S * qkvd; o->s_inner = dh; o->inner_div = G; }
-      GemmArgs g;
-      g.M = S; g.N = S; g.K = dh; g.nbatch = B * Hq; g.inner_count = Hq;
-      g.A[0] = Ao_m; g.B[0] = Bv_m;
-      g.C = F32(sc_m); g.ldc = S; g.c_outer = (int64_t)Hq * pp_stride; g.c_inner = pp_stride;
-      g.causal = CAUSAL_SKIP_UPPER;
-      RG(T, g);
-      GemmArgs h = g;
-      h.npairs = 2;
-      h.A[0] = Ao_m; h.B[0] = Bv_d;
-      h.A[1] = Ao_d; h.B[1] = Bv_m;
-      h.C = F32(sc_d);
-      RG(T, h);
+    float* gm = F32(dqkv_m);
+    float* gd = F32(dqkv_d);
+    if (fused) {
+      if constexpr (std::is_same<T, bf16_t>::value) {
+        FlashArgs fa = flash_args(OP(s.qkv_m), OP(s.qkv_d), att_scale);
+        fa.o_m = OP(s.o_m); fa.o_d = OP(s.o_d);
+        fa.stats = (float4*)(ws + s.st.off);
+        fa.do_m = OP(do_m); fa.do_d = OP(do_d);
+        fa.delta = (float2*)(ws + dl.off);
+        fa.g_m = gm; fa.g_d = gd; fa.ldg = qkvd;
+        CK(launch_flash_bwd(fa, B, st));
+      }
+    } else {
+      // dP = do v^T
+      {
+        GemmOperand Ao_m = kmaj(OP(do_m), (int64_t)Hq * dh), Ao_d = kmaj(OP(do_d), (int64_t)Hq * dh);
+        for (GemmOperand* o : {&Ao_m, &Ao_d}) { o->s_outer = (int64_t)S * Hq * dh; o->s_inner = dh; }
+        GemmOperand Bv_m = kmaj(qm + (Hq + Hk) * dh, qkvd), Bv_d = kmaj(qd + (Hq + Hk) * dh, qkvd);
+        for (GemmOperand* o : {&Bv_m, &Bv_d}) { o->s_outer = (int64_t)S * qkvd; o->s_inner = dh; o->inner_div = G; }
+        GemmArgs g;
+        g.M = S; g.N = S; g.K = dh; g.nbatch = B * Hq; g.inner_count = Hq;
+        g.A[0] = Ao_m; g.B[0] = Bv_m;
+        g.C = F32(sc_m); g.ldc = S; g.c_outer = (int64_t)Hq * pp_stride; g.c_inner = pp_stride;
+        g.causal = CAUSAL_SKIP_UPPER;
+        RG(T, g);
+        GemmArgs h = g;
+        h.npairs = 2;
+        h.A[0] = Ao_m; h.B[0] = Bv_d;
+        h.A[1] = Ao_d; h.B[1] = Bv_m;
+        h.C = F32(sc_d);
+        RG(T, h);
+      }
+      CK(launch_attn_dsoftmax<T>(PairT<T>{OP(dS_m), OP(dS_d)}, OP(s.P_m), OP(s.P_d), F32(sc_m), F32(sc_d), B * Hq * S, S, st));
+      // dv = P^T do ; dq = dS k / sqrt(dh) ; dk = dS^T q / sqrt(dh)
+      {
+        const bool grp = G > 1;
+        // helpers for the per-(b,h) outputs
+        auto out_into = [&](GemmArgs& g, bool to_tmp) {
+          if (to_tmp) {
+            g.ldc = (int64_t)Hq * dh; g.c_outer = (int64_t)S * Hq * dh; g.c_inner = dh;
+          } else {
+            g.ldc = qkvd; g.c_outer = (int64_t)S * qkvd; g.c_inner = dh;
+          }
+        };
+        // dv
+        GemmOperand At_m = mnmaj(OP(s.P_m), S), At_d = mnmaj(OP(s.P_d), S);
+        for (GemmOperand* o : {&At_m, &At_d}) { o->s_outer = (int64_t)Hq * pp_stride; o->s_inner = pp_stride; }
+        GemmOperand Bo_m = mnmaj(OP(do_m), (int64_t)Hq * dh), Bo_d = mnmaj(OP(do_d), (int64_t)Hq * dh);
+        for (GemmOperand* o : {&Bo_m, &Bo_d}) { o->s_outer = (int64_t)S * Hq * dh; o->s_inner = dh; }
+        const int voff = (Hq + Hk) * dh, koff = Hq * dh;
+        {
+          GemmArgs g;
+          g.M = S; g.N = dh; g.K = S; g.nbatch = B * Hq; g.inner_count = Hq; g.causal = CAUSAL_K_GE_M;
+          g.A[0] = At_m; g.B[0] = Bo_m;
+          out_into(g, grp);
+          g.C = grp ? F32(gqa_m) : gm + voff;
+          RG(T, g);
+          GemmArgs h = g;
+          h.npairs = 2;
+          h.A[0] = At_m; h.B[0] = Bo_d;
+          h.A[1] = At_d; h.B[1] = Bo_m;
+          h.C = grp ? F32(gqa_d) : gd + voff;
+          RG(T, h);
+          if (grp) {
+            CK(launch_group_sum(gm + voff, qkvd, F32(gqa_m), T_, Hk, G, dh, st));
+            CK(launch_group_sum(gd + voff, qkvd, F32(gqa_d), T_, Hk, G, dh, st));
+          }
+        }
+        // dq
+        {
+          GemmOperand As_m = kmaj(OP(dS_m), S), As_d = kmaj(OP(dS_d), S);
+          for (GemmOperand* o : {&As_m, &As_d}) { o->s_outer = (int64_t)Hq * pp_stride; o->s_inner = pp_stride; }
+          GemmOperand Bk_m = mnmaj(qm + koff, qkvd), Bk_d = mnmaj(qd + koff, qkvd);
+          for (GemmOperand* o : {&Bk_m, &Bk_d}) { o->s_outer = (int64_t)S * qkvd; o->s_inner = dh; o->inner_div = G; }
+          GemmArgs g;
+          g.M = S; g.N = dh; g.K = S; g.nbatch = B * Hq; g.inner_count = Hq; g.causal = CAUSAL_K_LE_M;
+          g.alpha = att_scale;
+          g.A[0] = As_m; g.B[0] = Bk_m;
+          out_into(g, false);
+          g.C = gm;
+          RG(T, g);
+          GemmArgs h = g;
+          h.npairs = 2;
+          h.A[0] = As_m; h.B[0] = Bk_d;
+          h.A[1] = As_d; h.B[1] = Bk_m;
+          h.C = gd;
+          RG(T, h);
+        }
+        // dk
+        {
+          GemmOperand Ast_m = mnmaj(OP(dS_m), S), Ast_d = mnmaj(OP(dS_d), S);
+          for (GemmOperand* o : {&Ast_m, &Ast_d}) { o->s_outer = (int64_t)Hq * pp_stride; o->s_inner = pp_stride; }
+          GemmOperand Bq_m = mnmaj(qm, qkvd), Bq_d = mnmaj(qd, qkvd);
+          for (GemmOperand* o : {&Bq_m, &Bq_d}) { o->s_outer = (int64_t)S * qkvd; o->s_inner = dh; }
+          GemmArgs g;
+          g.M = S; g.N = dh; g.K = S; g.nbatch = B * Hq; g.inner_count = Hq; g.causal = CAUSAL_K_GE_M;
+          g.alpha = att_scale;
+          g.A[0] = Ast_m; g.B[0] = Bq_m;
+          out_into(g, grp);
+          g.C = grp ? F32(gqa_m) : gm + koff;
+          RG(T, g);
+          GemmArgs h = g;
+          h.npairs = 2;
+          h.A[0] = Ast_m; h.B[0] = Bq_d;
+          h.A[1] = Ast_d; h.B[1] = Bq_m;
+          h.C = grp ? F32(gqa_d) : gd + koff;
+          RG(T, h);
+          if (grp) {
+            CK(launch_group_sum(gm + koff, qkvd, F32(gqa_m), T_, Hk, G, dh, st));
+            CK(launch_group_sum(gd + koff, qkvd, F32(gqa_d), T_, Hk, G, dh, st));
+          }
+        }
+      }
     }
-    CK(launch_attn_dsoftmax<T>(PairT<T>{OP(dS_m), OP(dS_d)}, OP(s.P_m), OP(s.P_d), F32(sc_m), F32(sc_d), B * Hq * S, S, st));
-    // dv = P^T do ; dq = dS k / sqrt(dh) ; dk = dS^T q / sqrt(dh)
     {
-      float* gm = F32(dqkv_m);
-      float* gd = F32(dqkv_d);
-      const bool grp = G > 1;
-      // helpers for the per-(b,h) outputs
-      auto out_into = [&](GemmArgs& g, bool to_tmp) {
-        if (to_tmp) {
-          g.ldc = (int64_t)Hq * dh; g.c_outer = (int64_t)S * Hq * dh; g.c_inner = dh;
-        } else {
-          g.ldc = qkvd; g.c_outer = (int64_t)S * qkvd; g.c_inner = dh;
-        }
-      };
-      // dv
-      GemmOperand At_m = mnmaj(OP(s.P_m), S), At_d = mnmaj(OP(s.P_d), S);
-      for (GemmOperand* o : {&At_m, &At_d}) { o->s_outer = (int64_t)Hq * pp_stride; o->s_inner = pp_stride; }
-      GemmOperand Bo_m = mnmaj(OP(do_m), (int64_t)Hq * dh), Bo_d = mnmaj(OP(do_d), (int64_t)Hq * dh);
-      for (GemmOperand* o : {&Bo_m, &Bo_d}) { o->s_outer = (int64_t)S * Hq * dh; o->s_inner = dh; }
-      const int voff = (Hq + Hk) * dh, koff = Hq * dh;
-      {
-        GemmArgs g;
-        g.M = S; g.N = dh; g.K = S; g.nbatch = B * Hq; g.inner_count = Hq; g.causal = CAUSAL_K_GE_M;
-        g.A[0] = At_m; g.B[0] = Bo_m;
-        out_into(g, grp);
-        g.C = grp ? F32(gqa_m) : gm + voff;
-        RG(T, g);
-        GemmArgs h = g;
-        h.npairs = 2;
-        h.A[0] = At_m; h.B[0] = Bo_d;
-        h.A[1] = At_d; h.B[1] = Bo_m;
-        h.C = grp ? F32(gqa_d) : gd + voff;
-        RG(T, h);
-        if (grp) {
-          CK(launch_group_sum(gm + voff, qkvd, F32(gqa_m), T_, Hk, G, dh, st));
-          CK(launch_group_sum(gd + voff, qkvd, F32(gqa_d), T_, Hk, G, dh, st));
-        }
-      }
-      // dq
-      {
-        GemmOperand As_m = kmaj(OP(dS_m), S), As_d = kmaj(OP(dS_d), S);
-        for (GemmOperand* o : {&As_m, &As_d}) { o->s_outer = (int64_t)Hq * pp_stride; o->s_inner = pp_stride; }
-        GemmOperand Bk_m = mnmaj(qm + koff, qkvd), Bk_d = mnmaj(qd + koff, qkvd);
-        for (GemmOperand* o : {&Bk_m, &Bk_d}) { o->s_outer = (int64_t)S * qkvd; o->s_inner = dh; o->inner_div = G; }
-        GemmArgs g;
-        g.M = S; g.N = dh; g.K = S; g.nbatch = B * Hq; g.inner_count = Hq; g.causal = CAUSAL_K_LE_M;
-        g.alpha = att_scale;
-        g.A[0] = As_m; g.B[0] = Bk_m;
-        out_into(g, false);
-        g.C = gm;
-        RG(T, g);
-        GemmArgs h = g;
-        h.npairs = 2;
-        h.A[0] = As_m; h.B[0] = Bk_d;
-        h.A[1] = As_d; h.B[1] = Bk_m;
-        h.C = gd;
-        RG(T, h);
-      }
-      // dk
-      {
-        GemmOperand Ast_m = mnmaj(OP(dS_m), S), Ast_d = mnmaj(OP(dS_d), S);
-        for (GemmOperand* o : {&Ast_m, &Ast_d}) { o->s_outer = (int64_t)Hq * pp_stride; o->s_inner = pp_stride; }
-        GemmOperand Bq_m = mnmaj(qm, qkvd), Bq_d = mnmaj(qd, qkvd);
-        for (GemmOperand* o : {&Bq_m, &Bq_d}) { o->s_outer = (int64_t)S * qkvd; o->s_inner = dh; }
-        GemmArgs g;
-        g.M = S; g.N = dh; g.K = S; g.nbatch = B * Hq; g.inner_count = Hq; g.causal = CAUSAL_K_GE_M;
-        g.alpha = att_scale;
-        g.A[0] = Ast_m; g.B[0] = Bq_m;
-        out_into(g, grp);
-        g.C = grp ? F32(gqa_m) : gm + koff;
-        RG(T, g);
-        GemmArgs h = g;
-        h.npairs = 2;
-        h.A[0] = Ast_m; h.B[0] = Bq_d;
-        h.A[1] = Ast_d; h.B[1] = Bq_m;
-        h.C = grp ? F32(gqa_d) : gd + koff;
-        RG(T, h);
-        if (grp) {
-          CK(launch_group_sum(gm + koff, qkvd, F32(gqa_m), T_, Hk, G, dh, st));
-          CK(launch_group_sum(gd + koff, qkvd, F32(gqa_d), T_, Hk, G, dh, st));
-        }
-      }
       if (gpt2) RC(colsum_hv(gd, qkvd, qkvd, R.bqkv));
       CK(launch_qkv_bwd_post<T>(PairT<T>{OP(dqkvo_m), OP(dqkvo_d)}, gm, gd, T_, S, Hq, Hk, dh,
                                 (const double*)(ws + rope.off), llama, st));
@@ -669,6 +707,7 @@ int Engine::hvp(const void* params, const float* v, double eps, const int32_t* t
   if ((int64_t)B * S > 16384) { err = "B*S must be <= 16384"; return FDH_ERR_UNSUPPORTED; }
   if (S > 4096) { err = "S must be <= 4096"; return FDH_ERR_UNSUPPORTED; }
   if (S % 8 || dh % 8) { err = "S and head_dim must be multiples of 8"; return FDH_ERR_UNSUPPORTED; }
+  if (fused && S % 128) { err = "this workspace uses fused attention: S must be a multiple of 128"; return FDH_ERR_UNSUPPORTED; }
   if (bf16) return hvp_t<bf16_t>((const bf16_t*)params, v, eps, tok, B, S, hv);
   return hvp_t<float>((const float*)params, v, eps, tok, B, S, hv);
 }

@@ -108,6 +108,31 @@ hipError_t launch_attn_dsoftmax(PairT<T> dS, const T* Pm, const T* Pd, const flo
 // GQA: sum groups of G consecutive query-head gradients into KV heads
 hipError_t launch_group_sum(float* out, int64_t out_ld, const float* in, int T_, int Hk, int G, int dh, hipStream_t s);
 
+// ---- attn.hip: fused causal attention of the pair (bf16 operands) ------------
+struct FlashArgs {
+  const bf16_t* qkv_m;   // [T][ld]: post-RoPE q (cols h*D), k (koff + kh*D), v (voff + kh*D)
+  const bf16_t* qkv_d;
+  int64_t ld;
+  int S, Hq, Hk, G, D;   // G = Hq / Hk query heads per key/value head
+  int koff, voff;
+  float scale;           // 1 / sqrt(D)
+  bf16_t* o_m;           // [T][ldo] attention output (forward), input of the backward
+  bf16_t* o_d;
+  int64_t ldo;
+  float4* stats;         // [B*Hq][S]: row max of the logits, u, w (forward -> backward)
+  const bf16_t* do_m;    // [T][ldo] output gradient (backward)
+  const bf16_t* do_d;
+  float2* delta;         // [B*Hq][S] row terms (backward scratch)
+  float* g_m;            // [T][ldg] fp32 gradients of q, k, v (same column layout as qkv)
+  float* g_d;
+  int64_t ldg;
+};
+// head dimension 64 or 128, S a multiple of 128
+bool flash_supported(int dh, int S);
+hipError_t launch_flash_fwd(const FlashArgs& a, int B, hipStream_t s);
+// row terms, dq (query columns of g) and dk, dv (key/value columns, summed over each group)
+hipError_t launch_flash_bwd(const FlashArgs& a, int B, hipStream_t s);
+
 // activations at both points
 template <typename T>
 hipError_t launch_gelu_fwd(PairT<T> z, const float* um, const float* ud, int64_t n, hipStream_t s);

@@ -1,0 +1,72 @@
+"""Fused attention kernels against the unfused attention path on the GPU.
+
+The unfused path (score/probability matrices through the GEMM and row
+kernels) is itself pinned to the fp64 oracle by the parity tests; here the
+fused kernels (forward, dQ, dK/dV) must reproduce its HVP on the same inputs
+to within bf16 rounding, per parameter block, at the workloads' head layouts:
+head dimension 128 (Llama 1.3B), 64 (GPT-2 medium) and grouped keys/values
+(Llama-3 8B: 32 query heads on 8 key/value heads).  The oracle comparison of
+the fused path itself runs in the parity tests, which use it for bf16 models.
+"""
+import numpy as np
+import pytest
+
+from oracle import model as M
+from synth.workloads import WORKLOADS
+from tests import micro
+from tests.gpu_util import need_gpu, rel_l2, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _both_paths(w, batch, seq, eps=1e-3):
+    torch = need_gpu()
+    from paper_2602_00816_amd import fdhvp as fd
+    out = []
+    for unfused in (False, True):
+        mod = fd.Model.from_workload(w)
+        mod.unfused_attention(unfused)
+        mod.set_workspace(batch, seq)
+        th = mod.init_params(1)
+        tok = mod.make_tokens(batch, seq, 2, "zipf")
+        v = mod.random_vector(3, "rademacher")
+        out.append(mod.hvp(th, v, eps, tok).double().cpu().numpy())
+        del mod
+        torch.cuda.synchronize()
+    cfg = micro.cfg_of(w, bf16=True)
+    return out[0], out[1], M.layout(cfg)
+
+
+@pytest.mark.parametrize("name,layers,batch,seq", [
+    ("llama-1.3b-bf16", 1, 1, 512),
+    ("gpt2-medium-bf16", 2, 2, 256),
+    ("llama3-8b-bf16", 1, 1, 384),
+])
+def test_fused_matches_unfused(name, layers, batch, seq):
+    w = dict(WORKLOADS[name], n_layers=layers)
+    say(f"fused vs unfused attention: {name}, {layers} layer(s), {batch}x{seq}")
+    fused, unfused, layout = _both_paths(w, batch, seq)
+    assert np.all(np.isfinite(fused))
+    err = rel_l2(fused, unfused)
+    say(f"  rel_l2 {err:.3e}")
+    assert err <= 2e-2
+    for e in layout:
+        ref = unfused[e.offset:e.offset + e.numel]
+        if e.numel >= 4096 and np.linalg.norm(ref) > 1e-3 * np.linalg.norm(unfused):
+            be = rel_l2(fused[e.offset:e.offset + e.numel], ref)
+            assert be <= 5e-2, (e.name, be)
+
+
+def test_fused_rejects_unaligned_sequence():
+    """A workspace planned for the fused path refuses S that is not a multiple of 128."""
+    torch = need_gpu()
+    from paper_2602_00816_amd import fdhvp as fd
+    w = dict(WORKLOADS["llama-1.3b-bf16"], n_layers=1)
+    mod = fd.Model.from_workload(w)
+    mod.set_workspace(1, 256)
+    th = mod.init_params(1)
+    tok = mod.make_tokens(1, 200, 2, "zipf")
+    v = mod.random_vector(3, "rademacher")
+    with pytest.raises(fd.FdhError):
+        mod.hvp(th, v, 1e-3, tok)
+    torch.cuda.synchronize()
