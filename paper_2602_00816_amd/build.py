@@ -22,11 +22,15 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-u
          "-I" + os.path.join(os.path.dirname(HERE), "include")]
 
 SOURCES = ["gemm.hip", "attn.hip", "rng.hip", "vec.hip", "lm.hip", "engine.hip", "capi.hip"]
+# The fused attention kernels keep their MFMA accumulators in VGPRs: with the
+# default AGPR form the allocator moves the output accumulators through VGPRs
+# around every score product.
+EXTRA = {"attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def _compile(src: str) -> str:
     obj = os.path.join(OUT, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *FLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stderr[-6000:]}")

@@ -20,9 +20,12 @@
 //   dV.m = P.m^T dO.m              dV.d = P.m^T dO.d + P.d^T dO.m
 //   dQ.m = dS.m K.m                dQ.d = dS.m K.d + dS.d K.m      (x scale)
 //   dK.m = dS.m^T Q.m              dK.d = dS.m^T Q.d + dS.d^T Q.m  (x scale)
-// The forward runs the softmax online over key blocks (running maximum of a,
-// rescaled accumulators of e^a cosh b V.m, e^a sinh b V.m, e^a cosh b V.d)
-// and stores per query row (max a, u, w) for the backward.
+// The forward runs the softmax online over key blocks with two accumulators,
+// Ac = sum e^a cosh b V.m and X = sum e^a (sinh b V.m + cosh b V.d), giving
+// O.m = u Ac and O.d = u X - w Ac; the term -w sum e^a sinh b V.m of O.m is
+// of order eps^2 relative, like the P.d V.d term the pair form drops.  The
+// reference maximum of a moves lazily (see flash_fwd_kernel), and per query
+// row (reference maximum, u, w) is stored for the backward.
 //
 // Three kernels, each with MFMA tiles oriented so that the probability-like
 // accumulator feeds the next MFMA straight from registers: a 32x32 (16x16)
@@ -196,52 +199,29 @@ __global__ __launch_bounds__(256) void flash_fwd_kernel(FlashArgs a) {
     for (int s = 0; s < KS; ++s) {
       qm[s] = *reinterpret_cast<const bf16x8_t*>(a.qkv_m + off + 16 * s);
       qd[s] = *reinterpret_cast<const bf16x8_t*>(a.qkv_d + off + 16 * s);
+      // keep the loop-invariant Q fragments in AGPRs (MFMA operands may come
+      // from either file), leaving the VGPRs to the per-block values
+      asm volatile("" : "+a"(qm[s]));
+      asm volatile("" : "+a"(qd[s]));
     }
   }
-  f32x16_t Ac[NT], As[NT], Bc[NT];
+  // Ac = sum e^a cosh b V.m;  X = sum e^a (sinh b V.m + cosh b V.d)
+  f32x16_t Ac[NT], X[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) Ac[t][r] = As[t][r] = Bc[t][r] = 0.f;
+    for (int r = 0; r < 16; ++r) Ac[t][r] = X[t][r] = 0.f;
   float zc = 0.f, zs = 0.f;
 
   const int nkb = (q0 + 128) / KB;
   const int lastw = qw / KB;   // this wavefront's diagonal block
 
-  // Pass 1: the exact row maximum of the logits a (only S.m = K.m Q.m^T, one
-  // product in six), so that the accumulating pass never rescales: an
-  // online rescale of the 192 accumulators inside the loop makes the
-  // compiler keep VGPR copies of them and spill the Q fragments.
+  // Reference maximum of the logits, moved lazily: only when a logit exceeds
+  // it by more than 8 (e^8 ~ 3e3 keeps every term and row sum far from
+  // overflow) are the accumulators and sums rescaled, which after the first
+  // block is rare.  The accumulators live in VGPRs (this file is compiled with
+  // VGPR-form MFMAs), so the rescale branch costs nothing when not taken.
   float mrun = NEG;
-  {
-    auto issue1 = [&](int kb) {
-      const bf16_t* src[1] = {a.qkv_m + (row0 + (int64_t)kb * KB) * a.ld + a.koff + kh * D};
-      dma_tiles<D, KB, 1>(ring[kb & 1], src, a.ld, wave, lane);
-    };
-    issue1(0);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    for (int kb = 0; kb < nkb; ++kb) {
-      if (kb + 1 < nkb) issue1(kb + 1);
-      const bf16_t* Km = ring[kb & 1];
-      f32x16_t sm;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sm[r] = 0.f;
-#pragma unroll
-      for (int s = 0; s < KS; ++s) sm = mma32(ld_k32<D>(Km, 0, s, lane), qm[s], sm);
-      const bool diag = kb >= lastw;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = kb * KB + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-        if (!diag || key <= qi) mrun = fmaxf(mrun, sm[r] * a.scale);
-      }
-      __builtin_amdgcn_s_waitcnt(0);
-      __syncthreads();
-    }
-    mrun = fmaxf(mrun, __shfl_xor(mrun, 32, 64));
-  }
-
-  // Pass 2: accumulate with the fixed reference maximum
   auto issue = [&](int kb) {
     const int64_t r = row0 + (int64_t)kb * KB;
     const bf16_t* src[4] = {a.qkv_m + r * a.ld + a.koff + kh * D, a.qkv_d + r * a.ld + a.koff + kh * D,
@@ -261,15 +241,26 @@ __global__ __launch_bounds__(256) void flash_fwd_kernel(FlashArgs a) {
       const bf16_t* Kd = Km + TILE;
       const bf16_t* Vm = Km + 2 * TILE;
       const bf16_t* Vd = Km + 3 * TILE;
-      f32x16_t sm, sd;
+      // four independent accumulation chains (S.m over even / odd k steps,
+      // the two terms of S.d) keep consecutive MFMAs independent
+      f32x16_t sm, sd, sm1, sd1;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) sm[r] = sd[r] = 0.f;
+      for (int r = 0; r < 16; ++r) sm[r] = sd[r] = sm1[r] = sd1[r] = 0.f;
 #pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        const bf16x8_t km = ld_k32<D>(Km, 0, s, lane), kd = ld_k32<D>(Kd, 0, s, lane);
-        sm = mma32(km, qm[s], sm);
-        sd = mma32(km, qd[s], sd);
-        sd = mma32(kd, qm[s], sd);
+      for (int s = 0; s < KS; s += 2) {
+        const bf16x8_t km0 = ld_k32<D>(Km, 0, s, lane), kd0 = ld_k32<D>(Kd, 0, s, lane);
+        const bf16x8_t km1 = ld_k32<D>(Km, 0, s + 1, lane), kd1 = ld_k32<D>(Kd, 0, s + 1, lane);
+        sm = mma32(km0, qm[s], sm);
+        sd = mma32(km0, qd[s], sd);
+        sd1 = mma32(kd0, qm[s], sd1);
+        sm1 = mma32(km1, qm[s + 1], sm1);
+        sd = mma32(km1, qd[s + 1], sd);
+        sd1 = mma32(kd1, qm[s + 1], sd1);
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        sm[r] += sm1[r];
+        sd[r] += sd1[r];
       }
       const bool diag = kb >= lastw;
       float bmax = 0.f;
@@ -285,6 +276,24 @@ __global__ __launch_bounds__(256) void flash_fwd_kernel(FlashArgs a) {
           const int key = kb * KB + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
           if (key > qi) sm[r] = NEG;
         }
+      }
+      float amax = NEG;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) amax = fmaxf(amax, sm[r]);
+      amax = fmaxf(amax, __shfl_xor(amax, 32, 64));
+      if (__any(amax > mrun + 8.f)) {
+        const float mnew = fmaxf(mrun, amax);
+        const float alpha = __expf(mrun - mnew);
+        mrun = mnew;
+        zc *= alpha;
+        zs *= alpha;
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            Ac[t][r] *= alpha;
+            X[t][r] *= alpha;
+          }
       }
       float pc[16], ps[16];
       auto terms = [&](auto ser) {
@@ -308,8 +317,8 @@ __global__ __launch_bounds__(256) void flash_fwd_kernel(FlashArgs a) {
         for (int t = 0; t < NT; ++t) {
           const bf16x8_t vm = ld_t32<D>(Vm, 16 * t2, 32 * t, lane), vd = ld_t32<D>(Vd, 16 * t2, 32 * t, lane);
           Ac[t] = mma32(vm, bc, Ac[t]);
-          As[t] = mma32(vm, bs, As[t]);
-          Bc[t] = mma32(vd, bc, Bc[t]);
+          X[t] = mma32(vm, bs, X[t]);
+          X[t] = mma32(vd, bc, X[t]);
         }
       }
     }
@@ -330,8 +339,8 @@ __global__ __launch_bounds__(256) void flash_fwd_kernel(FlashArgs a) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int r = 4 * g + e;
-        om[e] = f32_to_bf16(u * Ac[t][r] - w * As[t][r]);
-        od[e] = f32_to_bf16(u * As[t][r] - w * Ac[t][r] + u * Bc[t][r]);
+        om[e] = f32_to_bf16(u * Ac[t][r]);
+        od[e] = f32_to_bf16(u * X[t][r] - w * Ac[t][r]);
       }
       const int64_t o = orow + 32 * t + 8 * g;
       *reinterpret_cast<uint2*>(a.o_m + o) = make_uint2(om[0] | ((uint32_t)om[1] << 16), om[2] | ((uint32_t)om[3] << 16));

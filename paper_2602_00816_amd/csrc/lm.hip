@@ -570,20 +570,35 @@ __global__ __launch_bounds__(1024) void token_sort_kernel(uint32_t* keys, const 
   for (int i = threadIdx.x; i < T_; i += 1024) keys[i] = k[i];
 }
 
-// one workgroup per sorted position; only segment starts work
+// One workgroup per (sorted position, NT-column chunk); only segment starts
+// work.  The segment end is found by binary search in the sorted keys, and
+// the segment's rows are summed with 8 partial sums (row q of the segment
+// into partial q % 8, combined in a fixed order), so that frequent tokens
+// (hundreds of rows under a Zipf distribution) keep 8 loads in flight.
 __global__ void embed_bwd_kernel(float* hv, const uint32_t* keys, const float* dxd, int T_, int dm, double inv_eps,
                                  bool acc) {
   const int j = blockIdx.x;
   const uint32_t tk = keys[j] >> 14;
   if (j > 0 && (keys[j - 1] >> 14) == tk) return;
-  int e = j + 1;
-  while (e < T_ && (keys[e] >> 14) == tk) ++e;
-  for (int c = threadIdx.x; c < dm; c += NT) {
-    double s = 0.0;
-    for (int q = j; q < e; ++q) s += (double)dxd[(int64_t)(keys[q] & 0x3FFFu) * dm + c];
-    const int64_t idx = (int64_t)tk * dm + c;
-    hv[idx] = acc ? (float)((double)hv[idx] + s * inv_eps) : (float)(s * inv_eps);
+  int lo = j + 1, hi = T_;   // first position with a larger token
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if ((keys[mid] >> 14) == tk) lo = mid + 1;
+    else hi = mid;
   }
+  const int e = lo;
+  const int c = blockIdx.y * NT + threadIdx.x;
+  if (c >= dm) return;
+  double s[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
+  int q = j;
+  for (; q + 8 <= e; q += 8) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s[u] += (double)dxd[(int64_t)(keys[q + u] & 0x3FFFu) * dm + c];
+  }
+  for (int u = 0; q < e; ++q, ++u) s[u] += (double)dxd[(int64_t)(keys[q] & 0x3FFFu) * dm + c];
+  const double t = ((s[0] + s[1]) + (s[2] + s[3])) + ((s[4] + s[5]) + (s[6] + s[7]));
+  const int64_t idx = (int64_t)tk * dm + c;
+  hv[idx] = acc ? (float)((double)hv[idx] + t * inv_eps) : (float)(t * inv_eps);
 }
 
 __global__ void pos_bwd_kernel(float* hv, const float* dxd, int B, int S, int dm, double inv_eps) {
@@ -734,7 +749,8 @@ hipError_t launch_token_sort(uint32_t* keys, const int32_t* tok, int T_, int V, 
 }
 hipError_t launch_embed_bwd(float* hv, const uint32_t* keys, const float* dxd, int T_, int dm, double inv_eps, bool acc,
                             hipStream_t s) {
-  hipLaunchKernelGGL(embed_bwd_kernel, dim3(T_), dim3(NT), 0, s, hv, keys, dxd, T_, dm, inv_eps, acc);
+  hipLaunchKernelGGL(embed_bwd_kernel, dim3(T_, (dm + NT - 1) / NT), dim3(NT), 0, s, hv, keys, dxd, T_, dm, inv_eps,
+                     acc);
   return hipGetLastError();
 }
 hipError_t launch_pos_bwd(float* hv, const float* dxd, int B, int S, int dm, double inv_eps, hipStream_t s) {
