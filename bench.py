@@ -34,8 +34,9 @@ PEAK_F32_TFLOPS = 157.3
 PEAK_HBM_GBPS = 8000.0
 
 
-def alg_flops_per_hvp(w: dict) -> float:
-    """Algorithmic FLOPs of one HVP: two gradient passes, 6 N_mm T + 3 A_fwd each."""
+def alg_flops_per_hvp(w: dict) -> tuple[float, float]:
+    """Algorithmic FLOPs of one HVP, split into (weight products, attention
+    products): two gradient passes of 6 N_mm T and 3 A_fwd each."""
     d, F, V, L = w["d_model"], w["d_ff"], w["vocab"], w["n_layers"]
     H, Hk = w["n_heads"], w["n_kv_heads"]
     dh = d // H
@@ -47,7 +48,7 @@ def alg_flops_per_hvp(w: dict) -> float:
         per_layer = d * 3 * d + d * d + d * F + F * d
     n_mm = L * per_layer + d * V
     a_fwd = L * 2.0 * B * H * S * S * dh      # causal QK^T and PV
-    return 2.0 * (6.0 * n_mm * T + 3.0 * a_fwd)
+    return 2.0 * 6.0 * n_mm * T, 2.0 * 3.0 * a_fwd
 
 
 def committed_gemm_traffic(workload: str):
@@ -88,7 +89,7 @@ def cpu_baseline(w: dict, budget_s: float = 20.0) -> dict:
     t0 = time.perf_counter()
     OH.lm_hvp(cfg, theta, v, 1e-3, tok)
     dt = time.perf_counter() - t0
-    scale = alg_flops_per_hvp(w) / alg_flops_per_hvp(sample)
+    scale = sum(alg_flops_per_hvp(w)) / sum(alg_flops_per_hvp(sample))
     return {"value": 1.0 / (dt * scale), "unit": "FD-HVPs/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{w['family']} d={w['d_model']} with 2 of {w['n_layers']} layers, 1x1024 tokens, "
                       f"fp64 numpy HVP {dt:.2f} s, scaled x{scale:.1f} by algorithmic FLOPs to the full workload"}
@@ -164,9 +165,14 @@ def main():
 
     ms_step = t_total * 1e3 / K
     value = K / t_total
-    alg = alg_flops_per_hvp(w)
+    alg_mm, alg_att = alg_flops_per_hvp(w)
+    alg = alg_mm + alg_att
     gemm_ms_per_step = tm["gemm"]["ms"] / K
-    achieved = alg / (gemm_ms_per_step * 1e-3) / 1e12
+    fused = bool(tm["attention"]["launches"] > 0)
+    # with fused attention the GEMMs carry only the weight products
+    alg_gemm = alg_mm if fused else alg
+    achieved = alg_gemm / (gemm_ms_per_step * 1e-3) / 1e12
+    att_ms_per_step = tm["attention"]["ms"] / K
     executed = tm["gemm"]["flops"] / (tm["gemm"]["ms"] * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if w["dtype"] == "bf16" else PEAK_F32_TFLOPS
     lz_gbps = tm["lanczos"]["bytes"] / (tm["lanczos"]["ms"] * 1e-3) / 1e9 if tm["lanczos"]["ms"] > 0 else None
@@ -193,6 +199,9 @@ def main():
         "gemm_launches_per_step": tm["gemm"]["launches"] / K,
         "mfma_util_executed": executed / peak,
         "model_flop_util": alg / (ms_step * 1e-3) / 1e12 / peak,
+        "attention_fused": fused,
+        "attention_ms_per_step": att_ms_per_step if fused else None,
+        "attention_tflops": (alg_att / (att_ms_per_step * 1e-3) / 1e12) if fused else None,
         "lanczos_vec_ms_per_step": tm["lanczos"]["ms"] / K,
         "lanczos_vec_hbm_GBps": lz_gbps,
         "lanczos_vec_hbm_frac": (lz_gbps / PEAK_HBM_GBPS) if lz_gbps else None,

@@ -40,13 +40,15 @@ fdh_status fdh_testing_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, int3
 fdh_status fdh_testing_unfused_attention(fdh_ctx* ctx, int32_t on);
 
 /* Per-launch timing with HIP events recorded on the context stream around every
- * GEMM launch (category 0) and every Lanczos vector launch (category 1).
+ * GEMM launch (category 0), every Lanczos vector launch (category 1) and every
+ * fused attention forward and backward (category 2).
  * enable != 0 turns it on (and clears the accumulators).  While on, the event
  * pool is drained with a stream synchronisation every few thousand launches. */
 fdh_status fdh_testing_timing(fdh_ctx* ctx, int32_t enable);
 /* Waits for the stream, then writes for categories c = 0..3:
  * out[4c+0] launches, out[4c+1] summed milliseconds, out[4c+2] executed FLOPs
- * (GEMM: 2*rows*cols*k per tile, tails clipped), out[4c+3] algorithmic bytes
+ * (GEMM: 2*rows*cols*k per tile, tails clipped; attention: algorithmic causal
+ * products of both passes, without the backward's score recompute), out[4c+3] algorithmic bytes
  * (Lanczos: every operand read or written once).  Clears the accumulators. */
 fdh_status fdh_testing_timing_read(fdh_ctx* ctx, double* out16);
 

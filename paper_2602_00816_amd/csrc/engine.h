@@ -30,7 +30,8 @@ struct Span {  // carve of the workspace
 };
 
 // Optional per-launch timing with HIP events on the context stream (testing
-// hook used by the benchmark).  Categories: 0 GEMM, 1 Lanczos vector kernels.
+// hook used by the benchmark).  Categories: 0 GEMM, 1 Lanczos vector kernels,
+// 2 fused attention (forward launch, backward launches).
 struct Timing {
   static constexpr int NCAT = 4;
   static constexpr size_t POOL = 8192;

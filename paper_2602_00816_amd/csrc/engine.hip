@@ -433,7 +433,11 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, i
         FlashArgs fa = flash_args(OP(s.qkv_m), OP(s.qkv_d), att_scale);
         fa.o_m = OP(s.o_m); fa.o_d = OP(s.o_d);
         fa.stats = (float4*)(ws + s.st.off);
+        int e0 = 0;
+        if (timing.on) CK(timing.begin(st, &e0));
         CK(launch_flash_fwd(fa, B, st));
+        // algorithmic: causal S = q k^T and P v for both passes
+        if (timing.on) CK(timing.end(st, 2, e0, 4.0 * B * Hq * (double)S * S * dh, 0.0));
       }
     } else {
       // scores S = q k^T / sqrt(dh), causal
@@ -559,7 +563,11 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, i
         fa.do_m = OP(do_m); fa.do_d = OP(do_d);
         fa.delta = (float2*)(ws + dl.off);
         fa.g_m = gm; fa.g_d = gd; fa.ldg = qkvd;
+        int e0 = 0;
+        if (timing.on) CK(timing.begin(st, &e0));
         CK(launch_flash_bwd(fa, B, st));
+        // algorithmic: causal dP, dV, dQ, dK for both passes (the score recompute is not counted)
+        if (timing.on) CK(timing.end(st, 2, e0, 8.0 * B * Hq * (double)S * S * dh, 0.0));
       }
     } else {
       // dP = do v^T

@@ -274,7 +274,7 @@ class Model:
         out = np.zeros(16)
         self._check(self._L.fdh_testing_timing_read(self._h, out.ctypes.data_as(C.POINTER(C.c_double))),
                     "fdh_testing_timing_read")
-        cats = ["gemm", "lanczos", "c2", "c3"]
+        cats = ["gemm", "lanczos", "attention", "c3"]
         return {c: dict(launches=out[4 * i], ms=out[4 * i + 1], flops=out[4 * i + 2], bytes=out[4 * i + 3])
                 for i, c in enumerate(cats)}
 
