@@ -196,11 +196,14 @@ size_t Engine::plan(int B, int S, int m, const fdh_lanczos_opts* o, bool carve) 
     take(lz_w, (size_t)P * 4);
     take(lz_q, (size_t)P * 4);
     take(lz_qp, (size_t)P * 4);
-    take(lz_basis, (size_t)cap * P * (bdt == FDH_BF16 ? 2 : 4));
+    const int64_t ldq = (P + 7) / 8 * 8;
+    if (carve) lz_ldq = ldq;
+    take(lz_basis, (size_t)cap * ldq * (bdt == FDH_BF16 ? 2 : 4));
     take(lz_alpha, (size_t)m * 8);
     take(lz_beta, (size_t)m * 8);
-    take(lz_coef, 3 * 128 * 8);
-    take(lz_partial, (size_t)RED_BLOCKS * (cap + 2) * 8);
+    take(lz_coef, 128 * 8);
+    take(lz_gram, 128 * 128 * 8);
+    take(lz_partial, (size_t)RED_BLOCKS * std::max(2 * cap, 1) * 8);
     take(lz_flag, 2 * 4);
     take(lz_maxabs, 8);
   }
@@ -336,8 +339,11 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, i
   T* lo = OP(this->lo);
   const int64_t pp_stride = (int64_t)S * S;  // per (b,h) matrix
 
-  // perturbation operand: lo = eps * v in the operand type
-  CK(launch_scale_cast<T>(lo, v, eps, P, st));
+  // perturbation operand: lo = eps * v in the operand type (unless the
+  // Lanczos normalisation already wrote it for this v and eps)
+  const bool lo_ready = lo_for_v == v && lo_for_eps == eps;
+  lo_for_v = nullptr;
+  if (!lo_ready) CK(launch_scale_cast<T>(lo, v, eps, P, st));
   if (llama) CK(launch_rope_table((double*)(ws + rope.off), S, dh, (double)cfg.rope_base, st));
 
   // ---- linear helpers ----
@@ -740,10 +746,13 @@ int Engine::lanczos_t(int m, uint64_t seed, const fdh_lanczos_opts& o, double* a
   float* q = (float*)(ws + lz_q.off);
   float* qp = (float*)(ws + lz_qp.off);
   Bt* basis = (Bt*)(ws + lz_basis.off);
+  const int64_t ldq = lz_ldq;
+  lo_for_v = nullptr;
   LanczosDev D;
   D.alpha = (double*)(ws + lz_alpha.off);
   D.beta = (double*)(ws + lz_beta.off);
   D.coef = (double*)(ws + lz_coef.off);
+  D.gram = (double*)(ws + lz_gram.off);
   D.partial = (double*)(ws + lz_partial.off);
   D.flag = (int*)(ws + lz_flag.off);
   D.maxabs = (double*)(ws + lz_maxabs.off);
@@ -767,25 +776,34 @@ int Engine::lanczos_t(int m, uint64_t seed, const fdh_lanczos_opts& o, double* a
     if (timing.on) CK(timing.end(st, 1, e0, 0.0, bytes));
     return FDH_OK;
   };
-#define TV(bytes, call)                                 \
-  do {                                                  \
-    int rc_ = timed((bytes), [&]() { return (call); }); \
-    if (rc_ != FDH_OK) return rc_;                      \
+#define TV(bytes, ...)                                         \
+  do {                                                         \
+    int rc_ = timed((bytes), [&]() { return (__VA_ARGS__); }); \
+    if (rc_ != FDH_OK) return rc_;                             \
   } while (0)
   for (int k = 0; k < m; ++k) {
     int rc = hvp(b_params, q, b_eps, b_tokens, b_B, b_S, w);
     if (rc != FDH_OK) return rc;
     TV(16.0 * Pd, launch_lanczos_alpha(w, q, qp, D, k, P, st));
     const int nv = std::min(k + 1, cap);
-    TV((12.0 + nv * bb) * Pd, launch_lanczos_b<Bt>(w, q, basis, nv, D, k, P, st));
-    if (nv > 0) {
-      TV((8.0 + nv * bb) * Pd, launch_lanczos_cgs<Bt>(w, basis, nv, D, 0, false, k, P, st));
-      TV((8.0 + nv * bb) * Pd, launch_lanczos_cgs<Bt>(w, basis, nv, D, 1, true, k, P, st));
-    }
+    if (nv > 0) TV((12.0 + nv * bb) * Pd, launch_lanczos_project<Bt>(w, q, basis, ldq, nv, k % cap, D, k, P, st));
+    TV((nv > 0 ? 8.0 + nv * bb : 12.0) * Pd, launch_lanczos_update<Bt>(w, q, basis, ldq, nv, D, k, P, st));
     Bt* row = nullptr;
-    if (cap > 0 && k + 1 < m) row = basis + (int64_t)((k + 1) % cap) * P;
-    TV((8.0 + (row ? bb : 0.0)) * Pd, launch_lanczos_normalise<Bt>(w, qp, row, D, k, tol, P, st));
+    if (cap > 0 && k + 1 < m) row = basis + (int64_t)((k + 1) % cap) * ldq;
+    // the next HVP's perturbation operand is written here too
+    const bool next_lo = !quad && k + 1 < m;
+    const double ob = bf16 ? 2.0 : 4.0;
+    if (next_lo && bf16)
+      TV((8.0 + (row ? bb : 0.0) + ob) * Pd,
+         launch_lanczos_normalise<Bt, bf16_t>(w, qp, row, (bf16_t*)(ws + this->lo.off), b_eps, D, k, tol, P, st));
+    else
+      TV((8.0 + (row ? bb : 0.0) + (next_lo ? ob : 0.0)) * Pd,
+         launch_lanczos_normalise<Bt, float>(w, qp, row, next_lo ? (float*)(ws + this->lo.off) : nullptr, b_eps, D, k, tol, P, st));
     std::swap(q, qp);
+    if (next_lo) {
+      lo_for_v = q;
+      lo_for_eps = b_eps;
+    }
   }
 #undef TV
   std::vector<double> a(m), b(m);

@@ -35,24 +35,34 @@ hipError_t launch_quad_diag_hvp(const T* theta, const float* d, const float* v, 
 struct LanczosDev {
   double* alpha;     // [m]
   double* beta;      // [m]  beta[k] = beta_{k+2} in 1-based notation (residual after step k)
-  double* coef;      // [2 * cap] reorthogonalisation coefficients (two CGS passes)
-  double* partial;   // [RED_BLOCKS * (cap + 2)]
+  double* coef;      // [128] reorthogonalisation coefficients of the current step
+  double* gram;      // [128 * 128] Gram matrix Q^T Q of the stored basis rows (by slot)
+  double* partial;   // [RED_BLOCKS * max(2 * cap, 1)]
   int* flag;         // [2]: [0] = breakdown step + 1 (0 = none), [1] = spare
   double* maxabs;    // [1]  max_j |alpha_j| so far
 };
 
-// Step A:  w <- w - beta_k q_prev;  alpha_k = <w, q>  (beta_k = beta[k-1], 0 for k = 0)
+// The basis rows are stored with a row stride ldq that is a multiple of 8
+// elements.  One Lanczos step after w = H q_k:
+// Step A:  w <- w - beta_{k-1} q_prev;  alpha_k = <w, q>  (beta_{-1} = 0)
 hipError_t launch_lanczos_alpha(float* w, const float* q, const float* qprev, LanczosDev st, int k, int64_t n, hipStream_t s);
-// Step B:  w <- w - alpha_k q; then either ||w||^2 (no reorth) or coef[0..nv) = Q^T w
+// Step B (nv >= 1 stored rows, slot `newest` holds q_k):  with
+// w1 = w - alpha_k q (w is not written), p = Q^T w1 and g = Q^T Q_newest;
+// Gram row/column `newest` <- g; coef = 2 p - G p (both classical
+// Gram-Schmidt passes).
 template <typename B>
-hipError_t launch_lanczos_b(float* w, const float* q, const B* basis, int nv, LanczosDev st, int k, int64_t n, hipStream_t s);
-// CGS correction: w <- w - sum_j coef[pass][j] Q_j ; then coef[pass+1] = Q^T w (if another pass) or ||w||^2
+hipError_t launch_lanczos_project(const float* w, const float* q, const B* basis, int64_t ldq, int nv, int newest, LanczosDev st,
+                                  int k, int64_t n, hipStream_t s);
+// Step C:  w <- (w - alpha_k q) - Q coef (no rows when nv == 0); then ||w||^2
 template <typename B>
-hipError_t launch_lanczos_cgs(float* w, const B* basis, int nv, LanczosDev st, int pass, bool last, int k, int64_t n, hipStream_t s);
-// Normalise: beta_{k+1} = ||w|| (from the last reduction); breakdown test;
-// q_next = w / beta; basis slot row written.  tol relative to max |alpha|.
-template <typename B>
-hipError_t launch_lanczos_normalise(const float* w, float* qnext, B* basis_row, LanczosDev st, int k, double tol, int64_t n, hipStream_t s);
+hipError_t launch_lanczos_update(float* w, const float* q, const B* basis, int64_t ldq, int nv, LanczosDev st, int k, int64_t n,
+                                 hipStream_t s);
+// Step D:  beta_k = ||w||; breakdown test (tol relative to max |alpha|);
+// q_next = w / beta_k; basis row (if not null) = B(q_next); the next HVP's
+// perturbation operand (if lo is not null) = T(eps * q_next).
+template <typename B, typename T>
+hipError_t launch_lanczos_normalise(const float* w, float* qnext, B* basis_row, T* lo, double eps, LanczosDev st, int k, double tol,
+                                    int64_t n, hipStream_t s);
 
 // Per-block sums over host ranges [nblk][2]:
 // out[b*4 + {0,1,2,3}] = ||a_b||^2, ||b_b||^2, <a_b, b_b>, ||a_b - b_b||^2

@@ -10,19 +10,18 @@
 // order.  No floating-point atomics anywhere.
 #include "kernels.h"
 
+#include <type_traits>
+
 namespace fdh {
 
 namespace {
 
 constexpr int NT = 256;
-constexpr int JG = 16;   // basis rows reduced per sweep (fp64 accumulators per thread)
 
 __host__ __device__ inline int64_t red_chunk(int64_t n) {
   int64_t c = (n + RED_BLOCKS - 1) / RED_BLOCKS;
   return (c + 1023) / 1024 * 1024;
 }
-
-template <typename B> __device__ inline float ldb(const B* p, int64_t i) { return ldf(p, i); }
 
 unsigned grid_for(int64_t n) {
   int64_t g = (n + NT - 1) / NT;
@@ -54,224 +53,277 @@ __global__ void quad_diag_kernel(const T* th, const float* d, const float* v, do
 }
 
 // ---- Lanczos ----------------------------------------------------------------
-// Step A: w <- w - beta_k qprev ; partial = <w, q>
-__global__ void lz_alpha_kernel(float* w, const float* q, const float* qprev, const double* beta, int k,
-                                int64_t n, double* partial) {
+// Every pass works on groups of 8 consecutive elements per lane (two 16-byte
+// loads of an fp32 vector, one of a bf16 basis row).  Workgroup chunks start at
+// multiples of 1024 elements and basis rows at multiples of 8 (row stride
+// ldq), so every full group is aligned; the group that crosses the end of the
+// vector is loaded and stored element by element, with zeros past the end.
+struct V8 { float x[8]; };
+__device__ inline V8 ld8(const float* p, int64_t i) {
+  const float4 a = *reinterpret_cast<const float4*>(p + i), b = *reinterpret_cast<const float4*>(p + i + 4);
+  return V8{{a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w}};
+}
+__device__ inline V8 ld8(const bf16_t* p, int64_t i) {
+  const uint4 u = *reinterpret_cast<const uint4*>(p + i);
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+  V8 r;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    r.x[2 * t] = __uint_as_float(w[t] << 16);
+    r.x[2 * t + 1] = __uint_as_float(w[t] & 0xFFFF0000u);
+  }
+  return r;
+}
+__device__ inline void st8(float* p, int64_t i, const V8& v) {
+  *reinterpret_cast<float4*>(p + i) = make_float4(v.x[0], v.x[1], v.x[2], v.x[3]);
+  *reinterpret_cast<float4*>(p + i + 4) = make_float4(v.x[4], v.x[5], v.x[6], v.x[7]);
+}
+__device__ inline void st8(bf16_t* p, int64_t i, const V8& v) {
+  uint32_t w[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) w[t] = (uint32_t)f32_to_bf16(v.x[2 * t]) | ((uint32_t)f32_to_bf16(v.x[2 * t + 1]) << 16);
+  *reinterpret_cast<uint4*>(p + i) = make_uint4(w[0], w[1], w[2], w[3]);
+}
+// ne < 8 valid elements (the tail group)
+template <typename T> __device__ inline V8 ld8t(const T* p, int64_t i, int ne) {
+  V8 r;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) r.x[e] = e < ne ? ldf(p, i + e) : 0.f;
+  return r;
+}
+template <typename T> __device__ inline void st8t(T* p, int64_t i, const V8& v, int ne) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e)
+    if (e < ne) stf(p, i + e, v.x[e]);
+}
+// FULL: an aligned group of 8 (one branch-free vector access); otherwise the
+// tail group, element by element.  Keeping the two apart keeps the main loops
+// free of per-lane branches, so their loads issue back to back.
+template <bool FULL, typename T> __device__ inline V8 ldv(const T* p, int64_t i, int ne) {
+  if constexpr (FULL) return ld8(p, i);
+  else return ld8t(p, i, ne);
+}
+template <bool FULL, typename T> __device__ inline void stv(T* p, int64_t i, const V8& v, int ne) {
+  if constexpr (FULL) st8(p, i, v);
+  else st8t(p, i, v, ne);
+}
+using Full = std::true_type;
+using Tail = std::false_type;
+
+// Runs body(i, 8, Full) over the full groups of [i0, s1) with stride `step`
+// and body(i, s1 - i, Tail) for a final partial group of this lane.
+template <typename F>
+__device__ inline void for_groups(int64_t i0, int64_t s1, int64_t step, F&& body) {
+  int64_t i = i0;
+  for (; i + 8 <= s1; i += step) body(i, 8, Full{});
+  if (i < s1) body(i, (int)(s1 - i), Tail{});
+}
+
+// Step A: w <- w - beta_{k-1} qprev ; partial = <w, q>
+__global__ __launch_bounds__(NT) void lz_alpha_kernel(float* w, const float* q, const float* qprev, const double* beta,
+                                                      int k, int64_t n, double* partial) {
   __shared__ double sh[NT / 64];
   const double bk = (k > 0) ? beta[k - 1] : 0.0;
   const int64_t ch = red_chunk(n);
   const int64_t s0 = blockIdx.x * ch, s1 = min(n, s0 + ch);
   double acc = 0.0;
-  for (int64_t i = s0 + threadIdx.x; i < s1; i += NT) {
-    const float wi = (float)((double)w[i] - bk * (double)qprev[i]);
-    w[i] = wi;
-    acc += (double)wi * (double)q[i];
-  }
-  acc = block_sum<NT>(acc, sh);
-  if (threadIdx.x == 0) partial[blockIdx.x] = acc;
-}
-
-// 4-element groups: float4 for fp32 vectors, 4 basis entries (8 or 16 bytes)
-struct F4 { float x[4]; };
-__device__ inline F4 ld4(const float* p, int64_t i) {
-  const float4 v = *reinterpret_cast<const float4*>(p + i);
-  return F4{{v.x, v.y, v.z, v.w}};
-}
-__device__ inline void st4(float* p, int64_t i, const F4& f) {
-  *reinterpret_cast<float4*>(p + i) = make_float4(f.x[0], f.x[1], f.x[2], f.x[3]);
-}
-__device__ inline F4 ld4(const bf16_t* p, int64_t i) {
-  const uint2 u = *reinterpret_cast<const uint2*>(p + i);
-  return F4{{bf16_to_f32((bf16_t)(u.x & 0xFFFF)), bf16_to_f32((bf16_t)(u.x >> 16)), bf16_to_f32((bf16_t)(u.y & 0xFFFF)),
-             bf16_to_f32((bf16_t)(u.y >> 16))}};
-}
-__device__ inline void st4(bf16_t* p, int64_t i, const F4& f) {
-  uint2 u;
-  u.x = (uint32_t)f32_to_bf16(f.x[0]) | ((uint32_t)f32_to_bf16(f.x[1]) << 16);
-  u.y = (uint32_t)f32_to_bf16(f.x[2]) | ((uint32_t)f32_to_bf16(f.x[3]) << 16);
-  *reinterpret_cast<uint2*>(p + i) = u;
-}
-
-// Vectorised pass (n % 4 == 0): each thread owns groups of 4 consecutive
-// elements of its workgroup's chunk.  Same arithmetic as lz_pass_kernel.
-template <typename B>
-__global__ __launch_bounds__(NT) void lz_pass4_kernel(float* w, const float* x, const double* a_src, const double* c_src,
-                                                      int nv_upd, const B* basis, int nv_proj, int64_t n,
-                                                      double* partial) {
-  __shared__ double sh[NT / 64];
-  __shared__ double cs[128];
-  const int64_t ch = red_chunk(n);
-  const int64_t s0 = blockIdx.x * ch, s1 = min(n, s0 + ch);
-  const double a = a_src ? *a_src : 0.0;
-  for (int j = threadIdx.x; j < nv_upd; j += NT) cs[j] = c_src[j];
-  __syncthreads();
-  if (x || nv_upd > 0) {
-    for (int64_t i = s0 + 4 * threadIdx.x; i < s1; i += 4 * NT) {
-      F4 wv = ld4(w, i);
-      double acc4[4];
+  for_groups(s0 + 8 * threadIdx.x, s1, 8 * NT, [&](int64_t i, int ne, auto full) {
+    constexpr bool F = decltype(full)::value;
+    V8 wv = ldv<F>(w, i, ne);
+    const V8 pv = ldv<F>(qprev, i, ne), qv = ldv<F>(q, i, ne);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) acc4[e] = wv.x[e];
-      if (x) {
-        const F4 xv = ld4(x, i);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) acc4[e] -= a * (double)xv.x[e];
-      }
-      for (int j = 0; j < nv_upd; ++j) {
-        const F4 q = ld4(basis, (int64_t)j * n + i);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) acc4[e] -= cs[j] * (double)q.x[e];
-      }
-#pragma unroll
-      for (int e = 0; e < 4; ++e) wv.x[e] = (float)acc4[e];
-      st4(w, i, wv);
-    }
-  }
-  if (nv_proj == 0) {
-    double acc = 0.0;
-    for (int64_t i = s0 + 4 * threadIdx.x; i < s1; i += 4 * NT) {
-      const F4 wv = ld4(w, i);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) acc += (double)wv.x[e] * (double)wv.x[e];
-    }
-    acc = block_sum<NT>(acc, sh);
-    if (threadIdx.x == 0) partial[blockIdx.x] = acc;
-    return;
-  }
-  for (int j0 = 0; j0 < nv_proj; j0 += JG) {
-    double acc[JG];
-#pragma unroll
-    for (int j = 0; j < JG; ++j) acc[j] = 0.0;
-    const int nj = min(JG, nv_proj - j0);
-    for (int64_t i = s0 + 4 * threadIdx.x; i < s1; i += 4 * NT) {
-      const F4 wv = ld4(w, i);
-#pragma unroll
-      for (int j = 0; j < JG; ++j)
-        if (j < nj) {
-          const F4 q = ld4(basis, (int64_t)(j0 + j) * n + i);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) acc[j] += (double)wv.x[e] * (double)q.x[e];
-        }
-    }
-    for (int j = 0; j < nj; ++j) {
-      const double t = block_sum<NT>(acc[j], sh);
-      if (threadIdx.x == 0) partial[(int64_t)(j0 + j) * RED_BLOCKS + blockIdx.x] = t;
-    }
-  }
-}
-
-__global__ __launch_bounds__(NT) void lz_alpha4_kernel(float* w, const float* q, const float* qprev, const double* beta,
-                                                       int k, int64_t n, double* partial) {
-  __shared__ double sh[NT / 64];
-  const double bk = (k > 0) ? beta[k - 1] : 0.0;
-  const int64_t ch = red_chunk(n);
-  const int64_t s0 = blockIdx.x * ch, s1 = min(n, s0 + ch);
-  double acc = 0.0;
-  for (int64_t i = s0 + 4 * threadIdx.x; i < s1; i += 4 * NT) {
-    F4 wv = ld4(w, i);
-    const F4 pv = ld4(qprev, i), qv = ld4(q, i);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
+    for (int e = 0; e < 8; ++e) {
       wv.x[e] = (float)((double)wv.x[e] - bk * (double)pv.x[e]);
       acc += (double)wv.x[e] * (double)qv.x[e];
     }
-    st4(w, i, wv);
-  }
+    stv<F>(w, i, wv, ne);
+  });
   acc = block_sum<NT>(acc, sh);
   if (threadIdx.x == 0) partial[blockIdx.x] = acc;
 }
 
-template <typename B>
-__global__ void lz_scale4_kernel(const float* w, float* qn, B* row, const double* beta_k, const int* flag, int64_t n) {
-  const bool broken = flag[0] != 0;
-  const double inv = broken ? 0.0 : 1.0 / *beta_k;
-  const int64_t n4 = n / 4;
-  for (int64_t g = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; g < n4; g += (int64_t)gridDim.x * blockDim.x) {
-    const F4 wv = ld4(w, 4 * g);
-    F4 q;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) q.x[e] = (float)((double)wv.x[e] * inv);
-    st4(qn, 4 * g, q);
-    if (row) st4(row, 4 * g, q);
-  }
-}
-
-// Generic pass: w <- w - a*x - sum_j c_j Q_j (any part optional), then either
-// partial[j] = <w, Q_j> for j < nv_proj, or partial[0] = ||w||^2 when nv_proj == 0.
-template <typename B>
-__global__ void lz_pass_kernel(float* w, const float* x, const double* a_src, const double* c_src, int nv_upd,
-                               const B* basis, int nv_proj, int64_t n, double* partial) {
-  __shared__ double sh[NT / 64];
-  __shared__ double cs[128];
+// Step B (projections): with w1 = fp32(w - alpha_k q), p_j = <w1, Q_j> and
+// g_j = <Q_new, Q_j> for the nv stored rows (Q_new = the row of q_k); w is not
+// written (the update pass forms w1 again).  The NW wavefronts of a workgroup
+// walk the same 512-element tiles of the chunk (w, q and Q_new are read by
+// each; the copies after the first come from the L1/L2 caches) and split the
+// rows: wave v takes rows v, v+NW, ..., at most 4 NG of them, so a lane keeps
+// fp64 sums for 4 NG rows.  Rows are read in groups of 4 with their loads
+// issued together; rows of a group past this wave's count repeat row v and
+// their sums are dropped.
+// partial[j * RED_BLOCKS + b] = p_j, partial[(nv + j) * RED_BLOCKS + b] = g_j.
+template <typename B, int NW, int NG>
+__global__ __launch_bounds__(64 * NW, NG == 1 ? 4 : 1) void lz_project_kernel(const float* w, const float* q, const double* alpha_k,
+                                                             const B* basis, int64_t ldq, int nv, int newest, int64_t n,
+                                                             double* partial) {
+  constexpr int RW = 4 * NG;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int nr = nv > wave ? min(RW, (nv - wave + NW - 1) / NW) : 0;
+  if (nr == 0) return;
   const int64_t ch = red_chunk(n);
   const int64_t s0 = blockIdx.x * ch, s1 = min(n, s0 + ch);
-  const double a = a_src ? *a_src : 0.0;
-  for (int j = threadIdx.x; j < nv_upd; j += NT) cs[j] = c_src[j];
-  __syncthreads();
-  if (x || nv_upd > 0) {
-    for (int64_t i = s0 + threadIdx.x; i < s1; i += NT) {
-      double wi = w[i];
-      if (x) wi -= a * (double)x[i];
-      for (int j = 0; j < nv_upd; ++j) wi -= cs[j] * (double)ldb(basis, (int64_t)j * n + i);
-      w[i] = (float)wi;
-    }
-  }
-  if (nv_proj == 0) {
-    double acc = 0.0;
-    for (int64_t i = s0 + threadIdx.x; i < s1; i += NT) {
-      const double wi = w[i];
-      acc += wi * wi;
-    }
-    acc = block_sum<NT>(acc, sh);
-    if (threadIdx.x == 0) partial[blockIdx.x] = acc;
-    return;
-  }
-  for (int j0 = 0; j0 < nv_proj; j0 += JG) {
-    double acc[JG];
+  const double a = *alpha_k;
+  const B* rowp[RW];
 #pragma unroll
-    for (int j = 0; j < JG; ++j) acc[j] = 0.0;
-    const int nj = min(JG, nv_proj - j0);
-    for (int64_t i = s0 + threadIdx.x; i < s1; i += NT) {
-      const double wi = w[i];
+  for (int r = 0; r < RW; ++r) rowp[r] = basis + (int64_t)(r < nr ? wave + NW * r : wave) * ldq;
+  const B* qnp = basis + (int64_t)newest * ldq;
+  double pw[RW], pg[RW];
 #pragma unroll
-      for (int j = 0; j < JG; ++j)
-        if (j < nj) acc[j] += wi * (double)ldb(basis, (int64_t)(j0 + j) * n + i);
+  for (int r = 0; r < RW; ++r) pw[r] = pg[r] = 0.0;
+  for_groups(s0 + 8 * lane, s1, 512, [&](int64_t i, int ne, auto full) {
+    constexpr bool F = decltype(full)::value;
+    const V8 wv = ldv<F>(w, i, ne), qv = ldv<F>(q, i, ne), qn = ldv<F>(qnp, i, ne);
+    double w1[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) w1[e] = (double)(float)((double)wv.x[e] - a * (double)qv.x[e]);
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      if (4 * g < nr) {
+        V8 rows[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) rows[t] = ldv<F>(rowp[4 * g + t], i, ne);
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const double x = rows[t].x[e];
+            pw[4 * g + t] = fma(w1[e], x, pw[4 * g + t]);
+            pg[4 * g + t] = fma((double)qn.x[e], x, pg[4 * g + t]);
+          }
+      }
     }
-    for (int j = 0; j < nj; ++j) {
-      const double t = block_sum<NT>(acc[j], sh);
-      if (threadIdx.x == 0) partial[(int64_t)(j0 + j) * RED_BLOCKS + blockIdx.x] = t;
+  });
+#pragma unroll
+  for (int r = 0; r < RW; ++r) {
+    if (r < nr) {
+      const double tw = wave_sum(pw[r]), tg = wave_sum(pg[r]);
+      const int j = wave + NW * r;
+      if (lane == 0) {
+        partial[(int64_t)j * RED_BLOCKS + blockIdx.x] = tw;
+        partial[(int64_t)(nv + j) * RED_BLOCKS + blockIdx.x] = tg;
+      }
     }
   }
 }
 
-// mode 0: alpha[k] = sum, update maxabs.  mode 1: coef[dst + j] = sum_j for j < nv.
+// Step C: w <- fp32(w1 - sum_j c_j Q_j) with w1 = fp32(w - alpha_k q) (nv >= 0
+// rows, coefficients in coef), then partial = ||w||^2.  Rows are read in
+// groups of 8 with their loads issued together; a group's rows past nv read
+// row nv - 1 with coefficient zero.
+template <typename B>
+__global__ __launch_bounds__(NT) void lz_update_kernel(float* w, const float* q, const double* alpha_k, const B* basis,
+                                                       int64_t ldq, const double* coef, int nv, int64_t n, double* partial) {
+  __shared__ double sh[NT / 64];
+  __shared__ double cs[136];
+  for (int j = threadIdx.x; j < 136; j += NT) cs[j] = j < nv ? coef[j] : 0.0;
+  __syncthreads();
+  const double a = *alpha_k;
+  const int64_t ch = red_chunk(n);
+  const int64_t s0 = blockIdx.x * ch, s1 = min(n, s0 + ch);
+  double nrm = 0.0;
+  for_groups(s0 + 8 * threadIdx.x, s1, 8 * NT, [&](int64_t i, int ne, auto full) {
+    constexpr bool F = decltype(full)::value;
+    V8 wv = ldv<F>(w, i, ne);
+    const V8 qv = ldv<F>(q, i, ne);
+    double acc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = (double)(float)((double)wv.x[e] - a * (double)qv.x[e]);
+    for (int j0 = 0; j0 < nv; j0 += 8) {
+      V8 rows[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) rows[t] = ldv<F>(basis + (int64_t)min(j0 + t, nv - 1) * ldq, i, ne);
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const double c = cs[j0 + t];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] = fma(-c, (double)rows[t].x[e], acc[e]);
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      wv.x[e] = (float)acc[e];
+      nrm += (double)wv.x[e] * (double)wv.x[e];
+    }
+    stv<F>(w, i, wv, ne);
+  });
+  nrm = block_sum<NT>(nrm, sh);
+  if (threadIdx.x == 0) partial[blockIdx.x] = nrm;
+}
+
+// mode 0: alpha[k] = sum, update maxabs.
+// mode 1: projections.  p_j and g_j (j < nv) are summed; row and column
+//   `newest` of the Gram matrix G = Q^T Q of the stored rows are replaced by
+//   g; then c = p + (p - G p) = 2 p - G p, the coefficients of both classical
+//   Gram-Schmidt passes at once: the second pass's projections of
+//   w - Q p are p - G p exactly (low-synchronisation CGS2, Swirydowicz et al.,
+//   Numer. Linear Algebra Appl. 28, 2021).
 // mode 2: beta[k] = sqrt(sum); breakdown test against tol * maxabs.
-__global__ void lz_finish_kernel(LanczosDev st, int mode, int k, int nv, int dst, double tol) {
+__global__ void lz_finish_kernel(LanczosDev st, int mode, int k, int nv, int newest, double tol) {
+  __shared__ double sp[128];
   const int j = threadIdx.x;
-  const int ncol = (mode == 1) ? nv : 1;
-  if (j >= ncol) return;
+  const int ncol = (mode == 1) ? 2 * nv : 1;
   double s = 0.0;
-  for (int b = 0; b < RED_BLOCKS; ++b) s += st.partial[(int64_t)j * RED_BLOCKS + b];
+  if (j < ncol)
+    for (int b = 0; b < RED_BLOCKS; ++b) s += st.partial[(int64_t)j * RED_BLOCKS + b];
   if (mode == 0) {
-    st.alpha[k] = s;
-    st.maxabs[0] = fmax(st.maxabs[0], fabs(s));
+    if (j == 0) {
+      st.alpha[k] = s;
+      st.maxabs[0] = fmax(st.maxabs[0], fabs(s));
+    }
   } else if (mode == 1) {
-    st.coef[dst + j] = s;
-  } else {
+    if (j < nv) sp[j] = s;
+    if (j >= nv && j < 2 * nv) {
+      st.gram[(int64_t)newest * 128 + (j - nv)] = s;
+      st.gram[(int64_t)(j - nv) * 128 + newest] = s;
+    }
+    __syncthreads();
+    if (j < nv) {
+      double gp = 0.0;
+      for (int i = 0; i < nv; ++i) gp += st.gram[(int64_t)j * 128 + i] * sp[i];
+      st.coef[j] = 2.0 * sp[j] - gp;
+    }
+  } else if (j == 0) {
     const double b = sqrt(s);
     st.beta[k] = b;
     if (st.flag[0] == 0 && !(b > tol * st.maxabs[0])) st.flag[0] = k + 1;
   }
 }
 
-template <typename B>
-__global__ void lz_scale_kernel(const float* w, float* qn, B* row, const double* beta_k, const int* flag, int64_t n) {
+// Step D: beta_k from the last reduction; q_next = w / beta_k, the basis row
+// (if any) = B(q_next) and the next HVP's perturbation operand (if any)
+// lo = T(eps * q_next); after a breakdown all are zero.
+template <typename B, typename T>
+__global__ void lz_scale_kernel(const float* w, float* qn, B* row, T* lo, double eps, const double* beta_k, const int* flag,
+                                int64_t n) {
   const bool broken = flag[0] != 0;
   const double inv = broken ? 0.0 : 1.0 / *beta_k;
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
-    const float q = (float)((double)w[i] * inv);
-    qn[i] = q;
-    if (row) stf(row, i, q);
-  }
+  const int64_t step = 8 * (int64_t)gridDim.x * blockDim.x;
+  for_groups(8 * (blockIdx.x * (int64_t)blockDim.x + threadIdx.x), n, step, [&](int64_t i, int ne, auto full) {
+    constexpr bool F = decltype(full)::value;
+    const V8 wv = ldv<F>(w, i, ne);
+    V8 q, l;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      q.x[e] = (float)((double)wv.x[e] * inv);
+      l.x[e] = (float)(eps * (double)q.x[e]);
+    }
+    stv<F>(qn, i, q, ne);
+    if (row) stv<F>(row, i, q, ne);
+    if (lo) stv<F>(lo, i, l, ne);
+  });
+}
+
+// lo = T(eps * v), 8 elements per lane (16-byte aligned operands)
+template <typename T>
+__global__ void scale_cast8_kernel(T* lo, const float* v, double eps, int64_t n) {
+  const int64_t step = 8 * (int64_t)gridDim.x * blockDim.x;
+  for_groups(8 * (blockIdx.x * (int64_t)blockDim.x + threadIdx.x), n, step, [&](int64_t i, int ne, auto full) {
+    constexpr bool F = decltype(full)::value;
+    V8 x = ldv<F>(v, i, ne);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x.x[e] = (float)(eps * (double)x.x[e]);
+    stv<F>(lo, i, x, ne);
+  });
 }
 
 // sums over [s0, s1): ||a||^2, ||b||^2, <a, b>, ||a - b||^2
@@ -340,7 +392,10 @@ hipError_t launch_fill_f64(double* p, int64_t n, double v, hipStream_t s) {
 template <typename T>
 hipError_t launch_scale_cast(T* lo, const float* v, double eps, int64_t n, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(scale_cast_kernel<T>, dim3(grid_for(n)), dim3(NT), 0, s, lo, v, eps, n);
+  if ((uintptr_t)lo % 16 == 0 && (uintptr_t)v % 16 == 0)
+    hipLaunchKernelGGL(scale_cast8_kernel<T>, dim3(grid_for((n + 7) / 8)), dim3(NT), 0, s, lo, v, eps, n);
+  else
+    hipLaunchKernelGGL(scale_cast_kernel<T>, dim3(grid_for(n)), dim3(NT), 0, s, lo, v, eps, n);
   return hipGetLastError();
 }
 template hipError_t launch_scale_cast<float>(float*, const float*, double, int64_t, hipStream_t);
@@ -356,55 +411,55 @@ template hipError_t launch_quad_diag_hvp<float>(const float*, const float*, cons
 template hipError_t launch_quad_diag_hvp<bf16_t>(const bf16_t*, const float*, const float*, double, float*, int64_t, hipStream_t);
 
 hipError_t launch_lanczos_alpha(float* w, const float* q, const float* qprev, LanczosDev st, int k, int64_t n, hipStream_t s) {
-  if (n % 4 == 0)
-    hipLaunchKernelGGL(lz_alpha4_kernel, dim3(RED_BLOCKS), dim3(NT), 0, s, w, q, qprev, st.beta, k, n, st.partial);
-  else
-    hipLaunchKernelGGL(lz_alpha_kernel, dim3(RED_BLOCKS), dim3(NT), 0, s, w, q, qprev, st.beta, k, n, st.partial);
+  hipLaunchKernelGGL(lz_alpha_kernel, dim3(RED_BLOCKS), dim3(NT), 0, s, w, q, qprev, st.beta, k, n, st.partial);
   hipLaunchKernelGGL(lz_finish_kernel, dim3(1), dim3(256), 0, s, st, 0, k, 1, 0, 0.0);
   return hipGetLastError();
 }
 
 template <typename B>
-hipError_t launch_lanczos_b(float* w, const float* q, const B* basis, int nv, LanczosDev st, int k, int64_t n, hipStream_t s) {
-  if (n % 4 == 0)
-    hipLaunchKernelGGL(lz_pass4_kernel<B>, dim3(RED_BLOCKS), dim3(NT), 0, s, w, q, (const double*)(st.alpha + k),
-                       (const double*)nullptr, 0, basis, nv, n, st.partial);
-  else
-    hipLaunchKernelGGL(lz_pass_kernel<B>, dim3(RED_BLOCKS), dim3(NT), 0, s, w, q, (const double*)(st.alpha + k),
-                       (const double*)nullptr, 0, basis, nv, n, st.partial);
-  if (nv > 0) hipLaunchKernelGGL(lz_finish_kernel, dim3(1), dim3(256), 0, s, st, 1, k, nv, 0, 0.0);
+hipError_t launch_lanczos_project(const float* w, const float* q, const B* basis, int64_t ldq, int nv, int newest, LanczosDev st,
+                                  int k, int64_t n, hipStream_t s) {
+  if (nv < 1 || nv > 128 || newest < 0 || newest >= nv) return hipErrorInvalidValue;
+  const double* a = st.alpha + k;
+#define LZP(W, G) hipLaunchKernelGGL((lz_project_kernel<B, W, G>), dim3(RED_BLOCKS), dim3(64 * W), 0, s, w, q, a, basis, ldq, nv, newest, n, st.partial)
+  // rows of wave 0: ceil(nv / waves)
+  if (nv <= 16) LZP(4, 1);
+  else if (nv <= 32) LZP(8, 1);
+  else if (nv <= 64) LZP(8, 2);
+  else if (nv <= 96) LZP(8, 3);
+  else LZP(8, 4);
+#undef LZP
+  hipLaunchKernelGGL(lz_finish_kernel, dim3(1), dim3(256), 0, s, st, 1, k, nv, newest, 0.0);
   return hipGetLastError();
 }
 
 template <typename B>
-hipError_t launch_lanczos_cgs(float* w, const B* basis, int nv, LanczosDev st, int pass, bool last, int k, int64_t n, hipStream_t s) {
-  // coefficients of this pass live at coef[pass * 128]; the next pass writes coef[(pass+1) * 128]
-  if (n % 4 == 0)
-    hipLaunchKernelGGL(lz_pass4_kernel<B>, dim3(RED_BLOCKS), dim3(NT), 0, s, w, (const float*)nullptr, (const double*)nullptr,
-                       (const double*)(st.coef + pass * 128), nv, basis, last ? 0 : nv, n, st.partial);
-  else
-  hipLaunchKernelGGL(lz_pass_kernel<B>, dim3(RED_BLOCKS), dim3(NT), 0, s, w, (const float*)nullptr, (const double*)nullptr,
-                     (const double*)(st.coef + pass * 128), nv, basis, last ? 0 : nv, n, st.partial);
-  if (!last) hipLaunchKernelGGL(lz_finish_kernel, dim3(1), dim3(256), 0, s, st, 1, k, nv, (pass + 1) * 128, 0.0);
+hipError_t launch_lanczos_update(float* w, const float* q, const B* basis, int64_t ldq, int nv, LanczosDev st, int k, int64_t n,
+                                 hipStream_t s) {
+  if (nv < 0 || nv > 128) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(lz_update_kernel<B>, dim3(RED_BLOCKS), dim3(NT), 0, s, w, q, (const double*)(st.alpha + k), basis, ldq,
+                     (const double*)st.coef, nv, n, st.partial);
   return hipGetLastError();
 }
 
-template <typename B>
-hipError_t launch_lanczos_normalise(const float* w, float* qnext, B* basis_row, LanczosDev st, int k, double tol, int64_t n, hipStream_t s) {
+template <typename B, typename T>
+hipError_t launch_lanczos_normalise(const float* w, float* qnext, B* basis_row, T* lo, double eps, LanczosDev st, int k, double tol,
+                                    int64_t n, hipStream_t s) {
   hipLaunchKernelGGL(lz_finish_kernel, dim3(1), dim3(256), 0, s, st, 2, k, 1, 0, tol);
-  if (n % 4 == 0)
-    hipLaunchKernelGGL(lz_scale4_kernel<B>, dim3(grid_for(n / 4)), dim3(NT), 0, s, w, qnext, basis_row,
-                       (const double*)(st.beta + k), (const int*)st.flag, n);
-  else
-  hipLaunchKernelGGL(lz_scale_kernel<B>, dim3(grid_for(n)), dim3(NT), 0, s, w, qnext, basis_row,
+  hipLaunchKernelGGL((lz_scale_kernel<B, T>), dim3(grid_for((n + 7) / 8)), dim3(NT), 0, s, w, qnext, basis_row, lo, eps,
                      (const double*)(st.beta + k), (const int*)st.flag, n);
   return hipGetLastError();
 }
 
-#define INST_LZ(B)                                                                                              \
-  template hipError_t launch_lanczos_b<B>(float*, const float*, const B*, int, LanczosDev, int, int64_t, hipStream_t); \
-  template hipError_t launch_lanczos_cgs<B>(float*, const B*, int, LanczosDev, int, bool, int, int64_t, hipStream_t);  \
-  template hipError_t launch_lanczos_normalise<B>(const float*, float*, B*, LanczosDev, int, double, int64_t, hipStream_t);
+#define INST_LZ(B)                                                                                                   \
+  template hipError_t launch_lanczos_project<B>(const float*, const float*, const B*, int64_t, int, int, LanczosDev, int,   \
+                                                int64_t, hipStream_t);                                                \
+  template hipError_t launch_lanczos_update<B>(float*, const float*, const B*, int64_t, int, LanczosDev, int, int64_t, \
+                                               hipStream_t);                                                          \
+  template hipError_t launch_lanczos_normalise<B, float>(const float*, float*, B*, float*, double, LanczosDev, int, double,   \
+                                                         int64_t, hipStream_t);                                              \
+  template hipError_t launch_lanczos_normalise<B, bf16_t>(const float*, float*, B*, bf16_t*, double, LanczosDev, int, double, \
+                                                          int64_t, hipStream_t);
 INST_LZ(float)
 INST_LZ(bf16_t)
 

@@ -211,6 +211,29 @@ def test_lanczos_quad_diag_matches_oracle(reorth, window, basis):
     assert abs(a[0] - ao[0]) <= 1e-5 * scale
 
 
+@pytest.mark.parametrize("m,basis", [(24, "f32"), (40, "bf16"), (72, "f32"), (100, "bf16")])
+def test_lanczos_long_runs_match_oracle(m, basis):
+    """Full reorthogonalisation with up to 100 stored rows (every row-group
+    width of the projection kernel) on a length that is not a multiple of 8."""
+    torch = need_gpu()
+    from paper_2602_00816_amd import fdhvp as fd
+    say(f"lanczos long run m={m} {basis}")
+    P = 50003
+    rng = np.random.default_rng(4)
+    diag = np.concatenate([np.linspace(-5.0, 100.0, 40), rng.uniform(-1, 1, P - 40)]).astype(np.float32)
+    mod, o, _ = _quad_setup(torch, fd, diag, m, "full", 0, basis)
+    a, b, s, st = mod.lanczos(m, 5, o)
+    assert s == m and st == fd.OK
+    q1 = synth.rademacher_probe(5, P).astype(np.float64)
+    ao, bo, _ = OL.lanczos(lambda x: diag.astype(np.float64) * x, q1, m, OL.FULL, 0)
+    lam_g = np.sort(np.linalg.eigvalsh(OL.tridiag(a, b)))
+    lam_o = np.sort(np.linalg.eigvalsh(OL.tridiag(ao, bo)))
+    scale = np.abs(lam_o).max()
+    tol = 1e-5 if basis == "f32" else 5e-4
+    assert np.abs(lam_g[-5:] - lam_o[-5:]).max() <= tol * scale
+    assert abs(lam_g[0] - lam_o[0]) <= tol * scale
+
+
 def test_slq_quad_diag_trace_and_weights():
     torch = need_gpu()
     from paper_2602_00816_amd import fdhvp as fd
