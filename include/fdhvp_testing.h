@@ -39,6 +39,12 @@ fdh_status fdh_testing_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, int3
  * be compared on one model. */
 fdh_status fdh_testing_unfused_attention(fdh_ctx* ctx, int32_t on);
 
+/* on != 0 makes the weight-gradient GEMMs contract over the whole token range
+ * in one pass, where by default small output grids are cut into token slices
+ * whose fp32 partial products are added afterwards (fp64 sums in slice
+ * order), so that the two can be compared.  Takes effect at the next HVP. */
+fdh_status fdh_testing_unsplit_wgrad(fdh_ctx* ctx, int32_t on);
+
 /* Per-launch timing with HIP events recorded on the context stream around every
  * GEMM launch (category 0), every Lanczos vector launch (category 1) and every
  * fused attention forward and backward (category 2).

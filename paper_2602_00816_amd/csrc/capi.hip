@@ -248,6 +248,13 @@ extern "C" fdh_status fdh_testing_unfused_attention(fdh_ctx* ctx, int32_t on) {
   });
 }
 
+extern "C" fdh_status fdh_testing_unsplit_wgrad(fdh_ctx* ctx, int32_t on) {
+  return run(ctx, [&](fdh::Engine& e) -> int {
+    e.force_unsplit = on != 0;
+    return FDH_OK;
+  });
+}
+
 extern "C" fdh_status fdh_testing_timing(fdh_ctx* ctx, int32_t enable) {
   return run(ctx, [&](fdh::Engine& e) -> int {
     if (e.timing.on) {

@@ -72,6 +72,7 @@ class Engine {
   // 128, S a multiple of 128) or score/probability matrices in the workspace
   bool fused = false;
   bool force_unfused = false;   // testing: plan the unfused path even where the fused one applies
+  bool force_unsplit = false;   // testing: weight-gradient GEMMs over the whole token range
   fdh_lanczos_opts planO{};
   size_t plan(int B, int S, int m, const fdh_lanczos_opts* o, bool carve);
 
@@ -110,6 +111,7 @@ class Engine {
   Span xL_m, xL_d, f_m, f_d, lo, qkvf_m, qkvf_d, sc_m, sc_d, log_m, log_d, dlog_m, dlog_d, rowloss, losses;
   Span dx0_m, dx0_d, dx1_m, dx1_d, dxo_m, dxo_d, dz_m, dz_d, dgu_m, dgu_d, dudf, db_m, db_d, gpart, do_m, do_d, dS_m, dS_d;
   Span dqkv_m, dqkv_d, dqkvo_m, dqkvo_d, gqa_m, gqa_d, dl, da_m, da_d, colpart, keys, rope, cdf, gpartial, bpart, bout;
+  Span wsplit;  // split-K partial products of the weight-gradient GEMMs
   Span lz_w, lz_q, lz_qp, lz_basis, lz_alpha, lz_beta, lz_coef, lz_gram, lz_partial, lz_flag, lz_maxabs;
   int64_t lz_ldq = 0;  // basis row stride (elements, multiple of 8)
   // set by the Lanczos normalisation when it already wrote lo = eps * v for

@@ -120,6 +120,21 @@ Engine::Engine(const fdh_model_config& c, hipStream_t s) : cfg(c), stream(s) {
   P = off;
 }
 
+// Number of K slices for a weight-gradient GEMM (M x N output, contraction
+// over the T tokens).  A grid of fewer than 128 output tiles leaves most of
+// the 256 compute units idle; slicing the token range multiplies the
+// workgroups, up to one full wave of 256.  Larger grids are not sliced: there
+// the extra prologues, epilogues and the summation pass cost more than the
+// better balance gains (measured on the 1.3B shapes).
+static int wgrad_splits(int M, int N, int T_) {
+  const int64_t tiles = (int64_t)((M + 255) / 256) * ((N + 255) / 256);
+  if (tiles >= 128) return 1;
+  int best = 1;
+  for (int s : {2, 3, 4, 6, 8})
+    if (T_ % (64 * s) == 0 && T_ / s >= 1024 && tiles * s <= 256) best = s;
+  return best;
+}
+
 // ---------------------------------------------------------------------------
 // workspace plan
 // ---------------------------------------------------------------------------
@@ -169,7 +184,7 @@ size_t Engine::plan(int B, int S, int m, const fdh_lanczos_opts* o, bool carve) 
     take(dgu_m, tu * ob); take(dgu_d, tu * ob);
     take(dudf, gpt2 ? tz * 4 : 0);
     take(db_m, td * 4); take(db_d, td * 4);
-    take(gpart, td * 4);
+    take(gpart, std::max(td * 4, (size_t)2 * norm_bwd_groups((int)T_) * d * 8));
     take(do_m, ta * ob); take(do_d, ta * ob);
     take(dS_m, pp * ob); take(dS_d, pp * ob);
     take(dqkv_m, tq * 4); take(dqkv_d, tq * 4);
@@ -177,6 +192,16 @@ size_t Engine::plan(int B, int S, int m, const fdh_lanczos_opts* o, bool carve) 
     take(gqa_m, Hq != Hk && !fused ? ta * 4 : 0); take(gqa_d, Hq != Hk && !fused ? ta * 4 : 0);
     take(dl, fused ? rows * 8 : 0);
     take(da_m, td * 4); take(da_d, td * 4);
+    {
+      const int nu = gpt2 ? F : 2 * F;
+      size_t mx = 0;
+      const int shapes[5][2] = {{qkvd, d}, {d, Hq * dh}, {nu, d}, {d, F}, {V, d}};
+      for (const auto& sh : shapes) {
+        const int ns = wgrad_splits(sh[0], sh[1], (int)T_);
+        if (ns > 1) mx = std::max(mx, (size_t)ns * sh[0] * sh[1] * 4);
+      }
+      take(wsplit, mx);
+    }
     const size_t maxc = std::max<size_t>({(size_t)qkvd, (size_t)F, (size_t)d, (size_t)1});
     take(colpart, 64 * maxc * 8);
     take(keys, T_ * 4);
@@ -384,24 +409,67 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, i
     return FDH_OK;
   };
   // Hv_W = (dY.m^T X.d + dY.d^T X.m) / eps
+  // (with ns > 1 the token range is cut into ns slices, one GEMM batch entry
+  // each, into fp32 partial products that a second pass adds in slice order)
   auto lin_wgrad = [&](const T* dYm, const T* dYd, int N, const T* Xm, const T* Xd, int K, const ParamRef& W) -> int {
     GemmArgs g;
     g.M = N; g.N = K; g.K = T_; g.npairs = 2;
     g.A[0] = mnmaj(dYm, N); g.B[0] = mnmaj(Xd, K);
     g.A[1] = mnmaj(dYd, N); g.B[1] = mnmaj(Xm, K);
     g.C = hv + W.off; g.ldc = K; g.alpha = inv_eps;
+    const int ns = wgrad_splits(N, K, T_);
+    if (ns == 1 || force_unsplit || wsplit.bytes < (size_t)ns * N * K * 4) {
+      RG(T, g);
+      return FDH_OK;
+    }
+    const int kc = T_ / ns;
+    g.K = kc;
+    g.nbatch = ns;
+    for (int p = 0; p < 2; ++p) {
+      g.A[p].s_outer = (int64_t)kc * N;
+      g.B[p].s_outer = (int64_t)kc * K;
+    }
+    g.C = F32(wsplit); g.c_outer = (int64_t)N * K;
     RG(T, g);
+    int e0 = 0;
+    if (timing.on) CK(timing.begin(st, &e0));
+    CK(launch_sum_splits(hv + W.off, F32(wsplit), ns, (int64_t)N * K, st));
+    if (timing.on) CK(timing.end(st, 0, e0, 0.0, 0.0));
     return FDH_OK;
   };
   auto colsum_hv = [&](const float* X, int C, int64_t ld, const ParamRef& R) -> int {
     CK(launch_colsum(hv + R.off, X, T_, C, ld, 1.0 / eps, false, (double*)(ws + colpart.off), st));
     return FDH_OK;
   };
-  // fp32 pair -> operand pair (aliases in fp32 mode)
+  bool op_ready = false;  // dxo holds the operand-type copy of the last norm backward's output
+  // norm backward at both points into (dym, dyd) with its operand-type copy in
+  // dxo (bf16 models), then the gain (and LayerNorm bias) gradients
+  auto norm_back = [&](float* ym, float* yd, const float* rm, const float* rd, const float* xm_, const float* xd_,
+                       const float* gm_, const float* gd_, const ParamRef& gain, const ParamRef& bias) -> int {
+    const int nwg = norm_bwd_groups(T_);
+    double* gp = (double*)F32(gpart);
+    double* bp = ln ? gp + (int64_t)nwg * d : nullptr;
+    const PairT<T> yo = bf16 ? PairT<T>{OP(dxo_m), OP(dxo_d)} : PairT<T>{nullptr, nullptr};
+    CK(launch_norm_bwd<T>(PairF{ym, yd}, yo, rm, rd, xm_, xd_, gm_, gd_, T_, d, ln, th + gain.off, v + gain.off, eps, neps,
+                          gp, bp, st));
+    op_ready = bf16;
+    double* cp = (double*)(ws + colpart.off);
+    CK(launch_colsum_f64(hv + gain.off, gp, nwg, d, 1.0 / eps, false, cp, st));
+    if (ln) CK(launch_colsum_f64(hv + bias.off, bp, nwg, d, 1.0 / eps, false, cp, st));
+    return FDH_OK;
+  };
+  // fp32 pair -> operand pair (aliases in fp32 mode; skipped when the norm
+  // backward that produced the pair already wrote the copy)
   auto as_op = [&](const float* m, const float* dd, const Span& om, const Span& od, int64_t n, T** rm, T** rd) -> int {
     if (!bf16) {
       *rm = (T*)m;
       *rd = (T*)dd;
+      return FDH_OK;
+    }
+    if (op_ready) {
+      op_ready = false;
+      *rm = OP(om);
+      *rd = OP(od);
       return FDH_OK;
     }
     PairT<T> o{OP(om), OP(od)};
@@ -521,10 +589,7 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, i
   float* dxd = F32(dx0_d);
   float* dym = F32(dx1_m);
   float* dyd = F32(dx1_d);
-  CK(launch_norm_bwd<T>(PairF{dxm, dxd}, nullptr, nullptr, F32(xL_m), F32(xL_d), F32(db_m), F32(db_d), T_, d, ln,
-                        th + nfg.off, v + nfg.off, eps, neps, F32(gpart), st));
-  RC(colsum_hv(F32(gpart), d, d, nfg));
-  if (ln) RC(colsum_hv(F32(db_d), d, d, nfb));
+  RC(norm_back(dxm, dxd, nullptr, nullptr, F32(xL_m), F32(xL_d), F32(db_m), F32(db_d), nfg, nfb));
 
   for (int l = L - 1; l >= 0; --l) {
     const LayerRefs& R = layers[l];
@@ -546,10 +611,7 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, i
     RC(lin_wgrad(OP(dgu_m), OP(dgu_d), nu, OP(s.b_m), OP(s.b_d), d, R.w1));
     RC(lin_dgrad(OP(dgu_m), OP(dgu_d), nu, R.w1, d, F32(db_m), F32(db_d), OUT_F32));
     // norm 2 backward, residual: dy = dx + norm2'(db)
-    CK(launch_norm_bwd<T>(PairF{dym, dyd}, dxm, dxd, F32(s.xmid_m), F32(s.xmid_d), F32(db_m), F32(db_d), T_, d, ln,
-                          th + R.n2g.off, v + R.n2g.off, eps, neps, F32(gpart), st));
-    RC(colsum_hv(F32(gpart), d, d, R.n2g));
-    if (ln) RC(colsum_hv(F32(db_d), d, d, R.n2b));
+    RC(norm_back(dym, dyd, dxm, dxd, F32(s.xmid_m), F32(s.xmid_d), F32(db_m), F32(db_d), R.n2g, R.n2b));
     std::swap(dxm, dym);
     std::swap(dxd, dyd);
     // ---- attention ----  (dx = gradient w.r.t. x_mid)
@@ -684,10 +746,7 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, i
     }
     RC(lin_wgrad(OP(dqkvo_m), OP(dqkvo_d), qkvd, OP(s.a_m), OP(s.a_d), d, R.wqkv));
     RC(lin_dgrad(OP(dqkvo_m), OP(dqkvo_d), qkvd, R.wqkv, d, F32(da_m), F32(da_d), OUT_F32));
-    CK(launch_norm_bwd<T>(PairF{dym, dyd}, dxm, dxd, F32(s.x_in_m), F32(s.x_in_d), F32(da_m), F32(da_d), T_, d, ln,
-                          th + R.n1g.off, v + R.n1g.off, eps, neps, F32(gpart), st));
-    RC(colsum_hv(F32(gpart), d, d, R.n1g));
-    if (ln) RC(colsum_hv(F32(da_d), d, d, R.n1b));
+    RC(norm_back(dym, dyd, dxm, dxd, F32(s.x_in_m), F32(s.x_in_d), F32(da_m), F32(da_d), R.n1g, R.n1b));
     std::swap(dxm, dym);
     std::swap(dxd, dyd);
   }

@@ -24,6 +24,8 @@ constexpr int RED_BLOCKS = 1024;   // fixed grid of the deterministic reductions
 hipError_t launch_fill_f32(float* p, int64_t n, float v, hipStream_t s);
 hipError_t launch_copy16(void* dst, const void* src, size_t bytes, hipStream_t s);
 hipError_t launch_fill_f64(double* p, int64_t n, double v, hipStream_t s);
+// out[i] = sum_{j < ns} part[j * n + i], summed in fp64 in the order j = 0, 1, ...
+hipError_t launch_sum_splits(float* out, const float* part, int ns, int64_t n, hipStream_t s);
 // lo[i] = T(eps * v[i])
 template <typename T>
 hipError_t launch_scale_cast(T* lo, const float* v, double eps, int64_t n, hipStream_t s);
@@ -87,15 +89,26 @@ hipError_t launch_embed_fwd(PairF x, const int32_t* tok, int T_, int S, int dmod
 template <typename T>
 hipError_t launch_norm_fwd(PairT<T> y, const float* xm, const float* xd, int rows, int dmodel, bool layernorm,
                            const T* th_g, const float* v_g, const T* th_b, const float* v_b, double eps, float norm_eps, hipStream_t s);
-// Norm backward at both points: dx_out = dx_res + d/dx, gpart[t][j] = half difference of dy * xhat
+// Norm backward at both points: dx_out = dx_res + d/dx, and dx_op (if dx_op.m is
+// not null) = the operand-type copy of dx_out.  Rows are taken norm_bwd_groups(rows)
+// workgroups at a time: gpart[w][j] (fp64) = the workgroup's sum over its rows
+// of the half difference of dy * xhat (gain gradient), and with bpart (LayerNorm)
+// bpart[w][j] = its sum of dy.d (bias gradient); launch_colsum_f64 finishes both.
+// dmodel * (bpart ? 2 : 1) <= 8192.
+constexpr int NORM_BWD_ROWS = 8;
+inline int norm_bwd_groups(int rows) { return (rows + NORM_BWD_ROWS - 1) / NORM_BWD_ROWS; }
 template <typename T>
-hipError_t launch_norm_bwd(PairF dx_out, const float* dres_m, const float* dres_d, const float* xm, const float* xd,
-                           const float* dym, const float* dyd, int rows, int dmodel, bool layernorm,
-                           const T* th_g, const float* v_g, double eps, float norm_eps, float* gpart, hipStream_t s);
+hipError_t launch_norm_bwd(PairF dx_out, PairT<T> dx_op, const float* dres_m, const float* dres_d, const float* xm,
+                           const float* xd, const float* dym, const float* dyd, int rows, int dmodel, bool layernorm,
+                           const T* th_g, const float* v_g, double eps, float norm_eps, double* gpart, double* bpart,
+                           hipStream_t s);
 
 // out[j] = scale * sum_t X[t*ld + j] (deterministic); accumulate adds to out.  partial: [64 * C]
 hipError_t launch_colsum(float* out, const float* X, int rows, int C, int64_t ld, double scale, bool accumulate,
                          double* partial, hipStream_t s);
+// the same for fp64 rows X [rows][C]
+hipError_t launch_colsum_f64(float* out, const double* X, int rows, int C, double scale, bool accumulate, double* partial,
+                             hipStream_t s);
 
 // RoPE (Llama) or plain cast (GPT-2) of q,k,v columns into operand type
 template <typename T>

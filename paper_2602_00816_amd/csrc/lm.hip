@@ -103,64 +103,88 @@ __global__ __launch_bounds__(NT) void norm_fwd_kernel(PairT<T> y, const float* x
   }
 }
 
+// NORM_BWD_ROWS consecutive rows per workgroup.  Besides dx (and its operand-type
+// copy), each workgroup adds up the gain-gradient terms of its rows per column
+// in fp64, in row order (and dy.d for the LayerNorm bias), and writes one
+// partial row; a column sum over the workgroups finishes the gradient.  A
+// column's sum lives in LDS and is only ever touched by the thread that owns
+// the column, so no barrier guards it.
 template <typename T>
-__global__ __launch_bounds__(NT) void norm_bwd_kernel(PairF dx, const float* dresm, const float* dresd,
+__global__ __launch_bounds__(NT) void norm_bwd_kernel(PairF dx, PairT<T> dxo, const float* dresm, const float* dresd,
                                                       const float* xm, const float* xd, const float* dym,
-                                                      const float* dyd, int dm, bool ln, const T* thg,
-                                                      const float* vg, double eps, double neps, float* gpart) {
+                                                      const float* dyd, int rows, int dm, bool ln, const T* thg,
+                                                      const float* vg, double eps, double neps, double* gpart,
+                                                      double* bpart) {
+  extern __shared__ double cacc[];  // [dm] gain partials, then [dm] bias partials
   __shared__ double sh[NT / 64];
-  const int64_t row = blockIdx.x;
-  const int64_t o = row * dm;
-  double mup = 0.0, mum = 0.0;
-  if (ln) {
-    double sp = 0.0, sm = 0.0;
-    for (int j = threadIdx.x; j < dm; j += NT) {
-      sp += (double)xm[o + j] + (double)xd[o + j];
-      sm += (double)xm[o + j] - (double)xd[o + j];
+  for (int j = threadIdx.x; j < dm; j += NT) {
+    cacc[j] = 0.0;
+    if (bpart) cacc[dm + j] = 0.0;
+  }
+  const int r0 = blockIdx.x * NORM_BWD_ROWS, r1 = min(rows, r0 + NORM_BWD_ROWS);
+  for (int row = r0; row < r1; ++row) {
+    const int64_t o = (int64_t)row * dm;
+    double mup = 0.0, mum = 0.0;
+    if (ln) {
+      double sp = 0.0, sm = 0.0;
+      for (int j = threadIdx.x; j < dm; j += NT) {
+        sp += (double)xm[o + j] + (double)xd[o + j];
+        sm += (double)xm[o + j] - (double)xd[o + j];
+      }
+      mup = block_sum<NT>(sp, sh) / dm;
+      mum = block_sum<NT>(sm, sh) / dm;
     }
-    mup = block_sum<NT>(sp, sh) / dm;
-    mum = block_sum<NT>(sm, sh) / dm;
+    double qp = 0.0, qm = 0.0;
+    for (int j = threadIdx.x; j < dm; j += NT) {
+      const double a = (double)xm[o + j] + (double)xd[o + j] - mup;
+      const double b = (double)xm[o + j] - (double)xd[o + j] - mum;
+      qp += a * a;
+      qm += b * b;
+    }
+    const double rp = 1.0 / sqrt(block_sum<NT>(qp, sh) / dm + neps);
+    const double rmi = 1.0 / sqrt(block_sum<NT>(qm, sh) / dm + neps);
+    // means of dxhat and dxhat * xhat at both points
+    double s1p = 0.0, s1m = 0.0, s2p = 0.0, s2m = 0.0;
+    for (int j = threadIdx.x; j < dm; j += NT) {
+      const double g = ldf(thg, j), dg = eps * (double)vg[j];
+      const double xhp = ((double)xm[o + j] + (double)xd[o + j] - mup) * rp;
+      const double xhm = ((double)xm[o + j] - (double)xd[o + j] - mum) * rmi;
+      const double dhp = ((double)dym[o + j] + (double)dyd[o + j]) * (g + dg);
+      const double dhm = ((double)dym[o + j] - (double)dyd[o + j]) * (g - dg);
+      s1p += dhp;
+      s1m += dhm;
+      s2p += dhp * xhp;
+      s2m += dhm * xhm;
+    }
+    const double a1p = ln ? block_sum<NT>(s1p, sh) / dm : 0.0;
+    const double a1m = ln ? block_sum<NT>(s1m, sh) / dm : 0.0;
+    const double a2p = block_sum<NT>(s2p, sh) / dm;
+    const double a2m = block_sum<NT>(s2m, sh) / dm;
+    for (int j = threadIdx.x; j < dm; j += NT) {
+      const double g = ldf(thg, j), dg = eps * (double)vg[j];
+      const double xhp = ((double)xm[o + j] + (double)xd[o + j] - mup) * rp;
+      const double xhm = ((double)xm[o + j] - (double)xd[o + j] - mum) * rmi;
+      const double dyp = (double)dym[o + j] + (double)dyd[o + j];
+      const double dymi = (double)dym[o + j] - (double)dyd[o + j];
+      const double dhp = dyp * (g + dg), dhm = dymi * (g - dg);
+      const double dxp = rp * (dhp - a1p - xhp * a2p);
+      const double dxm = rmi * (dhm - a1m - xhm * a2m);
+      const double rm0 = dresm ? (double)dresm[o + j] : 0.0;
+      const double rd0 = dresd ? (double)dresd[o + j] : 0.0;
+      const float om = (float)(rm0 + 0.5 * (dxp + dxm)), od = (float)(rd0 + 0.5 * (dxp - dxm));
+      dx.m[o + j] = om;
+      dx.d[o + j] = od;
+      if (dxo.m) {
+        stf(dxo.m, o + j, om);
+        stf(dxo.d, o + j, od);
+      }
+      cacc[j] += 0.5 * (dyp * xhp - dymi * xhm);
+      if (bpart) cacc[dm + j] += (double)dyd[o + j];
+    }
   }
-  double qp = 0.0, qm = 0.0;
   for (int j = threadIdx.x; j < dm; j += NT) {
-    const double a = (double)xm[o + j] + (double)xd[o + j] - mup;
-    const double b = (double)xm[o + j] - (double)xd[o + j] - mum;
-    qp += a * a;
-    qm += b * b;
-  }
-  const double rp = 1.0 / sqrt(block_sum<NT>(qp, sh) / dm + neps);
-  const double rmi = 1.0 / sqrt(block_sum<NT>(qm, sh) / dm + neps);
-  // means of dxhat and dxhat * xhat at both points
-  double s1p = 0.0, s1m = 0.0, s2p = 0.0, s2m = 0.0;
-  for (int j = threadIdx.x; j < dm; j += NT) {
-    const double g = ldf(thg, j), dg = eps * (double)vg[j];
-    const double xhp = ((double)xm[o + j] + (double)xd[o + j] - mup) * rp;
-    const double xhm = ((double)xm[o + j] - (double)xd[o + j] - mum) * rmi;
-    const double dhp = ((double)dym[o + j] + (double)dyd[o + j]) * (g + dg);
-    const double dhm = ((double)dym[o + j] - (double)dyd[o + j]) * (g - dg);
-    s1p += dhp;
-    s1m += dhm;
-    s2p += dhp * xhp;
-    s2m += dhm * xhm;
-  }
-  const double a1p = ln ? block_sum<NT>(s1p, sh) / dm : 0.0;
-  const double a1m = ln ? block_sum<NT>(s1m, sh) / dm : 0.0;
-  const double a2p = block_sum<NT>(s2p, sh) / dm;
-  const double a2m = block_sum<NT>(s2m, sh) / dm;
-  for (int j = threadIdx.x; j < dm; j += NT) {
-    const double g = ldf(thg, j), dg = eps * (double)vg[j];
-    const double xhp = ((double)xm[o + j] + (double)xd[o + j] - mup) * rp;
-    const double xhm = ((double)xm[o + j] - (double)xd[o + j] - mum) * rmi;
-    const double dyp = (double)dym[o + j] + (double)dyd[o + j];
-    const double dymi = (double)dym[o + j] - (double)dyd[o + j];
-    const double dhp = dyp * (g + dg), dhm = dymi * (g - dg);
-    const double dxp = rp * (dhp - a1p - xhp * a2p);
-    const double dxm = rmi * (dhm - a1m - xhm * a2m);
-    const double rm0 = dresm ? (double)dresm[o + j] : 0.0;
-    const double rd0 = dresd ? (double)dresd[o + j] : 0.0;
-    dx.m[o + j] = (float)(rm0 + 0.5 * (dxp + dxm));
-    dx.d[o + j] = (float)(rd0 + 0.5 * (dxp - dxm));
-    gpart[o + j] = (float)(0.5 * (dyp * xhp - dymi * xhm));
+    gpart[(int64_t)blockIdx.x * dm + j] = cacc[j];
+    if (bpart) bpart[(int64_t)blockIdx.x * dm + j] = cacc[dm + j];
   }
 }
 
@@ -174,6 +198,16 @@ __global__ void colsum_stage1(double* partial, const float* X, int rows, int C, 
   const int r0 = c * per, r1 = min(rows, r0 + per);
   double s = 0.0;
   for (int r = r0; r < r1; ++r) s += (double)X[(int64_t)r * ld + j];
+  partial[(int64_t)c * C + j] = s;
+}
+__global__ void colsum64_stage1(double* partial, const double* X, int rows, int C) {
+  const int j = blockIdx.x * NT + threadIdx.x;
+  if (j >= C) return;
+  const int c = blockIdx.y;
+  const int per = (rows + COLSUM_CHUNKS - 1) / COLSUM_CHUNKS;
+  const int r0 = c * per, r1 = min(rows, r0 + per);
+  double s = 0.0;
+  for (int r = r0; r < r1; ++r) s += X[(int64_t)r * C + j];
   partial[(int64_t)c * C + j] = s;
 }
 __global__ void colsum_stage2(float* out, const double* partial, int C, double scale, bool acc) {
@@ -636,17 +670,26 @@ hipError_t launch_norm_fwd(PairT<T> y, const float* xm, const float* xd, int row
 }
 
 template <typename T>
-hipError_t launch_norm_bwd(PairF dx, const float* dresm, const float* dresd, const float* xm, const float* xd,
+hipError_t launch_norm_bwd(PairF dx, PairT<T> dxo, const float* dresm, const float* dresd, const float* xm, const float* xd,
                            const float* dym, const float* dyd, int rows, int dm, bool ln, const T* thg,
-                           const float* vg, double eps, float neps, float* gpart, hipStream_t s) {
-  hipLaunchKernelGGL(norm_bwd_kernel<T>, dim3(rows), dim3(NT), 0, s, dx, dresm, dresd, xm, xd, dym, dyd, dm, ln, thg,
-                     vg, eps, (double)neps, gpart);
+                           const float* vg, double eps, float neps, double* gpart, double* bpart, hipStream_t s) {
+  const size_t lds = (size_t)dm * (bpart ? 2 : 1) * sizeof(double);
+  if (lds > 64 * 1024) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(norm_bwd_kernel<T>, dim3(norm_bwd_groups(rows)), dim3(NT), lds, s, dx, dxo, dresm, dresd, xm, xd, dym,
+                     dyd, rows, dm, ln, thg, vg, eps, (double)neps, gpart, bpart);
   return hipGetLastError();
 }
 
 hipError_t launch_colsum(float* out, const float* X, int rows, int C, int64_t ld, double scale, bool acc, double* partial,
                          hipStream_t s) {
   hipLaunchKernelGGL(colsum_stage1, dim3(ceil_div(C, NT), COLSUM_CHUNKS), dim3(NT), 0, s, partial, X, rows, C, ld);
+  hipLaunchKernelGGL(colsum_stage2, dim3(ceil_div(C, NT)), dim3(NT), 0, s, out, (const double*)partial, C, scale, acc);
+  return hipGetLastError();
+}
+
+hipError_t launch_colsum_f64(float* out, const double* X, int rows, int C, double scale, bool acc, double* partial,
+                             hipStream_t s) {
+  hipLaunchKernelGGL(colsum64_stage1, dim3(ceil_div(C, NT), COLSUM_CHUNKS), dim3(NT), 0, s, partial, X, rows, C);
   hipLaunchKernelGGL(colsum_stage2, dim3(ceil_div(C, NT)), dim3(NT), 0, s, out, (const double*)partial, C, scale, acc);
   return hipGetLastError();
 }
@@ -764,9 +807,9 @@ hipError_t launch_pos_bwd(float* hv, const float* dxd, int B, int S, int dm, dou
                                           const float*, double, hipStream_t);                                          \
   template hipError_t launch_norm_fwd<T>(PairT<T>, const float*, const float*, int, int, bool, const T*, const float*, \
                                          const T*, const float*, double, float, hipStream_t);                          \
-  template hipError_t launch_norm_bwd<T>(PairF, const float*, const float*, const float*, const float*, const float*,  \
-                                         const float*, int, int, bool, const T*, const float*, double, float, float*,  \
-                                         hipStream_t);                                                                 \
+  template hipError_t launch_norm_bwd<T>(PairF, PairT<T>, const float*, const float*, const float*, const float*,      \
+                                         const float*, const float*, int, int, bool, const T*, const float*, double,    \
+                                         float, double*, double*, hipStream_t);                                        \
   template hipError_t launch_qkv_post<T>(PairT<T>, const float*, const float*, int, int, int, int, int, const double*, \
                                          bool, hipStream_t);                                                           \
   template hipError_t launch_qkv_bwd_post<T>(PairT<T>, float*, float*, int, int, int, int, int, const double*, bool,   \

@@ -383,6 +383,35 @@ hipError_t launch_copy16(void* dst, const void* src, size_t bytes, hipStream_t s
   return hipGetLastError();
 }
 
+namespace {
+__global__ void sum_splits_kernel(float* out, const float* part, int ns, int64_t n) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    double t = 0.0;
+    for (int j = 0; j < ns; ++j) t += (double)part[(int64_t)j * n + i];
+    out[i] = (float)t;
+  }
+}
+__global__ void sum_splits4_kernel(float4* out, const float4* part, int ns, int64_t n4) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n4; i += (int64_t)gridDim.x * blockDim.x) {
+    double t[4] = {0.0, 0.0, 0.0, 0.0};
+    for (int j = 0; j < ns; ++j) {
+      const float4 p = part[(int64_t)j * n4 + i];
+      t[0] += p.x; t[1] += p.y; t[2] += p.z; t[3] += p.w;
+    }
+    out[i] = make_float4((float)t[0], (float)t[1], (float)t[2], (float)t[3]);
+  }
+}
+}  // namespace
+
+hipError_t launch_sum_splits(float* out, const float* part, int ns, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (n % 4 == 0 && (uintptr_t)out % 16 == 0 && (uintptr_t)part % 16 == 0)
+    hipLaunchKernelGGL(sum_splits4_kernel, dim3(grid_for(n / 4)), dim3(NT), 0, s, (float4*)out, (const float4*)part, ns, n / 4);
+  else
+    hipLaunchKernelGGL(sum_splits_kernel, dim3(grid_for(n)), dim3(NT), 0, s, out, part, ns, n);
+  return hipGetLastError();
+}
+
 hipError_t launch_fill_f64(double* p, int64_t n, double v, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(fill_f64_kernel, dim3(grid_for(n)), dim3(NT), 0, s, p, n, v);

@@ -84,6 +84,7 @@ def lib():
         "fdh_last_error": (C.c_char_p, [vp]),
         "fdh_testing_gemm": (i32, [i32, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, i32, C.c_float, i32, vp]),
         "fdh_testing_unfused_attention": (i32, [vp, i32]),
+        "fdh_testing_unsplit_wgrad": (i32, [vp, i32]),
         "fdh_testing_timing": (i32, [vp, i32]),
         "fdh_testing_timing_read": (i32, [vp, pd]),
         "fdh_testing_copy": (i32, [vp, vp, C.c_size_t, vp]),
@@ -266,6 +267,10 @@ class Model:
     def unfused_attention(self, on: bool):
         """Plan the unfused attention path at the next set_workspace (testing)."""
         self._check(self._L.fdh_testing_unfused_attention(self._h, int(on)), "fdh_testing_unfused_attention")
+
+    def unsplit_wgrad(self, on: bool):
+        """Weight-gradient GEMMs over the whole token range (testing)."""
+        self._check(self._L.fdh_testing_unsplit_wgrad(self._h, int(on)), "fdh_testing_unsplit_wgrad")
 
     def timing(self, enable: bool):
         self._check(self._L.fdh_testing_timing(self._h, int(enable)), "fdh_testing_timing")

@@ -66,6 +66,12 @@ def test_hvp_parity_small(name, dtype, std):
         err = rel_l2(g, want)
         say(f"  rel_l2 = {err:.3e}")
         assert err <= tol
+        if dtype == "f32":
+            # every parameter block on its own, the norm gains and biases included
+            for e in M.layout(cfg):
+                wb = want[e.offset:e.offset + e.numel]
+                if np.linalg.norm(wb) > 1e-6 * np.linalg.norm(want):
+                    assert rel_l2(g[e.offset:e.offset + e.numel], wb) <= tol, e.name
     # loss values at the two points of the last call
     v = vs[-1].astype(np.float64)
     Lp = M.loss(cfg, theta.astype(np.float64) + eps * v, tok)
