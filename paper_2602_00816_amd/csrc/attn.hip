@@ -175,16 +175,44 @@ __device__ inline void dma_tiles(bf16_t* dst, const bf16_t* const (&src)[NTILE],
   }
 }
 
+// s_waitcnt with vmcnt = N (bits 3:0 and 15:14), expcnt and lgkmcnt at their maxima
+template <int N>
+__device__ inline void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Work item of a workgroup in a grid of nblk blocks (of queries or keys) x
+// nhead heads, with the block index `blk` taken so that the longest items run
+// first.  Workgroups are handed out in linear-id order and round-robin over
+// the eight XCDs (id mod 8); ordering the items by block first gives every XCD
+// the same mix of long and short items, where a (block fastest) ordering
+// would give XCD k only the blocks congruent to k mod 8 and, under the causal
+// mask, very different amounts of work.
+__device__ inline void work_item(int nhead, int& blk, int& head) {
+  const int id = blockIdx.x + gridDim.x * blockIdx.y;
+  blk = id / nhead;
+  head = id % nhead;
+}
+
 // ---------------------------------------------------------------------------
 // forward
 // ---------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(256) void flash_fwd_kernel(FlashArgs a) {
   constexpr int KB = 32, KS = D / 16, NT = D / 32, TILE = KB * D;
-  __shared__ __attribute__((aligned(1024))) bf16_t ring[2][4 * TILE];   // K.m K.d V.m V.d
+  // K is one block ahead of V: iteration kb forms the scores of block kb + 1
+  // while it turns the scores of block kb into the P V products.  Both rings
+  // have R stages; the loads run R - 1 blocks ahead of their use.
+  constexpr int R = 4;
+  constexpr int LPP = D / 16;   // DMA instructions per wavefront per (K, V) block pair
+  __shared__ __attribute__((aligned(1024))) bf16_t kring[R][2 * TILE];   // K.m K.d
+  __shared__ __attribute__((aligned(1024))) bf16_t vring[R][2 * TILE];   // V.m V.d
 
-  const int qb = gridDim.x - 1 - blockIdx.x;   // longest rows first
-  const int bh = blockIdx.y, b = bh / a.Hq, h = bh % a.Hq, kh = h / a.G;
+  int qb, bh;
+  work_item(gridDim.y, qb, bh);
+  qb = gridDim.x - 1 - qb;   // longest rows first
+  const int b = bh / a.Hq, h = bh % a.Hq, kh = h / a.G;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int q0 = qb * 128, qw = q0 + 32 * wave;
@@ -215,6 +243,34 @@ __global__ __launch_bounds__(256) void flash_fwd_kernel(FlashArgs a) {
 
   const int nkb = (q0 + 128) / KB;
   const int lastw = qw / KB;   // this wavefront's diagonal block
+  constexpr float LOG2E = 1.4426950408889634f;
+  // block j of K (or V) into stage j % R; past the last block the last block
+  // is loaded again (never read), so every iteration issues the same number
+  // of loads and the vmcnt waits are constants
+  auto issue_k = [&](int j) {
+    const int64_t r = row0 + (int64_t)min(j, nkb - 1) * KB;
+    const bf16_t* src[2] = {a.qkv_m + r * a.ld + a.koff + kh * D, a.qkv_d + r * a.ld + a.koff + kh * D};
+    dma_tiles<D, KB, 2>(kring[j % R], src, a.ld, wave, lane);
+  };
+  auto issue_v = [&](int j) {
+    const int64_t r = row0 + (int64_t)min(j, nkb - 1) * KB;
+    const bf16_t* src[2] = {a.qkv_m + r * a.ld + a.voff + kh * D, a.qkv_d + r * a.ld + a.voff + kh * D};
+    dma_tiles<D, KB, 2>(vring[j % R], src, a.ld, wave, lane);
+  };
+  // raw scores of the block in kring[st]: sm = K.m q.m, sd = K.m q.d + K.d q.m
+  auto scores = [&](int st, f32x16_t& sm, f32x16_t& sd) {
+    const bf16_t* Km = kring[st];
+    const bf16_t* Kd = Km + TILE;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sm[r] = sd[r] = 0.f;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const bf16x8_t km = ld_k32<D>(Km, 0, s, lane), kd = ld_k32<D>(Kd, 0, s, lane);
+      sm = mma32(km, qm[s], sm);
+      sd = mma32(km, qd[s], sd);
+      sd = mma32(kd, qm[s], sd);
+    }
+  };
 
   // Reference maximum of the logits, moved lazily: only when a logit exceeds
   // it by more than 8 (e^8 ~ 3e3 keeps every term and row sum far from
@@ -222,109 +278,154 @@ __global__ __launch_bounds__(256) void flash_fwd_kernel(FlashArgs a) {
   // block is rare.  The accumulators live in VGPRs (this file is compiled with
   // VGPR-form MFMAs), so the rescale branch costs nothing when not taken.
   float mrun = NEG;
-  auto issue = [&](int kb) {
-    const int64_t r = row0 + (int64_t)kb * KB;
-    const bf16_t* src[4] = {a.qkv_m + r * a.ld + a.koff + kh * D, a.qkv_d + r * a.ld + a.koff + kh * D,
-                            a.qkv_m + r * a.ld + a.voff + kh * D, a.qkv_d + r * a.ld + a.voff + kh * D};
-    dma_tiles<D, KB, 4>(ring[kb & 1], src, a.ld, wave, lane);
-  };
-  issue(0);
-  __builtin_amdgcn_s_waitcnt(0);
+  f32x16_t sm, sd;
+  // pair j = (K block j + 1, V block j); iteration kb issues pair kb + R - 1
+  // and needs pair kb + 1 at its end
+  issue_k(0);
+#pragma unroll
+  for (int j = 0; j < R - 1; ++j) {
+    issue_k(j + 1);
+    issue_v(j);
+  }
+  wait_vm<(R - 1) * LPP>();
+  __syncthreads();
+  scores(0, sm, sd);
+  wait_vm<(R - 2) * LPP>();
   __syncthreads();
   for (int kb = 0; kb < nkb; ++kb) {
-    if (kb + 1 < nkb) issue(kb + 1);
+    issue_k(kb + R);
+    issue_v(kb + R - 1);
     // every wavefront runs every block: past its diagonal all keys are masked
     // (exact zeros); a branch around the accumulator updates would make the
     // register allocator shuttle the accumulators through VGPRs each block
-    {
-      const bf16_t* Km = ring[kb & 1];
-      const bf16_t* Kd = Km + TILE;
-      const bf16_t* Vm = Km + 2 * TILE;
-      const bf16_t* Vd = Km + 3 * TILE;
-      // four independent accumulation chains (S.m over even / odd k steps,
-      // the two terms of S.d) keep consecutive MFMAs independent
-      f32x16_t sm, sd, sm1, sd1;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sm[r] = sd[r] = sm1[r] = sd1[r] = 0.f;
-#pragma unroll
-      for (int s = 0; s < KS; s += 2) {
-        const bf16x8_t km0 = ld_k32<D>(Km, 0, s, lane), kd0 = ld_k32<D>(Kd, 0, s, lane);
-        const bf16x8_t km1 = ld_k32<D>(Km, 0, s + 1, lane), kd1 = ld_k32<D>(Kd, 0, s + 1, lane);
-        sm = mma32(km0, qm[s], sm);
-        sd = mma32(km0, qd[s], sd);
-        sd1 = mma32(kd0, qm[s], sd1);
-        sm1 = mma32(km1, qm[s + 1], sm1);
-        sd = mma32(km1, qd[s + 1], sd);
-        sd1 = mma32(kd1, qm[s + 1], sd1);
-      }
+    if (kb >= lastw) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        sm[r] += sm1[r];
-        sd[r] += sd1[r];
-      }
-      const bool diag = kb >= lastw;
-      float bmax = 0.f;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        sm[r] *= a.scale;
-        sd[r] *= a.scale;
-        bmax = fmaxf(bmax, fabsf(sd[r]));
-      }
-      if (diag) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = kb * KB + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-          if (key > qi) sm[r] = NEG;
-        }
-      }
-      float amax = NEG;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) amax = fmaxf(amax, sm[r]);
-      amax = fmaxf(amax, __shfl_xor(amax, 32, 64));
-      if (__any(amax > mrun + 8.f)) {
-        const float mnew = fmaxf(mrun, amax);
-        const float alpha = __expf(mrun - mnew);
-        mrun = mnew;
-        zc *= alpha;
-        zs *= alpha;
-#pragma unroll
-        for (int t = 0; t < NT; ++t)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            Ac[t][r] *= alpha;
-            X[t][r] *= alpha;
-          }
-      }
-      float pc[16], ps[16];
-      auto terms = [&](auto ser) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float e = __expf(sm[r] - mrun);
-          float c, sn;
-          coshsinh<decltype(ser)::value>(sd[r], c, sn);
-          pc[r] = e * c;   // e^a cosh b
-          ps[r] = e * sn;  // e^a sinh b
-          zc += pc[r];
-          zs += ps[r];
-        }
-      };
-      if (!__any(bmax >= SERIES_MAX)) terms(std::true_type{});
-      else terms(std::false_type{});
-#pragma unroll
-      for (int t2 = 0; t2 < 2; ++t2) {
-        const bf16x8_t bc = pack8(pc + 8 * t2), bs = pack8(ps + 8 * t2);
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-          const bf16x8_t vm = ld_t32<D>(Vm, 16 * t2, 32 * t, lane), vd = ld_t32<D>(Vd, 16 * t2, 32 * t, lane);
-          Ac[t] = mma32(vm, bc, Ac[t]);
-          X[t] = mma32(vm, bs, X[t]);
-          X[t] = mma32(vd, bc, X[t]);
-        }
+        const int key = kb * KB + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+        if (key > qi) sm[r] = NEG;
       }
     }
-    __builtin_amdgcn_s_waitcnt(0);
+    float amax = NEG, bmax = 0.f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      amax = fmaxf(amax, sm[r]);
+      bmax = fmaxf(bmax, fabsf(sd[r]));
+    }
+    amax *= a.scale;
+    amax = fmaxf(amax, __shfl_xor(amax, 32, 64));
+    if (__any(amax > mrun + 8.f)) {
+      const float mnew = fmaxf(mrun, amax);
+      const float alpha = __expf(mrun - mnew);
+      mrun = mnew;
+      zc *= alpha;
+      zs *= alpha;
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          Ac[t][r] *= alpha;
+          X[t][r] *= alpha;
+        }
+    }
+    const float moff = -mrun * LOG2E;
+    // The scores of the next block (the last iteration forms them from a
+    // stale ring stage and drops them) overlap the element-wise terms of this
+    // one, taken with the two-term series of cosh b and sinh b: per k step,
+    // the fragment reads of the next step, the three score MFMAs and the terms
+    // of 16 / KS elements, in this order (scheduling barriers keep the
+    // compiler from regrouping them).
+    f32x16_t smn, sdn;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) smn[r] = sdn[r] = 0.f;
+    float pc[16], ps[16];
+    float zci = 0.f, zsi = 0.f;
+    {
+      constexpr int EPS = 16 / KS;   // elements per k step
+      const bf16_t* Km = kring[(kb + 1) % R];
+      const bf16_t* Kd = Km + TILE;
+      bf16x8_t kmf[2], kdf[2];
+      kmf[0] = ld_k32<D>(Km, 0, 0, lane);
+      kdf[0] = ld_k32<D>(Kd, 0, 0, lane);
+      auto term = [&](int r) {
+        const float e = __builtin_amdgcn_exp2f(fmaf(sm[r], a.c_exp, moff));
+        const float q2 = sd[r] * sd[r];
+        pc[r] = e * fmaf(q2, a.c_cosh, 1.f);              // e^a cosh b
+        ps[r] = e * (sd[r] * fmaf(q2, a.c_sinh, a.scale));  // e^a sinh b
+        zci += pc[r];
+        zsi += ps[r];
+        // materialise the terms here: the fix-up branch below overwrites them,
+        // and the compiler would otherwise sink this work past the MFMAs
+        asm volatile("" : "+v"(pc[r]), "+v"(ps[r]), "+v"(zci), "+v"(zsi));
+      };
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        if (s + 1 < KS) {
+          kmf[(s + 1) & 1] = ld_k32<D>(Km, 0, s + 1, lane);
+          kdf[(s + 1) & 1] = ld_k32<D>(Kd, 0, s + 1, lane);
+        }
+        smn = mma32(kmf[s & 1], qm[s], smn);
+#pragma unroll
+        for (int j = 0; j < EPS / 2; ++j) term(EPS * s + j);
+        sdn = mma32(kmf[s & 1], qd[s], sdn);
+#pragma unroll
+        for (int j = EPS / 2; j < EPS; ++j) term(EPS * s + j);
+        sdn = mma32(kdf[s & 1], qm[s], sdn);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    bf16x8_t bc[2], bs[2];
+    bc[0] = pack8(pc); bc[1] = pack8(pc + 8);
+    bs[0] = pack8(ps); bs[1] = pack8(ps + 8);
+    // some |b| past the series range (never at the workloads' eps): redo the
+    // terms with the exponential form
+    if (__any(bmax * a.scale >= SERIES_MAX)) {
+      zci = zsi = 0.f;
+#pragma unroll
+      for (int t2 = 0; t2 < 2; ++t2) {
+        float pc[8], ps[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int r = 8 * t2 + j;
+          const float e = __builtin_amdgcn_exp2f(fmaf(sm[r], a.c_exp, moff));
+          float c, sn;
+          coshsinh<false>(sd[r] * a.scale, c, sn);
+          pc[j] = e * c;
+          ps[j] = e * sn;
+          zci += pc[j];
+          zsi += ps[j];
+        }
+        bc[t2] = pack8(pc);
+        bs[t2] = pack8(ps);
+      }
+    }
+    zc += zci;
+    zs += zsi;
+    {
+      const bf16_t* Vm = vring[kb % R];
+      const bf16_t* Vd = Vm + TILE;
+      bf16x8_t vmf[2], vdf[2];
+      vmf[0] = ld_t32<D>(Vm, 0, 0, lane);
+      vdf[0] = ld_t32<D>(Vd, 0, 0, lane);
+#pragma unroll
+      for (int i = 0; i < 2 * NT; ++i) {
+        const int t2 = i / NT, t = i % NT;
+        if (i + 1 < 2 * NT) {
+          const int u2 = (i + 1) / NT, u = (i + 1) % NT;
+          vmf[(i + 1) & 1] = ld_t32<D>(Vm, 16 * u2, 32 * u, lane);
+          vdf[(i + 1) & 1] = ld_t32<D>(Vd, 16 * u2, 32 * u, lane);
+        }
+        Ac[t] = mma32(vmf[i & 1], bc[t2], Ac[t]);
+        X[t] = mma32(vmf[i & 1], bs[t2], X[t]);
+        X[t] = mma32(vdf[i & 1], bc[t2], X[t]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    sm = smn;
+    sd = sdn;
+    wait_vm<(R - 2) * LPP>();
     __syncthreads();
   }
+  __builtin_amdgcn_s_waitcnt(0);   // the clamped reloads of the last iterations
 
   zc += __shfl_xor(zc, 32, 64);
   zs += __shfl_xor(zs, 32, 64);
@@ -389,8 +490,10 @@ __global__ __launch_bounds__(256) void flash_bwd_q_kernel(FlashArgs a) {
   constexpr int KB = 32, KS = D / 16, NT = D / 32, TILE = KB * D;
   __shared__ __attribute__((aligned(1024))) bf16_t ring[2][4 * TILE];   // K.m K.d V.m V.d
 
-  const int qb = gridDim.x - 1 - blockIdx.x;
-  const int bh = blockIdx.y, b = bh / a.Hq, h = bh % a.Hq, kh = h / a.G;
+  int qb, bh;
+  work_item(gridDim.y, qb, bh);
+  qb = gridDim.x - 1 - qb;   // longest rows first
+  const int b = bh / a.Hq, h = bh % a.Hq, kh = h / a.G;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int q0 = qb * 128, qw = q0 + 32 * wave;
@@ -520,8 +623,9 @@ __global__ __launch_bounds__(256) void flash_bwd_kv_kernel(FlashArgs a) {
   __shared__ float4 sst[2][QB];                                         // m, u, w, D.m
   __shared__ __attribute__((aligned(16))) float sdd[2][QB];             // D.d
 
-  const int kblk = blockIdx.x;   // lowest keys (most queries) first
-  const int bkh = blockIdx.y, b = bkh / a.Hk, kh = bkh % a.Hk;
+  int kblk, bkh;
+  work_item(gridDim.y, kblk, bkh);   // lowest keys (most queries) first
+  const int b = bkh / a.Hk, kh = bkh % a.Hk;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int k0 = kblk * 64, kw = k0 + 16 * wave;
@@ -689,14 +793,25 @@ __global__ __launch_bounds__(256) void flash_bwd_kv_kernel(FlashArgs a) {
 
 bool flash_supported(int dh, int S) { return (dh == 64 || dh == 128) && S % 128 == 0; }
 
-hipError_t launch_flash_fwd(const FlashArgs& a, int B, hipStream_t s) {
+static FlashArgs with_constants(const FlashArgs& a0) {
+  FlashArgs a = a0;
+  const double sc = a.scale;
+  a.c_exp = (float)(sc * 1.4426950408889634);
+  a.c_cosh = (float)(0.5 * sc * sc);
+  a.c_sinh = (float)(sc * sc * sc / 6.0);
+  return a;
+}
+
+hipError_t launch_flash_fwd(const FlashArgs& a0, int B, hipStream_t s) {
+  const FlashArgs a = with_constants(a0);
   dim3 g(a.S / 128, B * a.Hq);
   if (a.D == 128) hipLaunchKernelGGL(flash_fwd_kernel<128>, g, dim3(256), 0, s, a);
   else hipLaunchKernelGGL(flash_fwd_kernel<64>, g, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
-hipError_t launch_flash_bwd(const FlashArgs& a, int B, hipStream_t s) {
+hipError_t launch_flash_bwd(const FlashArgs& a0, int B, hipStream_t s) {
+  const FlashArgs a = with_constants(a0);
   const int nrows = B * a.S * a.Hq;
   dim3 gd((nrows + 15) / 16);
   if (a.D == 128) hipLaunchKernelGGL(flash_delta_kernel<128>, gd, dim3(256), 0, s, a, nrows);

@@ -149,6 +149,8 @@ struct FlashArgs {
   float* g_m;            // [T][ldg] fp32 gradients of q, k, v (same column layout as qkv)
   float* g_d;
   int64_t ldg;
+  // derived from scale by the launchers: scale log2(e), scale^2 / 2, scale^3 / 6
+  float c_exp, c_cosh, c_sinh;
 };
 // head dimension 64 or 128, S a multiple of 128
 bool flash_supported(int dh, int S);
