@@ -95,7 +95,7 @@ hipError_t launch_norm_fwd(PairT<T> y, const float* xm, const float* xd, int row
 // of the half difference of dy * xhat (gain gradient), and with bpart (LayerNorm)
 // bpart[w][j] = its sum of dy.d (bias gradient); launch_colsum_f64 finishes both.
 // dmodel * (bpart ? 2 : 1) <= 8192.
-constexpr int NORM_BWD_ROWS = 8;
+constexpr int NORM_BWD_ROWS = 16;
 inline int norm_bwd_groups(int rows) { return (rows + NORM_BWD_ROWS - 1) / NORM_BWD_ROWS; }
 template <typename T>
 hipError_t launch_norm_bwd(PairF dx_out, PairT<T> dx_op, const float* dres_m, const float* dres_d, const float* xm,

@@ -188,6 +188,153 @@ __global__ __launch_bounds__(NT) void norm_bwd_kernel(PairF dx, PairT<T> dxo, co
   }
 }
 
+// Same computation with one wavefront per row (rows of 256 CPL columns): lane
+// l holds the float4 chunks at columns 256 c + 4 l.  The row reductions are
+// wavefront sums (no barriers); each pass rereads its operands, which after
+// the first pass come from the caches.  Each wavefront adds the
+// gain and bias terms of its rows per column in LDS (fp32, at most
+// NORM_BWD_ROWS / 4 rows), and the four wavefronts' sums are added in fp64 in
+// wavefront order.
+template <typename T>
+__device__ inline float4 ld4f(const T* p, int64_t i) {
+  if constexpr (sizeof(T) == 4) {
+    return *reinterpret_cast<const float4*>(p + i);
+  } else {
+    const uint2 u = *reinterpret_cast<const uint2*>(p + i);
+    return make_float4(bf16_to_f32((bf16_t)(u.x & 0xFFFF)), bf16_to_f32((bf16_t)(u.x >> 16)),
+                       bf16_to_f32((bf16_t)(u.y & 0xFFFF)), bf16_to_f32((bf16_t)(u.y >> 16)));
+  }
+}
+template <typename T>
+__device__ inline void st4f(T* p, int64_t i, float a, float b, float c, float d) {
+  if constexpr (sizeof(T) == 4) {
+    *reinterpret_cast<float4*>(p + i) = make_float4(a, b, c, d);
+  } else {
+    *reinterpret_cast<uint2*>(p + i) = make_uint2((uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16),
+                                                  (uint32_t)f32_to_bf16(c) | ((uint32_t)f32_to_bf16(d) << 16));
+  }
+}
+__device__ inline float f4e(const float4& v, int e) { return e == 0 ? v.x : (e == 1 ? v.y : (e == 2 ? v.z : v.w)); }
+
+template <typename T, int CPL>
+__global__ __launch_bounds__(NT) void norm_bwd_wave_kernel(PairF dx, PairT<T> dxo, const float* dresm, const float* dresd,
+                                                           const float* xm, const float* xd, const float* dym,
+                                                           const float* dyd, int rows, bool ln, const T* thg,
+                                                           const float* vg, double eps, double neps, double* gpart,
+                                                           double* bpart) {
+  constexpr int DM = 256 * CPL;
+  // per-wavefront column sums (gain, bias); a lane only touches its own columns
+  __shared__ float cg[4][DM], cb[4][DM];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int c = 0; c < CPL; ++c) {
+    *reinterpret_cast<float4*>(&cg[wave][256 * c + 4 * lane]) = make_float4(0.f, 0.f, 0.f, 0.f);
+    *reinterpret_cast<float4*>(&cb[wave][256 * c + 4 * lane]) = make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  auto ld = [](const float* p, int64_t i) { return *reinterpret_cast<const float4*>(p + i); };
+  const int r0 = blockIdx.x * NORM_BWD_ROWS;
+  for (int i = wave; i < NORM_BWD_ROWS; i += 4) {
+    const int row = r0 + i;
+    if (row >= rows) break;
+    const int64_t o = (int64_t)row * DM + 4 * lane;
+    double mup = 0.0, mum = 0.0;
+    if (ln) {
+      double sp = 0.0, sm = 0.0;
+#pragma unroll 2
+      for (int c = 0; c < CPL; ++c) {
+        const float4 xa = ld(xm, o + 256 * c), xb = ld(xd, o + 256 * c);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          sp += (double)f4e(xa, e) + (double)f4e(xb, e);
+          sm += (double)f4e(xa, e) - (double)f4e(xb, e);
+        }
+      }
+      mup = wave_sum(sp) / DM;
+      mum = wave_sum(sm) / DM;
+    }
+    double qp = 0.0, qm = 0.0;
+#pragma unroll 2
+    for (int c = 0; c < CPL; ++c) {
+      const float4 xa = ld(xm, o + 256 * c), xb = ld(xd, o + 256 * c);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const double p = (double)f4e(xa, e) + (double)f4e(xb, e) - mup;
+        const double q = (double)f4e(xa, e) - (double)f4e(xb, e) - mum;
+        qp += p * p;
+        qm += q * q;
+      }
+    }
+    const double rp = 1.0 / sqrt(wave_sum(qp) / DM + neps);
+    const double rmi = 1.0 / sqrt(wave_sum(qm) / DM + neps);
+    // means of dxhat and dxhat * xhat at both points
+    double s1p = 0.0, s1m = 0.0, s2p = 0.0, s2m = 0.0;
+#pragma unroll 2
+    for (int c = 0; c < CPL; ++c) {
+      const int col = 256 * c + 4 * lane;
+      const float4 xa = ld(xm, o + 256 * c), xb = ld(xd, o + 256 * c);
+      const float4 ya = ld(dym, o + 256 * c), yb = ld(dyd, o + 256 * c);
+      const float4 g4 = ld4f(thg, col), v4 = ld(vg, col);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const double g = f4e(g4, e), dg = eps * (double)f4e(v4, e);
+        const double xhp = ((double)f4e(xa, e) + (double)f4e(xb, e) - mup) * rp;
+        const double xhm = ((double)f4e(xa, e) - (double)f4e(xb, e) - mum) * rmi;
+        const double dhp = ((double)f4e(ya, e) + (double)f4e(yb, e)) * (g + dg);
+        const double dhm = ((double)f4e(ya, e) - (double)f4e(yb, e)) * (g - dg);
+        s1p += dhp;
+        s1m += dhm;
+        s2p += dhp * xhp;
+        s2m += dhm * xhm;
+      }
+    }
+    const double a1p = ln ? wave_sum(s1p) / DM : 0.0;
+    const double a1m = ln ? wave_sum(s1m) / DM : 0.0;
+    const double a2p = wave_sum(s2p) / DM;
+    const double a2m = wave_sum(s2m) / DM;
+#pragma unroll 2
+    for (int c = 0; c < CPL; ++c) {
+      const int col = 256 * c + 4 * lane;
+      const float4 xa = ld(xm, o + 256 * c), xb = ld(xd, o + 256 * c);
+      const float4 ya = ld(dym, o + 256 * c), yb = ld(dyd, o + 256 * c);
+      const float4 g4 = ld4f(thg, col), v4 = ld(vg, col);
+      const float4 ra = dresm ? ld(dresm, o + 256 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
+      const float4 rb = dresd ? ld(dresd, o + 256 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
+      float om[4], od[4], tg[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const double g = f4e(g4, e), dg = eps * (double)f4e(v4, e);
+        const double xhp = ((double)f4e(xa, e) + (double)f4e(xb, e) - mup) * rp;
+        const double xhm = ((double)f4e(xa, e) - (double)f4e(xb, e) - mum) * rmi;
+        const double dyp = (double)f4e(ya, e) + (double)f4e(yb, e);
+        const double dymi = (double)f4e(ya, e) - (double)f4e(yb, e);
+        const double dhp = dyp * (g + dg), dhm = dymi * (g - dg);
+        const double dxp = rp * (dhp - a1p - xhp * a2p);
+        const double dxm = rmi * (dhm - a1m - xhm * a2m);
+        om[e] = (float)((double)f4e(ra, e) + 0.5 * (dxp + dxm));
+        od[e] = (float)((double)f4e(rb, e) + 0.5 * (dxp - dxm));
+        tg[e] = (float)(0.5 * (dyp * xhp - dymi * xhm));
+      }
+      *reinterpret_cast<float4*>(dx.m + o + 256 * c) = make_float4(om[0], om[1], om[2], om[3]);
+      *reinterpret_cast<float4*>(dx.d + o + 256 * c) = make_float4(od[0], od[1], od[2], od[3]);
+      if (dxo.m) {
+        st4f(dxo.m, o + 256 * c, om[0], om[1], om[2], om[3]);
+        st4f(dxo.d, o + 256 * c, od[0], od[1], od[2], od[3]);
+      }
+      float4* pg = reinterpret_cast<float4*>(&cg[wave][col]);
+      float4* pb = reinterpret_cast<float4*>(&cb[wave][col]);
+      const float4 g0 = *pg, b0 = *pb;
+      *pg = make_float4(g0.x + tg[0], g0.y + tg[1], g0.z + tg[2], g0.w + tg[3]);
+      *pb = make_float4(b0.x + yb.x, b0.y + yb.y, b0.z + yb.z, b0.w + yb.w);
+    }
+  }
+  // the four wavefronts' column sums, added in fp64 in wavefront order
+  __syncthreads();
+  for (int j = threadIdx.x; j < DM; j += NT) {
+    gpart[(int64_t)blockIdx.x * DM + j] = (double)cg[0][j] + (double)cg[1][j] + (double)cg[2][j] + (double)cg[3][j];
+    if (bpart)
+      bpart[(int64_t)blockIdx.x * DM + j] = (double)cb[0][j] + (double)cb[1][j] + (double)cb[2][j] + (double)cb[3][j];
+  }
+}
+
 // ---- column sums ---------------------------------------------------------------
 constexpr int COLSUM_CHUNKS = 64;
 __global__ void colsum_stage1(double* partial, const float* X, int rows, int C, int64_t ld) {
@@ -673,10 +820,20 @@ template <typename T>
 hipError_t launch_norm_bwd(PairF dx, PairT<T> dxo, const float* dresm, const float* dresd, const float* xm, const float* xd,
                            const float* dym, const float* dyd, int rows, int dm, bool ln, const T* thg,
                            const float* vg, double eps, float neps, double* gpart, double* bpart, hipStream_t s) {
-  const size_t lds = (size_t)dm * (bpart ? 2 : 1) * sizeof(double);
-  if (lds > 64 * 1024) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(norm_bwd_kernel<T>, dim3(norm_bwd_groups(rows)), dim3(NT), lds, s, dx, dxo, dresm, dresd, xm, xd, dym,
-                     dyd, rows, dm, ln, thg, vg, eps, (double)neps, gpart, bpart);
+  const dim3 g(norm_bwd_groups(rows));
+  // one wavefront per row where the row is 512, 1024 or 2048 columns
+#define NBW(C) hipLaunchKernelGGL((norm_bwd_wave_kernel<T, C>), g, dim3(NT), 0, s, dx, dxo, dresm, dresd, xm, xd, dym, dyd, \
+                                  rows, ln, thg, vg, eps, (double)neps, gpart, bpart)
+  if (dm == 512) NBW(2);
+  else if (dm == 1024) NBW(4);
+  else if (dm == 2048) NBW(8);
+  else {
+    const size_t lds = (size_t)dm * (bpart ? 2 : 1) * sizeof(double);
+    if (lds > 64 * 1024) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(norm_bwd_kernel<T>, g, dim3(NT), lds, s, dx, dxo, dresm, dresd, xm, xd, dym, dyd, rows, dm, ln, thg,
+                       vg, eps, (double)neps, gpart, bpart);
+  }
+#undef NBW
   return hipGetLastError();
 }
 
