@@ -378,56 +378,50 @@ __global__ void rope_table_kernel(double* cs, int S, int dh, double base) {
   }
 }
 
-// Vectorised form: grid.y = token, each thread 4 consecutive columns (all
-// column offsets, and dh/2, are multiples of 4).  Same arithmetic as below.
+// Both channels in one pass.  A thread takes 4 consecutive columns f0..f0+3
+// of the first half of a q or k head together with their rotate-half
+// partners f0+dh/2.., reads each once and writes both rotated quadruples
+// (packed); v columns (and q/k without RoPE) are cast 4 at a time.
 template <typename T>
-__global__ void qkv_post4_kernel(T* out, const float* in, int S, int ncols, int qk_cols, int dh, const double* cs,
-                                 bool rope, bool inverse) {
+__global__ void qkv_rope_kernel(PairT<T> out, const float* inm, const float* ind, int S, int ncols, int nqk, int dh,
+                                const double* cs, bool rope, bool inverse) {
   const int t = blockIdx.y;
-  const int c = 4 * (blockIdx.x * blockDim.x + threadIdx.x);
-  if (c >= ncols) return;
-  const int64_t o = (int64_t)t * ncols + c;
-  const float4 x4 = *reinterpret_cast<const float4*>(in + o);
-  float x[4] = {x4.x, x4.y, x4.z, x4.w};
-  float r[4] = {x[0], x[1], x[2], x[3]};
-  if (rope && c < qk_cols) {
-    const int half = dh / 2;
-    const int hi = c % dh;
-    const bool lo_half = hi < half;
-    const float4 y4 = *reinterpret_cast<const float4*>(in + o + (lo_half ? half : -half));
-    const float y[4] = {y4.x, y4.y, y4.z, y4.w};
-    const double sgn = inverse ? -1.0 : 1.0;
+  const int u = blockIdx.x * blockDim.x + threadIdx.x;
+  const int half = dh / 2, qpu = half / 4;      // units per q/k head
+  const int qu = rope ? nqk * qpu : 0;          // rotated units
+  const int vu = (ncols - (rope ? nqk * dh : 0)) / 4;
+  const int64_t o = (int64_t)t * ncols;
+  if (u < qu) {
+    const int head = u / qpu, f0 = 4 * (u % qpu);
+    const int c = head * dh + f0;
     const double* row = cs + (int64_t)(t % S) * dh;
+    double co[4], si[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const int f = (hi + e) % half;
-      const double co = row[2 * f], si = row[2 * f + 1];
-      r[e] = lo_half ? (float)((double)x[e] * co - sgn * (double)y[e] * si)
-                     : (float)((double)x[e] * co + sgn * (double)y[e] * si);
+      co[e] = row[2 * (f0 + e)];
+      si[e] = inverse ? -row[2 * (f0 + e) + 1] : row[2 * (f0 + e) + 1];
     }
-  }
+    const float* ins[2] = {inm, ind};
+    T* outs[2] = {out.m, out.d};
 #pragma unroll
-  for (int e = 0; e < 4; ++e) stf(out, o + e, r[e]);
-}
-
-// forward: q/k columns rotated (rotate-half), v columns copied; one channel per call
-template <typename T>
-__global__ void qkv_post_kernel(T* out, const float* in, int T_, int S, int ncols, int qk_cols, int dh,
-                                const double* cs, bool rope, bool inverse) {
-  const int64_t n = (int64_t)T_ * ncols;
-  const int half = dh / 2;
-  GRID_LOOP(i, n) {
-    const int t = (int)(i / ncols), c = (int)(i % ncols);
-    double x = in[i];
-    if (rope && c < qk_cols) {
-      const int hi = c % dh;
-      const int f = hi % half;
-      const double co = cs[(int64_t)(t % S) * dh + 2 * f], si = cs[(int64_t)(t % S) * dh + 2 * f + 1];
-      const double sgn = inverse ? -1.0 : 1.0;
-      if (hi < half) x = x * co - sgn * (double)in[i + half] * si;
-      else x = x * co + sgn * (double)in[i - half] * si;
+    for (int ch = 0; ch < 2; ++ch) {
+      const float4 x = *reinterpret_cast<const float4*>(ins[ch] + o + c);
+      const float4 y = *reinterpret_cast<const float4*>(ins[ch] + o + c + half);
+      float lo[4], hi[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const double xe = f4e(x, e), ye = f4e(y, e);
+        lo[e] = (float)(xe * co[e] - ye * si[e]);
+        hi[e] = (float)(ye * co[e] + xe * si[e]);
+      }
+      st4f(outs[ch], o + c, lo[0], lo[1], lo[2], lo[3]);
+      st4f(outs[ch], o + c + half, hi[0], hi[1], hi[2], hi[3]);
     }
-    stf(out, i, (float)x);
+  } else if (u < qu + vu) {
+    const int c = (rope ? nqk * dh : 0) + 4 * (u - qu);
+    const float4 a = *reinterpret_cast<const float4*>(inm + o + c), b = *reinterpret_cast<const float4*>(ind + o + c);
+    st4f(out.m, o + c, a.x, a.y, a.z, a.w);
+    st4f(out.d, o + c, b.x, b.y, b.z, b.w);
   }
 }
 
@@ -859,24 +853,21 @@ hipError_t launch_rope_table(double* cs, int S, int dh, double base, hipStream_t
 template <typename T>
 hipError_t launch_qkv_post(PairT<T> out, const float* qm, const float* qd, int T_, int S, int Hq, int Hk, int dh,
                            const double* cs, bool rope, hipStream_t s) {
-  const int ncols = (Hq + 2 * Hk) * dh, qk = (Hq + Hk) * dh;
-  const unsigned g = grid_for((int64_t)T_ * ncols);
-  (void)g;
-  const dim3 g4(ceil_div(ncols / 4, NT), T_);
-  hipLaunchKernelGGL(qkv_post4_kernel<T>, g4, dim3(NT), 0, s, out.m, qm, S, ncols, qk, dh, cs, rope, false);
-  hipLaunchKernelGGL(qkv_post4_kernel<T>, g4, dim3(NT), 0, s, out.d, qd, S, ncols, qk, dh, cs, rope, false);
+  const int ncols = (Hq + 2 * Hk) * dh;
+  const int units = (rope ? (Hq + Hk) * dh / 8 : 0) + (ncols - (rope ? (Hq + Hk) * dh : 0)) / 4;
+  const dim3 g(ceil_div(units, NT), T_);
+  hipLaunchKernelGGL(qkv_rope_kernel<T>, g, dim3(NT), 0, s, out, qm, qd, S, ncols, Hq + Hk, dh, cs, rope, false);
   return hipGetLastError();
 }
 
 template <typename T>
 hipError_t launch_qkv_bwd_post(PairT<T> out, float* gm, float* gd, int T_, int S, int Hq, int Hk, int dh,
                                const double* cs, bool rope, hipStream_t s) {
-  const int ncols = (Hq + 2 * Hk) * dh, qk = (Hq + Hk) * dh;
-  const unsigned g = grid_for((int64_t)T_ * ncols);
-  (void)g;
-  const dim3 g4(ceil_div(ncols / 4, NT), T_);
-  hipLaunchKernelGGL(qkv_post4_kernel<T>, g4, dim3(NT), 0, s, out.m, (const float*)gm, S, ncols, qk, dh, cs, rope, true);
-  hipLaunchKernelGGL(qkv_post4_kernel<T>, g4, dim3(NT), 0, s, out.d, (const float*)gd, S, ncols, qk, dh, cs, rope, true);
+  const int ncols = (Hq + 2 * Hk) * dh;
+  const int units = (rope ? (Hq + Hk) * dh / 8 : 0) + (ncols - (rope ? (Hq + Hk) * dh : 0)) / 4;
+  const dim3 g(ceil_div(units, NT), T_);
+  hipLaunchKernelGGL(qkv_rope_kernel<T>, g, dim3(NT), 0, s, out, (const float*)gm, (const float*)gd, S, ncols, Hq + Hk, dh,
+                     cs, rope, true);
   return hipGetLastError();
 }
 
