@@ -216,6 +216,82 @@ __device__ inline void st4f(T* p, int64_t i, float a, float b, float c, float d)
 }
 __device__ inline float f4e(const float4& v, int e) { return e == 0 ? v.x : (e == 1 ? v.y : (e == 2 ? v.z : v.w)); }
 
+// Norm forward with one wavefront per row (rows of 256 CPL columns, lane l
+// at columns 256 c + 4 l), NORM_FWD_ROWS rows per workgroup: wavefront
+// reductions, x reread from the caches between the passes.  Same arithmetic
+// as norm_fwd_kernel.
+constexpr int NORM_FWD_ROWS = 8;
+template <typename T, int CPL>
+__global__ __launch_bounds__(NT) void norm_fwd_wave_kernel(PairT<T> y, const float* xm, const float* xd, int rows, bool ln,
+                                                           const T* thg, const float* vg, const T* thb, const float* vb,
+                                                           double eps, double neps) {
+  constexpr int DM = 256 * CPL;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  auto ld = [](const float* p, int64_t i) { return *reinterpret_cast<const float4*>(p + i); };
+  const int r0 = blockIdx.x * NORM_FWD_ROWS;
+  for (int i = wave; i < NORM_FWD_ROWS; i += 4) {
+    const int row = r0 + i;
+    if (row >= rows) break;
+    const int64_t o = (int64_t)row * DM + 4 * lane;
+    double mup = 0.0, mum = 0.0;
+    if (ln) {
+      double sp = 0.0, sm = 0.0;
+#pragma unroll 2
+      for (int c = 0; c < CPL; ++c) {
+        const float4 a = ld(xm, o + 256 * c), b = ld(xd, o + 256 * c);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          sp += (double)f4e(a, e) + (double)f4e(b, e);
+          sm += (double)f4e(a, e) - (double)f4e(b, e);
+        }
+      }
+      mup = wave_sum(sp) / DM;
+      mum = wave_sum(sm) / DM;
+    }
+    double qp = 0.0, qm = 0.0;
+#pragma unroll 2
+    for (int c = 0; c < CPL; ++c) {
+      const float4 a = ld(xm, o + 256 * c), b = ld(xd, o + 256 * c);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const double p = (double)f4e(a, e) + (double)f4e(b, e) - mup;
+        const double q = (double)f4e(a, e) - (double)f4e(b, e) - mum;
+        qp += p * p;
+        qm += q * q;
+      }
+    }
+    const double rp = 1.0 / sqrt(wave_sum(qp) / DM + neps);
+    const double rmi = 1.0 / sqrt(wave_sum(qm) / DM + neps);
+#pragma unroll 2
+    for (int c = 0; c < CPL; ++c) {
+      const int col = 256 * c + 4 * lane;
+      const float4 a = ld(xm, o + 256 * c), b = ld(xd, o + 256 * c);
+      const float4 g4 = ld4f(thg, col), v4 = ld(vg, col);
+      float4 b4 = make_float4(0.f, 0.f, 0.f, 0.f), w4 = b4;
+      if (thb) {
+        b4 = ld4f(thb, col);
+        w4 = ld(vb, col);
+      }
+      float om[4], od[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const double g = f4e(g4, e), dg = eps * (double)f4e(v4, e);
+        double op = ((double)f4e(a, e) + (double)f4e(b, e) - mup) * rp * (g + dg);
+        double on = ((double)f4e(a, e) - (double)f4e(b, e) - mum) * rmi * (g - dg);
+        if (thb) {
+          const double bb = f4e(b4, e), db = eps * (double)f4e(w4, e);
+          op += bb + db;
+          on += bb - db;
+        }
+        om[e] = (float)(0.5 * (op + on));
+        od[e] = (float)(0.5 * (op - on));
+      }
+      st4f(y.m, o + 256 * c, om[0], om[1], om[2], om[3]);
+      st4f(y.d, o + 256 * c, od[0], od[1], od[2], od[3]);
+    }
+  }
+}
+
 template <typename T, int CPL>
 __global__ __launch_bounds__(NT) void norm_bwd_wave_kernel(PairF dx, PairT<T> dxo, const float* dresm, const float* dresd,
                                                            const float* xm, const float* xd, const float* dym,
@@ -858,7 +934,14 @@ hipError_t launch_embed_fwd(PairF x, const int32_t* tok, int T_, int S, int dm, 
 template <typename T>
 hipError_t launch_norm_fwd(PairT<T> y, const float* xm, const float* xd, int rows, int dm, bool ln, const T* thg,
                            const float* vg, const T* thb, const float* vb, double eps, float neps, hipStream_t s) {
-  hipLaunchKernelGGL(norm_fwd_kernel<T>, dim3(rows), dim3(NT), 0, s, y, xm, xd, dm, ln, thg, vg, thb, vb, eps, (double)neps);
+  const dim3 g(ceil_div(rows, NORM_FWD_ROWS));
+#define NFW(C) hipLaunchKernelGGL((norm_fwd_wave_kernel<T, C>), g, dim3(NT), 0, s, y, xm, xd, rows, ln, thg, vg, thb, vb, eps, \
+                                  (double)neps)
+  if (dm == 512) NFW(2);
+  else if (dm == 1024) NFW(4);
+  else if (dm == 2048) NFW(8);
+  else hipLaunchKernelGGL(norm_fwd_kernel<T>, dim3(rows), dim3(NT), 0, s, y, xm, xd, dm, ln, thg, vg, thb, vb, eps, (double)neps);
+#undef NFW
   return hipGetLastError();
 }
 
