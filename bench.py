@@ -103,6 +103,7 @@ def main():
     ap.add_argument("--workload", default="llama-1.3b-bf16")
     ap.add_argument("--hvp-reps", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cg-steps", type=int, default=2, help="timed CG inverse-HVP steps after the Lanczos run")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one plain 1 GiB device copy first (reference for hardware byte counters)")
     args = ap.parse_args()
@@ -209,6 +210,27 @@ def main():
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
                      "traffic": committed_gemm_traffic(args.workload)},
     }
+    if args.cg_steps > 0:
+        # damped CG (H + lam I) x = b, lam well above the extreme Ritz values of the run
+        # (three times the largest Ritz value magnitude of the timed run)
+        from scipy.linalg import eigh_tridiagonal
+        ritz = eigh_tridiagonal(alpha[:steps], beta[:max(steps - 1, 0)], eigvals_only=True)
+        lam = 3.0 * float(np.abs(ritz).max())
+        b = mod.random_vector(SEED_PROBE + 1, "gaussian")
+        mod.timing(True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        _, res, cs, cst = mod.cg_solve(b, lam, args.cg_steps, 0.0)
+        torch.cuda.synchronize()
+        t_cg = time.perf_counter() - t0
+        tc = mod.timing_read()
+        mod.timing(False)
+        print(f"[bench] cg {cs} steps {t_cg:.2f} s", file=sys.stderr, flush=True)
+        vms = tc["lanczos"]["ms"]
+        out["cg"] = {"steps": cs, "status": cst, "lambda": lam, "ms_per_step": t_cg * 1e3 / max(cs, 1),
+                     "vec_ms_per_step": vms / max(cs, 1),
+                     "vec_hbm_GBps": tc["lanczos"]["bytes"] / (vms * 1e-3) / 1e9 if vms > 0 else None,
+                     "residual_ratio": float(res[-1] / res[0])}
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w)

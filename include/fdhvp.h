@@ -176,6 +176,21 @@ fdh_status fdh_block_stats(fdh_ctx* ctx, const float* a_dev, const float* b_dev,
  * used as scratch).  Waits for the stream. */
 fdh_status fdh_block_diagonal(fdh_ctx* ctx, const float* v_dev, double* stats_host);
 
+/* Conjugate gradient for the damped inverse HVP on the bound operator: solves
+ * (H + lambda I) x = b from x_0 = 0 (CG-based inverse-HVP solvers are the
+ * second consumer the introduction and section 4 name; the method is that of
+ * Hestenes and Stiefel).  b_dev, x_dev: float32 [P] on device, x overwritten,
+ * not aliasing b.  Stops after max_iters steps or once ||r_k|| <= rel_tol ||b||;
+ * res_host[max_iters + 1] receives ||r_0|| = ||b||, ||r_1||, ..., ||r_s||
+ * (s = *steps_done, zeros after).  Returns FDH_BREAKDOWN, with x = x_s, when a
+ * direction of non-positive curvature ((p, (H + lambda I) p) <= 0) stops it:
+ * raise lambda.  Each step is one FD-HVP plus three vector passes; fp32
+ * vectors, fp64 scalars with deterministic reductions; two scalars are read
+ * back per step (the call waits for the stream).  Needs fdh_bind and a
+ * workspace planned with m >= 1 (its Lanczos vectors hold r, p and A p). */
+fdh_status fdh_cg_solve(fdh_ctx* ctx, const float* b_dev, double lambda, int32_t max_iters, double rel_tol,
+                        float* x_dev, double* res_host, int32_t* steps_done);
+
 /* Number of transformer layers (blocks for fdh_block_stats). */
 int32_t fdh_num_blocks(const fdh_ctx* ctx);
 

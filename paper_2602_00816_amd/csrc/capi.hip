@@ -193,6 +193,16 @@ fdh_status fdh_block_diagonal(fdh_ctx* ctx, const float* v_dev, double* stats_ho
   return run(ctx, [&](fdh::Engine& e) { return e.block_diagonal(v_dev, stats_host); });
 }
 
+fdh_status fdh_cg_solve(fdh_ctx* ctx, const float* b_dev, double lambda, int32_t max_iters, double rel_tol,
+                        float* x_dev, double* res_host, int32_t* steps_done) {
+  return run(ctx, [&](fdh::Engine& e) -> int {
+    int s = 0;
+    int rc = e.cg_solve(b_dev, lambda, max_iters, rel_tol, x_dev, res_host, &s);
+    if (steps_done) *steps_done = s;
+    return rc;
+  });
+}
+
 const char* fdh_last_error(const fdh_ctx* ctx) {
   if (!ctx) return "null context";
   return ctx->err.c_str();

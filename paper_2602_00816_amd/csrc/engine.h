@@ -96,6 +96,7 @@ class Engine {
   int random_vector(float* out, uint64_t seed, int kind);
   int block_stats(const float* a, const float* b, double* out);
   int block_diagonal(const float* v, double* out);
+  int cg_solve(const float* b, double lam, int max_iters, double rel_tol, float* x, double* res, int* steps);
   std::vector<int64_t> layer_ranges() const;
 
  private:

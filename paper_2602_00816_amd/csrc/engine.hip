@@ -1046,6 +1046,85 @@ int Engine::block_stats(const float* a, const float* b, double* out) {
 
 // Exp I (section 6): h = H v, and per layer b, h_b = H v^(b) with v masked to
 // layer b (not renormalised); statistics of h^(b) against h_b^(b).
+// Conjugate gradient (Hestenes-Stiefel) for (H + lam I) x = b on the bound
+// operator, x_0 = 0.  r, p and A p live in the Lanczos vector spans; the
+// scalars on the device, (p, A p) and (r, r) read back after each step for the
+// breakdown and stopping tests.  The direction update also writes the next
+// HVP's perturbation operand.
+int Engine::cg_solve(const float* b, double lam, int max_iters, double rel_tol, float* x, double* res, int* steps) {
+  if (!b || !x || !res || !steps || max_iters < 0 || !(rel_tol >= 0.0) || !std::isfinite(lam)) {
+    err = "bad cg arguments";
+    return FDH_ERR_INVALID_ARG;
+  }
+  if ((const void*)b == (const void*)x) { err = "x aliases b"; return FDH_ERR_INVALID_ARG; }
+  if (!bound) { err = "call fdh_bind first"; return FDH_ERR_STATE; }
+  if (!ws || planM < 1) { err = "cg needs a workspace planned with m >= 1"; return FDH_ERR_WORKSPACE; }
+  hipStream_t st = stream;
+  float* r = (float*)(ws + lz_w.off);
+  float* p = (float*)(ws + lz_q.off);
+  float* ap = (float*)(ws + lz_qp.off);
+  double* sc = (double*)(ws + lz_coef.off);
+  double* part = (double*)(ws + lz_partial.off);
+  const double Pd = (double)P, ob = bf16 ? 2.0 : 4.0;
+  for (int k = 0; k <= max_iters; ++k) res[k] = 0.0;
+  *steps = 0;
+  lo_for_v = nullptr;
+  auto timed = [&](double bytes, auto&& launch) -> int {
+    int e0 = 0;
+    if (timing.on) CK(timing.begin(st, &e0));
+    CK(launch());
+    if (timing.on) CK(timing.end(st, 1, e0, 0.0, bytes));
+    return FDH_OK;
+  };
+  auto scalar = [&](int i, double* out) -> int {
+    CK(hipMemcpyAsync(out, sc + i, 8, hipMemcpyDeviceToHost, st));
+    CK(hipStreamSynchronize(st));
+    return FDH_OK;
+  };
+#define TC(bytes, ...)                                         \
+  do {                                                         \
+    int rc_ = timed((bytes), [&]() { return (__VA_ARGS__); }); \
+    if (rc_ != FDH_OK) return rc_;                             \
+  } while (0)
+  TC(16.0 * Pd, launch_cg_init(x, r, p, b, sc, part, P, st));
+  double rr = 0.0;
+  int rc = scalar(0, &rr);
+  if (rc != FDH_OK) return rc;
+  const double bnorm = std::sqrt(rr);
+  res[0] = bnorm;
+  if (!std::isfinite(bnorm)) { err = "non-finite right-hand side"; return FDH_ERR_NONFINITE; }
+  for (int k = 0; k < max_iters; ++k) {
+    rc = hvp(b_params, p, b_eps, b_tokens, b_B, b_S, ap);
+    if (rc != FDH_OK) return rc;
+    TC(12.0 * Pd, launch_cg_ap(ap, p, lam, sc, part, P, st));
+    double pap = 0.0;
+    rc = scalar(1, &pap);
+    if (rc != FDH_OK) return rc;
+    if (!std::isfinite(pap)) { err = "non-finite (p, A p)"; return FDH_ERR_NONFINITE; }
+    if (!(pap > 0.0)) return FDH_BREAKDOWN;
+    TC(24.0 * Pd, launch_cg_step(x, r, p, ap, sc, part, P, st));
+    double rn = 0.0;
+    rc = scalar(3, &rn);
+    if (rc != FDH_OK) return rc;
+    res[k + 1] = std::sqrt(rn);
+    *steps = k + 1;
+    if (!std::isfinite(rn)) { err = "non-finite residual"; return FDH_ERR_NONFINITE; }
+    if (res[k + 1] <= rel_tol * bnorm || k + 1 == max_iters) break;
+    const bool next_lo = !quad;
+    if (next_lo && bf16)
+      TC((12.0 + ob) * Pd, launch_cg_dir<bf16_t>(p, r, sc, (bf16_t*)(ws + this->lo.off), b_eps, P, st));
+    else
+      TC((12.0 + (next_lo ? ob : 0.0)) * Pd,
+         launch_cg_dir<float>(p, r, sc, next_lo ? (float*)(ws + this->lo.off) : nullptr, b_eps, P, st));
+    if (next_lo) {
+      lo_for_v = p;
+      lo_for_eps = b_eps;
+    }
+  }
+#undef TC
+  return FDH_OK;
+}
+
 int Engine::block_diagonal(const float* v, double* out) {
   if (quad || !v || !out) { err = "bad block_diagonal arguments"; return FDH_ERR_INVALID_ARG; }
   if (!bound) { err = "call fdh_bind first"; return FDH_ERR_STATE; }

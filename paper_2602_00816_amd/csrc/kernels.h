@@ -66,6 +66,20 @@ template <typename B, typename T>
 hipError_t launch_lanczos_normalise(const float* w, float* qnext, B* basis_row, T* lo, double eps, LanczosDev st, int k, double tol,
                                     int64_t n, hipStream_t s);
 
+// Conjugate gradient for (H + lam I) x = b: device scalars sc[5] = (r, r),
+// (p, A p), alpha, (r_new, r_new), beta; partial: [RED_BLOCKS].
+// init: x = 0, r = p = b, sc[0] = (b, b)
+hipError_t launch_cg_init(float* x, float* r, float* p, const float* b, double* sc, double* partial, int64_t n,
+                          hipStream_t s);
+// ap <- ap + lam p (ap holds H p); sc[1] = (p, A p), sc[2] = alpha (0 unless (p, A p) > 0)
+hipError_t launch_cg_ap(float* ap, const float* p, double lam, double* sc, double* partial, int64_t n, hipStream_t s);
+// x += alpha p, r -= alpha A p; sc[3] = (r, r), sc[4] = beta, sc[0] = (r, r)
+hipError_t launch_cg_step(float* x, float* r, const float* p, const float* ap, double* sc, double* partial, int64_t n,
+                          hipStream_t s);
+// p = r + beta p; lo (if not null) = T(eps p)
+template <typename T>
+hipError_t launch_cg_dir(float* p, const float* r, const double* sc, T* lo, double eps, int64_t n, hipStream_t s);
+
 // Per-block sums over host ranges [nblk][2]:
 // out[b*4 + {0,1,2,3}] = ||a_b||^2, ||b_b||^2, <a_b, b_b>, ||a_b - b_b||^2
 hipError_t launch_block_stats(const float* a, const float* b, const int64_t* ranges, int nblk, double* partial, double* out, hipStream_t s);

@@ -313,6 +313,114 @@ __global__ void lz_scale_kernel(const float* w, float* qn, B* row, T* lo, double
   });
 }
 
+// ---- conjugate gradient ------------------------------------------------------
+// The vector steps of CG for (H + lam I) x = b (Hestenes-Stiefel), same
+// chunked deterministic reductions as the Lanczos passes.  Scalars in sc:
+// [0] (r, r), [1] (p, A p), [2] alpha, [3] (r_new, r_new), [4] beta.
+// x = 0, r = p = b; partial = (b, b)
+__global__ __launch_bounds__(NT) void cg_init_kernel(float* x, float* r, float* p, const float* b, int64_t n,
+                                                     double* partial) {
+  __shared__ double sh[NT / 64];
+  const int64_t ch = red_chunk(n);
+  const int64_t s0 = blockIdx.x * ch, s1 = min(n, s0 + ch);
+  double acc = 0.0;
+  for_groups(s0 + 8 * threadIdx.x, s1, 8 * NT, [&](int64_t i, int ne, auto full) {
+    constexpr bool F = decltype(full)::value;
+    const V8 bv = ldv<F>(b, i, ne);
+    V8 z;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      z.x[e] = 0.f;
+      acc += (double)bv.x[e] * (double)bv.x[e];
+    }
+    stv<F>(x, i, z, ne);
+    stv<F>(r, i, bv, ne);
+    stv<F>(p, i, bv, ne);
+  });
+  acc = block_sum<NT>(acc, sh);
+  if (threadIdx.x == 0) partial[blockIdx.x] = acc;
+}
+// A p = H p + lam p (in place over H p); partial = (p, A p)
+__global__ __launch_bounds__(NT) void cg_ap_kernel(float* ap, const float* p, double lam, int64_t n, double* partial) {
+  __shared__ double sh[NT / 64];
+  const int64_t ch = red_chunk(n);
+  const int64_t s0 = blockIdx.x * ch, s1 = min(n, s0 + ch);
+  double acc = 0.0;
+  for_groups(s0 + 8 * threadIdx.x, s1, 8 * NT, [&](int64_t i, int ne, auto full) {
+    constexpr bool F = decltype(full)::value;
+    V8 av = ldv<F>(ap, i, ne);
+    const V8 pv = ldv<F>(p, i, ne);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      av.x[e] = (float)((double)av.x[e] + lam * (double)pv.x[e]);
+      acc += (double)pv.x[e] * (double)av.x[e];
+    }
+    stv<F>(ap, i, av, ne);
+  });
+  acc = block_sum<NT>(acc, sh);
+  if (threadIdx.x == 0) partial[blockIdx.x] = acc;
+}
+// x += alpha p, r -= alpha A p; partial = (r, r)
+__global__ __launch_bounds__(NT) void cg_step_kernel(float* x, float* r, const float* p, const float* ap,
+                                                     const double* sc, int64_t n, double* partial) {
+  __shared__ double sh[NT / 64];
+  const double alpha = sc[2];
+  const int64_t ch = red_chunk(n);
+  const int64_t s0 = blockIdx.x * ch, s1 = min(n, s0 + ch);
+  double acc = 0.0;
+  for_groups(s0 + 8 * threadIdx.x, s1, 8 * NT, [&](int64_t i, int ne, auto full) {
+    constexpr bool F = decltype(full)::value;
+    V8 xv = ldv<F>(x, i, ne), rv = ldv<F>(r, i, ne);
+    const V8 pv = ldv<F>(p, i, ne), av = ldv<F>(ap, i, ne);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      xv.x[e] = (float)((double)xv.x[e] + alpha * (double)pv.x[e]);
+      rv.x[e] = (float)((double)rv.x[e] - alpha * (double)av.x[e]);
+      acc += (double)rv.x[e] * (double)rv.x[e];
+    }
+    stv<F>(x, i, xv, ne);
+    stv<F>(r, i, rv, ne);
+  });
+  acc = block_sum<NT>(acc, sh);
+  if (threadIdx.x == 0) partial[blockIdx.x] = acc;
+}
+// p = r + beta p, and the next HVP's perturbation operand lo = T(eps p) if lo
+template <typename T>
+__global__ void cg_dir_kernel(float* p, const float* r, const double* sc, T* lo, double eps, int64_t n) {
+  const double beta = sc[4];
+  const int64_t step = 8 * (int64_t)gridDim.x * blockDim.x;
+  for_groups(8 * (blockIdx.x * (int64_t)blockDim.x + threadIdx.x), n, step, [&](int64_t i, int ne, auto full) {
+    constexpr bool F = decltype(full)::value;
+    V8 pv = ldv<F>(p, i, ne);
+    const V8 rv = ldv<F>(r, i, ne);
+    V8 l;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      pv.x[e] = (float)((double)rv.x[e] + beta * (double)pv.x[e]);
+      l.x[e] = (float)(eps * (double)pv.x[e]);
+    }
+    stv<F>(p, i, pv, ne);
+    if (lo) stv<F>(lo, i, l, ne);
+  });
+}
+// mode 0: sc[0] = sum.  mode 1: sc[1] = sum, sc[2] = sc[0] / sum (0 unless sum > 0).
+// mode 2: sc[3] = sum, sc[4] = sum / sc[0] (0 if sc[0] == 0), sc[0] = sum.
+__global__ void cg_finish_kernel(double* sc, const double* partial, int mode) {
+  if (threadIdx.x != 0) return;
+  double s = 0.0;
+  for (int b = 0; b < RED_BLOCKS; ++b) s += partial[b];
+  if (mode == 0) {
+    sc[0] = s;
+  } else if (mode == 1) {
+    sc[1] = s;
+    sc[2] = s > 0.0 ? sc[0] / s : 0.0;
+  } else {
+    sc[3] = s;
+    sc[4] = sc[0] > 0.0 ? s / sc[0] : 0.0;
+    sc[0] = s;
+  }
+}
+
 // lo = T(eps * v), 8 elements per lane (16-byte aligned operands)
 template <typename T>
 __global__ void scale_cast8_kernel(T* lo, const float* v, double eps, int64_t n) {
@@ -491,6 +599,31 @@ hipError_t launch_lanczos_normalise(const float* w, float* qnext, B* basis_row, 
                                                           int64_t, hipStream_t);
 INST_LZ(float)
 INST_LZ(bf16_t)
+
+hipError_t launch_cg_init(float* x, float* r, float* p, const float* b, double* sc, double* partial, int64_t n,
+                          hipStream_t s) {
+  hipLaunchKernelGGL(cg_init_kernel, dim3(RED_BLOCKS), dim3(NT), 0, s, x, r, p, b, n, partial);
+  hipLaunchKernelGGL(cg_finish_kernel, dim3(1), dim3(64), 0, s, sc, (const double*)partial, 0);
+  return hipGetLastError();
+}
+hipError_t launch_cg_ap(float* ap, const float* p, double lam, double* sc, double* partial, int64_t n, hipStream_t s) {
+  hipLaunchKernelGGL(cg_ap_kernel, dim3(RED_BLOCKS), dim3(NT), 0, s, ap, p, lam, n, partial);
+  hipLaunchKernelGGL(cg_finish_kernel, dim3(1), dim3(64), 0, s, sc, (const double*)partial, 1);
+  return hipGetLastError();
+}
+hipError_t launch_cg_step(float* x, float* r, const float* p, const float* ap, double* sc, double* partial, int64_t n,
+                          hipStream_t s) {
+  hipLaunchKernelGGL(cg_step_kernel, dim3(RED_BLOCKS), dim3(NT), 0, s, x, r, p, ap, (const double*)sc, n, partial);
+  hipLaunchKernelGGL(cg_finish_kernel, dim3(1), dim3(64), 0, s, sc, (const double*)partial, 2);
+  return hipGetLastError();
+}
+template <typename T>
+hipError_t launch_cg_dir(float* p, const float* r, const double* sc, T* lo, double eps, int64_t n, hipStream_t s) {
+  hipLaunchKernelGGL(cg_dir_kernel<T>, dim3(grid_for((n + 7) / 8)), dim3(NT), 0, s, p, r, sc, lo, eps, n);
+  return hipGetLastError();
+}
+template hipError_t launch_cg_dir<float>(float*, const float*, const double*, float*, double, int64_t, hipStream_t);
+template hipError_t launch_cg_dir<bf16_t>(float*, const float*, const double*, bf16_t*, double, int64_t, hipStream_t);
 
 hipError_t launch_block_stats(const float* a, const float* b, const int64_t* ranges, int nblk, double* partial, double* out, hipStream_t s) {
   // ranges: host array [nblk][2]; partial: device [256 * 4]; out: device [nblk * 4]

@@ -81,6 +81,7 @@ def lib():
         "fdh_slq_density": (i32, [vp, i32, i32, u64, C.POINTER(LanczosOpts), pd, pd, pi, pd]),
         "fdh_block_stats": (i32, [vp, vp, vp, pd]),
         "fdh_block_diagonal": (i32, [vp, vp, pd]),
+        "fdh_cg_solve": (i32, [vp, vp, C.c_double, i32, C.c_double, vp, pd, C.POINTER(C.c_int32)]),
         "fdh_last_error": (C.c_char_p, [vp]),
         "fdh_testing_gemm": (i32, [i32, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, i32, C.c_float, i32, vp]),
         "fdh_testing_unfused_attention": (i32, [vp, i32]),
@@ -263,6 +264,18 @@ class Model:
             weights.ctypes.data_as(C.POINTER(C.c_double)), steps.ctypes.data_as(C.POINTER(C.c_int32)),
             C.byref(tr)), "fdh_slq_density")
         return nodes, weights, steps, tr.value, st
+
+    def cg_solve(self, b, lam: float, max_iters: int, rel_tol: float = 0.0, x=None):
+        """CG for (H + lam I) x = b on the bound operator (b: float32 [P] on device).
+        Returns (x, residual norms ||r_0|| .. ||r_s||, s, status)."""
+        import torch
+        if x is None:
+            x = torch.empty_like(b)
+        res = np.zeros(max_iters + 1)
+        s = C.c_int32()
+        st = self._check(self._L.fdh_cg_solve(self._h, _ptr(b), float(lam), int(max_iters), float(rel_tol), _ptr(x),
+                                              res.ctypes.data_as(C.POINTER(C.c_double)), C.byref(s)), "fdh_cg_solve")
+        return x, res[:int(s.value) + 1], int(s.value), st
 
     def unfused_attention(self, on: bool):
         """Plan the unfused attention path at the next set_workspace (testing)."""
