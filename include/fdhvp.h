@@ -90,6 +90,21 @@ typedef struct fdh_lanczos_opts {
   float breakdown_tol;  /* stop when beta_{k+1} <= tol * max_j |alpha_j|; 0 selects 1e-5 */
 } fdh_lanczos_opts;
 
+/* Reduction of the per-target losses over a bound dataset. */
+typedef enum fdh_reduction {
+  FDH_REDUCE_MEAN = 0,        /* token-weighted mean over every kept target of every batch */
+  FDH_REDUCE_SUM = 1          /* their sum (the solution-token objective of section 7) */
+} fdh_reduction;
+
+/* One batch of a dataset (Algorithm 1's dataloader): device pointers, caller-owned. */
+typedef struct fdh_batch {
+  const int32_t* tokens;  /* int32 [B, S] input tokens */
+  const int32_t* labels;  /* int32 [B, S] aligned with the tokens: the logits at position t
+                           * are scored against labels[t + 1]; -100 drops that target
+                           * (padding, masked prompt).  NULL: the next token is the target. */
+  int32_t B, S;
+} fdh_batch;
+
 typedef struct fdh_block {
   char name[48];        /* e.g. "h3.wqkv" */
   int64_t offset;       /* element offset in the flat vector */
@@ -143,10 +158,37 @@ fdh_status fdh_hvp(fdh_ctx* ctx, const void* params_dev, const float* v_dev, dou
 /* Loss values L(theta + eps v), L(theta - eps v) of the most recent fdh_hvp. */
 fdh_status fdh_last_losses(fdh_ctx* ctx, double* loss_plus, double* loss_minus);
 
-/* Fix the operator used by fdh_lanczos / fdh_slq_density. The pointers are
- * kept (not copied) and must stay valid. */
+/* Fix the operator used by fdh_hvp_bound / fdh_lanczos / fdh_slq_density /
+ * fdh_cg_solve / fdh_block_diagonal: one batch of next-token targets (the same
+ * as fdh_bind_dataset with one unlabelled batch and FDH_REDUCE_MEAN).  The
+ * pointers are kept (not copied) and must stay valid. */
 fdh_status fdh_bind(fdh_ctx* ctx, const void* params_dev, const int32_t* tokens_dev,
                     int32_t B, int32_t S, double eps);
+
+/* Fix a dataset operator for fdh_hvp_bound / fdh_lanczos / fdh_slq_density /
+ * fdh_cg_solve / fdh_block_diagonal (Algorithm 1 with its dataloader loop,
+ * section 3.1): the FD-HVP of the loss over all nbatch batches, each batch
+ * weighted by its number of kept targets w_b, so that with FDH_REDUCE_MEAN
+ * the result is the HVP of the token-weighted mean loss
+ * sum_b w_b L_b / sum_b w_b (L_b the mean over batch b's targets), and with
+ * FDH_REDUCE_SUM that of the summed loss.  Batches may differ in B and S,
+ * each within the workspace plan (and S a multiple of 128 where the plan uses
+ * fused attention).  Padding is taken to sit after the real tokens (right
+ * padding) with label -100: causal attention then keeps it out of every kept
+ * target's context, so no attention mask is needed.  The batch array is
+ * copied, the device pointers are kept (not copied) and must stay valid.
+ * *n_targets (may be NULL) receives sum_b w_b.  Labelled batches are scanned
+ * on the device and the call waits for the stream; FDH_ERR_INVALID_ARG for a
+ * label outside [0, vocab) other than -100, or when no target is left.
+ * QUAD_DIAG contexts take nbatch = 0. */
+fdh_status fdh_bind_dataset(fdh_ctx* ctx, const void* params_dev, const fdh_batch* batches, int32_t nbatch,
+                            double eps, int32_t reduction, int64_t* n_targets);
+
+/* hv = H v of the bound operator (fdh_bind or fdh_bind_dataset): one FD-HVP
+ * per batch, accumulated into hv in batch order; fdh_last_losses then returns
+ * the dataset losses at theta +- eps v.  v, hv: float32 [P] on device, not
+ * aliasing each other or the parameters.  Enqueued on the context stream. */
+fdh_status fdh_hvp_bound(fdh_ctx* ctx, const float* v_dev, float* hv_dev);
 
 /* m Lanczos steps (section 4) from the Rademacher probe z/sqrt(P) drawn from
  * probe_seed.  alpha_host[m], beta_host[m] receive alpha_1..alpha_s and
@@ -172,7 +214,7 @@ fdh_status fdh_block_stats(fdh_ctx* ctx, const float* a_dev, const float* b_dev,
  * stats_host[4b + 0] = ||h^(b) - h_b^(b)||, [4b + 1] = that over ||h^(b)||,
  * [4b + 2] = cosine of h^(b) and h_b^(b), [4b + 3] = ||h^(b)||, all restricted
  * to the parameters of layer b.  Runs L + 1 FD-HVPs; v: float32 [P] on device.
- * Needs fdh_bind and a workspace planned with m >= 1 (its Lanczos vectors are
+ * Needs a bound operator and a workspace planned with m >= 1 (its Lanczos vectors are
  * used as scratch).  Waits for the stream. */
 fdh_status fdh_block_diagonal(fdh_ctx* ctx, const float* v_dev, double* stats_host);
 
@@ -186,7 +228,7 @@ fdh_status fdh_block_diagonal(fdh_ctx* ctx, const float* v_dev, double* stats_ho
  * direction of non-positive curvature ((p, (H + lambda I) p) <= 0) stops it:
  * raise lambda.  Each step is one FD-HVP plus three vector passes; fp32
  * vectors, fp64 scalars with deterministic reductions; two scalars are read
- * back per step (the call waits for the stream).  Needs fdh_bind and a
+ * back per step (the call waits for the stream).  Needs a bound operator and a
  * workspace planned with m >= 1 (its Lanczos vectors hold r, p and A p). */
 fdh_status fdh_cg_solve(fdh_ctx* ctx, const float* b_dev, double lambda, int32_t max_iters, double rel_tol,
                         float* x_dev, double* res_host, int32_t* steps_done);

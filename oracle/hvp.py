@@ -26,37 +26,41 @@ def fd_hvp(grad_fn, theta: np.ndarray, v: np.ndarray, eps: float) -> np.ndarray:
     return (gp - gm) / (2.0 * eps)
 
 
-def lm_grad_fn(cfg: M.ModelConfig, tokens: np.ndarray):
+def lm_grad_fn(cfg: M.ModelConfig, tokens: np.ndarray, labels=None):
     def g(th):
-        return M.loss_and_grad(cfg, th, tokens)[1]
+        return M.loss_and_grad(cfg, th, tokens, labels=labels)[1]
     return g
 
 
-def lm_hvp(cfg: M.ModelConfig, theta, v, eps: float, tokens) -> np.ndarray:
+def lm_hvp(cfg: M.ModelConfig, theta, v, eps: float, tokens, labels=None) -> np.ndarray:
     """FD-HVP of the mean next-token loss on one batch (Algorithm 1, one batch)."""
-    return fd_hvp(lm_grad_fn(cfg, tokens), theta, v, eps)
+    return fd_hvp(lm_grad_fn(cfg, tokens, labels), theta, v, eps)
 
 
 def lm_hvp_dataset(cfg: M.ModelConfig, theta, v, eps: float, batches) -> np.ndarray:
-    """Algorithm 1 over several batches with token weights w_b = B_b (S_b - 1).
+    """Algorithm 1 over several batches with token weights w_b = the number of
+    targets of batch b.
 
-    Each batch loss is a mean over its own targets, so w_b times its gradient is
-    the gradient of the summed loss; dividing by 2 eps sum_b w_b gives the HVP of
-    the token-weighted mean loss over all batches.
+    ``batches`` holds token arrays [B_b, S_b] or (tokens, labels) pairs (labels
+    as in model.loss_and_grad).  Each batch loss is a mean over its own targets,
+    so w_b times its gradient is the gradient of the summed loss; dividing by
+    2 eps sum_b w_b gives the HVP of the token-weighted mean loss over all
+    batches.
     """
     theta = np.asarray(theta, dtype=np.float64)
     v = np.asarray(v, dtype=np.float64)
+    items = [b if isinstance(b, tuple) else (b, None) for b in batches]
     acc = np.zeros_like(theta)
     wsum = 0.0
     tp = theta + eps * v
-    for tok in batches:
-        w = tok.shape[0] * (tok.shape[1] - 1)
-        acc += w * M.loss_and_grad(cfg, tp, tok)[1]
+    for tok, lab in items:
+        w = M.num_targets(tok, lab)
+        acc += w * M.loss_and_grad(cfg, tp, tok, labels=lab)[1]
         wsum += w
     tm = theta - eps * v
-    for tok in batches:
-        w = tok.shape[0] * (tok.shape[1] - 1)
-        acc -= w * M.loss_and_grad(cfg, tm, tok)[1]
+    for tok, lab in items:
+        w = M.num_targets(tok, lab)
+        acc -= w * M.loss_and_grad(cfg, tm, tok, labels=lab)[1]
     return acc / (2.0 * eps * wsum)
 
 

@@ -18,7 +18,7 @@ Llama family   token embedding; blocks
 
 LayerNorm eps and RMSNorm eps are taken from the config (1e-5), LayerNorm
 variance is the biased one.  The loss is the mean over the B*(S-1) next-token
-targets.  Everything is float64 numpy; the reverse pass is written by hand.
+targets, or over those whose label is not -100 when labels are given.  Everything is float64 numpy; the reverse pass is written by hand.
 
 Flat parameter layout (one vector, per-layer blocks contiguous, which is the
 layer partition of the block-diagonal test in section 6):
@@ -241,12 +241,21 @@ def _attention_bwd(cfg, do, cache):
     return dq, dk, dv
 
 
+IGNORE = -100   # label of positions that carry no target (padding, prompt)
+
+
 def loss_and_grad(cfg: ModelConfig, theta: np.ndarray, tokens: np.ndarray,
-                  want_grad: bool = True):
+                  want_grad: bool = True, labels=None):
     """Mean next-token cross-entropy L(theta) and its gradient (float64).
 
     ``theta`` is the flat parameter vector (any float dtype; used in float64),
-    ``tokens`` int [B, S].  Returns (L, grad) with grad float64 of length P.
+    ``tokens`` int [B, S].  The logits at position t predict the label at
+    position t + 1: without ``labels`` that is tokens[:, t + 1]; with
+    ``labels`` (int [B, S], aligned with the tokens as in section 7.1, where
+    padding positions carry the label -100) it is labels[:, t + 1], and
+    positions whose label is -100 are left out of the mean.  The mean is over
+    the remaining targets (zero loss and gradient when there are none).
+    Returns (L, grad) with grad float64 of length P.
     """
     theta = np.asarray(theta, dtype=np.float64)
     W = unflatten(cfg, theta)
@@ -313,14 +322,16 @@ def loss_and_grad(cfg: ModelConfig, theta: np.ndarray, tokens: np.ndarray,
         wh = W["head"]
     logits = f @ wh.T                       # [B, S, V]
     zl = logits[:, :-1, :]
-    tgt = tok[:, 1:]
+    raw = tok[:, 1:] if labels is None else np.asarray(labels, dtype=np.int64)[:, 1:]
+    valid = raw != IGNORE
+    tgt = np.where(valid, raw, 0)
     zmax = zl.max(-1, keepdims=True)
     ez = np.exp(zl - zmax)
     sez = ez.sum(-1, keepdims=True)
     lse = np.log(sez) + zmax
-    N = B * (S - 1)
+    N = int(valid.sum())
     picked = np.take_along_axis(zl, tgt[..., None], axis=-1)
-    loss = float((lse - picked).sum() / N)
+    loss = float(((lse - picked)[..., 0] * valid).sum() / N) if N else 0.0
     if not want_grad:
         return loss, None
 
@@ -328,7 +339,8 @@ def loss_and_grad(cfg: ModelConfig, theta: np.ndarray, tokens: np.ndarray,
     g = {e.name: np.zeros(e.shape) for e in layout(cfg)}
     dz = ez / sez
     np.put_along_axis(dz, tgt[..., None], np.take_along_axis(dz, tgt[..., None], -1) - 1.0, -1)
-    dz /= N
+    dz *= valid[..., None]
+    dz /= max(N, 1)
     dlogits = np.zeros_like(logits)
     dlogits[:, :-1, :] = dz
     dl2 = dlogits.reshape(-1, cfg.vocab)
@@ -408,5 +420,13 @@ def loss_and_grad(cfg: ModelConfig, theta: np.ndarray, tokens: np.ndarray,
     return loss, grad
 
 
-def loss(cfg: ModelConfig, theta, tokens) -> float:
-    return loss_and_grad(cfg, theta, tokens, want_grad=False)[0]
+def loss(cfg: ModelConfig, theta, tokens, labels=None) -> float:
+    return loss_and_grad(cfg, theta, tokens, want_grad=False, labels=labels)[0]
+
+
+def num_targets(tokens, labels=None) -> int:
+    """Number of targets the mean loss is taken over."""
+    tok = np.asarray(tokens)
+    if labels is None:
+        return tok.shape[0] * (tok.shape[1] - 1)
+    return int((np.asarray(labels)[:, 1:] != IGNORE).sum())

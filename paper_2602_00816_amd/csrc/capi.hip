@@ -153,17 +153,32 @@ fdh_status fdh_last_losses(fdh_ctx* ctx, double* loss_plus, double* loss_minus) 
 
 fdh_status fdh_bind(fdh_ctx* ctx, const void* params_dev, const int32_t* tokens_dev, int32_t B, int32_t S, double eps) {
   return run(ctx, [&](fdh::Engine& e) -> int {
-    if (!params_dev || (!e.quad && !tokens_dev)) { e.err = "null pointer"; return FDH_ERR_INVALID_ARG; }
-    if (!(eps > 0.0) || !(eps < 1e300)) { e.err = "eps must be positive and finite"; return FDH_ERR_INVALID_ARG; }
-    if (!e.quad && (B < 1 || S < 2)) { e.err = "need B >= 1 and S >= 2"; return FDH_ERR_INVALID_ARG; }
-    e.b_params = params_dev;
-    e.b_tokens = tokens_dev;
-    e.b_B = B;
-    e.b_S = S;
-    e.b_eps = eps;
-    e.bound = true;
-    return FDH_OK;
+    if (e.quad) return e.bind_batches(params_dev, nullptr, 0, eps, FDH_REDUCE_MEAN, nullptr);
+    fdh::BatchRef b;
+    b.tok = tokens_dev;
+    b.B = B;
+    b.S = S;
+    return e.bind_batches(params_dev, &b, 1, eps, FDH_REDUCE_MEAN, nullptr);
   });
+}
+
+fdh_status fdh_bind_dataset(fdh_ctx* ctx, const void* params_dev, const fdh_batch* batches, int32_t nbatch, double eps,
+                            int32_t reduction, int64_t* n_targets) {
+  return run(ctx, [&](fdh::Engine& e) -> int {
+    if (nbatch < 0 || (nbatch > 0 && !batches)) { e.err = "bad batch list"; return FDH_ERR_INVALID_ARG; }
+    std::vector<fdh::BatchRef> bt((size_t)nbatch);
+    for (int i = 0; i < nbatch; ++i) {
+      bt[i].tok = batches[i].tokens;
+      bt[i].lab = batches[i].labels;
+      bt[i].B = batches[i].B;
+      bt[i].S = batches[i].S;
+    }
+    return e.bind_batches(params_dev, bt.data(), nbatch, eps, reduction, n_targets);
+  });
+}
+
+fdh_status fdh_hvp_bound(fdh_ctx* ctx, const float* v_dev, float* hv_dev) {
+  return run(ctx, [&](fdh::Engine& e) { return e.hvp_bound(v_dev, hv_dev); });
 }
 
 fdh_status fdh_lanczos(fdh_ctx* ctx, int32_t m, uint64_t probe_seed, const fdh_lanczos_opts* o, double* alpha_host,

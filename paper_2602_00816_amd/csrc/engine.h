@@ -25,6 +25,12 @@ struct Entry {
   int layer, kind;
 };
 
+struct BatchRef {  // one token batch of a bound dataset (device pointers, caller-owned)
+  const int32_t* tok = nullptr;
+  const int32_t* lab = nullptr;  // nullptr: next-token targets
+  int B = 0, S = 0;
+};
+
 struct Span {  // carve of the workspace
   size_t off = 0, bytes = 0;
 };
@@ -76,17 +82,22 @@ class Engine {
   fdh_lanczos_opts planO{};
   size_t plan(int B, int S, int m, const fdh_lanczos_opts* o, bool carve);
 
-  // operator binding for Lanczos
+  // operator binding for Lanczos / CG / the block-diagonal test: parameters,
+  // step and the batches whose token-weighted average the operator is
+  std::vector<BatchRef> b_data;
   const void* b_params = nullptr;
-  const int32_t* b_tokens = nullptr;
-  int b_B = 0, b_S = 0;
   double b_eps = 0.0;
+  double b_inv_n = 0.0;   // scale of every kept cross-entropy row (1 / targets, or 1 for a sum)
+  int64_t b_targets = 0;
   bool bound = false;
   const float* quad_diag = nullptr;
   Timing timing;
 
   // entry points (return fdh_status)
   int hvp(const void* params, const float* v, double eps, const int32_t* tok, int B, int S, float* hv);
+  int hvp_batches(const void* params, const float* v, double eps, const BatchRef* bt, int nb, double inv_n, float* hv);
+  int bind_batches(const void* params, const BatchRef* bt, int nb, double eps, int reduction, int64_t* targets);
+  int hvp_bound(const float* v, float* hv);
   int last_losses(double* lp, double* lm);
   int lanczos(int m, uint64_t seed, const fdh_lanczos_opts& o, double* alpha, double* beta, int* steps);
   int slq(int probes, int m, uint64_t seed, const fdh_lanczos_opts& o, double* nodes, double* weights, int* steps,
@@ -100,7 +111,10 @@ class Engine {
   std::vector<int64_t> layer_ranges() const;
 
  private:
-  template <typename T> int hvp_t(const T* th, const float* v, double eps, const int32_t* tok, int B, int S, float* hv);
+  int check_batch(const int32_t* tok, int B, int S);
+  template <typename T>
+  int hvp_t(const T* th, const float* v, double eps, const int32_t* tok, const int32_t* lab, int B, int S, double inv_n,
+            bool acc, float* hv);
   template <typename B> int lanczos_t(int m, uint64_t seed, const fdh_lanczos_opts& o, double* alpha, double* beta, int* steps);
   template <typename T> void* wsp(const Span& s) const { return (void*)(ws + s.off); }
 
@@ -112,6 +126,7 @@ class Engine {
   Span xL_m, xL_d, f_m, f_d, lo, qkvf_m, qkvf_d, sc_m, sc_d, log_m, log_d, dlog_m, dlog_d, rowloss, losses;
   Span dx0_m, dx0_d, dx1_m, dx1_d, dxo_m, dxo_d, dz_m, dz_d, dgu_m, dgu_d, dudf, db_m, db_d, gpart, do_m, do_d, dS_m, dS_d;
   Span dqkv_m, dqkv_d, dqkvo_m, dqkvo_d, gqa_m, gqa_d, dl, da_m, da_d, colpart, keys, rope, cdf, gpartial, bpart, bout;
+  Span tcount;  // two int64 counters of fdh_bind_dataset
   Span wsplit;  // split-K partial products of the weight-gradient GEMMs
   Span lz_w, lz_q, lz_qp, lz_basis, lz_alpha, lz_beta, lz_coef, lz_gram, lz_partial, lz_flag, lz_maxabs;
   int64_t lz_ldq = 0;  // basis row stride (elements, multiple of 8)

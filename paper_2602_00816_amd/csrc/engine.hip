@@ -177,6 +177,7 @@ size_t Engine::plan(int B, int S, int m, const fdh_lanczos_opts* o, bool carve) 
     take(dlog_m, T_ * V * ob); take(dlog_d, T_ * V * ob);
     take(rowloss, 2 * T_ * 8);
     take(losses, 2 * 8);
+    take(tcount, 2 * 8);
     take(dx0_m, td * 4); take(dx0_d, td * 4);
     take(dx1_m, td * 4); take(dx1_d, td * 4);
     take(dxo_m, td * ob); take(dxo_d, td * ob);
@@ -339,8 +340,12 @@ static int run_gemm(Engine& e, GemmArgs& g) {
 // ---------------------------------------------------------------------------
 // lockstep FD-HVP
 // ---------------------------------------------------------------------------
+// One batch of the FD-HVP.  The cross-entropy rows are scaled by inv_n; with
+// acc the batch's Hv is added to hv (and its losses to the loss pair), which
+// is how several batches form the token-weighted dataset average (Algorithm 1).
 template <typename T>
-int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, int B, int S, float* hv) {
+int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, const int32_t* lab, int B, int S,
+                  double inv_n, bool acc, float* hv) {
   hipStream_t st = stream;
   const int T_ = B * S;
   const float feps = (float)eps;
@@ -365,8 +370,9 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, i
   const int64_t pp_stride = (int64_t)S * S;  // per (b,h) matrix
 
   // perturbation operand: lo = eps * v in the operand type (unless the
-  // Lanczos normalisation already wrote it for this v and eps)
-  const bool lo_ready = lo_for_v == v && lo_for_eps == eps;
+  // Lanczos normalisation already wrote it for this v and eps, or an earlier
+  // batch of the same product did)
+  const bool lo_ready = acc || (lo_for_v == v && lo_for_eps == eps);
   lo_for_v = nullptr;
   if (!lo_ready) CK(launch_scale_cast<T>(lo, v, eps, P, st));
   if (llama) CK(launch_rope_table((double*)(ws + rope.off), S, dh, (double)cfg.rope_base, st));
@@ -419,6 +425,7 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, i
     g.C = hv + W.off; g.ldc = K; g.alpha = inv_eps;
     const int ns = wgrad_splits(N, K, T_);
     if (ns == 1 || force_unsplit || wsplit.bytes < (size_t)ns * N * K * 4) {
+      if (acc) g.beta = 1.f;
       RG(T, g);
       return FDH_OK;
     }
@@ -433,12 +440,12 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, i
     RG(T, g);
     int e0 = 0;
     if (timing.on) CK(timing.begin(st, &e0));
-    CK(launch_sum_splits(hv + W.off, F32(wsplit), ns, (int64_t)N * K, st));
+    CK(launch_sum_splits(hv + W.off, F32(wsplit), ns, (int64_t)N * K, acc, st));
     if (timing.on) CK(timing.end(st, 0, e0, 0.0, 0.0));
     return FDH_OK;
   };
   auto colsum_hv = [&](const float* X, int C, int64_t ld, const ParamRef& R) -> int {
-    CK(launch_colsum(hv + R.off, X, T_, C, ld, 1.0 / eps, false, (double*)(ws + colpart.off), st));
+    CK(launch_colsum(hv + R.off, X, T_, C, ld, 1.0 / eps, acc, (double*)(ws + colpart.off), st));
     return FDH_OK;
   };
   bool op_ready = false;  // dxo holds the operand-type copy of the last norm backward's output
@@ -454,8 +461,8 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, i
                           gp, bp, st));
     op_ready = bf16;
     double* cp = (double*)(ws + colpart.off);
-    CK(launch_colsum_f64(hv + gain.off, gp, nwg, d, 1.0 / eps, false, cp, st));
-    if (ln) CK(launch_colsum_f64(hv + bias.off, bp, nwg, d, 1.0 / eps, false, cp, st));
+    CK(launch_colsum_f64(hv + gain.off, gp, nwg, d, 1.0 / eps, acc, cp, st));
+    if (ln) CK(launch_colsum_f64(hv + bias.off, bp, nwg, d, 1.0 / eps, acc, cp, st));
     return FDH_OK;
   };
   // fp32 pair -> operand pair (aliases in fp32 mode; skipped when the norm
@@ -576,10 +583,9 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, i
   CK(launch_norm_fwd<T>(PairT<T>{OP(f_m), OP(f_d)}, F32(xL_m), F32(xL_d), T_, d, ln, th + nfg.off, v + nfg.off,
                         ln ? th + nfb.off : nullptr, ln ? v + nfb.off : nullptr, eps, neps, st));
   RC(lin_fwd(OP(f_m), OP(f_d), d, head, ParamRef{}, F32(log_m), F32(log_d), nullptr, nullptr, V));
-  const double inv_n = 1.0 / ((double)B * (S - 1));
-  CK(launch_ce<T>(PairT<T>{OP(dlog_m), OP(dlog_d)}, (double*)(ws + rowloss.off), F32(log_m), F32(log_d), tok, T_, S, V,
-                  inv_n, st));
-  CK(launch_loss_sum((double*)(ws + losses.off), (const double*)(ws + rowloss.off), T_, st));
+  CK(launch_ce<T>(PairT<T>{OP(dlog_m), OP(dlog_d)}, (double*)(ws + rowloss.off), F32(log_m), F32(log_d), tok, lab, T_,
+                  S, V, inv_n, st));
+  CK(launch_loss_sum((double*)(ws + losses.off), (const double*)(ws + rowloss.off), T_, acc, st));
 
   // ================= backward =================
   // head
@@ -752,15 +758,28 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, i
   }
   // embeddings (difference channel of the gradient w.r.t. the embedding output)
   CK(launch_token_sort((uint32_t*)(ws + keys.off), tok, T_, V, st));
-  if (!gpt2) CK(launch_fill_f32(hv + wte.off, (int64_t)V * d, 0.f, st));
-  CK(launch_embed_bwd(hv + wte.off, (const uint32_t*)(ws + keys.off), dxd, T_, d, 1.0 / eps, gpt2, st));
+  // (GPT-2 ties the embedding to the head, whose gradient is already in hv)
+  if (!gpt2 && !acc) CK(launch_fill_f32(hv + wte.off, (int64_t)V * d, 0.f, st));
+  CK(launch_embed_bwd(hv + wte.off, (const uint32_t*)(ws + keys.off), dxd, T_, d, 1.0 / eps, gpt2 || acc, st));
   if (gpt2) {
-    CK(launch_pos_bwd(hv + wpe.off, dxd, B, S, d, 1.0 / eps, st));
-    if (Smax > S) CK(launch_fill_f32(hv + wpe.off + (int64_t)S * d, (int64_t)(Smax - S) * d, 0.f, st));
+    CK(launch_pos_bwd(hv + wpe.off, dxd, B, S, d, 1.0 / eps, acc, st));
+    if (Smax > S && !acc) CK(launch_fill_f32(hv + wpe.off + (int64_t)S * d, (int64_t)(Smax - S) * d, 0.f, st));
   }
   (void)dxm;
   return FDH_OK;
 #undef RC
+}
+
+int Engine::check_batch(const int32_t* tok, int B, int S) {
+  if (!tok) { err = "null tokens"; return FDH_ERR_INVALID_ARG; }
+  if (B < 1 || S < 2) { err = "need B >= 1 and S >= 2"; return FDH_ERR_INVALID_ARG; }
+  if (!ws) { err = "no workspace"; return FDH_ERR_WORKSPACE; }
+  if (B > planB || S > planS || S > Smax) { err = "batch larger than the workspace plan (or S > max_seq)"; return FDH_ERR_WORKSPACE; }
+  if ((int64_t)B * S > 16384) { err = "B*S must be <= 16384"; return FDH_ERR_UNSUPPORTED; }
+  if (S > 4096) { err = "S must be <= 4096"; return FDH_ERR_UNSUPPORTED; }
+  if (S % 8 || dh % 8) { err = "S and head_dim must be multiples of 8"; return FDH_ERR_UNSUPPORTED; }
+  if (fused && S % 128) { err = "this workspace uses fused attention: S must be a multiple of 128"; return FDH_ERR_UNSUPPORTED; }
+  return FDH_OK;
 }
 
 int Engine::hvp(const void* params, const float* v, double eps, const int32_t* tok, int B, int S, float* hv) {
@@ -773,16 +792,82 @@ int Engine::hvp(const void* params, const float* v, double eps, const int32_t* t
     else CK(launch_quad_diag_hvp<float>((const float*)params, quad_diag, v, eps, hv, P, stream));
     return FDH_OK;
   }
-  if (!tok) { err = "null tokens"; return FDH_ERR_INVALID_ARG; }
-  if (B < 1 || S < 2) { err = "need B >= 1 and S >= 2"; return FDH_ERR_INVALID_ARG; }
-  if (!ws) { err = "no workspace"; return FDH_ERR_WORKSPACE; }
-  if (B > planB || S > planS || S > Smax) { err = "batch larger than the workspace plan (or S > max_seq)"; return FDH_ERR_WORKSPACE; }
-  if ((int64_t)B * S > 16384) { err = "B*S must be <= 16384"; return FDH_ERR_UNSUPPORTED; }
-  if (S > 4096) { err = "S must be <= 4096"; return FDH_ERR_UNSUPPORTED; }
-  if (S % 8 || dh % 8) { err = "S and head_dim must be multiples of 8"; return FDH_ERR_UNSUPPORTED; }
-  if (fused && S % 128) { err = "this workspace uses fused attention: S must be a multiple of 128"; return FDH_ERR_UNSUPPORTED; }
-  if (bf16) return hvp_t<bf16_t>((const bf16_t*)params, v, eps, tok, B, S, hv);
-  return hvp_t<float>((const float*)params, v, eps, tok, B, S, hv);
+  const int rc = check_batch(tok, B, S);
+  if (rc != FDH_OK) return rc;
+  const double inv_n = 1.0 / ((double)B * (S - 1));
+  if (bf16) return hvp_t<bf16_t>((const bf16_t*)params, v, eps, tok, nullptr, B, S, inv_n, false, hv);
+  return hvp_t<float>((const float*)params, v, eps, tok, nullptr, B, S, inv_n, false, hv);
+}
+
+int Engine::hvp_batches(const void* params, const float* v, double eps, const BatchRef* bt, int nb, double inv_n,
+                        float* hv) {
+  if (!params || !v || !hv || !bt) { err = "null pointer"; return FDH_ERR_INVALID_ARG; }
+  if (nb < 1) { err = "need at least one batch"; return FDH_ERR_INVALID_ARG; }
+  if ((const void*)hv == params || (const void*)hv == (const void*)v) { err = "hv aliases an input"; return FDH_ERR_INVALID_ARG; }
+  for (int i = 0; i < nb; ++i) {
+    const int rc = check_batch(bt[i].tok, bt[i].B, bt[i].S);
+    if (rc != FDH_OK) return rc;
+  }
+  for (int i = 0; i < nb; ++i) {
+    const BatchRef& b = bt[i];
+    const int rc = bf16 ? hvp_t<bf16_t>((const bf16_t*)params, v, eps, b.tok, b.lab, b.B, b.S, inv_n, i > 0, hv)
+                        : hvp_t<float>((const float*)params, v, eps, b.tok, b.lab, b.B, b.S, inv_n, i > 0, hv);
+    if (rc != FDH_OK) return rc;
+  }
+  return FDH_OK;
+}
+
+int Engine::bind_batches(const void* params, const BatchRef* bt, int nb, double eps, int reduction, int64_t* targets) {
+  if (!params) { err = "null pointer"; return FDH_ERR_INVALID_ARG; }
+  if (!(eps > 0.0) || !std::isfinite(eps)) { err = "eps must be positive and finite"; return FDH_ERR_INVALID_ARG; }
+  if (reduction != FDH_REDUCE_MEAN && reduction != FDH_REDUCE_SUM) { err = "unknown reduction"; return FDH_ERR_INVALID_ARG; }
+  if (quad) {
+    if (nb != 0) { err = "QUAD_DIAG takes no batches"; return FDH_ERR_INVALID_ARG; }
+    b_params = params;
+    b_data.clear();
+    b_eps = eps;
+    b_inv_n = 1.0;
+    b_targets = 0;
+    bound = true;
+    return FDH_OK;
+  }
+  if (nb < 1 || !bt) { err = "need at least one batch"; return FDH_ERR_INVALID_ARG; }
+  int64_t cnt[2] = {0, 0};
+  bool any_labels = false;
+  for (int i = 0; i < nb; ++i) {
+    const int rc = check_batch(bt[i].tok, bt[i].B, bt[i].S);
+    if (rc != FDH_OK) return rc;
+    if (bt[i].lab) any_labels = true;
+    else cnt[0] += (int64_t)bt[i].B * (bt[i].S - 1);
+  }
+  if (any_labels) {
+    // count the kept targets and the invalid labels on the device (one small
+    // launch per labelled batch), then wait for the two integers
+    int64_t* dc = (int64_t*)(ws + tcount.off);
+    CK(launch_fill_f64((double*)dc, 2, 0.0, stream));
+    for (int i = 0; i < nb; ++i)
+      if (bt[i].lab) CK(launch_count_targets(dc, bt[i].lab, bt[i].B, bt[i].S, V, stream));
+    int64_t h[2];
+    CK(hipMemcpyAsync(h, dc, sizeof h, hipMemcpyDeviceToHost, stream));
+    CK(hipStreamSynchronize(stream));
+    if (h[1] != 0) { err = "labels must be in [0, vocab) or -100"; return FDH_ERR_INVALID_ARG; }
+    cnt[0] += h[0];
+  }
+  if (cnt[0] == 0) { err = "the batches hold no targets (every label is -100)"; return FDH_ERR_INVALID_ARG; }
+  b_params = params;
+  b_data.assign(bt, bt + nb);
+  b_eps = eps;
+  b_targets = cnt[0];
+  b_inv_n = reduction == FDH_REDUCE_MEAN ? 1.0 / (double)cnt[0] : 1.0;
+  bound = true;
+  if (targets) *targets = cnt[0];
+  return FDH_OK;
+}
+
+int Engine::hvp_bound(const float* v, float* hv) {
+  if (!bound) { err = "call fdh_bind first"; return FDH_ERR_STATE; }
+  if (quad) return hvp(b_params, v, b_eps, nullptr, 0, 0, hv);
+  return hvp_batches(b_params, v, b_eps, b_data.data(), (int)b_data.size(), b_inv_n, hv);
 }
 
 int Engine::last_losses(double* lp, double* lm) {
@@ -841,7 +926,7 @@ int Engine::lanczos_t(int m, uint64_t seed, const fdh_lanczos_opts& o, double* a
     if (rc_ != FDH_OK) return rc_;                             \
   } while (0)
   for (int k = 0; k < m; ++k) {
-    int rc = hvp(b_params, q, b_eps, b_tokens, b_B, b_S, w);
+    int rc = hvp_bound(q, w);
     if (rc != FDH_OK) return rc;
     TV(16.0 * Pd, launch_lanczos_alpha(w, q, qp, D, k, P, st));
     const int nv = std::min(k + 1, cap);
@@ -1094,7 +1179,7 @@ int Engine::cg_solve(const float* b, double lam, int max_iters, double rel_tol, 
   res[0] = bnorm;
   if (!std::isfinite(bnorm)) { err = "non-finite right-hand side"; return FDH_ERR_NONFINITE; }
   for (int k = 0; k < max_iters; ++k) {
-    rc = hvp(b_params, p, b_eps, b_tokens, b_B, b_S, ap);
+    rc = hvp_bound(p, ap);
     if (rc != FDH_OK) return rc;
     TC(12.0 * Pd, launch_cg_ap(ap, p, lam, sc, part, P, st));
     double pap = 0.0;
@@ -1132,13 +1217,13 @@ int Engine::block_diagonal(const float* v, double* out) {
   float* h = (float*)(ws + lz_w.off);
   float* vb = (float*)(ws + lz_q.off);
   float* hb = (float*)(ws + lz_qp.off);
-  int rc = hvp(b_params, v, b_eps, b_tokens, b_B, b_S, h);
+  int rc = hvp_bound(v, h);
   if (rc != FDH_OK) return rc;
   std::vector<int64_t> ranges = layer_ranges();
   std::vector<double> s4(4);
   for (int l = 0; l < L; ++l) {
     CK(launch_mask_range(vb, v, ranges[2 * l], ranges[2 * l + 1], P, stream));
-    rc = hvp(b_params, vb, b_eps, b_tokens, b_B, b_S, hb);
+    rc = hvp_bound(vb, hb);
     if (rc != FDH_OK) return rc;
     CK(launch_block_stats(h, hb, &ranges[2 * l], 1, (double*)(ws + bpart.off), (double*)(ws + bout.off), stream));
     CK(hipMemcpyAsync(s4.data(), ws + bout.off, 32, hipMemcpyDeviceToHost, stream));

@@ -24,8 +24,9 @@ constexpr int RED_BLOCKS = 1024;   // fixed grid of the deterministic reductions
 hipError_t launch_fill_f32(float* p, int64_t n, float v, hipStream_t s);
 hipError_t launch_copy16(void* dst, const void* src, size_t bytes, hipStream_t s);
 hipError_t launch_fill_f64(double* p, int64_t n, double v, hipStream_t s);
-// out[i] = sum_{j < ns} part[j * n + i], summed in fp64 in the order j = 0, 1, ...
-hipError_t launch_sum_splits(float* out, const float* part, int ns, int64_t n, hipStream_t s);
+// out[i] = sum_{j < ns} part[j * n + i] (acc: out[i] += that sum), summed in fp64
+// in the order j = 0, 1, ...
+hipError_t launch_sum_splits(float* out, const float* part, int ns, int64_t n, bool acc, hipStream_t s);
 // lo[i] = T(eps * v[i])
 template <typename T>
 hipError_t launch_scale_cast(T* lo, const float* v, double eps, int64_t n, hipStream_t s);
@@ -184,16 +185,23 @@ template <typename T>
 hipError_t launch_swiglu_bwd(PairT<T> dgu, const float* gum, const float* gud, const float* dzm, const float* dzd,
                              int rows, int F, hipStream_t s);
 
-// cross-entropy at both points: dlogits (operand type) and per-row losses (fp64, [2][T])
+// cross-entropy at both points: dlogits (operand type) and per-row losses (fp64, [2][T]),
+// every kept row scaled by inv_n; targets from lab (int32 [B, S], IGNORE_LABEL
+// drops a target) or, with lab == nullptr, the next token
+constexpr int IGNORE_LABEL = -100;
 template <typename T>
 hipError_t launch_ce(PairT<T> dl, double* rowloss, const float* lm, const float* ld, const int32_t* tok,
-                     int T_, int S, int V, double inv_n, hipStream_t s);
-hipError_t launch_loss_sum(double* out2, const double* rowloss, int T_, hipStream_t s);
+                     const int32_t* lab, int T_, int S, int V, double inv_n, hipStream_t s);
+// out2 = (or += with acc) the sums of the two rows of rowloss
+hipError_t launch_loss_sum(double* out2, const double* rowloss, int T_, bool acc, hipStream_t s);
+// out2[0] += targets of a [B, S] batch, out2[1] += labels outside [0, V) other than IGNORE_LABEL
+hipError_t launch_count_targets(int64_t* out2, const int32_t* lab, int B, int S, int V, hipStream_t s);
 
 // embedding backward (difference channel only): deterministic sort + segment sums
 hipError_t launch_token_sort(uint32_t* keys, const int32_t* tok, int T_, int V, hipStream_t s);
 hipError_t launch_embed_bwd(float* hv_e, const uint32_t* keys, const float* dxd, int T_, int dmodel, double inv_eps,
                             bool accumulate, hipStream_t s);
-hipError_t launch_pos_bwd(float* hv_p, const float* dxd, int B, int S, int dmodel, double inv_eps, hipStream_t s);
+hipError_t launch_pos_bwd(float* hv_p, const float* dxd, int B, int S, int dmodel, double inv_eps, bool accumulate,
+                          hipStream_t s);
 
 }  // namespace fdh

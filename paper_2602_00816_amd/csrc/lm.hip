@@ -800,19 +800,24 @@ __global__ void swiglu_bwd_kernel(PairT<T> dgu, const float* gum, const float* g
 }
 
 // ---- cross-entropy, both points -------------------------------------------------------------
+// The logits of position t predict the label of position t + 1: the next token,
+// or lab[t + 1] when labels are given; a label of IGNORE_LABEL (padding,
+// masked prompt) leaves the row out.  inv_n scales every kept row.
 template <typename T>
 __global__ __launch_bounds__(NT) void ce_kernel(PairT<T> dl, double* rowloss, const float* lm, const float* ld,
-                                                const int32_t* tok, int T_, int S, int V, double inv_n) {
+                                                const int32_t* tok, const int32_t* lab, int T_, int S, int V,
+                                                double inv_n) {
   __shared__ double sh[NT / 64];
   const int64_t t = blockIdx.x;
   const int64_t o = t * (int64_t)V;
-  const bool has_target = (t % S) != (S - 1);
-  if (!has_target) {
+  const bool last = (t % S) == (S - 1);
+  const int raw = last ? IGNORE_LABEL : (lab ? lab[t + 1] : tok[t + 1]);
+  if (raw == IGNORE_LABEL) {
     for (int j = threadIdx.x; j < V; j += NT) put_pair(dl, o + j, 0.0, 0.0);
     if (threadIdx.x == 0) { rowloss[t] = 0.0; rowloss[T_ + t] = 0.0; }
     return;
   }
-  const int y = clamp_tok(tok[t + 1], V);
+  const int y = clamp_tok(raw, V);
   double mx = -1e300;
   for (int j = threadIdx.x; j < V; j += NT) mx = fmax(mx, (double)lm[o + j]);
   mx = block_max<NT>(mx, sh);
@@ -838,14 +843,41 @@ __global__ __launch_bounds__(NT) void ce_kernel(PairT<T> dl, double* rowloss, co
   }
 }
 
-__global__ void loss_sum_kernel(double* out2, const double* rowloss, int T_) {
+__global__ void loss_sum_kernel(double* out2, const double* rowloss, int T_, bool acc) {
   __shared__ double sh[NT / 64];
   double a = 0.0, b = 0.0;
   // fixed assignment of rows to threads, fixed reduction tree
   for (int t = threadIdx.x; t < T_; t += NT) { a += rowloss[t]; b += rowloss[T_ + t]; }
   a = block_sum<NT>(a, sh);
   b = block_sum<NT>(b, sh);
-  if (threadIdx.x == 0) { out2[0] = a; out2[1] = b; }
+  if (threadIdx.x == 0) {
+    out2[0] = acc ? out2[0] + a : a;
+    out2[1] = acc ? out2[1] + b : b;
+  }
+}
+
+// out[0] += number of targets of one [B, S] batch (positions t % S < S - 1
+// whose label at t + 1 is not IGNORE_LABEL; all of them without labels),
+// out[1] += number of labels outside [0, V) other than IGNORE_LABEL.
+__global__ void count_targets_kernel(int64_t* out, const int32_t* lab, int B, int S, int V) {
+  __shared__ double sh[NT / 64];
+  const int64_t n = (int64_t)B * S;
+  double c = 0.0, bad = 0.0;
+  for (int64_t i = threadIdx.x; i < n; i += NT) {
+    const int64_t t = i % S;
+    if (t == S - 1) continue;
+    const int y = lab ? lab[i + 1] : 0;
+    if (y == IGNORE_LABEL) continue;
+    if (y < 0 || y >= V) bad += 1.0;
+    else c += 1.0;
+  }
+  // counts below 2^53 are exact in fp64
+  c = block_sum<NT>(c, sh);
+  bad = block_sum<NT>(bad, sh);
+  if (threadIdx.x == 0) {
+    out[0] += (int64_t)c;
+    out[1] += (int64_t)bad;
+  }
 }
 
 // ---- embedding backward --------------------------------------------------------------
@@ -904,13 +936,14 @@ __global__ void embed_bwd_kernel(float* hv, const uint32_t* keys, const float* d
   hv[idx] = acc ? (float)((double)hv[idx] + t * inv_eps) : (float)(t * inv_eps);
 }
 
-__global__ void pos_bwd_kernel(float* hv, const float* dxd, int B, int S, int dm, double inv_eps) {
+__global__ void pos_bwd_kernel(float* hv, const float* dxd, int B, int S, int dm, double inv_eps, bool acc) {
   const int64_t n = (int64_t)S * dm;
   GRID_LOOP(i, n) {
     const int s = (int)(i / dm), c = (int)(i % dm);
     double a = 0.0;
     for (int b = 0; b < B; ++b) a += (double)dxd[((int64_t)b * S + s) * dm + c];
-    hv[i] = (float)(a * inv_eps);
+    const float x = (float)(a * inv_eps);
+    hv[i] = acc ? hv[i] + x : x;
   }
 }
 
@@ -1065,13 +1098,17 @@ hipError_t launch_swiglu_bwd(PairT<T> dgu, const float* gum, const float* gud, c
 }
 
 template <typename T>
-hipError_t launch_ce(PairT<T> dl, double* rowloss, const float* lm, const float* ld, const int32_t* tok, int T_, int S,
-                     int V, double inv_n, hipStream_t s) {
-  hipLaunchKernelGGL(ce_kernel<T>, dim3(T_), dim3(NT), 0, s, dl, rowloss, lm, ld, tok, T_, S, V, inv_n);
+hipError_t launch_ce(PairT<T> dl, double* rowloss, const float* lm, const float* ld, const int32_t* tok,
+                     const int32_t* lab, int T_, int S, int V, double inv_n, hipStream_t s) {
+  hipLaunchKernelGGL(ce_kernel<T>, dim3(T_), dim3(NT), 0, s, dl, rowloss, lm, ld, tok, lab, T_, S, V, inv_n);
   return hipGetLastError();
 }
-hipError_t launch_loss_sum(double* out2, const double* rowloss, int T_, hipStream_t s) {
-  hipLaunchKernelGGL(loss_sum_kernel, dim3(1), dim3(NT), 0, s, out2, rowloss, T_);
+hipError_t launch_loss_sum(double* out2, const double* rowloss, int T_, bool acc, hipStream_t s) {
+  hipLaunchKernelGGL(loss_sum_kernel, dim3(1), dim3(NT), 0, s, out2, rowloss, T_, acc);
+  return hipGetLastError();
+}
+hipError_t launch_count_targets(int64_t* out2, const int32_t* lab, int B, int S, int V, hipStream_t s) {
+  hipLaunchKernelGGL(count_targets_kernel, dim3(1), dim3(NT), 0, s, out2, lab, B, S, V);
   return hipGetLastError();
 }
 
@@ -1086,8 +1123,8 @@ hipError_t launch_embed_bwd(float* hv, const uint32_t* keys, const float* dxd, i
                      acc);
   return hipGetLastError();
 }
-hipError_t launch_pos_bwd(float* hv, const float* dxd, int B, int S, int dm, double inv_eps, hipStream_t s) {
-  hipLaunchKernelGGL(pos_bwd_kernel, dim3(grid_for((int64_t)S * dm)), dim3(NT), 0, s, hv, dxd, B, S, dm, inv_eps);
+hipError_t launch_pos_bwd(float* hv, const float* dxd, int B, int S, int dm, double inv_eps, bool acc, hipStream_t s) {
+  hipLaunchKernelGGL(pos_bwd_kernel, dim3(grid_for((int64_t)S * dm)), dim3(NT), 0, s, hv, dxd, B, S, dm, inv_eps, acc);
   return hipGetLastError();
 }
 
@@ -1113,8 +1150,8 @@ hipError_t launch_pos_bwd(float* hv, const float* dxd, int B, int S, int dm, dou
   template hipError_t launch_swiglu_fwd<T>(PairT<T>, const float*, const float*, int, int, hipStream_t);               \
   template hipError_t launch_swiglu_bwd<T>(PairT<T>, const float*, const float*, const float*, const float*, int, int, \
                                            hipStream_t);                                                               \
-  template hipError_t launch_ce<T>(PairT<T>, double*, const float*, const float*, const int32_t*, int, int, int,       \
-                                   double, hipStream_t);
+  template hipError_t launch_ce<T>(PairT<T>, double*, const float*, const float*, const int32_t*, const int32_t*, int, \
+                                   int, int, double, hipStream_t);
 INST_T(float)
 INST_T(bf16_t)
 

@@ -492,31 +492,38 @@ hipError_t launch_copy16(void* dst, const void* src, size_t bytes, hipStream_t s
 }
 
 namespace {
-__global__ void sum_splits_kernel(float* out, const float* part, int ns, int64_t n) {
+// out = sum of the ns partial products in slice order (acc: out += that sum)
+__global__ void sum_splits_kernel(float* out, const float* part, int ns, int64_t n, bool acc) {
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
     double t = 0.0;
     for (int j = 0; j < ns; ++j) t += (double)part[(int64_t)j * n + i];
-    out[i] = (float)t;
+    out[i] = acc ? out[i] + (float)t : (float)t;
   }
 }
-__global__ void sum_splits4_kernel(float4* out, const float4* part, int ns, int64_t n4) {
+__global__ void sum_splits4_kernel(float4* out, const float4* part, int ns, int64_t n4, bool acc) {
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n4; i += (int64_t)gridDim.x * blockDim.x) {
     double t[4] = {0.0, 0.0, 0.0, 0.0};
     for (int j = 0; j < ns; ++j) {
       const float4 p = part[(int64_t)j * n4 + i];
       t[0] += p.x; t[1] += p.y; t[2] += p.z; t[3] += p.w;
     }
-    out[i] = make_float4((float)t[0], (float)t[1], (float)t[2], (float)t[3]);
+    float4 r = make_float4((float)t[0], (float)t[1], (float)t[2], (float)t[3]);
+    if (acc) {
+      const float4 o = out[i];
+      r.x += o.x; r.y += o.y; r.z += o.z; r.w += o.w;
+    }
+    out[i] = r;
   }
 }
 }  // namespace
 
-hipError_t launch_sum_splits(float* out, const float* part, int ns, int64_t n, hipStream_t s) {
+hipError_t launch_sum_splits(float* out, const float* part, int ns, int64_t n, bool acc, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   if (n % 4 == 0 && (uintptr_t)out % 16 == 0 && (uintptr_t)part % 16 == 0)
-    hipLaunchKernelGGL(sum_splits4_kernel, dim3(grid_for(n / 4)), dim3(NT), 0, s, (float4*)out, (const float4*)part, ns, n / 4);
+    hipLaunchKernelGGL(sum_splits4_kernel, dim3(grid_for(n / 4)), dim3(NT), 0, s, (float4*)out, (const float4*)part, ns,
+                       n / 4, acc);
   else
-    hipLaunchKernelGGL(sum_splits_kernel, dim3(grid_for(n)), dim3(NT), 0, s, out, part, ns, n);
+    hipLaunchKernelGGL(sum_splits_kernel, dim3(grid_for(n)), dim3(NT), 0, s, out, part, ns, n, acc);
   return hipGetLastError();
 }
 

@@ -22,6 +22,8 @@ DTYPE = {"f32": 0, "bf16": 1}
 REORTH = {"none": 0, "full": 1, "window": 2}
 TOKENS = {"uniform": 0, "zipf": 1}
 VEC = {"rademacher": 0, "gaussian": 1}
+REDUCTION = {"mean": 0, "sum": 1}
+IGNORE = -100
 
 
 class FdhError(RuntimeError):
@@ -41,6 +43,10 @@ class ModelConfig(C.Structure):
 class LanczosOpts(C.Structure):
     _fields_ = [("reorth", C.c_int32), ("window", C.c_int32), ("basis_dtype", C.c_int32),
                 ("breakdown_tol", C.c_float)]
+
+
+class Batch(C.Structure):
+    _fields_ = [("tokens", C.c_void_p), ("labels", C.c_void_p), ("B", C.c_int32), ("S", C.c_int32)]
 
 
 class Block(C.Structure):
@@ -77,6 +83,8 @@ def lib():
         "fdh_hvp": (i32, [vp, vp, vp, f64, vp, i32, i32, vp]),
         "fdh_last_losses": (i32, [vp, pd, pd]),
         "fdh_bind": (i32, [vp, vp, vp, i32, i32, f64]),
+        "fdh_bind_dataset": (i32, [vp, vp, C.POINTER(Batch), i32, f64, i32, C.POINTER(i64)]),
+        "fdh_hvp_bound": (i32, [vp, vp, vp]),
         "fdh_lanczos": (i32, [vp, i32, u64, C.POINTER(LanczosOpts), pd, pd, pi]),
         "fdh_slq_density": (i32, [vp, i32, i32, u64, C.POINTER(LanczosOpts), pd, pd, pi, pd]),
         "fdh_block_stats": (i32, [vp, vp, vp, pd]),
@@ -244,6 +252,31 @@ class Model:
         B, S = (tokens.shape if tokens is not None else (0, 0))
         self._keep = [params, tokens]
         self._check(self._L.fdh_bind(self._h, _ptr(params), _ptr(tokens), B, S, float(eps)), "fdh_bind")
+
+    def bind_dataset(self, params, batches, eps: float, reduction: str = "mean") -> int:
+        """Bind the token-weighted dataset operator over ``batches``: a list of
+        int32 [B, S] token tensors or (tokens, labels) pairs on the device
+        (labels aligned with the tokens, -100 = no target).  Returns the number
+        of kept targets."""
+        import torch
+        items = [b if isinstance(b, tuple) else (b, None) for b in batches]
+        for tok, lab in items:
+            if tok.dtype != torch.int32 or (lab is not None and (lab.dtype != torch.int32 or lab.shape != tok.shape)):
+                raise ValueError("tokens and labels must be int32 tensors of one shape")
+        arr = (Batch * len(items))(*[Batch(_ptr(t), _ptr(l), t.shape[0], t.shape[1]) for t, l in items])
+        n = C.c_int64()
+        self._keep = [params] + [x for it in items for x in it if x is not None]
+        self._check(self._L.fdh_bind_dataset(self._h, _ptr(params), arr, len(items), float(eps), REDUCTION[reduction],
+                                             C.byref(n)), "fdh_bind_dataset")
+        return int(n.value)
+
+    def hvp_bound(self, v, out=None):
+        """H v of the bound operator (float32 [P]); enqueued on the context stream."""
+        import torch
+        if out is None:
+            out = torch.empty(self.num_params, dtype=torch.float32, device="cuda")
+        self._check(self._L.fdh_hvp_bound(self._h, _ptr(v), _ptr(out)), "fdh_hvp_bound")
+        return out
 
     def lanczos(self, m: int, probe_seed: int, o: LanczosOpts):
         a = np.zeros(m)

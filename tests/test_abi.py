@@ -82,6 +82,13 @@ def test_argument_validation_without_gpu_work():
     o = fd.opts("full")
     assert lib.fdh_lanczos(h, 4, 1, C.byref(o), a.ctypes.data_as(C.POINTER(C.c_double)),
                            a.ctypes.data_as(C.POINTER(C.c_double)), C.byref(s)) == -5
+    # dataset binding: reduction, empty list, and a batch beyond the (absent) plan
+    one = (fd.Batch * 1)(fd.Batch(16, 0, 8, 64))
+    n = C.c_int64()
+    assert lib.fdh_bind_dataset(h, C.c_void_p(16), one, 1, 1e-3, 7, C.byref(n)) == -1
+    assert lib.fdh_bind_dataset(h, C.c_void_p(16), one, 0, 1e-3, 0, C.byref(n)) == -1
+    assert lib.fdh_bind_dataset(h, C.c_void_p(16), one, 1, 1e-3, 0, C.byref(n)) == -2
+    assert lib.fdh_hvp_bound(h, C.c_void_p(16), C.c_void_p(32)) == -5
     # bad configurations
     bad = fd.ModelConfig(0, 2, 60, 4, 4, 256, 256, 64, 0, 1e-5, 1e4, 0, 0)   # head_dim 15
     out = C.c_void_p()

@@ -101,3 +101,41 @@ def test_dataset_average_equals_concatenated_batch():
     a = O.lm_hvp_dataset(cfg, theta, v, 1e-3, [t1, t2])
     b = O.lm_hvp(cfg, theta, v, 1e-3, np.concatenate([t1, t2]))
     assert np.linalg.norm(a - b) <= 1e-9 * np.linalg.norm(b)
+
+
+def test_dataset_weights_are_target_counts():
+    """Batches of different shapes and label masks: the weighted average of
+    Algorithm 1 equals the HVP of the mean over every kept target, computed
+    here on one padded batch that holds all rows (right padding with ignored
+    labels does not change a row's targets, by causality)."""
+    cfg, theta, _ = micro.inputs(micro.MICRO["llama"])
+    t1 = synth.tokens(20, 2, 8, cfg.vocab)
+    t2 = synth.tokens(21, 3, 6, cfg.vocab)
+    l1 = t1.astype(np.int64).copy()
+    l1[0, :3] = M.IGNORE                         # prompt mask
+    l2 = t2.astype(np.int64).copy()
+    l2[1, 4:] = M.IGNORE                         # padding
+    v = synth.gaussian_direction(8, theta.size)
+    a = O.lm_hvp_dataset(cfg, theta, v, 1e-3, [(t1, l1), (t2, l2)])
+    # one batch [5, 8]: t2's rows right-padded to 8 with ignored labels
+    pad = np.zeros((3, 2), dtype=t2.dtype)
+    tok = np.concatenate([t1, np.concatenate([t2, pad], 1)])
+    lab = np.concatenate([l1, np.concatenate([l2, np.full((3, 2), M.IGNORE)], 1)])
+    b = O.lm_hvp(cfg, theta, v, 1e-3, tok, lab)
+    assert M.num_targets(tok, lab) == M.num_targets(t1, l1) + M.num_targets(t2, l2)
+    assert np.linalg.norm(a - b) <= 1e-8 * np.linalg.norm(b)
+    # and it is not the plain average of the two batch HVPs (unequal weights)
+    c = 0.5 * (O.lm_hvp(cfg, theta, v, 1e-3, t1, l1) + O.lm_hvp(cfg, theta, v, 1e-3, t2, l2))
+    assert np.linalg.norm(a - c) > 1e-3 * np.linalg.norm(b)
+
+
+@pytest.mark.parametrize("fam", ["gpt2", "llama"])
+def test_fd_hvp_with_labels_against_exact_autograd_hvp(fam):
+    cfg, theta, tok = micro.inputs(micro.MICRO[fam], seed=7)
+    lab = tok.astype(np.int64).copy()
+    lab[0, 6:] = M.IGNORE
+    lab[1, :3] = M.IGNORE
+    v = synth.gaussian_direction(9, theta.size)
+    exact = torch_ref.exact_hvp(micro.MICRO[fam], theta, v, tok, lab)
+    fd = O.lm_hvp(cfg, theta, v, 1e-3, tok, lab)
+    assert np.linalg.norm(fd - exact) <= 1e-5 * np.linalg.norm(exact)

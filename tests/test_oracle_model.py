@@ -126,3 +126,76 @@ def test_softmax_regression_head_hessian_closed_form():
     # nothing outside the head block is touched by curvature from the head alone
     # except through the embedding/normf coupling, which is real; check the
     # head block only
+
+
+# ---- labels: padding and prompt masks (the ignore label -100) ----
+
+def _labelled(fam, seed=3, batch=3, seq=8):
+    cfg, theta, tok = micro.inputs(micro.MICRO[fam], batch=batch, seq=seq, seed=seed)
+    lab = tok.astype(np.int64).copy()
+    lab[0, 5:] = M.IGNORE          # right padding of row 0
+    lab[1, :4] = M.IGNORE          # masked prompt of row 1
+    lab[2, 2] = (lab[2, 2] + 3) % cfg.vocab   # a label that differs from the next input token
+    return cfg, theta, tok, lab
+
+
+@pytest.mark.parametrize("fam", ["gpt2", "llama"])
+def test_labels_match_library_cross_entropy_with_ignore_index(fam):
+    """Loss and gradient against torch's cross_entropy(ignore_index=-100) in an
+    independent float64 statement of the model."""
+    cfg, theta, tok, lab = _labelled(fam)
+    L, g = M.loss_and_grad(cfg, theta, tok, labels=lab)
+    import torch
+    t = torch.tensor(theta, requires_grad=True)
+    ref = torch_ref.loss(micro.MICRO[fam], t, tok, lab)
+    (gr,) = torch.autograd.grad(ref, t)
+    assert abs(L - float(ref.detach())) <= 1e-12 * abs(L)
+    assert np.linalg.norm(g - gr.numpy()) <= 1e-10 * np.linalg.norm(g)
+    assert M.num_targets(tok, lab) == 3 * 7 - 3 - 3
+
+
+@pytest.mark.parametrize("fam", ["gpt2", "llama"])
+def test_right_padding_equals_truncated_batch(fam):
+    """Causal attention: tokens after position t cannot change the logits at t,
+    so a row padded on the right with ignored labels has the loss and gradient
+    of the unpadded row (here all rows are cut to 5 tokens)."""
+    cfg, theta, tok = micro.inputs(micro.MICRO[fam], batch=2, seq=8, seed=4)
+    short = tok[:, :5]
+    padded = tok.copy()
+    padded[:, 5:] = (padded[:, 5:] * 7 + 1) % cfg.vocab   # arbitrary pad token ids
+    lab = padded.astype(np.int64).copy()
+    lab[:, 5:] = M.IGNORE
+    lab[:, :5] = short
+    L1, g1 = M.loss_and_grad(cfg, theta, short)
+    L2, g2 = M.loss_and_grad(cfg, theta, padded, labels=lab)
+    assert abs(L1 - L2) <= 1e-13 * abs(L1)
+    if cfg.family == "gpt2":
+        # the position rows 5..7 only feed ignored targets: zero gradient there
+        wpe = next(e for e in M.layout(cfg) if e.name == "wpe")
+        rows = g2[wpe.offset:wpe.offset + wpe.numel].reshape(cfg.max_seq, cfg.d_model)
+        assert np.abs(rows[5:]).max() == 0.0
+    assert np.linalg.norm(g1 - g2) <= 1e-12 * np.linalg.norm(g1)
+
+
+def test_labels_loss_is_target_weighted_split():
+    """A partition of the targets into two label masks: N L = N_a L_a + N_b L_b."""
+    cfg, theta, tok = micro.inputs(micro.MICRO["llama"], batch=2, seq=8, seed=5)
+    rng = np.random.default_rng(0)
+    pick = rng.random(tok.shape) < 0.5
+    la = np.where(pick, tok, M.IGNORE)
+    lb = np.where(~pick, tok, M.IGNORE)
+    na, nb = M.num_targets(tok, la), M.num_targets(tok, lb)
+    assert na + nb == M.num_targets(tok) == 14
+    L, g = M.loss_and_grad(cfg, theta, tok)
+    La, ga = M.loss_and_grad(cfg, theta, tok, labels=la)
+    Lb, gb = M.loss_and_grad(cfg, theta, tok, labels=lb)
+    assert abs(14 * L - na * La - nb * Lb) <= 1e-12 * abs(14 * L)
+    assert np.linalg.norm(14 * g - na * ga - nb * gb) <= 1e-12 * np.linalg.norm(14 * g)
+
+
+def test_all_ignored_batch_has_zero_loss_and_gradient():
+    cfg, theta, tok = micro.inputs(micro.MICRO["gpt2"], batch=2, seq=8, seed=6)
+    lab = np.full(tok.shape, M.IGNORE)
+    L, g = M.loss_and_grad(cfg, theta, tok, labels=lab)
+    assert L == 0.0 and not g.any()
+    assert M.num_targets(tok, lab) == 0

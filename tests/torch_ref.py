@@ -62,7 +62,7 @@ def _rope(x, base):
     return torch.cat([x1 * c - x2 * s, x2 * c + x1 * s], -1)
 
 
-def loss(cfg, flat, tokens):
+def loss(cfg, flat, tokens, labels=None):
     W = _params(cfg, flat)
     tok = torch.as_tensor(tokens, dtype=torch.long)
     B, S = tok.shape
@@ -107,19 +107,21 @@ def loss(cfg, flat, tokens):
     else:
         f = _rms(x, W["gf"], eps)
         logits = f @ W["head"].T
+    # torch's ignore_index=-100 drops those targets from the mean
+    tgt = tok if labels is None else torch.as_tensor(labels, dtype=torch.long)
     return torch.nn.functional.cross_entropy(
-        logits[:, :-1].reshape(-1, cfg["vocab"]), tok[:, 1:].reshape(-1))
+        logits[:, :-1].reshape(-1, cfg["vocab"]), tgt[:, 1:].reshape(-1), ignore_index=-100)
 
 
-def grad(cfg, theta, tokens):
+def grad(cfg, theta, tokens, labels=None):
     t = torch.tensor(theta, dtype=torch.float64, requires_grad=True)
-    (g,) = torch.autograd.grad(loss(cfg, t, tokens), t)
+    (g,) = torch.autograd.grad(loss(cfg, t, tokens, labels), t)
     return g.numpy()
 
 
-def exact_hvp(cfg, theta, v, tokens):
+def exact_hvp(cfg, theta, v, tokens, labels=None):
     t = torch.tensor(theta, dtype=torch.float64, requires_grad=True)
     vv = torch.tensor(v, dtype=torch.float64)
-    (g,) = torch.autograd.grad(loss(cfg, t, tokens), t, create_graph=True)
+    (g,) = torch.autograd.grad(loss(cfg, t, tokens, labels), t, create_graph=True)
     (hv,) = torch.autograd.grad(g @ vv, t)
     return hv.numpy()
