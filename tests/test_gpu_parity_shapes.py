@@ -1,8 +1,9 @@
 """HVP parity at the workloads' real layer shapes (full width, vocabulary and
 head layout; reduced depth and token count so the fp64 oracle finishes in
-seconds), and at the full small fp32 workload.  Also properties that must
-hold at the full 1.3B size: symmetry and agreement of the Lanczos alpha_1
-with v^T H v."""
+seconds; the 8B vocabulary is cut as well), and at the full small fp32
+workload.  Also properties that must hold at the full 1.3B and 8B sizes:
+symmetry, and agreement of the Lanczos alpha_1 (and beta_2) with the moments
+of the probe under separately computed products."""
 import numpy as np
 import pytest
 
@@ -42,6 +43,18 @@ def test_llama_1_3b_layer_shapes_bf16():
     w = dict(WORKLOADS["llama-1.3b-bf16"], n_layers=1)
     say("llama-1.3b shapes, 1 layer, 1x256 tokens")
     errs = _parity(w, 1, 256)
+    say(f"  rel_l2 {errs}")
+    assert max(errs) <= 5e-2
+
+
+def test_llama3_8b_layer_shapes_bf16():
+    # full width, MLP and grouped-query head layout (32 query heads on 8
+    # key/value heads, RoPE base 5e5); the vocabulary is cut to 4096 so that
+    # the fp64 oracle's vectors stay at 2 GB (the full vocabulary runs in the
+    # fused-attention test and in the full-size test below)
+    w = dict(WORKLOADS["llama3-8b-bf16"], n_layers=1, vocab=4096)
+    say("llama3-8b shapes, 1 layer, vocab 4096, 1x128 tokens")
+    errs = _parity(w, 1, 128)
     say(f"  rel_l2 {errs}")
     assert max(errs) <= 5e-2
 
@@ -89,3 +102,52 @@ def test_full_1_3b_properties():
     say(f"v.Hv = {vhv:.6e}, alpha_1 = {al[0]:.6e}")
     assert abs(al[0] - vhv) <= 1e-4 * abs(vhv) + 1e-6
     assert np.all(np.isfinite(hv.cpu().numpy()))
+
+
+def _dot(torch, x, y, chunk=1 << 28):
+    """fp64 dot product of two float32 device vectors, in chunks (no 64 GB copies)."""
+    return sum(float(torch.dot(x[i:i + chunk].double(), y[i:i + chunk].double())) for i in range(0, x.numel(), chunk))
+
+
+def test_full_8b_properties_and_window_lanczos():
+    """The Llama-3-8B workload at full depth and size (1 x 2048 tokens, P = 8.03e9):
+    (u, Hv) = (v, Hu); then its window-8 Lanczos run (10 steps, so the window
+    slides) against the moment identities alpha_1 = q^T H q and
+    alpha_1^2 + beta_2^2 = ||H q||^2 of the probe q."""
+    torch = need_gpu()
+    from paper_2602_00816_amd import fdhvp as fd
+    w = WORKLOADS["llama3-8b-bf16"]
+    B, S = w["batch"], w["seq"]
+    # the window-8 workspace (273 GB) and theta (16 GB) leave 20 GB of the
+    # 288 GiB: give back what earlier tests left cached first, so that theta is
+    # not carved out of one of their segments
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    mod = fd.Model.from_workload(w)
+    P = mod.num_params
+    mod.set_workspace(B, S)
+    th = mod.init_params(1)
+    tok = mod.make_tokens(B, S, 2, "zipf")
+    v = mod.random_vector(3, "rademacher")
+    u = mod.random_vector(4, "gaussian")
+    hv = mod.hvp(th, v, 1e-3, tok)
+    hu = mod.hvp(th, u, 1e-3, tok)
+    assert bool(torch.isfinite(hv).all()) and bool(torch.isfinite(hu).all())
+    a, b = _dot(torch, u, hv), _dot(torch, v, hu)
+    nhv, nhu = np.sqrt(_dot(torch, hv, hv)), np.sqrt(_dot(torch, hu, hu))
+    noise = (nhv + nhu) / np.sqrt(P)
+    say(f"8B: u.Hv = {a:.6e}, v.Hu = {b:.6e}, noise scale {noise:.3e}")
+    assert abs(a - b) <= 5e-2 * max(abs(a), abs(b)) + 5e-2 * noise
+    vhv = _dot(torch, v, hv)
+    del hv, hu, u, v
+    mod._ws = None
+    torch.cuda.empty_cache()
+    m = 10
+    o = fd.opts("window", w["window"], "bf16")
+    mod.set_workspace(B, S, m, o)
+    mod.bind(th, tok, 1e-3)
+    al, be, s, st = mod.lanczos(m, 3, o)
+    say(f"8B window-8 Lanczos: steps {s}, alpha {al}, beta {be}")
+    assert s == m and np.all(np.isfinite(al)) and np.all(np.isfinite(be))
+    assert abs(al[0] - vhv) <= 1e-4 * abs(vhv) + 1e-12
+    assert abs(al[0] ** 2 + be[0] ** 2 - nhv ** 2) <= 1e-4 * nhv ** 2
