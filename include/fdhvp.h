@@ -204,6 +204,23 @@ fdh_status fdh_slq_density(fdh_ctx* ctx, int32_t probes, int32_t m, uint64_t see
                            const fdh_lanczos_opts* o, double* nodes_host, double* weights_host,
                            int32_t* steps_done, double* trace_est);
 
+/* Ritz-value diagnostics for runs that lose orthogonality (no or windowed
+ * reorthogonalisation; Theorem 4.1's spurious duplicate "ghost" eigenvalues).
+ * Host-only, no context.  alpha[s], beta[s] as returned by fdh_lanczos
+ * (beta[s - 1] = beta_{s+1} is the residual norm), 1 <= s <= 128.  With
+ * norm = max_i |theta_i| over the Ritz values theta_i of T_s (ascending):
+ * nodes[i] = theta_i; weights[i] = (U_1i)^2; resid[i] = beta_{s+1} |U_si|,
+ * the residual norm of the Ritz pair while the basis stays orthonormal;
+ * copies[i] = size of its cluster (Ritz values chained by gaps <= tol * norm);
+ * spurious[i] = 1 for a simple Ritz value that is also an eigenvalue of T_s
+ * without its first row and column, within tol * norm (the test of Cullum and
+ * Willoughby, 1985); *n_ghosts = sum over clusters of (size - 1).  Any output
+ * pointer may be NULL.  FDH_ERR_INVALID_ARG for s outside [1, 128], a null
+ * input or tol < 0. */
+fdh_status fdh_ritz_diagnostics(const double* alpha, const double* beta, int32_t s, double tol, double* nodes,
+                                double* weights, double* resid, int32_t* copies, int32_t* spurious,
+                                int32_t* n_ghosts);
+
 /* Per transformer layer b (section 6): out_host[3b..3b+2] = ||a_b||^2, ||b_b||^2,
  * <a_b, b_b> over the parameters of layer b; a, b float32 [P] on device. */
 fdh_status fdh_block_stats(fdh_ctx* ctx, const float* a_dev, const float* b_dev, double* out_host);

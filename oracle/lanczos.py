@@ -74,6 +74,50 @@ def ritz(alpha, beta):
     return lam, U[0, :] ** 2
 
 
+def ritz_diagnostics(alpha, beta, tol: float = 1e-8):
+    """Diagnostics of the Ritz values of T_s for runs that lose orthogonality.
+
+    Theorem 4.1 (and the GPT-OSS run of section 7, which stores no basis and
+    does not reorthogonalise) concern the spurious duplicate ("ghost") Ritz
+    values that appear once Lanczos vectors lose orthogonality.  Per Ritz value
+    theta_i (ascending) this returns, with norm = max_i |theta_i|:
+    * weight_i = (U_1i)^2, the Gauss weight;
+    * resid_i = beta_{s+1} |U_si|, the residual norm ||H z_i - theta_i z_i|| of
+      the Ritz pair (Paige's bound, exact while the basis is orthonormal);
+    * copies_i: the size of its cluster, Ritz values chained by gaps
+      <= tol * norm (a converged eigenvalue repeated by lost orthogonality);
+    * spurious_i: the test of Cullum and Willoughby (Lanczos Algorithms for
+      Large Symmetric Eigenvalue Computations, 1985): a simple Ritz value
+      (copies_i = 1) that is also an eigenvalue of T_s with its first row and
+      column removed, within tol * norm;
+    and the number of ghosts, sum over clusters of (size - 1).
+    """
+    a = np.asarray(alpha, dtype=np.float64)
+    b = np.asarray(beta, dtype=np.float64)
+    s = a.size
+    lam, U = np.linalg.eigh(tridiag(a, b))
+    norm = float(np.abs(lam).max())
+    weight = U[0, :] ** 2
+    resid = abs(b[s - 1]) * np.abs(U[s - 1, :])
+    copies = np.ones(s, dtype=np.int64)
+    start = 0
+    for i in range(1, s + 1):
+        if i == s or lam[i] - lam[i - 1] > tol * norm:
+            copies[start:i] = i - start
+            start = i
+    mu = np.linalg.eigvalsh(tridiag(a[1:], b[1:])) if s > 1 else np.zeros(0)
+    spurious = np.zeros(s, dtype=bool)
+    for i in range(s):
+        if copies[i] == 1 and mu.size and np.abs(mu - lam[i]).min() <= tol * norm:
+            spurious[i] = True
+    ghosts = 0
+    i = 0
+    while i < s:
+        ghosts += int(copies[i]) - 1
+        i += int(copies[i])
+    return lam, weight, resid, copies, spurious, ghosts
+
+
 def slq(hvp, probes, m: int, reorth: int = FULL, window: int = 0):
     """SLQ over unit probes: per-probe nodes, weights, and tr(H) ~ P mean alpha_1."""
     nodes, weights, alpha1, steps = [], [], [], []

@@ -81,6 +81,15 @@ void fdh_destroy(fdh_ctx* ctx) {
 
 int64_t fdh_num_params(const fdh_ctx* ctx) { return (ctx && ctx->eng) ? ctx->eng->P : -1; }
 
+fdh_status fdh_ritz_diagnostics(const double* alpha, const double* beta, int32_t s, double tol, double* nodes,
+                                double* weights, double* resid, int32_t* copies, int32_t* spurious, int32_t* n_ghosts) {
+  try {
+    return (fdh_status)fdh::ritz_diagnostics(alpha, beta, s, tol, nodes, weights, resid, copies, spurious, n_ghosts);
+  } catch (...) {
+    return FDH_ERR_INVALID_ARG;
+  }
+}
+
 int32_t fdh_num_blocks(const fdh_ctx* ctx) { return (ctx && ctx->eng) ? ctx->eng->L : -1; }
 
 fdh_status fdh_param_layout(const fdh_ctx* ctx, fdh_block* out, int32_t cap, int32_t* n) {

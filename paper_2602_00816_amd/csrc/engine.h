@@ -55,6 +55,9 @@ struct Timing {
   ~Timing();
 };
 
+int ritz_diagnostics(const double* alpha, const double* beta, int s, double tol, double* nodes, double* weights,
+                     double* resid, int32_t* copies, int32_t* spurious, int32_t* ghosts);
+
 class Engine {
  public:
   explicit Engine(const fdh_model_config& cfg, hipStream_t stream);

@@ -1026,6 +1026,58 @@ static void tridiag_eig(int n, std::vector<double>& dd, const std::vector<double
   for (int i = 0; i < n; ++i) dd[i] = A[(size_t)i * n + i];
 }
 
+// Ritz-value diagnostics of T_s (ghost eigenvalues after lost orthogonality,
+// Theorem 4.1; the spurious-value test of Cullum and Willoughby, 1985): Ritz
+// values ascending with their Gauss weights, residual bounds
+// beta_{s+1} |U_si|, cluster sizes (chains of gaps <= tol * max|theta|) and
+// the spurious flags (simple values that are also eigenvalues of T without
+// its first row and column, within tol * max|theta|).
+int ritz_diagnostics(const double* alpha, const double* beta, int s, double tol, double* nodes, double* weights,
+                     double* resid, int32_t* copies, int32_t* spurious, int32_t* ghosts) {
+  if (!alpha || !beta || s < 1 || s > 128 || !(tol >= 0.0)) return FDH_ERR_INVALID_ARG;
+  std::vector<double> dd(alpha, alpha + s), e(beta, beta + (s - 1)), z;
+  tridiag_eig(s, dd, e, z);
+  std::vector<int> idx(s);
+  for (int i = 0; i < s; ++i) idx[i] = i;
+  std::sort(idx.begin(), idx.end(), [&](int x, int y) { return dd[x] < dd[y]; });
+  std::vector<double> lam(s);
+  double norm = 0.0;
+  for (int i = 0; i < s; ++i) {
+    lam[i] = dd[idx[i]];
+    norm = std::max(norm, std::fabs(lam[i]));
+  }
+  const double thr = tol * norm;
+  std::vector<int32_t> cp(s, 1);
+  int32_t ng = 0;
+  for (int i0 = 0, i = 1; i <= s; ++i) {
+    if (i == s || lam[i] - lam[i - 1] > thr) {
+      for (int k = i0; k < i; ++k) cp[k] = i - i0;
+      ng += i - i0 - 1;
+      i0 = i;
+    }
+  }
+  std::vector<double> mu;
+  if (s > 1) {
+    std::vector<double> e2(beta + 1, beta + (s - 1)), z2;
+    mu.assign(alpha + 1, alpha + s);
+    tridiag_eig(s - 1, mu, e2, z2);
+  }
+  for (int i = 0; i < s; ++i) {
+    const int c = idx[i];
+    if (nodes) nodes[i] = lam[i];
+    if (weights) weights[i] = z[c] * z[c];                                   // row 0 of the eigenvectors
+    if (resid) resid[i] = std::fabs(beta[s - 1]) * std::fabs(z[(size_t)(s - 1) * s + c]);
+    if (copies) copies[i] = cp[i];
+    if (spurious) {
+      double dmin = INFINITY;
+      for (double x : mu) dmin = std::min(dmin, std::fabs(x - lam[i]));
+      spurious[i] = (cp[i] == 1 && dmin <= thr) ? 1 : 0;
+    }
+  }
+  if (ghosts) *ghosts = ng;
+  return FDH_OK;
+}
+
 int Engine::slq(int probes, int m, uint64_t seed, const fdh_lanczos_opts& o, double* nodes, double* weights, int* steps,
                 double* trace) {
   if (probes < 1 || !nodes || !weights || !steps) { err = "bad slq arguments"; return FDH_ERR_INVALID_ARG; }

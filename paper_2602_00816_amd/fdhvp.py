@@ -91,6 +91,7 @@ def lib():
         "fdh_block_diagonal": (i32, [vp, vp, pd]),
         "fdh_cg_solve": (i32, [vp, vp, C.c_double, i32, C.c_double, vp, pd, C.POINTER(C.c_int32)]),
         "fdh_last_error": (C.c_char_p, [vp]),
+        "fdh_ritz_diagnostics": (i32, [pd, pd, i32, f64, pd, pd, pd, pi, pi, pi]),
         "fdh_testing_gemm": (i32, [i32, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, i32, C.c_float, i32, vp]),
         "fdh_testing_unfused_attention": (i32, [vp, i32]),
         "fdh_testing_unsplit_wgrad": (i32, [vp, i32]),
@@ -341,6 +342,25 @@ class Model:
         self._check(self._L.fdh_block_stats(self._h, _ptr(a), _ptr(b), out.ctypes.data_as(C.POINTER(C.c_double))),
                     "fdh_block_stats")
         return out
+
+
+def ritz_diagnostics(alpha, beta, tol: float = 1e-8):
+    """Ritz-value diagnostics of T_s (include/fdhvp.h: fdh_ritz_diagnostics).
+    Returns (nodes, weights, resid, copies, spurious, n_ghosts)."""
+    a = np.ascontiguousarray(alpha, dtype=np.float64)
+    b = np.ascontiguousarray(beta, dtype=np.float64)
+    s = a.size
+    if b.size < s:
+        raise ValueError("beta needs as many entries as alpha")
+    nodes, weights, resid = np.zeros(s), np.zeros(s), np.zeros(s)
+    copies, spurious, ng = np.zeros(s, np.int32), np.zeros(s, np.int32), C.c_int32()
+    dp = lambda x: x.ctypes.data_as(C.POINTER(C.c_double))
+    ip = lambda x: x.ctypes.data_as(C.POINTER(C.c_int32))
+    st = lib().fdh_ritz_diagnostics(dp(a), dp(b), s, float(tol), dp(nodes), dp(weights), dp(resid), ip(copies),
+                                    ip(spurious), C.byref(ng))
+    if st != OK:
+        raise FdhError(st, "fdh_ritz_diagnostics")
+    return nodes, weights, resid, copies, spurious.astype(bool), int(ng.value)
 
 
 def testing_copy(dst, src, nbytes: int):

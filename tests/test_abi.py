@@ -89,6 +89,12 @@ def test_argument_validation_without_gpu_work():
     assert lib.fdh_bind_dataset(h, C.c_void_p(16), one, 0, 1e-3, 0, C.byref(n)) == -1
     assert lib.fdh_bind_dataset(h, C.c_void_p(16), one, 1, 1e-3, 0, C.byref(n)) == -2
     assert lib.fdh_hvp_bound(h, C.c_void_p(16), C.c_void_p(32)) == -5
+    # Ritz diagnostics: s outside [1, 128], negative tolerance (host code, no GPU)
+    z = np.zeros(4)
+    pz = z.ctypes.data_as(C.POINTER(C.c_double))
+    assert lib.fdh_ritz_diagnostics(pz, pz, 0, 1e-8, None, None, None, None, None, None) == -1
+    assert lib.fdh_ritz_diagnostics(pz, pz, 129, 1e-8, None, None, None, None, None, None) == -1
+    assert lib.fdh_ritz_diagnostics(pz, pz, 4, -1.0, None, None, None, None, None, None) == -1
     # bad configurations
     bad = fd.ModelConfig(0, 2, 60, 4, 4, 256, 256, 64, 0, 1e-5, 1e4, 0, 0)   # head_dim 15
     out = C.c_void_p()
