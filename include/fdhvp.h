@@ -190,6 +190,23 @@ fdh_status fdh_bind_dataset(fdh_ctx* ctx, const void* params_dev, const fdh_batc
  * aliasing each other or the parameters.  Enqueued on the context stream. */
 fdh_status fdh_hvp_bound(fdh_ctx* ctx, const float* v_dev, float* hv_dev);
 
+/* Krylov-basis offload (section 7 notes that storing the whole Krylov
+ * subspace bounds the scale and names offloading part of it to host memory):
+ * keep at most device_rows stored Lanczos rows in the workspace and the
+ * remaining ones in host_rows, caller-owned pinned host memory mapped for the
+ * device (hipHostMalloc), of at least (stored rows - device_rows) * row bytes,
+ * where stored rows = m (full) or min(m, window) and row bytes =
+ * round_up(P, 8) * (2 for a bf16 basis, 4 for fp32).  Takes effect for the
+ * following fdh_workspace_bytes / fdh_set_workspace (the workspace then holds
+ * device_rows rows) and Lanczos runs; device_rows < 0 keeps every row on the
+ * device (the default) and forgets host_rows.  The projection and update
+ * passes read the host rows over the host link at every step, so each host
+ * row adds about 2 * row bytes / link bandwidth to a step; results are the
+ * same bits as with every row on the device.  FDH_ERR_INVALID_ARG when
+ * host_rows is not mapped pinned memory or device_rows > 128; a Lanczos run
+ * whose host part does not fit host_bytes fails with FDH_ERR_WORKSPACE. */
+fdh_status fdh_set_basis_offload(fdh_ctx* ctx, int32_t device_rows, void* host_rows, size_t host_bytes);
+
 /* m Lanczos steps (section 4) from the Rademacher probe z/sqrt(P) drawn from
  * probe_seed.  alpha_host[m], beta_host[m] receive alpha_1..alpha_s and
  * beta_2..beta_{s+1} (the last is the residual norm), s = *steps_done <= m;

@@ -186,6 +186,10 @@ fdh_status fdh_bind_dataset(fdh_ctx* ctx, const void* params_dev, const fdh_batc
   });
 }
 
+fdh_status fdh_set_basis_offload(fdh_ctx* ctx, int32_t device_rows, void* host_rows, size_t host_bytes) {
+  return run(ctx, [&](fdh::Engine& e) { return e.set_basis_offload(device_rows, host_rows, host_bytes); });
+}
+
 fdh_status fdh_hvp_bound(fdh_ctx* ctx, const float* v_dev, float* hv_dev) {
   return run(ctx, [&](fdh::Engine& e) { return e.hvp_bound(v_dev, hv_dev); });
 }

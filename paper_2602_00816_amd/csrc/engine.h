@@ -111,6 +111,7 @@ class Engine {
   int block_stats(const float* a, const float* b, double* out);
   int block_diagonal(const float* v, double* out);
   int cg_solve(const float* b, double lam, int max_iters, double rel_tol, float* x, double* res, int* steps);
+  int set_basis_offload(int device_rows, void* host, size_t bytes);
   std::vector<int64_t> layer_ranges() const;
 
  private:
@@ -133,6 +134,12 @@ class Engine {
   Span wsplit;  // split-K partial products of the weight-gradient GEMMs
   Span lz_w, lz_q, lz_qp, lz_basis, lz_alpha, lz_beta, lz_coef, lz_gram, lz_partial, lz_flag, lz_maxabs;
   int64_t lz_ldq = 0;  // basis row stride (elements, multiple of 8)
+  int lz_dev_rows = 0;  // basis rows held in the workspace
+  // basis offload: at most off_rows rows in the workspace (-1: all), the rest
+  // in caller-owned pinned host memory (device-side address)
+  int off_rows = -1;
+  void* host_rows_dev = nullptr;
+  size_t host_rows_bytes = 0;
   // set by the Lanczos normalisation when it already wrote lo = eps * v for
   // the next HVP (of this v and eps); consumed by that HVP
   const float* lo_for_v = nullptr;

@@ -224,7 +224,10 @@ size_t Engine::plan(int B, int S, int m, const fdh_lanczos_opts* o, bool carve) 
     take(lz_qp, (size_t)P * 4);
     const int64_t ldq = (P + 7) / 8 * 8;
     if (carve) lz_ldq = ldq;
-    take(lz_basis, (size_t)cap * ldq * (bdt == FDH_BF16 ? 2 : 4));
+    // with the basis offload only the first off_rows rows live in the workspace
+    const int ndev = off_rows >= 0 ? std::min(cap, off_rows) : cap;
+    if (carve) lz_dev_rows = ndev;
+    take(lz_basis, (size_t)ndev * ldq * (bdt == FDH_BF16 ? 2 : 4));
     take(lz_alpha, (size_t)m * 8);
     take(lz_beta, (size_t)m * 8);
     take(lz_coef, 128 * 8);
@@ -889,8 +892,6 @@ int Engine::lanczos_t(int m, uint64_t seed, const fdh_lanczos_opts& o, double* a
   float* w = (float*)(ws + lz_w.off);
   float* q = (float*)(ws + lz_q.off);
   float* qp = (float*)(ws + lz_qp.off);
-  Bt* basis = (Bt*)(ws + lz_basis.off);
-  const int64_t ldq = lz_ldq;
   lo_for_v = nullptr;
   LanczosDev D;
   D.alpha = (double*)(ws + lz_alpha.off);
@@ -902,6 +903,17 @@ int Engine::lanczos_t(int m, uint64_t seed, const fdh_lanczos_opts& o, double* a
   D.maxabs = (double*)(ws + lz_maxabs.off);
   const int cap = o.reorth == FDH_REORTH_FULL ? m : (o.reorth == FDH_REORTH_WINDOW ? std::min(m, o.window) : 0);
   const double tol = o.breakdown_tol > 0.f ? (double)o.breakdown_tol : 1e-5;
+  // stored rows: the first ones in the workspace, the rest (basis offload) in
+  // the caller's pinned host memory
+  BasisRows<Bt> R;
+  R.dev = (Bt*)(ws + lz_basis.off);
+  R.host = (Bt*)host_rows_dev;
+  R.ndev = std::min(cap, lz_dev_rows);
+  R.ldq = lz_ldq;
+  if (cap > R.ndev && (!R.host || host_rows_bytes < (size_t)(cap - R.ndev) * (size_t)lz_ldq * sizeof(Bt))) {
+    err = "the basis offload needs a host buffer of (stored rows - device rows) * row bytes";
+    return FDH_ERR_WORKSPACE;
+  }
 
   CK(launch_fill_f64(D.alpha, m, 0.0, st));
   CK(launch_fill_f64(D.beta, m, 0.0, st));
@@ -909,7 +921,7 @@ int Engine::lanczos_t(int m, uint64_t seed, const fdh_lanczos_opts& o, double* a
   CK(launch_fill_f32((float*)D.flag, 2, 0.f, st));
   CK(launch_fill_f32(qp, P, 0.f, st));
   CK(launch_rademacher(q, P, seed, st));
-  if (cap > 0) CK(launch_scale_cast<Bt>(basis, q, 1.0, P, st));  // slot 0 = q_1
+  if (cap > 0) CK(launch_scale_cast<Bt>(R.row(0), q, 1.0, P, st));  // slot 0 = q_1
 
   const double bb = sizeof(Bt), Pd = (double)P;
   // one timed vector launch (algorithmic bytes: each operand touched once)
@@ -930,10 +942,10 @@ int Engine::lanczos_t(int m, uint64_t seed, const fdh_lanczos_opts& o, double* a
     if (rc != FDH_OK) return rc;
     TV(16.0 * Pd, launch_lanczos_alpha(w, q, qp, D, k, P, st));
     const int nv = std::min(k + 1, cap);
-    if (nv > 0) TV((12.0 + nv * bb) * Pd, launch_lanczos_project<Bt>(w, q, basis, ldq, nv, k % cap, D, k, P, st));
-    TV((nv > 0 ? 8.0 + nv * bb : 12.0) * Pd, launch_lanczos_update<Bt>(w, q, basis, ldq, nv, D, k, P, st));
+    if (nv > 0) TV((12.0 + nv * bb) * Pd, launch_lanczos_project<Bt>(w, q, R, nv, k % cap, D, k, P, st));
+    TV((nv > 0 ? 8.0 + nv * bb : 12.0) * Pd, launch_lanczos_update<Bt>(w, q, R, nv, D, k, P, st));
     Bt* row = nullptr;
-    if (cap > 0 && k + 1 < m) row = basis + (int64_t)((k + 1) % cap) * ldq;
+    if (cap > 0 && k + 1 < m) row = R.row((k + 1) % cap);
     // the next HVP's perturbation operand is written here too
     const bool next_lo = !quad && k + 1 < m;
     const double ob = bf16 ? 2.0 : 4.0;
@@ -1075,6 +1087,30 @@ int ritz_diagnostics(const double* alpha, const double* beta, int s, double tol,
     }
   }
   if (ghosts) *ghosts = ng;
+  return FDH_OK;
+}
+
+int Engine::set_basis_offload(int device_rows, void* host, size_t bytes) {
+  if (device_rows < 0) {
+    off_rows = -1;
+    host_rows_dev = nullptr;
+    host_rows_bytes = 0;
+    return FDH_OK;
+  }
+  if (device_rows > 128) { err = "device_rows must be <= 128"; return FDH_ERR_INVALID_ARG; }
+  void* dptr = nullptr;
+  if (host) {
+    // the kernels take the device-side address of the pinned host memory
+    const hipError_t e = hipHostGetDevicePointer(&dptr, host, 0);
+    if (e != hipSuccess || !dptr) {
+      (void)hipGetLastError();
+      err = "host_rows must be pinned host memory mapped for the device (hipHostMalloc)";
+      return FDH_ERR_INVALID_ARG;
+    }
+  }
+  off_rows = device_rows;
+  host_rows_dev = dptr;
+  host_rows_bytes = host ? bytes : 0;
   return FDH_OK;
 }
 

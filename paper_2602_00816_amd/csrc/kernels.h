@@ -45,8 +45,21 @@ struct LanczosDev {
   double* maxabs;    // [1]  max_j |alpha_j| so far
 };
 
-// The basis rows are stored with a row stride ldq that is a multiple of 8
-// elements.  One Lanczos step after w = H q_k:
+// The stored Krylov rows, ldq elements apart (a multiple of 8): rows
+// [0, ndev) in device memory at dev, rows [ndev, cap) at host, a device-side
+// address of pinned host memory (the basis offload), read over the host link.
+template <typename B>
+struct BasisRows {
+  B* dev = nullptr;
+  B* host = nullptr;
+  int ndev = 0;
+  int64_t ldq = 0;
+  __host__ __device__ B* row(int j) const {
+    return j < ndev ? dev + (int64_t)j * ldq : host + (int64_t)(j - ndev) * ldq;
+  }
+};
+
+// One Lanczos step after w = H q_k:
 // Step A:  w <- w - beta_{k-1} q_prev;  alpha_k = <w, q>  (beta_{-1} = 0)
 hipError_t launch_lanczos_alpha(float* w, const float* q, const float* qprev, LanczosDev st, int k, int64_t n, hipStream_t s);
 // Step B (nv >= 1 stored rows, slot `newest` holds q_k):  with
@@ -54,11 +67,11 @@ hipError_t launch_lanczos_alpha(float* w, const float* q, const float* qprev, La
 // Gram row/column `newest` <- g; coef = 2 p - G p (both classical
 // Gram-Schmidt passes).
 template <typename B>
-hipError_t launch_lanczos_project(const float* w, const float* q, const B* basis, int64_t ldq, int nv, int newest, LanczosDev st,
+hipError_t launch_lanczos_project(const float* w, const float* q, BasisRows<B> rows, int nv, int newest, LanczosDev st,
                                   int k, int64_t n, hipStream_t s);
 // Step C:  w <- (w - alpha_k q) - Q coef (no rows when nv == 0); then ||w||^2
 template <typename B>
-hipError_t launch_lanczos_update(float* w, const float* q, const B* basis, int64_t ldq, int nv, LanczosDev st, int k, int64_t n,
+hipError_t launch_lanczos_update(float* w, const float* q, BasisRows<B> rows, int nv, LanczosDev st, int k, int64_t n,
                                  hipStream_t s);
 // Step D:  beta_k = ||w||; breakdown test (tol relative to max |alpha|);
 // q_next = w / beta_k; basis row (if not null) = B(q_next); the next HVP's

@@ -154,7 +154,7 @@ __global__ __launch_bounds__(NT) void lz_alpha_kernel(float* w, const float* q, 
 // partial[j * RED_BLOCKS + b] = p_j, partial[(nv + j) * RED_BLOCKS + b] = g_j.
 template <typename B, int NW, int NG>
 __global__ __launch_bounds__(64 * NW, NG == 1 ? 4 : 1) void lz_project_kernel(const float* w, const float* q, const double* alpha_k,
-                                                             const B* basis, int64_t ldq, int nv, int newest, int64_t n,
+                                                             BasisRows<B> R, int nv, int newest, int64_t n,
                                                              double* partial) {
   constexpr int RW = 4 * NG;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
@@ -165,8 +165,8 @@ __global__ __launch_bounds__(64 * NW, NG == 1 ? 4 : 1) void lz_project_kernel(co
   const double a = *alpha_k;
   const B* rowp[RW];
 #pragma unroll
-  for (int r = 0; r < RW; ++r) rowp[r] = basis + (int64_t)(r < nr ? wave + NW * r : wave) * ldq;
-  const B* qnp = basis + (int64_t)newest * ldq;
+  for (int r = 0; r < RW; ++r) rowp[r] = R.row(r < nr ? wave + NW * r : wave);
+  const B* qnp = R.row(newest);
   double pw[RW], pg[RW];
 #pragma unroll
   for (int r = 0; r < RW; ++r) pw[r] = pg[r] = 0.0;
@@ -211,8 +211,8 @@ __global__ __launch_bounds__(64 * NW, NG == 1 ? 4 : 1) void lz_project_kernel(co
 // groups of 8 with their loads issued together; a group's rows past nv read
 // row nv - 1 with coefficient zero.
 template <typename B>
-__global__ __launch_bounds__(NT) void lz_update_kernel(float* w, const float* q, const double* alpha_k, const B* basis,
-                                                       int64_t ldq, const double* coef, int nv, int64_t n, double* partial) {
+__global__ __launch_bounds__(NT) void lz_update_kernel(float* w, const float* q, const double* alpha_k, BasisRows<B> R,
+                                                       const double* coef, int nv, int64_t n, double* partial) {
   __shared__ double sh[NT / 64];
   __shared__ double cs[136];
   for (int j = threadIdx.x; j < 136; j += NT) cs[j] = j < nv ? coef[j] : 0.0;
@@ -231,7 +231,7 @@ __global__ __launch_bounds__(NT) void lz_update_kernel(float* w, const float* q,
     for (int j0 = 0; j0 < nv; j0 += 8) {
       V8 rows[8];
 #pragma unroll
-      for (int t = 0; t < 8; ++t) rows[t] = ldv<F>(basis + (int64_t)min(j0 + t, nv - 1) * ldq, i, ne);
+      for (int t = 0; t < 8; ++t) rows[t] = ldv<F>(R.row(min(j0 + t, nv - 1)), i, ne);
 #pragma unroll
       for (int t = 0; t < 8; ++t) {
         const double c = cs[j0 + t];
@@ -561,11 +561,11 @@ hipError_t launch_lanczos_alpha(float* w, const float* q, const float* qprev, La
 }
 
 template <typename B>
-hipError_t launch_lanczos_project(const float* w, const float* q, const B* basis, int64_t ldq, int nv, int newest, LanczosDev st,
+hipError_t launch_lanczos_project(const float* w, const float* q, BasisRows<B> rows, int nv, int newest, LanczosDev st,
                                   int k, int64_t n, hipStream_t s) {
   if (nv < 1 || nv > 128 || newest < 0 || newest >= nv) return hipErrorInvalidValue;
   const double* a = st.alpha + k;
-#define LZP(W, G) hipLaunchKernelGGL((lz_project_kernel<B, W, G>), dim3(RED_BLOCKS), dim3(64 * W), 0, s, w, q, a, basis, ldq, nv, newest, n, st.partial)
+#define LZP(W, G) hipLaunchKernelGGL((lz_project_kernel<B, W, G>), dim3(RED_BLOCKS), dim3(64 * W), 0, s, w, q, a, rows, nv, newest, n, st.partial)
   // rows of wave 0: ceil(nv / waves)
   if (nv <= 16) LZP(4, 1);
   else if (nv <= 32) LZP(8, 1);
@@ -578,10 +578,10 @@ hipError_t launch_lanczos_project(const float* w, const float* q, const B* basis
 }
 
 template <typename B>
-hipError_t launch_lanczos_update(float* w, const float* q, const B* basis, int64_t ldq, int nv, LanczosDev st, int k, int64_t n,
+hipError_t launch_lanczos_update(float* w, const float* q, BasisRows<B> rows, int nv, LanczosDev st, int k, int64_t n,
                                  hipStream_t s) {
   if (nv < 0 || nv > 128) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(lz_update_kernel<B>, dim3(RED_BLOCKS), dim3(NT), 0, s, w, q, (const double*)(st.alpha + k), basis, ldq,
+  hipLaunchKernelGGL(lz_update_kernel<B>, dim3(RED_BLOCKS), dim3(NT), 0, s, w, q, (const double*)(st.alpha + k), rows,
                      (const double*)st.coef, nv, n, st.partial);
   return hipGetLastError();
 }
@@ -596,9 +596,9 @@ hipError_t launch_lanczos_normalise(const float* w, float* qnext, B* basis_row, 
 }
 
 #define INST_LZ(B)                                                                                                   \
-  template hipError_t launch_lanczos_project<B>(const float*, const float*, const B*, int64_t, int, int, LanczosDev, int,   \
+  template hipError_t launch_lanczos_project<B>(const float*, const float*, BasisRows<B>, int, int, LanczosDev, int,      \
                                                 int64_t, hipStream_t);                                                \
-  template hipError_t launch_lanczos_update<B>(float*, const float*, const B*, int64_t, int, LanczosDev, int, int64_t, \
+  template hipError_t launch_lanczos_update<B>(float*, const float*, BasisRows<B>, int, LanczosDev, int, int64_t,    \
                                                hipStream_t);                                                          \
   template hipError_t launch_lanczos_normalise<B, float>(const float*, float*, B*, float*, double, LanczosDev, int, double,   \
                                                          int64_t, hipStream_t);                                              \

@@ -85,6 +85,7 @@ def lib():
         "fdh_bind": (i32, [vp, vp, vp, i32, i32, f64]),
         "fdh_bind_dataset": (i32, [vp, vp, C.POINTER(Batch), i32, f64, i32, C.POINTER(i64)]),
         "fdh_hvp_bound": (i32, [vp, vp, vp]),
+        "fdh_set_basis_offload": (i32, [vp, i32, vp, C.c_size_t]),
         "fdh_lanczos": (i32, [vp, i32, u64, C.POINTER(LanczosOpts), pd, pd, pi]),
         "fdh_slq_density": (i32, [vp, i32, i32, u64, C.POINTER(LanczosOpts), pd, pd, pi, pd]),
         "fdh_block_stats": (i32, [vp, vp, vp, pd]),
@@ -278,6 +279,15 @@ class Model:
             out = torch.empty(self.num_params, dtype=torch.float32, device="cuda")
         self._check(self._L.fdh_hvp_bound(self._h, _ptr(v), _ptr(out)), "fdh_hvp_bound")
         return out
+
+    def set_basis_offload(self, device_rows: int, host_rows=None):
+        """Keep at most device_rows Lanczos rows on the device and the rest in
+        host_rows (a pinned host tensor, e.g. torch.empty(n, dtype=torch.uint8,
+        pin_memory=True)); device_rows < 0 undoes it.  Call before set_workspace."""
+        self._host_rows = host_rows
+        nbytes = 0 if host_rows is None else host_rows.numel() * host_rows.element_size()
+        self._check(self._L.fdh_set_basis_offload(self._h, int(device_rows), _ptr(host_rows), nbytes),
+                    "fdh_set_basis_offload")
 
     def lanczos(self, m: int, probe_seed: int, o: LanczosOpts):
         a = np.zeros(m)

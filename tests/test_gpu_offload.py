@@ -1,0 +1,110 @@
+"""Krylov-basis offload (fdh_set_basis_offload): stored Lanczos rows beyond
+device_rows live in pinned host memory and are read by the same kernels over
+the host link.  The arithmetic is unchanged, so every run must reproduce the
+all-device run bit for bit:
+
+* the diagonal operator (P = 1,000,003, a ragged tail), full
+  reorthogonalisation with fp32 and bf16 bases, 0 and 7 rows on the device;
+  a sliding window of 6 rows with 2 on the device;
+* the 1.3B workload at its bench size, 6 steps with a bf16 basis, 3 of the 6
+  rows on the host (8.2 GB pinned), with both runs timed;
+* the workspace shrinks by the offloaded rows, and a host buffer that is too
+  small is refused before any step runs.
+"""
+import time
+
+import numpy as np
+import pytest
+
+from synth.workloads import WORKLOADS
+from tests.gpu_util import need_gpu, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _pinned(torch, nbytes):
+    return torch.empty(max(nbytes, 1), dtype=torch.uint8, pin_memory=True)
+
+
+def _quad_run(torch, fd, diag, m, o, device_rows=None):
+    P = diag.numel()
+    mod = fd.Model("quad_diag", quad_n=P)
+    host = None
+    if device_rows is not None:
+        cap = m if o.reorth == fd.REORTH["full"] else min(m, o.window)
+        row = (P + 7) // 8 * 8 * (2 if o.basis_dtype == fd.DTYPE["bf16"] else 4)
+        host = _pinned(torch, (cap - device_rows) * row)
+        mod.set_basis_offload(device_rows, host)
+    mod.set_workspace(0, 0, m, o)
+    mod.set_quad_diag(diag)
+    th = torch.zeros(P, dtype=torch.float32, device="cuda")
+    mod.bind(th, None, 1e-3)
+    a, b, s, st = mod.lanczos(m, 7, o)
+    return a, b, s
+
+
+@pytest.mark.parametrize("reorth,window,basis,rows", [
+    ("full", 0, "f32", 0), ("full", 0, "f32", 7), ("full", 0, "bf16", 0), ("full", 0, "bf16", 7),
+    ("window", 6, "bf16", 2),
+])
+def test_offload_reproduces_device_basis_bitwise(reorth, window, basis, rows):
+    torch = need_gpu()
+    from paper_2602_00816_amd import fdhvp as fd
+    P, m = 1_000_003, 24 if reorth == "full" else 20
+    rng = np.random.default_rng(3)
+    diag = torch.from_numpy(rng.uniform(-1.0, 4.0, P).astype(np.float32)).cuda()
+    o = fd.opts(reorth, window, basis)
+    a0, b0, s0 = _quad_run(torch, fd, diag, m, o)
+    a1, b1, s1 = _quad_run(torch, fd, diag, m, o, rows)
+    say(f"offload {reorth}/{basis} rows on device {rows}: steps {s1}, alpha_m {a1[-1]:.9e}")
+    assert s0 == s1 == m
+    assert np.array_equal(a0, a1) and np.array_equal(b0, b1)
+
+
+def test_offload_workspace_and_host_buffer_checks():
+    torch = need_gpu()
+    from paper_2602_00816_amd import fdhvp as fd
+    P, m = 100_003, 10
+    o = fd.opts("full", 0, "f32")
+    mod = fd.Model("quad_diag", quad_n=P)
+    full = mod.workspace_bytes(0, 0, m, o)
+    row = (P + 7) // 8 * 8 * 4
+    small = _pinned(torch, (m - 4) * row - 4)
+    mod.set_basis_offload(4, small)
+    assert full - mod.workspace_bytes(0, 0, m, o) >= (m - 4) * row
+    mod.set_workspace(0, 0, m, o)
+    diag = torch.ones(P, dtype=torch.float32, device="cuda")
+    mod.set_quad_diag(diag)
+    mod.bind(torch.zeros(P, dtype=torch.float32, device="cuda"), None, 1e-3)
+    with pytest.raises(fd.FdhError, match="host"):
+        mod.lanczos(m, 1, o)
+
+
+def test_offload_1_3b_bitwise_and_timed():
+    torch = need_gpu()
+    from paper_2602_00816_amd import fdhvp as fd
+    w = WORKLOADS["llama-1.3b-bf16"]
+    B, S = w["batch"], w["seq"]
+    m, dev_rows = 6, 3
+    o = fd.opts("full", 0, "bf16")
+    out = []
+    for rows in (None, dev_rows):
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        mod = fd.Model.from_workload(w)
+        if rows is not None:
+            P = mod.num_params
+            mod.set_basis_offload(rows, _pinned(torch, (m - rows) * ((P + 7) // 8 * 8) * 2))
+        mod.set_workspace(B, S, m, o)
+        th = mod.init_params(1)
+        tok = mod.make_tokens(B, S, 2, "zipf")
+        mod.bind(th, tok, 1e-3)
+        mod.lanczos(1, 3, o)                       # warm-up
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        a, b, s, st = mod.lanczos(m, 3, o)
+        dt = (time.perf_counter() - t0) / m
+        out.append((a, b, dt))
+        say(f"1.3B lanczos m={m}, rows on device {rows if rows is not None else m}: {dt * 1e3:.1f} ms/step")
+        del mod, th, tok
+    assert np.array_equal(out[0][0], out[1][0]) and np.array_equal(out[0][1], out[1][1])
