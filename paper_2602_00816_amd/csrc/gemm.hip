@@ -105,7 +105,7 @@ __device__ inline void mma_tile<bf16_t>(const bf16_t* sA, const bf16_t* sB, f32x
     for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int j = 0; j < 2; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
   }
 }
 
@@ -125,35 +125,155 @@ __device__ inline void mma_tile<float>(const float* sA, const float* sB, f32x16_
     for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int j = 0; j < 2; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i], bfr[j], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(bfr[j], af[i], acc[i][j], 0, 0, 0);
   }
 }
 
 // shared epilogue: accumulator block (i, j) of a wavefront whose 32x32 block
-// origin is (rb, cb); lane layout of the 32x32 MFMA output
+// origin is (rb, cb).  Every MFMA takes the B fragment as its first operand, so
+// the block holds C^T in the MFMA output layout: lane l owns row rb + (l & 31)
+// of C and, for g = 0..3, the four consecutive columns cb + 8g + 4(l >> 5) + 0..3
+// (accumulator elements 4g..4g+3).  Each such quad is stored, and the residual
+// or previous C loaded, as one vector where the addresses are aligned.
+template <typename T>
+__device__ inline void store_quad(const GemmArgs& a, const float (&x)[4], int64_t idx, bool vec) {
+  if (a.out_type == OUT_F32) {
+    float* C = reinterpret_cast<float*>(a.C);
+    float4 v = make_float4(x[0], x[1], x[2], x[3]);
+    if (vec) {
+      if (a.resid) {
+        const float4 r = *reinterpret_cast<const float4*>(a.resid + idx);
+        v.x += r.x; v.y += r.y; v.z += r.z; v.w += r.w;
+      }
+      if (a.beta != 0.f) {
+        const float4 c = *reinterpret_cast<const float4*>(C + idx);
+        v.x += a.beta * c.x; v.y += a.beta * c.y; v.z += a.beta * c.z; v.w += a.beta * c.w;
+      }
+      *reinterpret_cast<float4*>(C + idx) = v;
+    }
+  } else if (vec) {
+    T* C = reinterpret_cast<T*>(a.C);
+    if constexpr (sizeof(T) == 2) {
+      uint2 u;
+      u.x = (uint32_t)f32_to_bf16(x[0]) | ((uint32_t)f32_to_bf16(x[1]) << 16);
+      u.y = (uint32_t)f32_to_bf16(x[2]) | ((uint32_t)f32_to_bf16(x[3]) << 16);
+      *reinterpret_cast<uint2*>(C + idx) = u;
+    } else {
+      *reinterpret_cast<float4*>(C + idx) = make_float4(x[0], x[1], x[2], x[3]);
+    }
+  }
+}
+
 template <typename T>
 __device__ inline void store_block(const GemmArgs& a, const f32x16_t& acc, int64_t coff, int rb, int cb, int lane) {
-  const int col = cb + (lane & 31);
-  if (col >= a.N) return;
-  float badd = 0.f;
-  if (a.bias_theta) badd += a.bias_theta_scale * ldf(reinterpret_cast<const T*>(a.bias_theta), col);
-  if (a.bias_v) badd += a.bias_v_scale * a.bias_v[col];
+  const int row = rb + (lane & 31);
+  if (row >= a.M) return;
+  const int64_t rbase = coff + (int64_t)row * a.ldc;
+  // vector path: row starts and column quads aligned for 16-byte (fp32) or
+  // 8-byte (bf16) accesses
+  const size_t ob = a.out_type == OUT_F32 ? 4 : sizeof(T);
+  const bool aligned = a.ldc % 4 == 0 && coff % 4 == 0 && (uintptr_t)a.C % (4 * ob) == 0 &&
+                       (!a.resid || (uintptr_t)a.resid % 16 == 0);
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int row = rb + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-    if (row < a.M) {
-      const int64_t idx = coff + (int64_t)row * a.ldc + col;
-      float x = a.alpha * acc[r] + badd;
-      if (a.out_type == OUT_F32) {
-        float* C = reinterpret_cast<float*>(a.C);
-        if (a.resid) x += a.resid[idx];
-        if (a.beta != 0.f) x += a.beta * C[idx];
-        C[idx] = x;
-      } else {
-        stf(reinterpret_cast<T*>(a.C), idx, x);
+  for (int g = 0; g < 4; ++g) {
+    const int col0 = cb + 8 * g + 4 * (lane >> 5);
+    if (col0 >= a.N) continue;
+    float x[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int col = min(col0 + r, a.N - 1);
+      float badd = 0.f;
+      if (a.bias_theta) badd += a.bias_theta_scale * ldf(reinterpret_cast<const T*>(a.bias_theta), col);
+      if (a.bias_v) badd += a.bias_v_scale * a.bias_v[col];
+      x[r] = a.alpha * acc[4 * g + r] + badd;
+    }
+    if (aligned && col0 + 3 < a.N) {
+      store_quad<T>(a, x, rbase + col0, true);
+    } else {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        if (col0 + r >= a.N) break;
+        const int64_t idx = rbase + col0 + r;
+        float y = x[r];
+        if (a.out_type == OUT_F32) {
+          float* C = reinterpret_cast<float*>(a.C);
+          if (a.resid) y += a.resid[idx];
+          if (a.beta != 0.f) y += a.beta * C[idx];
+          C[idx] = y;
+        } else {
+          stf(reinterpret_cast<T*>(a.C), idx, y);
+        }
       }
     }
   }
+}
+
+// LDS-staged epilogue of one 32x32 block: the wavefront writes its block
+// (scaled by alpha) to its own staging area of 32 rows x 36 floats, then reads
+// it back so that lane l holds row 8k + (l >> 3), columns 4(l & 7) + 0..3:
+// every global access then covers eight rows of 128 contiguous bytes.  The
+// caller guarantees the staging area is not in use by the main loop any more.
+constexpr int STG_LD = 36;
+constexpr int STG_FLOATS = 32 * STG_LD;
+// four staging areas fit one ring stage of the DMA kernels (256 x 32 + 128 x 32 bf16 at the smallest)
+static_assert(4 * STG_FLOATS * 4 <= (256 + 128) * 32 * 2, "staging areas exceed a ring stage");
+
+__device__ inline void wave_lds_order() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+template <typename T>
+__device__ inline void store_block_lds(const GemmArgs& a, const f32x16_t& acc, int64_t coff, int rb, int cb, int lane,
+                                       float* stg) {
+  {
+    const int wr = lane & 31, wh = lane >> 5;
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+      *reinterpret_cast<float4*>(stg + wr * STG_LD + 8 * g + 4 * wh) =
+          make_float4(a.alpha * acc[4 * g], a.alpha * acc[4 * g + 1], a.alpha * acc[4 * g + 2], a.alpha * acc[4 * g + 3]);
+  }
+  wave_lds_order();
+  const int c4 = 4 * (lane & 7);
+  const int col0 = cb + c4;
+  float badd[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int col = min(col0 + r, a.N - 1);
+    if (a.bias_theta) badd[r] += a.bias_theta_scale * ldf(reinterpret_cast<const T*>(a.bias_theta), col);
+    if (a.bias_v) badd[r] += a.bias_v_scale * a.bias_v[col];
+  }
+  const size_t ob = a.out_type == OUT_F32 ? 4 : sizeof(T);
+  const bool aligned = a.ldc % 4 == 0 && coff % 4 == 0 && (uintptr_t)a.C % (4 * ob) == 0 &&
+                       (!a.resid || (uintptr_t)a.resid % 16 == 0);
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int lr = 8 * k + (lane >> 3);
+    const float4 v = *reinterpret_cast<const float4*>(stg + lr * STG_LD + c4);
+    const int row = rb + lr;
+    if (row >= a.M || col0 >= a.N) continue;
+    const float x[4] = {v.x + badd[0], v.y + badd[1], v.z + badd[2], v.w + badd[3]};
+    const int64_t base = coff + (int64_t)row * a.ldc + col0;
+    if (aligned && col0 + 3 < a.N) {
+      store_quad<T>(a, x, base, true);
+    } else {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        if (col0 + r >= a.N) break;
+        float y = x[r];
+        if (a.out_type == OUT_F32) {
+          float* C = reinterpret_cast<float*>(a.C);
+          if (a.resid) y += a.resid[base + r];
+          if (a.beta != 0.f) y += a.beta * C[base + r];
+          C[base + r] = y;
+        } else {
+          stf(reinterpret_cast<T*>(a.C), base + r, y);
+        }
+      }
+    }
+  }
+  wave_lds_order();   // the next block's writes come after these reads
 }
 
 template <typename T, bool AK, bool BKM>
@@ -389,7 +509,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_bf16_big(GemmArgs a) {
       for (int i = 0; i < IM; ++i)
 #pragma clang loop unroll(full)
         for (int j = 0; j < JN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
     }
     if (t + 1 < total) {
       la.store(sA[cur ^ 1], tid);
@@ -594,7 +714,7 @@ __global__ __launch_bounds__(64 * 2 * WN) void gemm_bf16_dma(GemmArgs a) {
       for (int i = 0; i < IM; ++i)
 #pragma clang loop unroll(full)
         for (int j = 0; j < JN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
     }
   };
 
@@ -609,11 +729,16 @@ __global__ __launch_bounds__(64 * 2 * WN) void gemm_bf16_dma(GemmArgs a) {
   }
 
   const int64_t coff = batch_off(z, a.inner_count, a.c_outer, a.c_inner, a.c_div);
+  // stage the output through the ring once every wavefront is done with it
+  wait_vm<0>();
+  __syncthreads();
+  const int wv = threadIdx.x >> 6;
+  float* stg = reinterpret_cast<float*>(wv < 4 ? st0 : st1) + (wv & 3) * STG_FLOATS;
 #pragma clang loop unroll(full)
   for (int i = 0; i < IM; ++i)
 #pragma clang loop unroll(full)
     for (int j = 0; j < JN; ++j)
-      store_block<bf16_t>(a, acc[i][j], coff, m0 + wm * 128 + i * 32, n0 + wn * WTN + j * 32, lane);
+      store_block_lds<bf16_t>(a, acc[i][j], coff, m0 + wm * 128 + i * 32, n0 + wn * WTN + j * 32, lane, stg);
 }
 
 // ===========================================================================
@@ -736,7 +861,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4(GemmArgs a) {
   };
   auto mma = [&](const bf16x8_t (&f)[IM + JN], int e) {
     const int i = e / JN, j = e % JN;
-    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[i], f[IM + j], acc[i][j], 0, 0, 0);
+    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[IM + j], f[i], acc[i][j], 0, 0, 0);
   };
 
   auto step = [&](auto s, int t) {
@@ -790,11 +915,14 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4(GemmArgs a) {
   }
 
   const int64_t coff = batch_off(z, a.inner_count, a.c_outer, a.c_inner, a.c_div);
+  // stage the output through the ring once every wavefront is done with it
+  __syncthreads();
+  float* stg = reinterpret_cast<float*>(st0) + (threadIdx.x >> 6) * STG_FLOATS;
 #pragma clang loop unroll(full)
   for (int i = 0; i < IM; ++i)
 #pragma clang loop unroll(full)
     for (int j = 0; j < JN; ++j)
-      store_block<bf16_t>(a, acc[i][j], coff, m0 + wm * 128 + i * 32, n0 + wn * 128 + j * 32, lane);
+      store_block_lds<bf16_t>(a, acc[i][j], coff, m0 + wm * 128 + i * 32, n0 + wn * 128 + j * 32, lane, stg);
 }
 
 // ===========================================================================
@@ -923,7 +1051,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4k64(GemmArgs a) {
   };
   auto mma = [&](const bf16x8_t (&f)[IM + JN], int e) {
     const int i = e / JN, j = e % JN;
-    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[i], f[IM + j], acc[i][j], 0, 0, 0);
+    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[IM + j], f[i], acc[i][j], 0, 0, 0);
   };
   // one half slice: MFMAs on `use`, fragments of the next half slice into `load`
   auto half = [&](const bf16x8_t (&use)[IM + JN], bf16x8_t (&load)[IM + JN], const bf16_t* st, int kk) {
