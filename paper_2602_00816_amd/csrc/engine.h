@@ -127,7 +127,7 @@ class Engine {
     Span x_in_m, x_in_d, a_m, a_d, qkv_m, qkv_d, P_m, P_d, st, o_m, o_d, xmid_m, xmid_d, b_m, b_d, u_m, u_d, z_m, z_d;
   };
   std::vector<LayerSpans> ls;
-  Span xL_m, xL_d, f_m, f_d, lo, qkvf_m, qkvf_d, sc_m, sc_d, log_m, log_d, dlog_m, dlog_d, rowloss, losses;
+  Span xL_m, xL_d, f_m, f_d, lo, sc_m, sc_d, log_m, log_d, dlog_m, dlog_d, rowloss, losses;
   Span dx0_m, dx0_d, dx1_m, dx1_d, dxo_m, dxo_d, dz_m, dz_d, dgu_m, dgu_d, dudf, db_m, db_d, gpart, do_m, do_d, dS_m, dS_d;
   Span dqkv_m, dqkv_d, dqkvo_m, dqkvo_d, gqa_m, gqa_d, dl, da_m, da_d, colpart, keys, rope, cdf, gpartial, bpart, bout;
   Span tcount;  // two int64 counters of fdh_bind_dataset

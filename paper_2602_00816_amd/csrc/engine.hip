@@ -165,13 +165,12 @@ size_t Engine::plan(int B, int S, int m, const fdh_lanczos_opts* o, bool carve) 
       take(s.o_m, ta * ob); take(s.o_d, ta * ob);
       take(s.xmid_m, td * 4); take(s.xmid_d, td * 4);
       take(s.b_m, td * ob); take(s.b_d, td * ob);
-      take(s.u_m, tu * 4); take(s.u_d, tu * 4);
+      take(s.u_m, tu * ob); take(s.u_d, tu * ob);
       take(s.z_m, tz * ob); take(s.z_d, tz * ob);
     }
     take(xL_m, td * 4); take(xL_d, td * 4);
     take(f_m, td * ob); take(f_d, td * ob);
     take(lo, (size_t)P * ob);
-    take(qkvf_m, tq * 4); take(qkvf_d, tq * 4);
     take(sc_m, pp * 4); take(sc_d, pp * 4);
     take(log_m, T_ * V * 4); take(log_d, T_ * V * 4);
     take(dlog_m, T_ * V * ob); take(dlog_d, T_ * V * ob);
@@ -381,13 +380,16 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, c
   if (llama) CK(launch_rope_table((double*)(ws + rope.off), S, dh, (double)cfg.rope_base, st));
 
   // ---- linear helpers ----
-  auto lin_fwd = [&](const T* Xm, const T* Xd, int K, const ParamRef& W, const ParamRef& bias, float* Ym, float* Yd,
-                     const float* Rm, const float* Rd, int N) -> int {
+  // Y = X W^T (+ bias) (+ residual R, fp32 output only) at both points; out:
+  // fp32 (residual stream, logits) or the operand type (q/k/v and the MLP
+  // input product, which only feed operand-type consumers)
+  auto lin_fwd = [&](const T* Xm, const T* Xd, int K, const ParamRef& W, const ParamRef& bias, void* Ym, void* Yd,
+                     const float* Rm, const float* Rd, int N, int out) -> int {
     GemmArgs g;
     g.M = T_; g.N = N; g.K = K;
     g.A[0] = kmaj(Xm, K);
     g.B[0] = kmaj(th + W.off, K);
-    g.C = Ym; g.ldc = N;
+    g.C = Ym; g.ldc = N; g.out_type = out;
     g.resid = Rm;
     if (bias.valid()) g.bias_theta = th + bias.off;
     RG(T, g);
@@ -395,7 +397,7 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, c
     h.M = T_; h.N = N; h.K = K; h.npairs = 2;
     h.A[0] = kmaj(Xd, K); h.B[0] = kmaj(th + W.off, K);
     h.A[1] = kmaj(Xm, K); h.B[1] = kmaj(lo + W.off, K);
-    h.C = Yd; h.ldc = N;
+    h.C = Yd; h.ldc = N; h.out_type = out;
     h.resid = Rd;
     if (bias.valid()) { h.bias_v = v + bias.off; h.bias_v_scale = feps; }
     RG(T, h);
@@ -509,9 +511,9 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, c
     CK(launch_norm_fwd<T>(PairT<T>{OP(s.a_m), OP(s.a_d)}, xm, xd, T_, d, ln, th + R.n1g.off, v + R.n1g.off,
                           ln ? th + R.n1b.off : nullptr, ln ? v + R.n1b.off : nullptr, eps, neps, st));
     // qkv projection
-    RC(lin_fwd(OP(s.a_m), OP(s.a_d), d, R.wqkv, R.bqkv, F32(qkvf_m), F32(qkvf_d), nullptr, nullptr, qkvd));
-    CK(launch_qkv_post<T>(PairT<T>{OP(s.qkv_m), OP(s.qkv_d)}, F32(qkvf_m), F32(qkvf_d), T_, S, Hq, Hk, dh,
-                          (const double*)(ws + rope.off), llama, st));
+    RC(lin_fwd(OP(s.a_m), OP(s.a_d), d, R.wqkv, R.bqkv, OP(s.qkv_m), OP(s.qkv_d), nullptr, nullptr, qkvd, OUT_OP));
+    if (llama)
+      CK(launch_rope_inplace<T>(PairT<T>{OP(s.qkv_m), OP(s.qkv_d)}, T_, S, Hq, Hk, dh, (const double*)(ws + rope.off), st));
     if (fused) {
       if constexpr (std::is_same<T, bf16_t>::value) {
         FlashArgs fa = flash_args(OP(s.qkv_m), OP(s.qkv_d), att_scale);
@@ -569,23 +571,23 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, c
       }
     }
     // output projection + residual
-    RC(lin_fwd(OP(s.o_m), OP(s.o_d), Hq * dh, R.wo, R.bo, F32(s.xmid_m), F32(s.xmid_d), xm, xd, d));
+    RC(lin_fwd(OP(s.o_m), OP(s.o_d), Hq * dh, R.wo, R.bo, F32(s.xmid_m), F32(s.xmid_d), xm, xd, d, OUT_F32));
     // norm 2
     CK(launch_norm_fwd<T>(PairT<T>{OP(s.b_m), OP(s.b_d)}, F32(s.xmid_m), F32(s.xmid_d), T_, d, ln, th + R.n2g.off,
                           v + R.n2g.off, ln ? th + R.n2b.off : nullptr, ln ? v + R.n2b.off : nullptr, eps, neps, st));
     // MLP
     const int nu = gpt2 ? F : 2 * F;
-    RC(lin_fwd(OP(s.b_m), OP(s.b_d), d, R.w1, R.b1, F32(s.u_m), F32(s.u_d), nullptr, nullptr, nu));
-    if (gpt2) CK(launch_gelu_fwd<T>(PairT<T>{OP(s.z_m), OP(s.z_d)}, F32(s.u_m), F32(s.u_d), (int64_t)T_ * F, st));
-    else CK(launch_swiglu_fwd<T>(PairT<T>{OP(s.z_m), OP(s.z_d)}, F32(s.u_m), F32(s.u_d), T_, F, st));
+    RC(lin_fwd(OP(s.b_m), OP(s.b_d), d, R.w1, R.b1, OP(s.u_m), OP(s.u_d), nullptr, nullptr, nu, OUT_OP));
+    if (gpt2) CK(launch_gelu_fwd<T>(PairT<T>{OP(s.z_m), OP(s.z_d)}, OP(s.u_m), OP(s.u_d), (int64_t)T_ * F, st));
+    else CK(launch_swiglu_fwd<T>(PairT<T>{OP(s.z_m), OP(s.z_d)}, OP(s.u_m), OP(s.u_d), T_, F, st));
     float* nxm = (l + 1 < L) ? F32(ls[l + 1].x_in_m) : F32(xL_m);
     float* nxd = (l + 1 < L) ? F32(ls[l + 1].x_in_d) : F32(xL_d);
-    RC(lin_fwd(OP(s.z_m), OP(s.z_d), F, R.w2, R.b2, nxm, nxd, F32(s.xmid_m), F32(s.xmid_d), d));
+    RC(lin_fwd(OP(s.z_m), OP(s.z_d), F, R.w2, R.b2, nxm, nxd, F32(s.xmid_m), F32(s.xmid_d), d, OUT_F32));
   }
   // final norm + head + cross-entropy
   CK(launch_norm_fwd<T>(PairT<T>{OP(f_m), OP(f_d)}, F32(xL_m), F32(xL_d), T_, d, ln, th + nfg.off, v + nfg.off,
                         ln ? th + nfb.off : nullptr, ln ? v + nfb.off : nullptr, eps, neps, st));
-  RC(lin_fwd(OP(f_m), OP(f_d), d, head, ParamRef{}, F32(log_m), F32(log_d), nullptr, nullptr, V));
+  RC(lin_fwd(OP(f_m), OP(f_d), d, head, ParamRef{}, F32(log_m), F32(log_d), nullptr, nullptr, V, OUT_F32));
   CK(launch_ce<T>(PairT<T>{OP(dlog_m), OP(dlog_d)}, (double*)(ws + rowloss.off), F32(log_m), F32(log_d), tok, lab, T_,
                   S, V, inv_n, st));
   CK(launch_loss_sum((double*)(ws + losses.off), (const double*)(ws + rowloss.off), T_, acc, st));
@@ -611,11 +613,11 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, c
     RC(lin_dgrad(gom, god, d, R.w2, F, F32(dz_m), F32(dz_d), OUT_F32));
     const int nu = gpt2 ? F : 2 * F;
     if (gpt2) {
-      CK(launch_gelu_bwd<T>(PairT<T>{OP(dgu_m), OP(dgu_d)}, F32(dudf), F32(s.u_m), F32(s.u_d), F32(dz_m), F32(dz_d),
+      CK(launch_gelu_bwd<T>(PairT<T>{OP(dgu_m), OP(dgu_d)}, F32(dudf), OP(s.u_m), OP(s.u_d), F32(dz_m), F32(dz_d),
                             (int64_t)T_ * F, st));
       RC(colsum_hv(F32(dudf), F, F, R.b1));
     } else {
-      CK(launch_swiglu_bwd<T>(PairT<T>{OP(dgu_m), OP(dgu_d)}, F32(s.u_m), F32(s.u_d), F32(dz_m), F32(dz_d), T_, F, st));
+      CK(launch_swiglu_bwd<T>(PairT<T>{OP(dgu_m), OP(dgu_d)}, OP(s.u_m), OP(s.u_d), F32(dz_m), F32(dz_d), T_, F, st));
     }
     RC(lin_wgrad(OP(dgu_m), OP(dgu_d), nu, OP(s.b_m), OP(s.b_d), d, R.w1));
     RC(lin_dgrad(OP(dgu_m), OP(dgu_d), nu, R.w1, d, F32(db_m), F32(db_d), OUT_F32));

@@ -138,10 +138,10 @@ hipError_t launch_colsum(float* out, const float* X, int rows, int C, int64_t ld
 hipError_t launch_colsum_f64(float* out, const double* X, int rows, int C, double scale, bool accumulate, double* partial,
                              hipStream_t s);
 
-// RoPE (Llama) or plain cast (GPT-2) of q,k,v columns into operand type
+// RoPE (Llama) of the q and k columns, in place on both channels of the
+// operand-type projection output [T, (Hq + 2 Hk) dh]; v is left as it is
 template <typename T>
-hipError_t launch_qkv_post(PairT<T> out, const float* qm, const float* qd, int T_, int S, int Hq, int Hk, int dh,
-                           const double* rope_cs, bool rope, hipStream_t s);
+hipError_t launch_rope_inplace(PairT<T> qkv, int T_, int S, int Hq, int Hk, int dh, const double* cs, hipStream_t s);
 // backward RoPE on dq/dk columns (fp32, in place) + cast of dq,dk,dv into operand type
 template <typename T>
 hipError_t launch_qkv_bwd_post(PairT<T> out, float* gm, float* gd, int T_, int S, int Hq, int Hk, int dh,
@@ -188,14 +188,14 @@ hipError_t launch_flash_bwd(const FlashArgs& a, int B, hipStream_t s);
 
 // activations at both points
 template <typename T>
-hipError_t launch_gelu_fwd(PairT<T> z, const float* um, const float* ud, int64_t n, hipStream_t s);
+hipError_t launch_gelu_fwd(PairT<T> z, const T* um, const T* ud, int64_t n, hipStream_t s);
 template <typename T>
-hipError_t launch_gelu_bwd(PairT<T> du, float* dud_f32, const float* um, const float* ud, const float* dzm, const float* dzd,
+hipError_t launch_gelu_bwd(PairT<T> du, float* dud_f32, const T* um, const T* ud, const float* dzm, const float* dzd,
                            int64_t n, hipStream_t s);
 template <typename T>
-hipError_t launch_swiglu_fwd(PairT<T> z, const float* gum, const float* gud, int rows, int F, hipStream_t s);
+hipError_t launch_swiglu_fwd(PairT<T> z, const T* gum, const T* gud, int rows, int F, hipStream_t s);
 template <typename T>
-hipError_t launch_swiglu_bwd(PairT<T> dgu, const float* gum, const float* gud, const float* dzm, const float* dzd,
+hipError_t launch_swiglu_bwd(PairT<T> dgu, const T* gum, const T* gud, const float* dzm, const float* dzd,
                              int rows, int F, hipStream_t s);
 
 // cross-entropy at both points: dlogits (operand type) and per-row losses (fp64, [2][T]),

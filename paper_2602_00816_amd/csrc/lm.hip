@@ -458,14 +458,14 @@ __global__ void rope_table_kernel(double* cs, int S, int dh, double base) {
 // of the first half of a q or k head together with their rotate-half
 // partners f0+dh/2.., reads each once and writes both rotated quadruples
 // (packed); v columns (and q/k without RoPE) are cast 4 at a time.
-template <typename T>
-__global__ void qkv_rope_kernel(PairT<T> out, const float* inm, const float* ind, int S, int ncols, int nqk, int dh,
-                                const double* cs, bool rope, bool inverse) {
+template <typename T, typename TI>
+__global__ void qkv_rope_kernel(PairT<T> out, const TI* inm, const TI* ind, int S, int ncols, int nqk, int dh,
+                                const double* cs, bool rope, bool inverse, bool copy_v) {
   const int t = blockIdx.y;
   const int u = blockIdx.x * blockDim.x + threadIdx.x;
   const int half = dh / 2, qpu = half / 4;      // units per q/k head
   const int qu = rope ? nqk * qpu : 0;          // rotated units
-  const int vu = (ncols - (rope ? nqk * dh : 0)) / 4;
+  const int vu = copy_v ? (ncols - (rope ? nqk * dh : 0)) / 4 : 0;
   const int64_t o = (int64_t)t * ncols;
   if (u < qu) {
     const int head = u / qpu, f0 = 4 * (u % qpu);
@@ -477,12 +477,13 @@ __global__ void qkv_rope_kernel(PairT<T> out, const float* inm, const float* ind
       co[e] = row[2 * (f0 + e)];
       si[e] = inverse ? -row[2 * (f0 + e) + 1] : row[2 * (f0 + e) + 1];
     }
-    const float* ins[2] = {inm, ind};
+    const TI* ins[2] = {inm, ind};
     T* outs[2] = {out.m, out.d};
 #pragma unroll
     for (int ch = 0; ch < 2; ++ch) {
-      const float4 x = *reinterpret_cast<const float4*>(ins[ch] + o + c);
-      const float4 y = *reinterpret_cast<const float4*>(ins[ch] + o + c + half);
+      // (in place when ins == outs: this thread alone reads and writes these 8 elements)
+      const float4 x = ld4f(ins[ch], o + c);
+      const float4 y = ld4f(ins[ch], o + c + half);
       float lo[4], hi[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -495,7 +496,7 @@ __global__ void qkv_rope_kernel(PairT<T> out, const float* inm, const float* ind
     }
   } else if (u < qu + vu) {
     const int c = (rope ? nqk * dh : 0) + 4 * (u - qu);
-    const float4 a = *reinterpret_cast<const float4*>(inm + o + c), b = *reinterpret_cast<const float4*>(ind + o + c);
+    const float4 a = ld4f(inm, o + c), b = ld4f(ind, o + c);
     st4f(out.m, o + c, a.x, a.y, a.z, a.w);
     st4f(out.d, o + c, b.x, b.y, b.z, b.w);
   }
@@ -703,17 +704,19 @@ __device__ inline double gelu_t_grad(double u) {
 __device__ inline double sigm(double x) { return 1.0 / (1.0 + exp(-x)); }
 
 template <typename T>
-__global__ void gelu_fwd_kernel(PairT<T> z, const float* um, const float* ud, int64_t n) {
+__global__ void gelu_fwd_kernel(PairT<T> z, const T* um, const T* ud, int64_t n) {
   GRID_LOOP(i, n) {
-    const double up = (double)um[i] + (double)ud[i], un = (double)um[i] - (double)ud[i];
+    const double a = ldf(um, i), b = ldf(ud, i);
+    const double up = a + b, un = a - b;
     put_pair(z, i, gelu_t(up), gelu_t(un));
   }
 }
 template <typename T>
-__global__ void gelu_bwd_kernel(PairT<T> du, float* dudf, const float* um, const float* ud, const float* dzm,
+__global__ void gelu_bwd_kernel(PairT<T> du, float* dudf, const T* um, const T* ud, const float* dzm,
                                 const float* dzd, int64_t n) {
   GRID_LOOP(i, n) {
-    const double up = (double)um[i] + (double)ud[i], un = (double)um[i] - (double)ud[i];
+    const double a = ldf(um, i), b = ldf(ud, i);
+    const double up = a + b, un = a - b;
     const double gp = ((double)dzm[i] + (double)dzd[i]) * gelu_t_grad(up);
     const double gn = ((double)dzm[i] - (double)dzd[i]) * gelu_t_grad(un);
     put_pair(du, i, gp, gn);
@@ -723,13 +726,13 @@ __global__ void gelu_bwd_kernel(PairT<T> du, float* dudf, const float* um, const
 // Vectorised forms: grid.y = row, each thread 4 consecutive columns of the
 // F gate (and F up) columns; F % 4 == 0.  Same arithmetic as the scalar forms.
 template <typename T>
-__global__ void swiglu_fwd4_kernel(PairT<T> z, const float* gum, const float* gud, int F) {
+__global__ void swiglu_fwd4_kernel(PairT<T> z, const T* gum, const T* gud, int F) {
   const int c = 4 * (blockIdx.x * blockDim.x + threadIdx.x);
   if (c >= F) return;
   const int64_t t = blockIdx.y;
   const int64_t ig = t * 2 * F + c, iu = ig + F, io = t * F + c;
-  const float4 gm = *reinterpret_cast<const float4*>(gum + ig), gd = *reinterpret_cast<const float4*>(gud + ig);
-  const float4 um = *reinterpret_cast<const float4*>(gum + iu), ud = *reinterpret_cast<const float4*>(gud + iu);
+  const float4 gm = ld4f(gum, ig), gd = ld4f(gud, ig);
+  const float4 um = ld4f(gum, iu), ud = ld4f(gud, iu);
   float om[4], od[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
@@ -743,14 +746,14 @@ __global__ void swiglu_fwd4_kernel(PairT<T> z, const float* gum, const float* gu
   st4f(z.d, io, od[0], od[1], od[2], od[3]);
 }
 template <typename T>
-__global__ void swiglu_bwd4_kernel(PairT<T> dgu, const float* gum, const float* gud, const float* dzm, const float* dzd,
+__global__ void swiglu_bwd4_kernel(PairT<T> dgu, const T* gum, const T* gud, const float* dzm, const float* dzd,
                                    int F) {
   const int c = 4 * (blockIdx.x * blockDim.x + threadIdx.x);
   if (c >= F) return;
   const int64_t t = blockIdx.y;
   const int64_t ig = t * 2 * F + c, iu = ig + F, io = t * F + c;
-  const float4 gm = *reinterpret_cast<const float4*>(gum + ig), gd = *reinterpret_cast<const float4*>(gud + ig);
-  const float4 um = *reinterpret_cast<const float4*>(gum + iu), ud = *reinterpret_cast<const float4*>(gud + iu);
+  const float4 gm = ld4f(gum, ig), gd = ld4f(gud, ig);
+  const float4 um = ld4f(gum, iu), ud = ld4f(gud, iu);
   const float4 zm = *reinterpret_cast<const float4*>(dzm + io), zd = *reinterpret_cast<const float4*>(dzd + io);
   float am[4], ad[4], bm[4], bd[4];
 #pragma unroll
@@ -773,25 +776,25 @@ __global__ void swiglu_bwd4_kernel(PairT<T> dgu, const float* gum, const float* 
 }
 
 template <typename T>
-__global__ void swiglu_fwd_kernel(PairT<T> z, const float* gum, const float* gud, int rows, int F) {
+__global__ void swiglu_fwd_kernel(PairT<T> z, const T* gum, const T* gud, int rows, int F) {
   const int64_t n = (int64_t)rows * F;
   GRID_LOOP(i, n) {
     const int64_t t = i / F, c = i % F;
     const int64_t ig = t * 2 * F + c, iu = ig + F;
-    const double gp = (double)gum[ig] + (double)gud[ig], gn = (double)gum[ig] - (double)gud[ig];
-    const double vp = (double)gum[iu] + (double)gud[iu], vn = (double)gum[iu] - (double)gud[iu];
+    const double gp = (double)ldf(gum, ig) + (double)ldf(gud, ig), gn = (double)ldf(gum, ig) - (double)ldf(gud, ig);
+    const double vp = (double)ldf(gum, iu) + (double)ldf(gud, iu), vn = (double)ldf(gum, iu) - (double)ldf(gud, iu);
     put_pair(z, i, gp * sigm(gp) * vp, gn * sigm(gn) * vn);
   }
 }
 template <typename T>
-__global__ void swiglu_bwd_kernel(PairT<T> dgu, const float* gum, const float* gud, const float* dzm, const float* dzd,
+__global__ void swiglu_bwd_kernel(PairT<T> dgu, const T* gum, const T* gud, const float* dzm, const float* dzd,
                                   int rows, int F) {
   const int64_t n = (int64_t)rows * F;
   GRID_LOOP(i, n) {
     const int64_t t = i / F, c = i % F;
     const int64_t ig = t * 2 * F + c, iu = ig + F;
-    const double gp = (double)gum[ig] + (double)gud[ig], gn = (double)gum[ig] - (double)gud[ig];
-    const double vp = (double)gum[iu] + (double)gud[iu], vn = (double)gum[iu] - (double)gud[iu];
+    const double gp = (double)ldf(gum, ig) + (double)ldf(gud, ig), gn = (double)ldf(gum, ig) - (double)ldf(gud, ig);
+    const double vp = (double)ldf(gum, iu) + (double)ldf(gud, iu), vn = (double)ldf(gum, iu) - (double)ldf(gud, iu);
     const double zp = (double)dzm[i] + (double)dzd[i], zn = (double)dzm[i] - (double)dzd[i];
     const double sp = sigm(gp), sn = sigm(gn);
     put_pair(dgu, ig, zp * vp * sp * (1.0 + gp * (1.0 - sp)), zn * vn * sn * (1.0 + gn * (1.0 - sn)));
@@ -1019,12 +1022,12 @@ hipError_t launch_rope_table(double* cs, int S, int dh, double base, hipStream_t
 }
 
 template <typename T>
-hipError_t launch_qkv_post(PairT<T> out, const float* qm, const float* qd, int T_, int S, int Hq, int Hk, int dh,
-                           const double* cs, bool rope, hipStream_t s) {
+hipError_t launch_rope_inplace(PairT<T> qkv, int T_, int S, int Hq, int Hk, int dh, const double* cs, hipStream_t s) {
   const int ncols = (Hq + 2 * Hk) * dh;
-  const int units = (rope ? (Hq + Hk) * dh / 8 : 0) + (ncols - (rope ? (Hq + Hk) * dh : 0)) / 4;
+  const int units = (Hq + Hk) * dh / 8;
   const dim3 g(ceil_div(units, NT), T_);
-  hipLaunchKernelGGL(qkv_rope_kernel<T>, g, dim3(NT), 0, s, out, qm, qd, S, ncols, Hq + Hk, dh, cs, rope, false);
+  hipLaunchKernelGGL((qkv_rope_kernel<T, T>), g, dim3(NT), 0, s, qkv, (const T*)qkv.m, (const T*)qkv.d, S, ncols, Hq + Hk, dh,
+                     cs, true, false, false);
   return hipGetLastError();
 }
 
@@ -1034,8 +1037,8 @@ hipError_t launch_qkv_bwd_post(PairT<T> out, float* gm, float* gd, int T_, int S
   const int ncols = (Hq + 2 * Hk) * dh;
   const int units = (rope ? (Hq + Hk) * dh / 8 : 0) + (ncols - (rope ? (Hq + Hk) * dh : 0)) / 4;
   const dim3 g(ceil_div(units, NT), T_);
-  hipLaunchKernelGGL(qkv_rope_kernel<T>, g, dim3(NT), 0, s, out, (const float*)gm, (const float*)gd, S, ncols, Hq + Hk, dh,
-                     cs, rope, true);
+  hipLaunchKernelGGL((qkv_rope_kernel<T, float>), g, dim3(NT), 0, s, out, (const float*)gm, (const float*)gd, S, ncols,
+                     Hq + Hk, dh, cs, rope, true, true);
   return hipGetLastError();
 }
 
@@ -1068,18 +1071,18 @@ hipError_t launch_group_sum(float* out, int64_t out_ld, const float* in, int T_,
 }
 
 template <typename T>
-hipError_t launch_gelu_fwd(PairT<T> z, const float* um, const float* ud, int64_t n, hipStream_t s) {
+hipError_t launch_gelu_fwd(PairT<T> z, const T* um, const T* ud, int64_t n, hipStream_t s) {
   hipLaunchKernelGGL(gelu_fwd_kernel<T>, dim3(grid_for(n)), dim3(NT), 0, s, z, um, ud, n);
   return hipGetLastError();
 }
 template <typename T>
-hipError_t launch_gelu_bwd(PairT<T> du, float* dudf, const float* um, const float* ud, const float* dzm, const float* dzd,
+hipError_t launch_gelu_bwd(PairT<T> du, float* dudf, const T* um, const T* ud, const float* dzm, const float* dzd,
                            int64_t n, hipStream_t s) {
   hipLaunchKernelGGL(gelu_bwd_kernel<T>, dim3(grid_for(n)), dim3(NT), 0, s, du, dudf, um, ud, dzm, dzd, n);
   return hipGetLastError();
 }
 template <typename T>
-hipError_t launch_swiglu_fwd(PairT<T> z, const float* gum, const float* gud, int rows, int F, hipStream_t s) {
+hipError_t launch_swiglu_fwd(PairT<T> z, const T* gum, const T* gud, int rows, int F, hipStream_t s) {
   if (F % 4 == 0 && rows <= 65535)
     hipLaunchKernelGGL(swiglu_fwd4_kernel<T>, dim3(ceil_div(F / 4, NT), rows), dim3(NT), 0, s, z, gum, gud, F);
   else
@@ -1087,7 +1090,7 @@ hipError_t launch_swiglu_fwd(PairT<T> z, const float* gum, const float* gud, int
   return hipGetLastError();
 }
 template <typename T>
-hipError_t launch_swiglu_bwd(PairT<T> dgu, const float* gum, const float* gud, const float* dzm, const float* dzd, int rows,
+hipError_t launch_swiglu_bwd(PairT<T> dgu, const T* gum, const T* gud, const float* dzm, const float* dzd, int rows,
                              int F, hipStream_t s) {
   if (F % 4 == 0 && rows <= 65535)
     hipLaunchKernelGGL(swiglu_bwd4_kernel<T>, dim3(ceil_div(F / 4, NT), rows), dim3(NT), 0, s, dgu, gum, gud, dzm, dzd, F);
@@ -1137,18 +1140,17 @@ hipError_t launch_pos_bwd(float* hv, const float* dxd, int B, int S, int dm, dou
   template hipError_t launch_norm_bwd<T>(PairF, PairT<T>, const float*, const float*, const float*, const float*,      \
                                          const float*, const float*, int, int, bool, const T*, const float*, double,    \
                                          float, double*, double*, hipStream_t);                                        \
-  template hipError_t launch_qkv_post<T>(PairT<T>, const float*, const float*, int, int, int, int, int, const double*, \
-                                         bool, hipStream_t);                                                           \
+  template hipError_t launch_rope_inplace<T>(PairT<T>, int, int, int, int, int, const double*, hipStream_t);          \
   template hipError_t launch_qkv_bwd_post<T>(PairT<T>, float*, float*, int, int, int, int, int, const double*, bool,   \
                                              hipStream_t);                                                             \
   template hipError_t launch_attn_softmax<T>(PairT<T>, const float*, const float*, int, int, hipStream_t);             \
   template hipError_t launch_attn_dsoftmax<T>(PairT<T>, const T*, const T*, const float*, const float*, int, int,      \
                                               hipStream_t);                                                            \
-  template hipError_t launch_gelu_fwd<T>(PairT<T>, const float*, const float*, int64_t, hipStream_t);                  \
-  template hipError_t launch_gelu_bwd<T>(PairT<T>, float*, const float*, const float*, const float*, const float*,     \
+  template hipError_t launch_gelu_fwd<T>(PairT<T>, const T*, const T*, int64_t, hipStream_t);                          \
+  template hipError_t launch_gelu_bwd<T>(PairT<T>, float*, const T*, const T*, const float*, const float*,             \
                                          int64_t, hipStream_t);                                                        \
-  template hipError_t launch_swiglu_fwd<T>(PairT<T>, const float*, const float*, int, int, hipStream_t);               \
-  template hipError_t launch_swiglu_bwd<T>(PairT<T>, const float*, const float*, const float*, const float*, int, int, \
+  template hipError_t launch_swiglu_fwd<T>(PairT<T>, const T*, const T*, int, int, hipStream_t);                       \
+  template hipError_t launch_swiglu_bwd<T>(PairT<T>, const T*, const T*, const float*, const float*, int, int,         \
                                            hipStream_t);                                                               \
   template hipError_t launch_ce<T>(PairT<T>, double*, const float*, const float*, const int32_t*, const int32_t*, int, \
                                    int, int, double, hipStream_t);

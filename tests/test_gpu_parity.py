@@ -58,7 +58,7 @@ def test_hvp_parity_small(name, dtype, std):
         # stress case at 10x the workloads' init scale: the bf16 rounding of the
         # mean-channel GEMM operands moves the point at which H is taken by
         # ~2^-9 relative per layer, amplified by the sharper non-linearities;
-        # measured 8.5e-2 on gfx950.  The 5e-2 bar applies at the workloads'
+        # measured 8e-2 to 1.1e-1 on gfx950.  The 5e-2 bar applies at the workloads'
         # N(0, 0.02) init (measured 3e-3 to 5e-3).
         tol = 1.5e-1
     for v, g in zip(vs, got):
