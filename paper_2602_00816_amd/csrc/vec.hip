@@ -260,11 +260,22 @@ __global__ __launch_bounds__(NT) void lz_update_kernel(float* w, const float* q,
 // mode 2: beta[k] = sqrt(sum); breakdown test against tol * maxabs.
 __global__ void lz_finish_kernel(LanczosDev st, int mode, int k, int nv, int newest, double tol) {
   __shared__ double sp[128];
+  __shared__ double colsum[256];
   const int j = threadIdx.x;
   const int ncol = (mode == 1) ? 2 * nv : 1;
-  double s = 0.0;
-  if (j < ncol)
-    for (int b = 0; b < RED_BLOCKS; ++b) s += st.partial[(int64_t)j * RED_BLOCKS + b];
+  // column sums of the partials in a fixed order: wavefront w takes columns
+  // w, w + 4, ...; lane l adds partials l, l + 64, ..., then a fixed butterfly
+  {
+    const int wv = threadIdx.x >> 6, ln = threadIdx.x & 63;
+    for (int c = wv; c < ncol; c += (int)(blockDim.x >> 6)) {
+      double t = 0.0;
+      for (int b = ln; b < RED_BLOCKS; b += 64) t += st.partial[(int64_t)c * RED_BLOCKS + b];
+      t = wave_sum(t);
+      if (ln == 0) colsum[c] = t;
+    }
+  }
+  __syncthreads();
+  const double s = j < ncol ? colsum[j] : 0.0;
   if (mode == 0) {
     if (j == 0) {
       st.alpha[k] = s;
@@ -406,9 +417,11 @@ __global__ void cg_dir_kernel(float* p, const float* r, const double* sc, T* lo,
 // mode 0: sc[0] = sum.  mode 1: sc[1] = sum, sc[2] = sc[0] / sum (0 unless sum > 0).
 // mode 2: sc[3] = sum, sc[4] = sum / sc[0] (0 if sc[0] == 0), sc[0] = sum.
 __global__ void cg_finish_kernel(double* sc, const double* partial, int mode) {
+  // one wavefront: lane l adds partials l, l + 64, ... in order, then a fixed butterfly
+  double t = 0.0;
+  for (int b = threadIdx.x; b < RED_BLOCKS; b += 64) t += partial[b];
+  const double s = wave_sum(t);
   if (threadIdx.x != 0) return;
-  double s = 0.0;
-  for (int b = 0; b < RED_BLOCKS; ++b) s += partial[b];
   if (mode == 0) {
     sc[0] = s;
   } else if (mode == 1) {
