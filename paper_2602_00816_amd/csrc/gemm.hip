@@ -135,23 +135,23 @@ __device__ inline void mma_tile<float>(const float* sA, const float* sB, f32x16_
 // of C and, for g = 0..3, the four consecutive columns cb + 8g + 4(l >> 5) + 0..3
 // (accumulator elements 4g..4g+3).  Each such quad is stored, and the residual
 // or previous C loaded, as one vector where the addresses are aligned.
+// four consecutive outputs at C[idx..idx+3], 16-byte (fp32) or 8-byte (bf16)
+// aligned: one vector store, with the residual and previous C read as vectors
 template <typename T>
-__device__ inline void store_quad(const GemmArgs& a, const float (&x)[4], int64_t idx, bool vec) {
+__device__ inline void store_quad(const GemmArgs& a, const float (&x)[4], int64_t idx) {
   if (a.out_type == OUT_F32) {
     float* C = reinterpret_cast<float*>(a.C);
     float4 v = make_float4(x[0], x[1], x[2], x[3]);
-    if (vec) {
-      if (a.resid) {
-        const float4 r = *reinterpret_cast<const float4*>(a.resid + idx);
-        v.x += r.x; v.y += r.y; v.z += r.z; v.w += r.w;
-      }
-      if (a.beta != 0.f) {
-        const float4 c = *reinterpret_cast<const float4*>(C + idx);
-        v.x += a.beta * c.x; v.y += a.beta * c.y; v.z += a.beta * c.z; v.w += a.beta * c.w;
-      }
-      *reinterpret_cast<float4*>(C + idx) = v;
+    if (a.resid) {
+      const float4 r = *reinterpret_cast<const float4*>(a.resid + idx);
+      v.x += r.x; v.y += r.y; v.z += r.z; v.w += r.w;
     }
-  } else if (vec) {
+    if (a.beta != 0.f) {
+      const float4 c = *reinterpret_cast<const float4*>(C + idx);
+      v.x += a.beta * c.x; v.y += a.beta * c.y; v.z += a.beta * c.z; v.w += a.beta * c.w;
+    }
+    *reinterpret_cast<float4*>(C + idx) = v;
+  } else {
     T* C = reinterpret_cast<T*>(a.C);
     if constexpr (sizeof(T) == 2) {
       uint2 u;
@@ -188,7 +188,7 @@ __device__ inline void store_block(const GemmArgs& a, const f32x16_t& acc, int64
       x[r] = a.alpha * acc[4 * g + r] + badd;
     }
     if (aligned && col0 + 3 < a.N) {
-      store_quad<T>(a, x, rbase + col0, true);
+      store_quad<T>(a, x, rbase + col0);
     } else {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -256,7 +256,7 @@ __device__ inline void store_block_lds(const GemmArgs& a, const f32x16_t& acc, i
     const float x[4] = {v.x + badd[0], v.y + badd[1], v.z + badd[2], v.w + badd[3]};
     const int64_t base = coff + (int64_t)row * a.ldc + col0;
     if (aligned && col0 + 3 < a.N) {
-      store_quad<T>(a, x, base, true);
+      store_quad<T>(a, x, base);
     } else {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
