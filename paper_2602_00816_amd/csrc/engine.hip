@@ -231,7 +231,7 @@ size_t Engine::plan(int B, int S, int m, const fdh_lanczos_opts* o, bool carve) 
     take(lz_beta, (size_t)m * 8);
     take(lz_coef, 128 * 8);
     take(lz_gram, 128 * 128 * 8);
-    take(lz_partial, (size_t)RED_BLOCKS * std::max(2 * cap, 1) * 8);
+    take(lz_partial, (size_t)RED_BLOCKS * (2 * cap + 1) * 8);
     take(lz_flag, 2 * 4);
     take(lz_maxabs, 8);
   }
@@ -942,10 +942,16 @@ int Engine::lanczos_t(int m, uint64_t seed, const fdh_lanczos_opts& o, double* a
   for (int k = 0; k < m; ++k) {
     int rc = hvp_bound(q, w);
     if (rc != FDH_OK) return rc;
-    TV(16.0 * Pd, launch_lanczos_alpha(w, q, qp, D, k, P, st));
     const int nv = std::min(k + 1, cap);
-    if (nv > 0) TV((12.0 + nv * bb) * Pd, launch_lanczos_project<Bt>(w, q, R, nv, k % cap, D, k, P, st));
-    TV((nv > 0 ? 8.0 + nv * bb : 12.0) * Pd, launch_lanczos_update<Bt>(w, q, R, nv, D, k, P, st));
+    if (nv > 0) {
+      // step A fused into the projection (reads w, q_prev, q and the rows) and
+      // formed again in the update (reads w, q_prev, q, the rows, writes w)
+      TV((12.0 + nv * bb) * Pd, launch_lanczos_project<Bt>(w, q, qp, R, nv, k % cap, D, k, P, st));
+      TV((16.0 + nv * bb) * Pd, launch_lanczos_update<Bt>(w, q, qp, R, nv, D, k, P, st));
+    } else {
+      TV(16.0 * Pd, launch_lanczos_alpha(w, q, qp, D, k, P, st));
+      TV(12.0 * Pd, launch_lanczos_update<Bt>(w, q, nullptr, R, 0, D, k, P, st));
+    }
     Bt* row = nullptr;
     if (cap > 0 && k + 1 < m) row = R.row((k + 1) % cap);
     // the next HVP's perturbation operand is written here too

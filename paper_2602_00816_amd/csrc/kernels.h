@@ -40,7 +40,7 @@ struct LanczosDev {
   double* beta;      // [m]  beta[k] = beta_{k+2} in 1-based notation (residual after step k)
   double* coef;      // [128] reorthogonalisation coefficients of the current step
   double* gram;      // [128 * 128] Gram matrix Q^T Q of the stored basis rows (by slot)
-  double* partial;   // [RED_BLOCKS * max(2 * cap, 1)]
+  double* partial;   // [RED_BLOCKS * (2 * cap + 1)]
   int* flag;         // [2]: [0] = breakdown step + 1 (0 = none), [1] = spare
   double* maxabs;    // [1]  max_j |alpha_j| so far
 };
@@ -62,17 +62,19 @@ struct BasisRows {
 // One Lanczos step after w = H q_k:
 // Step A:  w <- w - beta_{k-1} q_prev;  alpha_k = <w, q>  (beta_{-1} = 0)
 hipError_t launch_lanczos_alpha(float* w, const float* q, const float* qprev, LanczosDev st, int k, int64_t n, hipStream_t s);
-// Step B (nv >= 1 stored rows, slot `newest` holds q_k):  with
-// w1 = w - alpha_k q (w is not written), p = Q^T w1 and g = Q^T Q_newest;
-// Gram row/column `newest` <- g; coef = 2 p - G p (both classical
-// Gram-Schmidt passes).
+// Step B (nv >= 1 stored rows, slot `newest` holds q_k), with step A fused:
+// w' = w - beta_{k-1} q_prev (formed, not stored), alpha_k = <w', q>,
+// p = Q^T w' - alpha_k g and g = Q^T Q_newest; alpha[k] written; Gram
+// row/column `newest` <- g; coef = 2 p - G p (both classical Gram-Schmidt passes).
 template <typename B>
-hipError_t launch_lanczos_project(const float* w, const float* q, BasisRows<B> rows, int nv, int newest, LanczosDev st,
-                                  int k, int64_t n, hipStream_t s);
-// Step C:  w <- (w - alpha_k q) - Q coef (no rows when nv == 0); then ||w||^2
+hipError_t launch_lanczos_project(const float* w, const float* q, const float* qprev, BasisRows<B> rows, int nv, int newest,
+                                  LanczosDev st, int k, int64_t n, hipStream_t s);
+// Step C:  w <- (w' - alpha_k q) - Q coef (no rows when nv == 0); then ||w||^2.
+// w' = w - beta_{k-1} qprev when qprev is given (step A fused into step B),
+// else w itself (step A ran and stored it).
 template <typename B>
-hipError_t launch_lanczos_update(float* w, const float* q, BasisRows<B> rows, int nv, LanczosDev st, int k, int64_t n,
-                                 hipStream_t s);
+hipError_t launch_lanczos_update(float* w, const float* q, const float* qprev, BasisRows<B> rows, int nv, LanczosDev st,
+                                 int k, int64_t n, hipStream_t s);
 // Step D:  beta_k = ||w||; breakdown test (tol relative to max |alpha|);
 // q_next = w / beta_k; basis row (if not null) = B(q_next); the next HVP's
 // perturbation operand (if lo is not null) = T(eps * q_next).

@@ -153,7 +153,8 @@ __global__ __launch_bounds__(NT) void lz_alpha_kernel(float* w, const float* q, 
 // their sums are dropped.
 // partial[j * RED_BLOCKS + b] = p_j, partial[(nv + j) * RED_BLOCKS + b] = g_j.
 template <typename B, int NW, int NG>
-__global__ __launch_bounds__(64 * NW, NG == 1 ? 4 : 1) void lz_project_kernel(const float* w, const float* q, const double* alpha_k,
+__global__ __launch_bounds__(64 * NW, NG == 1 ? 4 : 1) void lz_project_kernel(const float* w, const float* q,
+                                                             const float* qprev, const double* beta, int k,
                                                              BasisRows<B> R, int nv, int newest, int64_t n,
                                                              double* partial) {
   constexpr int RW = 4 * NG;
@@ -162,20 +163,27 @@ __global__ __launch_bounds__(64 * NW, NG == 1 ? 4 : 1) void lz_project_kernel(co
   if (nr == 0) return;
   const int64_t ch = red_chunk(n);
   const int64_t s0 = blockIdx.x * ch, s1 = min(n, s0 + ch);
-  const double a = *alpha_k;
+  const double bk = (k > 0) ? beta[k - 1] : 0.0;
   const B* rowp[RW];
 #pragma unroll
   for (int r = 0; r < RW; ++r) rowp[r] = R.row(r < nr ? wave + NW * r : wave);
   const B* qnp = R.row(newest);
-  double pw[RW], pg[RW];
+  double pw[RW], pg[RW], pa = 0.0;
 #pragma unroll
   for (int r = 0; r < RW; ++r) pw[r] = pg[r] = 0.0;
   for_groups(s0 + 8 * lane, s1, 512, [&](int64_t i, int ne, auto full) {
     constexpr bool F = decltype(full)::value;
-    const V8 wv = ldv<F>(w, i, ne), qv = ldv<F>(q, i, ne), qn = ldv<F>(qnp, i, ne);
+    const V8 wv = ldv<F>(w, i, ne), pv = ldv<F>(qprev, i, ne), qn = ldv<F>(qnp, i, ne);
+    // w' = fp32(w - beta_{k-1} q_{k-1}), the alpha pass's rounding; alpha_k =
+    // <w', q_k> (wavefront 0) and p_j = <w', Q_j> - alpha_k <Q_newest, Q_j>
     double w1[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) w1[e] = (double)(float)((double)wv.x[e] - a * (double)qv.x[e]);
+    for (int e = 0; e < 8; ++e) w1[e] = (double)(float)((double)wv.x[e] - bk * (double)pv.x[e]);
+    if (wave == 0) {
+      const V8 qv = ldv<F>(q, i, ne);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pa = fma(w1[e], (double)qv.x[e], pa);
+    }
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
       if (4 * g < nr) {
@@ -204,6 +212,10 @@ __global__ __launch_bounds__(64 * NW, NG == 1 ? 4 : 1) void lz_project_kernel(co
       }
     }
   }
+  if (wave == 0) {
+    const double ta = wave_sum(pa);
+    if (lane == 0) partial[(int64_t)(2 * nv) * RED_BLOCKS + blockIdx.x] = ta;
+  }
 }
 
 // Step C: w <- fp32(w1 - sum_j c_j Q_j) with w1 = fp32(w - alpha_k q) (nv >= 0
@@ -211,13 +223,17 @@ __global__ __launch_bounds__(64 * NW, NG == 1 ? 4 : 1) void lz_project_kernel(co
 // groups of 8 with their loads issued together; a group's rows past nv read
 // row nv - 1 with coefficient zero.
 template <typename B>
-__global__ __launch_bounds__(NT) void lz_update_kernel(float* w, const float* q, const double* alpha_k, BasisRows<B> R,
+__global__ __launch_bounds__(NT) void lz_update_kernel(float* w, const float* q, const float* qprev, const double* beta,
+                                                       int k, const double* alpha_k, BasisRows<B> R,
                                                        const double* coef, int nv, int64_t n, double* partial) {
   __shared__ double sh[NT / 64];
   __shared__ double cs[136];
   for (int j = threadIdx.x; j < 136; j += NT) cs[j] = j < nv ? coef[j] : 0.0;
   __syncthreads();
   const double a = *alpha_k;
+  // with qprev the alpha pass was fused into the projection: w' = fp32(w -
+  // beta_{k-1} q_{k-1}) is formed here again, with the same rounding
+  const double bk = (qprev && k > 0) ? beta[k - 1] : 0.0;
   const int64_t ch = red_chunk(n);
   const int64_t s0 = blockIdx.x * ch, s1 = min(n, s0 + ch);
   double nrm = 0.0;
@@ -225,6 +241,11 @@ __global__ __launch_bounds__(NT) void lz_update_kernel(float* w, const float* q,
     constexpr bool F = decltype(full)::value;
     V8 wv = ldv<F>(w, i, ne);
     const V8 qv = ldv<F>(q, i, ne);
+    if (qprev) {
+      const V8 pv = ldv<F>(qprev, i, ne);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) wv.x[e] = (float)((double)wv.x[e] - bk * (double)pv.x[e]);
+    }
     double acc[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[e] = (double)(float)((double)wv.x[e] - a * (double)qv.x[e]);
@@ -260,9 +281,9 @@ __global__ __launch_bounds__(NT) void lz_update_kernel(float* w, const float* q,
 // mode 2: beta[k] = sqrt(sum); breakdown test against tol * maxabs.
 __global__ void lz_finish_kernel(LanczosDev st, int mode, int k, int nv, int newest, double tol) {
   __shared__ double sp[128];
-  __shared__ double colsum[256];
+  __shared__ double colsum[2 * 128 + 1];
   const int j = threadIdx.x;
-  const int ncol = (mode == 1) ? 2 * nv : 1;
+  const int ncol = (mode == 1) ? 2 * nv + 1 : 1;
   // column sums of the partials in a fixed order: wavefront w takes columns
   // w, w + 4, ...; lane l adds partials l, l + 64, ..., then a fixed butterfly
   {
@@ -275,7 +296,16 @@ __global__ void lz_finish_kernel(LanczosDev st, int mode, int k, int nv, int new
     }
   }
   __syncthreads();
-  const double s = j < ncol ? colsum[j] : 0.0;
+  double s = j < ncol ? colsum[j] : 0.0;
+  if (mode == 1) {
+    // alpha_k, and p_j = <w', Q_j> - alpha_k g_j with g_j = <Q_newest, Q_j>
+    const double al = colsum[2 * nv];
+    if (j == 0) {
+      st.alpha[k] = al;
+      st.maxabs[0] = fmax(st.maxabs[0], fabs(al));
+    }
+    if (j < nv) s -= al * colsum[nv + j];
+  }
   if (mode == 0) {
     if (j == 0) {
       st.alpha[k] = s;
@@ -574,11 +604,11 @@ hipError_t launch_lanczos_alpha(float* w, const float* q, const float* qprev, La
 }
 
 template <typename B>
-hipError_t launch_lanczos_project(const float* w, const float* q, BasisRows<B> rows, int nv, int newest, LanczosDev st,
-                                  int k, int64_t n, hipStream_t s) {
+hipError_t launch_lanczos_project(const float* w, const float* q, const float* qprev, BasisRows<B> rows, int nv, int newest,
+                                  LanczosDev st, int k, int64_t n, hipStream_t s) {
   if (nv < 1 || nv > 128 || newest < 0 || newest >= nv) return hipErrorInvalidValue;
-  const double* a = st.alpha + k;
-#define LZP(W, G) hipLaunchKernelGGL((lz_project_kernel<B, W, G>), dim3(RED_BLOCKS), dim3(64 * W), 0, s, w, q, a, rows, nv, newest, n, st.partial)
+#define LZP(W, G) hipLaunchKernelGGL((lz_project_kernel<B, W, G>), dim3(RED_BLOCKS), dim3(64 * W), 0, s, w, q, qprev, \
+                                     (const double*)st.beta, k, rows, nv, newest, n, st.partial)
   // rows of wave 0: ceil(nv / waves)
   if (nv <= 16) LZP(4, 1);
   else if (nv <= 32) LZP(8, 1);
@@ -591,11 +621,11 @@ hipError_t launch_lanczos_project(const float* w, const float* q, BasisRows<B> r
 }
 
 template <typename B>
-hipError_t launch_lanczos_update(float* w, const float* q, BasisRows<B> rows, int nv, LanczosDev st, int k, int64_t n,
-                                 hipStream_t s) {
+hipError_t launch_lanczos_update(float* w, const float* q, const float* qprev, BasisRows<B> rows, int nv, LanczosDev st,
+                                 int k, int64_t n, hipStream_t s) {
   if (nv < 0 || nv > 128) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(lz_update_kernel<B>, dim3(RED_BLOCKS), dim3(NT), 0, s, w, q, (const double*)(st.alpha + k), rows,
-                     (const double*)st.coef, nv, n, st.partial);
+  hipLaunchKernelGGL(lz_update_kernel<B>, dim3(RED_BLOCKS), dim3(NT), 0, s, w, q, qprev, (const double*)st.beta, k,
+                     (const double*)(st.alpha + k), rows, (const double*)st.coef, nv, n, st.partial);
   return hipGetLastError();
 }
 
@@ -609,10 +639,10 @@ hipError_t launch_lanczos_normalise(const float* w, float* qnext, B* basis_row, 
 }
 
 #define INST_LZ(B)                                                                                                   \
-  template hipError_t launch_lanczos_project<B>(const float*, const float*, BasisRows<B>, int, int, LanczosDev, int,      \
-                                                int64_t, hipStream_t);                                                \
-  template hipError_t launch_lanczos_update<B>(float*, const float*, BasisRows<B>, int, LanczosDev, int, int64_t,    \
-                                               hipStream_t);                                                          \
+  template hipError_t launch_lanczos_project<B>(const float*, const float*, const float*, BasisRows<B>, int, int,      \
+                                                LanczosDev, int, int64_t, hipStream_t);                               \
+  template hipError_t launch_lanczos_update<B>(float*, const float*, const float*, BasisRows<B>, int, LanczosDev, int, \
+                                               int64_t, hipStream_t);                                                 \
   template hipError_t launch_lanczos_normalise<B, float>(const float*, float*, B*, float*, double, LanczosDev, int, double,   \
                                                          int64_t, hipStream_t);                                              \
   template hipError_t launch_lanczos_normalise<B, bf16_t>(const float*, float*, B*, bf16_t*, double, LanczosDev, int, double, \
