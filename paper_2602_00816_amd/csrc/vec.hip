@@ -152,26 +152,31 @@ __global__ __launch_bounds__(NT) void lz_alpha_kernel(float* w, const float* q, 
 // issued together; rows of a group past this wave's count repeat row v and
 // their sums are dropped.
 // partial[j * RED_BLOCKS + b] = p_j, partial[(nv + j) * RED_BLOCKS + b] = g_j.
-template <typename B, int NW, int NG>
+// ES (element split, nv <= 4 NG): every wavefront takes all rows over its own
+// quarter of the chunk's groups, and the wavefronts' sums are added in a fixed
+// order; otherwise wavefronts split the rows and each streams the whole chunk.
+template <typename B, int NW, int NG, bool ES>
 __global__ __launch_bounds__(64 * NW, NG == 1 ? 4 : 1) void lz_project_kernel(const float* w, const float* q,
                                                              const float* qprev, const double* beta, int k,
                                                              BasisRows<B> R, int nv, int newest, int64_t n,
                                                              double* partial) {
   constexpr int RW = 4 * NG;
+  __shared__ double red[ES ? NW : 1][2 * RW + 1];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
-  const int nr = nv > wave ? min(RW, (nv - wave + NW - 1) / NW) : 0;
-  if (nr == 0) return;
+  const int nr = ES ? nv : (nv > wave ? min(RW, (nv - wave + NW - 1) / NW) : 0);
+  if (!ES && nr == 0) return;
   const int64_t ch = red_chunk(n);
   const int64_t s0 = blockIdx.x * ch, s1 = min(n, s0 + ch);
   const double bk = (k > 0) ? beta[k - 1] : 0.0;
   const B* rowp[RW];
 #pragma unroll
-  for (int r = 0; r < RW; ++r) rowp[r] = R.row(r < nr ? wave + NW * r : wave);
+  for (int r = 0; r < RW; ++r) rowp[r] = ES ? R.row(r < nr ? r : 0) : R.row(r < nr ? wave + NW * r : wave);
   const B* qnp = R.row(newest);
   double pw[RW], pg[RW], pa = 0.0;
 #pragma unroll
   for (int r = 0; r < RW; ++r) pw[r] = pg[r] = 0.0;
-  for_groups(s0 + 8 * lane, s1, 512, [&](int64_t i, int ne, auto full) {
+  const int64_t i0 = ES ? s0 + 512 * wave + 8 * lane : s0 + 8 * lane;
+  for_groups(i0, s1, ES ? 512 * NW : 512, [&](int64_t i, int ne, auto full) {
     constexpr bool F = decltype(full)::value;
     const V8 wv = ldv<F>(w, i, ne), pv = ldv<F>(qprev, i, ne), qn = ldv<F>(qnp, i, ne);
     // w' = fp32(w - beta_{k-1} q_{k-1}), the alpha pass's rounding; alpha_k =
@@ -179,7 +184,7 @@ __global__ __launch_bounds__(64 * NW, NG == 1 ? 4 : 1) void lz_project_kernel(co
     double w1[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) w1[e] = (double)(float)((double)wv.x[e] - bk * (double)pv.x[e]);
-    if (wave == 0) {
+    if (ES || wave == 0) {
       const V8 qv = ldv<F>(q, i, ne);
 #pragma unroll
       for (int e = 0; e < 8; ++e) pa = fma(w1[e], (double)qv.x[e], pa);
@@ -201,20 +206,43 @@ __global__ __launch_bounds__(64 * NW, NG == 1 ? 4 : 1) void lz_project_kernel(co
       }
     }
   });
+  if constexpr (ES) {
 #pragma unroll
-  for (int r = 0; r < RW; ++r) {
-    if (r < nr) {
-      const double tw = wave_sum(pw[r]), tg = wave_sum(pg[r]);
-      const int j = wave + NW * r;
-      if (lane == 0) {
-        partial[(int64_t)j * RED_BLOCKS + blockIdx.x] = tw;
-        partial[(int64_t)(nv + j) * RED_BLOCKS + blockIdx.x] = tg;
+    for (int r = 0; r < RW; ++r) {
+      if (r < nr) {
+        const double tw = wave_sum(pw[r]), tg = wave_sum(pg[r]);
+        if (lane == 0) {
+          red[wave][r] = tw;
+          red[wave][RW + r] = tg;
+        }
       }
     }
-  }
-  if (wave == 0) {
     const double ta = wave_sum(pa);
-    if (lane == 0) partial[(int64_t)(2 * nv) * RED_BLOCKS + blockIdx.x] = ta;
+    if (lane == 0) red[wave][2 * RW] = ta;
+    __syncthreads();
+    const int t = threadIdx.x;
+    if (t < 2 * nv + 1) {
+      const int c = t < nv ? t : (t < 2 * nv ? RW + (t - nv) : 2 * RW);
+      double sum = 0.0;
+      for (int v = 0; v < NW; ++v) sum += red[v][c];
+      partial[(int64_t)t * RED_BLOCKS + blockIdx.x] = sum;
+    }
+  } else {
+#pragma unroll
+    for (int r = 0; r < RW; ++r) {
+      if (r < nr) {
+        const double tw = wave_sum(pw[r]), tg = wave_sum(pg[r]);
+        const int j = wave + NW * r;
+        if (lane == 0) {
+          partial[(int64_t)j * RED_BLOCKS + blockIdx.x] = tw;
+          partial[(int64_t)(nv + j) * RED_BLOCKS + blockIdx.x] = tg;
+        }
+      }
+    }
+    if (wave == 0) {
+      const double ta = wave_sum(pa);
+      if (lane == 0) partial[(int64_t)(2 * nv) * RED_BLOCKS + blockIdx.x] = ta;
+    }
   }
 }
 
@@ -607,14 +635,17 @@ template <typename B>
 hipError_t launch_lanczos_project(const float* w, const float* q, const float* qprev, BasisRows<B> rows, int nv, int newest,
                                   LanczosDev st, int k, int64_t n, hipStream_t s) {
   if (nv < 1 || nv > 128 || newest < 0 || newest >= nv) return hipErrorInvalidValue;
-#define LZP(W, G) hipLaunchKernelGGL((lz_project_kernel<B, W, G>), dim3(RED_BLOCKS), dim3(64 * W), 0, s, w, q, qprev, \
-                                     (const double*)st.beta, k, rows, nv, newest, n, st.partial)
-  // rows of wave 0: ceil(nv / waves)
-  if (nv <= 16) LZP(4, 1);
-  else if (nv <= 32) LZP(8, 1);
-  else if (nv <= 64) LZP(8, 2);
-  else if (nv <= 96) LZP(8, 3);
-  else LZP(8, 4);
+#define LZP(W, G, E) hipLaunchKernelGGL((lz_project_kernel<B, W, G, E>), dim3(RED_BLOCKS), dim3(64 * W), 0, s, w, q, \
+                                        qprev, (const double*)st.beta, k, rows, nv, newest, n, st.partial)
+  // few rows: the wavefronts split the elements; more: they split the rows
+  // (wave 0 takes ceil(nv / waves) of them)
+  if (nv <= 4) LZP(4, 1, true);
+  else if (nv <= 8) LZP(4, 2, true);
+  else if (nv <= 16) LZP(4, 4, true);
+  else if (nv <= 32) LZP(8, 1, false);
+  else if (nv <= 64) LZP(8, 2, false);
+  else if (nv <= 96) LZP(8, 3, false);
+  else LZP(8, 4, false);
 #undef LZP
   hipLaunchKernelGGL(lz_finish_kernel, dim3(1), dim3(256), 0, s, st, 1, k, nv, newest, 0.0);
   return hipGetLastError();
