@@ -642,7 +642,8 @@ hipError_t launch_lanczos_project(const float* w, const float* q, const float* q
   if (nv <= 4) LZP(4, 1, true);
   else if (nv <= 8) LZP(4, 2, true);
   else if (nv <= 16) LZP(4, 4, true);
-  else if (nv <= 32) LZP(8, 1, false);
+  else if (nv <= 24) LZP(4, 6, true);
+  else if (nv <= 32) LZP(4, 8, true);
   else if (nv <= 64) LZP(8, 2, false);
   else if (nv <= 96) LZP(8, 3, false);
   else LZP(8, 4, false);
