@@ -112,6 +112,12 @@ def _ptr(t) -> int:
     return 0 if t is None else int(t.data_ptr())
 
 
+def _check_tokens(t):
+    import torch
+    if t is not None and (t.dtype != torch.int32 or t.dim() != 2 or not t.is_cuda or not t.is_contiguous()):
+        raise ValueError("tokens must be a contiguous int32 [B, S] tensor on the device")
+
+
 def _stream():
     import torch
     return C.c_void_p(torch.cuda.current_stream().cuda_stream)
@@ -147,7 +153,8 @@ class Model:
             raise FdhError(st, "fdh_create rejected the configuration")
         self._h = h
         self._ws = None
-        self._keep = []
+        self._keep = []        # tensors the bound operator points to
+        self._diag = None      # QUAD_DIAG diagonal the context points to
 
     @classmethod
     def from_workload(cls, w: dict, stream=None):
@@ -231,7 +238,7 @@ class Model:
         return v
 
     def set_quad_diag(self, diag):
-        self._keep.append(diag)
+        self._diag = diag
         self._check(self._L.fdh_set_quad_diag(self._h, _ptr(diag)), "fdh_set_quad_diag")
 
     # ---- the hot path ----
@@ -240,6 +247,7 @@ class Model:
         import torch
         if out is None:
             out = torch.empty(self.num_params, dtype=torch.float32, device="cuda")
+        _check_tokens(tokens)
         B, S = (tokens.shape if tokens is not None else (0, 0))
         self._check(self._L.fdh_hvp(self._h, _ptr(params), _ptr(v), float(eps), _ptr(tokens), B, S, _ptr(out)),
                     "fdh_hvp")
@@ -251,6 +259,7 @@ class Model:
         return lp.value, lm.value
 
     def bind(self, params, tokens, eps: float):
+        _check_tokens(tokens)
         B, S = (tokens.shape if tokens is not None else (0, 0))
         self._keep = [params, tokens]
         self._check(self._L.fdh_bind(self._h, _ptr(params), _ptr(tokens), B, S, float(eps)), "fdh_bind")
@@ -263,8 +272,11 @@ class Model:
         import torch
         items = [b if isinstance(b, tuple) else (b, None) for b in batches]
         for tok, lab in items:
-            if tok.dtype != torch.int32 or (lab is not None and (lab.dtype != torch.int32 or lab.shape != tok.shape)):
-                raise ValueError("tokens and labels must be int32 tensors of one shape")
+            for x in (tok, lab):
+                if x is not None and (x.dtype != torch.int32 or x.dim() != 2 or not x.is_cuda or not x.is_contiguous()):
+                    raise ValueError("tokens and labels must be contiguous int32 [B, S] tensors on the device")
+            if lab is not None and lab.shape != tok.shape:
+                raise ValueError("labels must have the shape of their tokens")
         arr = (Batch * len(items))(*[Batch(_ptr(t), _ptr(l), t.shape[0], t.shape[1]) for t, l in items])
         n = C.c_int64()
         self._keep = [params] + [x for it in items for x in it if x is not None]
