@@ -38,3 +38,31 @@ def test_block_diagonal_matches_oracle(name, dtype):
     assert np.allclose(got[:, 0], st["abs"], rtol=tol, atol=tol * np.abs(st["abs"]).max())
     assert np.allclose(got[:, 1], st["rel"], rtol=tol, atol=tol)
     assert np.allclose(got[:, 2], st["cos"], rtol=tol, atol=tol)
+
+
+def test_block_diagonal_full_gpt2_medium():
+    """Exp I at the GPT-2-medium workload's full size (24 layers, 8 x 1024
+    tokens, bf16): the statistics are finite, deterministic and consistent
+    with one another (rel = abs / ||h^(b)||, |cos| <= 1, and abs^2 >=
+    ||h^(b)||^2 (1 - cos^2), the distance from h^(b) to the line through
+    h_b^(b)); the summary is printed as the paper's table reports it."""
+    torch = need_gpu()
+    from paper_2602_00816_amd import fdhvp as fd
+    from synth.workloads import WORKLOADS
+    w = WORKLOADS["gpt2-medium-bf16"]
+    B, S, L = w["batch"], w["seq"], w["n_layers"]
+    mod = fd.Model.from_workload(w)
+    mod.set_workspace(B, S, 1, fd.opts("none"))
+    th = mod.init_params(1)
+    tok = mod.make_tokens(B, S, 2, w["token_dist"])
+    mod.bind(th, tok, w["eps"][0])
+    v = mod.random_vector(synth.workloads.SEED_GAUSS, "gaussian")
+    st = mod.block_diagonal(v)
+    assert st.shape == (L, 4) and np.all(np.isfinite(st))
+    assert np.array_equal(st, mod.block_diagonal(v))
+    ab, rel, cos, nh = st[:, 0], st[:, 1], st[:, 2], st[:, 3]
+    assert np.all(nh > 0) and np.allclose(rel, ab / nh, rtol=1e-9)
+    assert np.all(np.abs(cos) <= 1.0 + 1e-12)
+    assert np.all(ab ** 2 >= nh ** 2 * (1.0 - cos ** 2) * (1.0 - 1e-6))
+    say(f"gpt2-medium Exp I over {L} blocks: abs {ab.mean():.4g} +- {ab.std():.3g}, "
+        f"rel {rel.mean():.4f} +- {rel.std():.4f}, cos {cos.mean():.4f} +- {cos.std():.4f}")
