@@ -188,3 +188,33 @@ def test_eps_sweep_small_gpt2_shapes_fp32():
     # no u / eps growth: the GPU's rounding error does not grow as the step shrinks
     assert max(r[0] for r in rows.values()) <= 1e-5
     assert rows[1e-4][0] <= 3.0 * rows[1e-3][0]
+
+
+def test_slq_small_gpt2_full_config():
+    """The small fp32 workload's SLQ configuration at full size (4 Rademacher
+    probes, m = 80, full reorthogonalisation with an fp32 basis, eps = 1e-3):
+    Gauss weights sum to one per probe, the trace estimate is P times the mean
+    alpha_1, and the extreme Ritz value, which converges first, agrees across
+    the four independent probes to 1e-3 relative."""
+    torch = need_gpu()
+    from paper_2602_00816_amd import fdhvp as fd
+    w = WORKLOADS["small-gpt2-fp32"]
+    B, S, m, probes = w["batch"], w["seq"], w["m"], w["probes"]
+    mod = fd.Model.from_workload(w)
+    o = fd.opts(w["reorth"], w["window"], w["basis"])
+    mod.set_workspace(B, S, m, o)
+    th = mod.init_params(1)
+    tok = mod.make_tokens(B, S, 2, w["token_dist"])
+    mod.bind(th, tok, 1e-3)
+    nodes, weights, steps, trace, st = mod.slq_density(probes, m, synth.workloads.SEED_PROBE, o)
+    assert np.all(steps == m)
+    assert np.allclose(weights.sum(1), 1.0, atol=1e-9)
+    lmax = nodes.max(1)
+    lmin = nodes.min(1)
+    say(f"small-gpt2 SLQ: lambda_max {lmax}, lambda_min {lmin}, trace {trace:.6e}")
+    assert np.abs(lmax - lmax.mean()).max() <= 1e-3 * np.abs(lmax).max()
+    alpha1 = []
+    for j in range(probes):
+        a, b, s, _ = mod.lanczos(1, synth.workloads.SEED_PROBE + j, o)
+        alpha1.append(a[0])
+    assert abs(trace - mod.num_params * np.mean(alpha1)) <= 1e-9 * abs(trace) + 1e-12
