@@ -152,25 +152,27 @@ __global__ __launch_bounds__(NT) void lz_alpha_kernel(float* w, const float* q, 
 // issued together; rows of a group past this wave's count repeat row v and
 // their sums are dropped.
 // partial[j * RED_BLOCKS + b] = p_j, partial[(nv + j) * RED_BLOCKS + b] = g_j.
-// ES (element split, nv <= 4 NG): every wavefront takes all rows over its own
-// quarter of the chunk's groups, and the wavefronts' sums are added in a fixed
-// order; otherwise wavefronts split the rows and each streams the whole chunk.
+// ES (element split): every wavefront takes the rows [r0, r0 + nrl) (nrl <=
+// 4 NG) over its own quarter of the chunk's groups, and the wavefronts' sums
+// are added in a fixed order; alpha's partial is formed by the launch with wa.
+// Otherwise (row split) wavefronts take every NW-th row, each streaming the
+// whole chunk, and r0, nrl and wa are not used.
 template <typename B, int NW, int NG, bool ES>
 __global__ __launch_bounds__(64 * NW, NG == 1 ? 4 : 1) void lz_project_kernel(const float* w, const float* q,
                                                              const float* qprev, const double* beta, int k,
-                                                             BasisRows<B> R, int nv, int newest, int64_t n,
-                                                             double* partial) {
+                                                             BasisRows<B> R, int nv, int newest, int r0, int nrl,
+                                                             bool wa, int64_t n, double* partial) {
   constexpr int RW = 4 * NG;
   __shared__ double red[ES ? NW : 1][2 * RW + 1];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
-  const int nr = ES ? nv : (nv > wave ? min(RW, (nv - wave + NW - 1) / NW) : 0);
+  const int nr = ES ? nrl : (nv > wave ? min(RW, (nv - wave + NW - 1) / NW) : 0);
   if (!ES && nr == 0) return;
   const int64_t ch = red_chunk(n);
   const int64_t s0 = blockIdx.x * ch, s1 = min(n, s0 + ch);
   const double bk = (k > 0) ? beta[k - 1] : 0.0;
   const B* rowp[RW];
 #pragma unroll
-  for (int r = 0; r < RW; ++r) rowp[r] = ES ? R.row(r < nr ? r : 0) : R.row(r < nr ? wave + NW * r : wave);
+  for (int r = 0; r < RW; ++r) rowp[r] = ES ? R.row(r0 + (r < nr ? r : 0)) : R.row(r < nr ? wave + NW * r : wave);
   const B* qnp = R.row(newest);
   double pw[RW], pg[RW], pa = 0.0;
 #pragma unroll
@@ -184,7 +186,7 @@ __global__ __launch_bounds__(64 * NW, NG == 1 ? 4 : 1) void lz_project_kernel(co
     double w1[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) w1[e] = (double)(float)((double)wv.x[e] - bk * (double)pv.x[e]);
-    if (ES || wave == 0) {
+    if (ES ? wa : wave == 0) {
       const V8 qv = ldv<F>(q, i, ne);
 #pragma unroll
       for (int e = 0; e < 8; ++e) pa = fma(w1[e], (double)qv.x[e], pa);
@@ -220,12 +222,14 @@ __global__ __launch_bounds__(64 * NW, NG == 1 ? 4 : 1) void lz_project_kernel(co
     const double ta = wave_sum(pa);
     if (lane == 0) red[wave][2 * RW] = ta;
     __syncthreads();
+    // partial columns: p'_j at j, g_j at nv + j, alpha's part at 2 nv
     const int t = threadIdx.x;
-    if (t < 2 * nv + 1) {
-      const int c = t < nv ? t : (t < 2 * nv ? RW + (t - nv) : 2 * RW);
+    if (t < 2 * nr + (wa ? 1 : 0)) {
+      const int c = t < nr ? t : (t < 2 * nr ? RW + (t - nr) : 2 * RW);
+      const int col = t < nr ? r0 + t : (t < 2 * nr ? nv + r0 + (t - nr) : 2 * nv);
       double sum = 0.0;
       for (int v = 0; v < NW; ++v) sum += red[v][c];
-      partial[(int64_t)t * RED_BLOCKS + blockIdx.x] = sum;
+      partial[(int64_t)col * RED_BLOCKS + blockIdx.x] = sum;
     }
   } else {
 #pragma unroll
@@ -635,18 +639,24 @@ template <typename B>
 hipError_t launch_lanczos_project(const float* w, const float* q, const float* qprev, BasisRows<B> rows, int nv, int newest,
                                   LanczosDev st, int k, int64_t n, hipStream_t s) {
   if (nv < 1 || nv > 128 || newest < 0 || newest >= nv) return hipErrorInvalidValue;
-#define LZP(W, G, E) hipLaunchKernelGGL((lz_project_kernel<B, W, G, E>), dim3(RED_BLOCKS), dim3(64 * W), 0, s, w, q, \
-                                        qprev, (const double*)st.beta, k, rows, nv, newest, n, st.partial)
-  // few rows: the wavefronts split the elements; more: they split the rows
-  // (wave 0 takes ceil(nv / waves) of them)
-  if (nv <= 4) LZP(4, 1, true);
-  else if (nv <= 8) LZP(4, 2, true);
-  else if (nv <= 16) LZP(4, 4, true);
-  else if (nv <= 24) LZP(4, 6, true);
-  else if (nv <= 32) LZP(4, 8, true);
-  else if (nv <= 64) LZP(8, 2, false);
-  else if (nv <= 96) LZP(8, 3, false);
-  else LZP(8, 4, false);
+#define LZP(W, G, E, R0, NRL, WA)                                                                                  \
+  hipLaunchKernelGGL((lz_project_kernel<B, W, G, E>), dim3(RED_BLOCKS), dim3(64 * W), 0, s, w, q, qprev,              \
+                     (const double*)st.beta, k, rows, nv, newest, R0, NRL, WA, n, st.partial)
+  // element split over up to 32 rows per launch (two launches up to 64 rows,
+  // the second without alpha); beyond, the wavefronts split the rows
+  auto es = [&](int r0, int nrl, bool wa) {
+    if (nrl <= 4) LZP(4, 1, true, r0, nrl, wa);
+    else if (nrl <= 8) LZP(4, 2, true, r0, nrl, wa);
+    else if (nrl <= 16) LZP(4, 4, true, r0, nrl, wa);
+    else if (nrl <= 24) LZP(4, 6, true, r0, nrl, wa);
+    else LZP(4, 8, true, r0, nrl, wa);
+  };
+  if (nv <= 32) es(0, nv, true);
+  else if (nv <= 64) {
+    es(0, 32, true);
+    es(32, nv - 32, false);
+  } else if (nv <= 96) LZP(8, 3, false, 0, nv, true);
+  else LZP(8, 4, false, 0, nv, true);
 #undef LZP
   hipLaunchKernelGGL(lz_finish_kernel, dim3(1), dim3(256), 0, s, st, 1, k, nv, newest, 0.0);
   return hipGetLastError();
