@@ -142,43 +142,36 @@ __global__ __launch_bounds__(NT) void lz_alpha_kernel(float* w, const float* q, 
   if (threadIdx.x == 0) partial[blockIdx.x] = acc;
 }
 
-// Step B (projections): with w1 = fp32(w - alpha_k q), p_j = <w1, Q_j> and
-// g_j = <Q_new, Q_j> for the nv stored rows (Q_new = the row of q_k); w is not
-// written (the update pass forms w1 again).  The NW wavefronts of a workgroup
-// walk the same 512-element tiles of the chunk (w, q and Q_new are read by
-// each; the copies after the first come from the L1/L2 caches) and split the
-// rows: wave v takes rows v, v+NW, ..., at most 4 NG of them, so a lane keeps
-// fp64 sums for 4 NG rows.  Rows are read in groups of 4 with their loads
-// issued together; rows of a group past this wave's count repeat row v and
-// their sums are dropped.
-// partial[j * RED_BLOCKS + b] = p_j, partial[(nv + j) * RED_BLOCKS + b] = g_j.
-// ES (element split): every wavefront takes the rows [r0, r0 + nrl) (nrl <=
-// 4 NG) over its own quarter of the chunk's groups, and the wavefronts' sums
-// are added in a fixed order; alpha's partial is formed by the launch with wa.
-// Otherwise (row split) wavefronts take every NW-th row, each streaming the
-// whole chunk, and r0, nrl and wa are not used.
-template <typename B, int NW, int NG, bool ES>
+// Step B (projections, with step A fused): w' = fp32(w - beta_{k-1} q_{k-1})
+// is formed on the fly (not written; the update pass forms it again),
+// alpha_k = <w', q_k>, p'_j = <w', Q_j> and g_j = <Q_new, Q_j> for the stored
+// rows (Q_new = the row of q_k); the finish kernel takes p_j = p'_j - alpha_k g_j.
+// One launch covers up to 32 rows: every wavefront of a workgroup takes all of
+// them, [r0, r0 + nrl), over its own share of the chunk's 8-element groups
+// (a lane keeps fp64 sums for 4 NG rows; rows are read in groups of 4 with
+// their loads issued together), and the wavefronts' sums are added in a fixed
+// order.  alpha's partial is formed by the launch with wa.
+// partial[j * RED_BLOCKS + b] = p'_j, [(nv + j) * ...] = g_j, [2 nv * ...] = alpha part.
+template <typename B, int NW, int NG>
 __global__ __launch_bounds__(64 * NW, NG == 1 ? 4 : 1) void lz_project_kernel(const float* w, const float* q,
                                                              const float* qprev, const double* beta, int k,
                                                              BasisRows<B> R, int nv, int newest, int r0, int nrl,
                                                              bool wa, int64_t n, double* partial) {
   constexpr int RW = 4 * NG;
-  __shared__ double red[ES ? NW : 1][2 * RW + 1];
+  __shared__ double red[NW][2 * RW + 1];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
-  const int nr = ES ? nrl : (nv > wave ? min(RW, (nv - wave + NW - 1) / NW) : 0);
-  if (!ES && nr == 0) return;
+  const int nr = nrl;
   const int64_t ch = red_chunk(n);
   const int64_t s0 = blockIdx.x * ch, s1 = min(n, s0 + ch);
   const double bk = (k > 0) ? beta[k - 1] : 0.0;
   const B* rowp[RW];
 #pragma unroll
-  for (int r = 0; r < RW; ++r) rowp[r] = ES ? R.row(r0 + (r < nr ? r : 0)) : R.row(r < nr ? wave + NW * r : wave);
+  for (int r = 0; r < RW; ++r) rowp[r] = R.row(r0 + (r < nr ? r : 0));
   const B* qnp = R.row(newest);
   double pw[RW], pg[RW], pa = 0.0;
 #pragma unroll
   for (int r = 0; r < RW; ++r) pw[r] = pg[r] = 0.0;
-  const int64_t i0 = ES ? s0 + 512 * wave + 8 * lane : s0 + 8 * lane;
-  for_groups(i0, s1, ES ? 512 * NW : 512, [&](int64_t i, int ne, auto full) {
+  for_groups(s0 + 512 * wave + 8 * lane, s1, 512 * NW, [&](int64_t i, int ne, auto full) {
     constexpr bool F = decltype(full)::value;
     const V8 wv = ldv<F>(w, i, ne), pv = ldv<F>(qprev, i, ne), qn = ldv<F>(qnp, i, ne);
     // w' = fp32(w - beta_{k-1} q_{k-1}), the alpha pass's rounding; alpha_k =
@@ -186,7 +179,7 @@ __global__ __launch_bounds__(64 * NW, NG == 1 ? 4 : 1) void lz_project_kernel(co
     double w1[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) w1[e] = (double)(float)((double)wv.x[e] - bk * (double)pv.x[e]);
-    if (ES ? wa : wave == 0) {
+    if (wa) {
       const V8 qv = ldv<F>(q, i, ne);
 #pragma unroll
       for (int e = 0; e < 8; ++e) pa = fma(w1[e], (double)qv.x[e], pa);
@@ -208,45 +201,27 @@ __global__ __launch_bounds__(64 * NW, NG == 1 ? 4 : 1) void lz_project_kernel(co
       }
     }
   });
-  if constexpr (ES) {
 #pragma unroll
-    for (int r = 0; r < RW; ++r) {
-      if (r < nr) {
-        const double tw = wave_sum(pw[r]), tg = wave_sum(pg[r]);
-        if (lane == 0) {
-          red[wave][r] = tw;
-          red[wave][RW + r] = tg;
-        }
+  for (int r = 0; r < RW; ++r) {
+    if (r < nr) {
+      const double tw = wave_sum(pw[r]), tg = wave_sum(pg[r]);
+      if (lane == 0) {
+        red[wave][r] = tw;
+        red[wave][RW + r] = tg;
       }
     }
-    const double ta = wave_sum(pa);
-    if (lane == 0) red[wave][2 * RW] = ta;
-    __syncthreads();
-    // partial columns: p'_j at j, g_j at nv + j, alpha's part at 2 nv
-    const int t = threadIdx.x;
-    if (t < 2 * nr + (wa ? 1 : 0)) {
-      const int c = t < nr ? t : (t < 2 * nr ? RW + (t - nr) : 2 * RW);
-      const int col = t < nr ? r0 + t : (t < 2 * nr ? nv + r0 + (t - nr) : 2 * nv);
-      double sum = 0.0;
-      for (int v = 0; v < NW; ++v) sum += red[v][c];
-      partial[(int64_t)col * RED_BLOCKS + blockIdx.x] = sum;
-    }
-  } else {
-#pragma unroll
-    for (int r = 0; r < RW; ++r) {
-      if (r < nr) {
-        const double tw = wave_sum(pw[r]), tg = wave_sum(pg[r]);
-        const int j = wave + NW * r;
-        if (lane == 0) {
-          partial[(int64_t)j * RED_BLOCKS + blockIdx.x] = tw;
-          partial[(int64_t)(nv + j) * RED_BLOCKS + blockIdx.x] = tg;
-        }
-      }
-    }
-    if (wave == 0) {
-      const double ta = wave_sum(pa);
-      if (lane == 0) partial[(int64_t)(2 * nv) * RED_BLOCKS + blockIdx.x] = ta;
-    }
+  }
+  const double ta = wave_sum(pa);
+  if (lane == 0) red[wave][2 * RW] = ta;
+  __syncthreads();
+  // partial columns: p'_j at j, g_j at nv + j, alpha's part at 2 nv
+  const int t = threadIdx.x;
+  if (t < 2 * nr + (wa ? 1 : 0)) {
+    const int c = t < nr ? t : (t < 2 * nr ? RW + (t - nr) : 2 * RW);
+    const int col = t < nr ? r0 + t : (t < 2 * nr ? nv + r0 + (t - nr) : 2 * nv);
+    double sum = 0.0;
+    for (int v = 0; v < NW; ++v) sum += red[v][c];
+    partial[(int64_t)col * RED_BLOCKS + blockIdx.x] = sum;
   }
 }
 
@@ -639,24 +614,19 @@ template <typename B>
 hipError_t launch_lanczos_project(const float* w, const float* q, const float* qprev, BasisRows<B> rows, int nv, int newest,
                                   LanczosDev st, int k, int64_t n, hipStream_t s) {
   if (nv < 1 || nv > 128 || newest < 0 || newest >= nv) return hipErrorInvalidValue;
-#define LZP(W, G, E, R0, NRL, WA)                                                                                  \
-  hipLaunchKernelGGL((lz_project_kernel<B, W, G, E>), dim3(RED_BLOCKS), dim3(64 * W), 0, s, w, q, qprev,              \
+#define LZP(W, G, R0, NRL, WA)                                                                                     \
+  hipLaunchKernelGGL((lz_project_kernel<B, W, G>), dim3(RED_BLOCKS), dim3(64 * W), 0, s, w, q, qprev,                 \
                      (const double*)st.beta, k, rows, nv, newest, R0, NRL, WA, n, st.partial)
-  // element split over up to 32 rows per launch (two launches up to 64 rows,
-  // the second without alpha); beyond, the wavefronts split the rows
+  // element split over up to 32 rows per launch (further launches for the
+  // next 32 rows each, without alpha)
   auto es = [&](int r0, int nrl, bool wa) {
-    if (nrl <= 4) LZP(4, 1, true, r0, nrl, wa);
-    else if (nrl <= 8) LZP(4, 2, true, r0, nrl, wa);
-    else if (nrl <= 16) LZP(4, 4, true, r0, nrl, wa);
-    else if (nrl <= 24) LZP(4, 6, true, r0, nrl, wa);
-    else LZP(4, 8, true, r0, nrl, wa);
+    if (nrl <= 4) LZP(4, 1, r0, nrl, wa);
+    else if (nrl <= 8) LZP(4, 2, r0, nrl, wa);
+    else if (nrl <= 16) LZP(4, 4, r0, nrl, wa);
+    else if (nrl <= 24) LZP(4, 6, r0, nrl, wa);
+    else LZP(4, 8, r0, nrl, wa);
   };
-  if (nv <= 32) es(0, nv, true);
-  else if (nv <= 64) {
-    es(0, 32, true);
-    es(32, nv - 32, false);
-  } else if (nv <= 96) LZP(8, 3, false, 0, nv, true);
-  else LZP(8, 4, false, 0, nv, true);
+  for (int r0 = 0; r0 < nv; r0 += 32) es(r0, std::min(32, nv - r0), r0 == 0);
 #undef LZP
   hipLaunchKernelGGL(lz_finish_kernel, dim3(1), dim3(256), 0, s, st, 1, k, nv, newest, 0.0);
   return hipGetLastError();
