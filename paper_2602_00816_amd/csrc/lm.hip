@@ -703,6 +703,27 @@ __device__ inline double gelu_t_grad(double u) {
 }
 __device__ inline double sigm(double x) { return 1.0 / (1.0 + exp(-x)); }
 
+// SwiGLU output at both points, (s(a) v_a, s(b) v_b) with s(x) = x sigmoid(x),
+// gate a, b = gm +- gd and up u = um +- ud, returned as its half sum om and half
+// difference od, in fp32 without forming the two values and subtracting them:
+//   (s(a) + s(b)) / 2 is taken directly;
+//   (s(a) - s(b)) / 2 = (gd (sig(a) + sig(b)) + gm (sig(a) - sig(b))) / 2, and
+//   sig(a) - sig(b) = sig(a) sig(-b) (1 - e^(-2 gd)) with expm1 for the last
+//   factor, so the difference channel keeps fp32 relative accuracy for any gd
+//   (no loss of order gd / gm);
+//   om = S um + D ud and od = S ud + D um for the gate's half sum S and half
+//   difference D.
+__device__ inline void swiglu_pair(float gm, float gd, float um, float ud, float& om, float& od) {
+  const float a = gm + gd, b = gm - gd;
+  const float eb = expf(-b);
+  const float sa = 1.f / (1.f + expf(-a)), sb = 1.f / (1.f + eb);
+  const float snb = b < 0.f ? 1.f - sb : eb * sb;   // sig(-b), accurate on both sides
+  const float dsig = sa * snb * -expm1f(-2.f * gd);
+  const float S = 0.5f * (a * sa + b * sb), D = 0.5f * (gd * (sa + sb) + gm * dsig);
+  om = S * um + D * ud;
+  od = S * ud + D * um;
+}
+
 template <typename T>
 __global__ void gelu_fwd_kernel(PairT<T> z, const T* um, const T* ud, int64_t n) {
   GRID_LOOP(i, n) {
@@ -735,13 +756,7 @@ __global__ void swiglu_fwd4_kernel(PairT<T> z, const T* gum, const T* gud, int F
   const float4 um = ld4f(gum, iu), ud = ld4f(gud, iu);
   float om[4], od[4];
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const double gp = (double)f4e(gm, e) + (double)f4e(gd, e), gn = (double)f4e(gm, e) - (double)f4e(gd, e);
-    const double vp = (double)f4e(um, e) + (double)f4e(ud, e), vn = (double)f4e(um, e) - (double)f4e(ud, e);
-    const double p = gp * sigm(gp) * vp, q = gn * sigm(gn) * vn;
-    om[e] = (float)(0.5 * (p + q));
-    od[e] = (float)(0.5 * (p - q));
-  }
+  for (int e = 0; e < 4; ++e) swiglu_pair(f4e(gm, e), f4e(gd, e), f4e(um, e), f4e(ud, e), om[e], od[e]);
   st4f(z.m, io, om[0], om[1], om[2], om[3]);
   st4f(z.d, io, od[0], od[1], od[2], od[3]);
 }
@@ -781,9 +796,10 @@ __global__ void swiglu_fwd_kernel(PairT<T> z, const T* gum, const T* gud, int ro
   GRID_LOOP(i, n) {
     const int64_t t = i / F, c = i % F;
     const int64_t ig = t * 2 * F + c, iu = ig + F;
-    const double gp = (double)ldf(gum, ig) + (double)ldf(gud, ig), gn = (double)ldf(gum, ig) - (double)ldf(gud, ig);
-    const double vp = (double)ldf(gum, iu) + (double)ldf(gud, iu), vn = (double)ldf(gum, iu) - (double)ldf(gud, iu);
-    put_pair(z, i, gp * sigm(gp) * vp, gn * sigm(gn) * vn);
+    float om, od;
+    swiglu_pair(ldf(gum, ig), ldf(gud, ig), ldf(gum, iu), ldf(gud, iu), om, od);
+    stf(z.m, i, om);
+    stf(z.d, i, od);
   }
 }
 template <typename T>
