@@ -221,6 +221,18 @@ __device__ inline float f4e(const float4& v, int e) { return e == 0 ? v.x : (e =
 // reductions, x reread from the caches between the passes.  Same arithmetic
 // as norm_fwd_kernel.
 constexpr int NORM_FWD_ROWS = 8;
+// An empty statement that claims to modify the cached row values, so that the
+// compiler recomputes their fp64 conversions in each pass instead of keeping
+// them live (twice the registers) from the previous one.  No instruction.
+template <int CPL>
+__device__ inline void reload_barrier(float4 (&a)[CPL], float4 (&b)[CPL]) {
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) {
+    asm volatile("" : "+v"(a[c].x), "+v"(a[c].y), "+v"(a[c].z), "+v"(a[c].w));
+    asm volatile("" : "+v"(b[c].x), "+v"(b[c].y), "+v"(b[c].z), "+v"(b[c].w));
+  }
+}
+
 template <typename T, int CPL>
 __global__ __launch_bounds__(NT) void norm_fwd_wave_kernel(PairT<T> y, const float* xm, const float* xd, int rows, bool ln,
                                                            const T* thg, const float* vg, const T* thb, const float* vb,
@@ -233,12 +245,19 @@ __global__ __launch_bounds__(NT) void norm_fwd_wave_kernel(PairT<T> y, const flo
     const int row = r0 + i;
     if (row >= rows) break;
     const int64_t o = (int64_t)row * DM + 4 * lane;
+    // the lane's 4 CPL elements of both channels, loaded once (all loads in flight together)
+    float4 xa[CPL], xb[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      xa[c] = ld(xm, o + 256 * c);
+      xb[c] = ld(xd, o + 256 * c);
+    }
     double mup = 0.0, mum = 0.0;
     if (ln) {
       double sp = 0.0, sm = 0.0;
-#pragma unroll 2
+#pragma unroll
       for (int c = 0; c < CPL; ++c) {
-        const float4 a = ld(xm, o + 256 * c), b = ld(xd, o + 256 * c);
+        const float4 a = xa[c], b = xb[c];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           sp += (double)f4e(a, e) + (double)f4e(b, e);
@@ -248,10 +267,12 @@ __global__ __launch_bounds__(NT) void norm_fwd_wave_kernel(PairT<T> y, const flo
       mup = wave_sum(sp) / DM;
       mum = wave_sum(sm) / DM;
     }
+    // keep the fp32 values, not their fp64 conversions, live across the passes
+    reload_barrier<CPL>(xa, xb);
     double qp = 0.0, qm = 0.0;
-#pragma unroll 2
+#pragma unroll
     for (int c = 0; c < CPL; ++c) {
-      const float4 a = ld(xm, o + 256 * c), b = ld(xd, o + 256 * c);
+      const float4 a = xa[c], b = xb[c];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const double p = (double)f4e(a, e) + (double)f4e(b, e) - mup;
@@ -262,10 +283,11 @@ __global__ __launch_bounds__(NT) void norm_fwd_wave_kernel(PairT<T> y, const flo
     }
     const double rp = 1.0 / sqrt(wave_sum(qp) / DM + neps);
     const double rmi = 1.0 / sqrt(wave_sum(qm) / DM + neps);
-#pragma unroll 2
+    reload_barrier<CPL>(xa, xb);
+#pragma unroll
     for (int c = 0; c < CPL; ++c) {
       const int col = 256 * c + 4 * lane;
-      const float4 a = ld(xm, o + 256 * c), b = ld(xd, o + 256 * c);
+      const float4 a = xa[c], b = xb[c];
       const float4 g4 = ld4f(thg, col), v4 = ld(vg, col);
       float4 b4 = make_float4(0.f, 0.f, 0.f, 0.f), w4 = b4;
       if (thb) {
