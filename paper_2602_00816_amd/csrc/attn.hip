@@ -39,8 +39,10 @@
 //                 heads of its group), S = Q K^T tiles, dV = P^T dO, dK = dS^T Q
 // K/V (or Q/dO) tiles are streamed into a double-buffered LDS ring by direct
 // global-to-LDS loads.  LDS tiles are [rows][D] with the 16-byte chunk c of
-// row r at c ^ f(r), f a bit reversal of low row bits, which keeps 16-byte
-// row reads and both kinds of transposing reads free of bank conflicts.
+// row r at c ^ f(r), f a bit reversal of low row bits.  Hardware counters
+// show no bank conflicts for the 32-row 16-byte fragment reads and both kinds
+// of transposing reads; the 16-row fragment reads of flash_bwd_kv (ld_k16)
+// still conflict.
 #include "common.h"
 #include "kernels.h"
 
