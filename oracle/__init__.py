@@ -20,5 +20,10 @@ Contents (each function names the passage of the paper it follows):
 * ``block``   - the block-diagonal hypothesis statistics (section 6, Exp I).
 
 Parity status: every function here is pinned by ``tests/test_oracle_*.py``
-against closed forms, invariants or brute force; none is "parity unpinned".
+against closed forms, invariants or brute force.  The windowed
+reorthogonalisation (Appendix C's window of r stored vectors) is pinned by the
+orthogonality pattern it must leave: each new Lanczos vector orthogonal to
+rounding level against exactly the r most recent vectors, and measurably not
+against the one just outside the window, on a spectrum whose Ritz values
+converge early.
 """

@@ -132,15 +132,3 @@ def slq(hvp, probes, m: int, reorth: int = FULL, window: int = 0):
         steps.append(len(a))
     trace = P * float(np.mean(alpha1))
     return nodes, weights, trace, steps
-
-
-def density(nodes, weights, grid: np.ndarray, sigma: float) -> np.ndarray:
-    """Gaussian-broadened density (1/s) sum_j sum_i tau_i delta(lambda - lambda_i).
-
-    The paper does not state its display kernel; this is for plotting only.
-    """
-    out = np.zeros_like(grid, dtype=np.float64)
-    for lam, tau in zip(nodes, weights):
-        for l, t in zip(lam, tau):
-            out += t * np.exp(-0.5 * ((grid - l) / sigma) ** 2) / (sigma * np.sqrt(2 * np.pi))
-    return out / len(nodes)

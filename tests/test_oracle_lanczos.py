@@ -104,6 +104,39 @@ def test_window_at_least_m_equals_full():
     assert np.array_equal(a1, a2) and np.array_equal(b1, b2)
 
 
+@pytest.mark.parametrize("r", [1, 2, 4, 8])
+def test_window_orthogonality_pattern(r):
+    """Appendix C's window: the new Lanczos vector is reorthogonalised against
+    the r most recent vectors (q_k among them).  Pinned by the orthogonality
+    that leaves behind, on a spectrum with three outlying eigenvalues whose
+    Ritz values converge within a few steps (so that plain Lanczos loses
+    orthogonality quickly): every q_{k+1} is orthogonal to rounding level
+    (1e-13) to each vector of its window, and its product with the vector just
+    outside the window rises to far above that in some step (at least 1e-12
+    and a thousand times the largest in-window product; the three-term
+    recurrence itself keeps q_{k-1} close, so r = 1 shows the smallest gap).  A
+    window one vector too wide passes the first test but fails the second; one
+    too narrow fails the first."""
+    P = 400
+    d = np.concatenate([[100.0, 80.0, 60.0], np.linspace(-1, 1, P - 3)])
+    q = np.random.default_rng(0).standard_normal(P)
+    m = 60
+    _, _, Q = L.lanczos(_diag_op(d), q, m, reorth=L.WINDOW, window=r)
+    Q = np.array(Q)
+    assert len(Q) == m + 1
+    inside, outside = [], []
+    for k in range(1, len(Q)):
+        inside += [abs(Q[k] @ Q[j]) for j in range(max(0, k - r), k)]
+        if k - r - 1 >= 0:
+            outside.append(abs(Q[k] @ Q[k - r - 1]))
+    assert max(inside) <= 1e-13
+    assert max(outside) >= 1e-12 and max(outside) >= 1e3 * max(inside)
+    # r = 1 and r = 2 keep only what the three-term recurrence already removes
+    # in exact arithmetic: far older vectors lose orthogonality as without
+    # reorthogonalisation
+    assert max(abs(Q[k] @ Q[0]) for k in range(r + 1, len(Q))) >= 1e-6
+
+
 def test_no_reorth_ghosts_appear():
     # section 4: without reorthogonalisation, converged Ritz values repeat ("ghosts")
     P = 400
