@@ -21,11 +21,13 @@
  *    fdh_param_layout (per-layer blocks contiguous).  Element type float32
  *    (dtype FDH_F32) or bfloat16 bit patterns, uint16 (FDH_BF16).  Directions
  *    v and products Hv are always float32 of length fdh_num_params().
- *  - Tokens: int32 [B, S] row-major, values in [0, vocab).
+ *  - Tokens: int32 [B, S] row-major, values in [0, vocab); a token outside
+ *    that range is an FDH_ERR_INVALID_ARG (never clamped into a wrong answer).
  *  - Streams: all device work is enqueued on the stream given to fdh_create,
- *    in call order.  fdh_hvp returns without waiting.  Calls that return host
- *    results (lanczos, slq_density, block_stats, last_losses) wait for the
- *    stream before returning.
+ *    in call order.  fdh_hvp and fdh_hvp_bound wait for the stream at their
+ *    end, to report non-finite values and bad tokens; so do the calls that
+ *    return host results (lanczos, slq_density, block_stats, last_losses,
+ *    the binds, cg_solve, block_diagonal).
  *  - Errors: every call returns an fdh_status; negative values are errors and
  *    leave outputs unspecified; fdh_last_error gives a message.  No call
  *    throws.  One context per host thread.
@@ -133,12 +135,15 @@ fdh_status fdh_param_layout(const fdh_ctx* ctx, fdh_block* out, int32_t cap, int
 fdh_status fdh_workspace_bytes(const fdh_ctx* ctx, int32_t B, int32_t S, int32_t m,
                                const fdh_lanczos_opts* o, size_t* bytes);
 /* Hand the library a device buffer of at least the queried size, 256-byte aligned.
- * The caller keeps ownership and must keep it alive while the context uses it. */
+ * The caller keeps ownership and must keep it alive while the context uses it.
+ * On an error the workspace and carve already in use stay in force.  dev = NULL
+ * with bytes = 0 detaches the workspace (the other arguments are ignored): the
+ * context then holds no pointer into caller memory until the next call. */
 fdh_status fdh_set_workspace(fdh_ctx* ctx, void* dev, size_t bytes, int32_t B, int32_t S,
                              int32_t m, const fdh_lanczos_opts* o);
 
-/* Synthetic inputs (SplitMix64 counter generator, see DESIGN notes in the
- * source): theta with N(0, 0.02) matrices, unit gains, zero biases (bf16 by
+/* Synthetic inputs (the SplitMix64 counter generator of Steele, Lea and Flood,
+ * OOPSLA 2014, in counter form): theta with N(0, 0.02) matrices, unit gains, zero biases (bf16 by
  * round-to-nearest-even); tokens uniform or Zipf(1.1); unit vectors. */
 fdh_status fdh_init_params(fdh_ctx* ctx, void* params_dev, uint64_t seed);
 fdh_status fdh_make_tokens(fdh_ctx* ctx, int32_t* tokens_dev, int32_t B, int32_t S,
@@ -151,7 +156,11 @@ fdh_status fdh_set_quad_diag(fdh_ctx* ctx, const float* diag_dev);
 /* Hv ~= (grad L(theta + eps v) - grad L(theta - eps v)) / (2 eps) on one batch
  * (section 3.1; Algorithm 1 with a single batch).  params: P elements of the
  * context dtype; v, hv: float32 [P]; tokens int32 [B, S] (ignored for QUAD_DIAG).
- * hv must not alias params or v. */
+ * hv must not alias params or v.  Waits for the stream before returning.
+ * Language-model families: FDH_ERR_NONFINITE when v holds a NaN or an
+ * infinity, or when the product does (both scanned on the device, one extra
+ * read of Hv); FDH_ERR_INVALID_ARG when a token lies outside [0, vocab).  On
+ * either error hv is unspecified.  (QUAD_DIAG, a test operator, is not scanned.) */
 fdh_status fdh_hvp(fdh_ctx* ctx, const void* params_dev, const float* v_dev, double eps,
                    const int32_t* tokens_dev, int32_t B, int32_t S, float* hv_dev);
 
@@ -160,8 +169,9 @@ fdh_status fdh_last_losses(fdh_ctx* ctx, double* loss_plus, double* loss_minus);
 
 /* Fix the operator used by fdh_hvp_bound / fdh_lanczos / fdh_slq_density /
  * fdh_cg_solve / fdh_block_diagonal: one batch of next-token targets (the same
- * as fdh_bind_dataset with one unlabelled batch and FDH_REDUCE_MEAN).  The
- * pointers are kept (not copied) and must stay valid. */
+ * as fdh_bind_dataset with one unlabelled batch and FDH_REDUCE_MEAN, whose
+ * token scan and wait it shares).  The pointers are kept (not copied) and must
+ * stay valid. */
 fdh_status fdh_bind(fdh_ctx* ctx, const void* params_dev, const int32_t* tokens_dev,
                     int32_t B, int32_t S, double eps);
 
@@ -177,9 +187,10 @@ fdh_status fdh_bind(fdh_ctx* ctx, const void* params_dev, const int32_t* tokens_
  * padding) with label -100: causal attention then keeps it out of every kept
  * target's context, so no attention mask is needed.  The batch array is
  * copied, the device pointers are kept (not copied) and must stay valid.
- * *n_targets (may be NULL) receives sum_b w_b.  Labelled batches are scanned
+ * *n_targets (may be NULL) receives sum_b w_b.  Tokens and labels are scanned
  * on the device and the call waits for the stream; FDH_ERR_INVALID_ARG for a
- * label outside [0, vocab) other than -100, or when no target is left.
+ * token outside [0, vocab), a label outside [0, vocab) other than -100, or
+ * when no target is left.
  * QUAD_DIAG contexts take nbatch = 0. */
 fdh_status fdh_bind_dataset(fdh_ctx* ctx, const void* params_dev, const fdh_batch* batches, int32_t nbatch,
                             double eps, int32_t reduction, int64_t* n_targets);
@@ -187,7 +198,8 @@ fdh_status fdh_bind_dataset(fdh_ctx* ctx, const void* params_dev, const fdh_batc
 /* hv = H v of the bound operator (fdh_bind or fdh_bind_dataset): one FD-HVP
  * per batch, accumulated into hv in batch order; fdh_last_losses then returns
  * the dataset losses at theta +- eps v.  v, hv: float32 [P] on device, not
- * aliasing each other or the parameters.  Enqueued on the context stream. */
+ * aliasing each other or the parameters.  Waits for the stream and reports
+ * non-finite values and bad tokens as fdh_hvp does. */
 fdh_status fdh_hvp_bound(fdh_ctx* ctx, const float* v_dev, float* hv_dev);
 
 /* Krylov-basis offload (section 7 notes that storing the whole Krylov

@@ -58,6 +58,12 @@ fdh_status fdh_testing_timing(fdh_ctx* ctx, int32_t enable);
  * (Lanczos: every operand read or written once).  Clears the accumulators. */
 fdh_status fdh_testing_timing_read(fdh_ctx* ctx, double* out16);
 
+/* Digest (FNV-1a) of the workspace carve the context has adopted: every
+ * buffer's offset and size, the basis geometry, the attention path, the plan
+ * and the workspace pointer.  Host-only; lets tests check that size queries
+ * and rejected fdh_set_workspace calls leave the carve in use untouched. */
+fdh_status fdh_testing_layout_digest(const fdh_ctx* ctx, uint64_t* out);
+
 /* Plain device copy of `bytes` bytes (16-byte vectors), enqueued on hip_stream;
  * used to calibrate hardware byte counters against a known traffic. */
 fdh_status fdh_testing_copy(void* dst, const void* src, size_t bytes, void* hip_stream);

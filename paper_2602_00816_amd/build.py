@@ -2,7 +2,8 @@
 
 Every source under csrc/ is compiled with hipcc (packed-fp32 code generation
 disabled) into an object, in parallel, and linked into one shared library next
-to this file.  Usage: ``python -m paper_2602_00816_amd.build`` or ``build()``.
+to this file.  Usage: ``python -m paper_2602_00816_amd.build [--incremental]``
+or ``build()``.
 """
 from __future__ import annotations
 
@@ -28,8 +29,19 @@ SOURCES = ["gemm.hip", "attn.hip", "rng.hip", "vec.hip", "lm.hip", "engine.hip",
 EXTRA = {"attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
-def _compile(src: str) -> str:
+def _headers_mtime() -> float:
+    inc = os.path.join(os.path.dirname(HERE), "include")
+    paths = [os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".h")]
+    paths += [os.path.join(inc, f) for f in os.listdir(inc) if f.endswith(".h")]
+    return max(os.path.getmtime(p) for p in paths)
+
+
+def _compile(src: str, incremental: bool = False, hdr: float = 0.0) -> str:
     obj = os.path.join(OUT, os.path.splitext(src)[0] + ".o")
+    if incremental and os.path.exists(obj):
+        t = os.path.getmtime(obj)
+        if t >= os.path.getmtime(os.path.join(CSRC, src)) and t >= hdr:
+            return obj
     cmd = [HIPCC, *FLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
@@ -37,11 +49,14 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
+def build(verbose: bool = False, incremental: bool = False) -> str:
+    """Compile every source (or, with incremental, only those whose object is
+    older than the source or any header) and link the library."""
     os.makedirs(OUT, exist_ok=True)
     workers = min(len(SOURCES), max(1, (os.cpu_count() or 2)))
+    hdr = _headers_mtime()
     with cf.ThreadPoolExecutor(workers) as ex:
-        objs = list(ex.map(_compile, SOURCES))
+        objs = list(ex.map(lambda f: _compile(f, incremental, hdr), SOURCES))
     tmp = LIB + ".tmp"
     cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -54,5 +69,5 @@ def build(verbose: bool = False) -> str:
 
 
 if __name__ == "__main__":
-    build(verbose=True)
+    build(verbose=True, incremental="--incremental" in sys.argv)
     sys.exit(0)

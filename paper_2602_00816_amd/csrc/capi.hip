@@ -112,22 +112,17 @@ fdh_status fdh_param_layout(const fdh_ctx* ctx, fdh_block* out, int32_t cap, int
 fdh_status fdh_workspace_bytes(const fdh_ctx* ctx, int32_t B, int32_t S, int32_t m, const fdh_lanczos_opts* o,
                                size_t* bytes) {
   if (!ctx || !ctx->eng || !bytes || B < 0 || S < 0 || m < 0 || (m > 0 && !o)) return FDH_ERR_INVALID_ARG;
-  *bytes = ctx->eng->plan(B, S, m, o, false);
+  try {
+    *bytes = ctx->eng->plan(B, S, m, o, nullptr);  // a query: the adopted carve is left alone
+  } catch (...) {
+    return FDH_ERR_INVALID_ARG;
+  }
   return FDH_OK;
 }
 
 fdh_status fdh_set_workspace(fdh_ctx* ctx, void* dev, size_t bytes, int32_t B, int32_t S, int32_t m,
                              const fdh_lanczos_opts* o) {
-  return run(ctx, [&](fdh::Engine& e) -> int {
-    if (!dev || B < 0 || S < 0 || m < 0 || (m > 0 && !o)) { e.err = "bad workspace arguments"; return FDH_ERR_INVALID_ARG; }
-    if ((reinterpret_cast<uintptr_t>(dev) & 255) != 0) { e.err = "workspace must be 256-byte aligned"; return FDH_ERR_WORKSPACE; }
-    const size_t need = e.plan(B, S, m, o, false);
-    if (bytes < need) { e.err = "workspace smaller than fdh_workspace_bytes"; return FDH_ERR_WORKSPACE; }
-    e.plan(B, S, m, o, true);
-    e.ws = (char*)dev;
-    e.ws_bytes = bytes;
-    return FDH_OK;
-  });
+  return run(ctx, [&](fdh::Engine& e) { return e.set_workspace(dev, bytes, B, S, m, o); });
 }
 
 fdh_status fdh_init_params(fdh_ctx* ctx, void* params_dev, uint64_t seed) {
@@ -319,6 +314,12 @@ extern "C" fdh_status fdh_testing_timing_read(fdh_ctx* ctx, double* out16) {
     e.timing.reset();
     return FDH_OK;
   });
+}
+
+extern "C" fdh_status fdh_testing_layout_digest(const fdh_ctx* ctx, uint64_t* out) {
+  if (!ctx || !ctx->eng || !out) return FDH_ERR_INVALID_ARG;
+  *out = ctx->eng->layout_digest();
+  return FDH_OK;
 }
 
 extern "C" fdh_status fdh_testing_copy(void* dst, const void* src, size_t bytes, void* hip_stream) {

@@ -58,7 +58,34 @@ struct Timing {
 int ritz_diagnostics(const double* alpha, const double* beta, int s, double tol, double* nodes, double* weights,
                      double* resid, int32_t* copies, int32_t* spurious, int32_t* ghosts);
 
-class Engine {
+// One carve of the workspace: the span of every buffer for a plan (largest
+// token batch, Lanczos steps and options) and the attention path it serves.
+// Engine::plan fills a WsLayout; the engine adopts it only once a workspace
+// large enough for it has been handed over, so that size queries never move
+// the buffers in use.
+struct WsLayout {
+  struct LayerSpans {
+    Span x_in_m, x_in_d, a_m, a_d, qkv_m, qkv_d, P_m, P_d, st, o_m, o_d, xmid_m, xmid_d, b_m, b_d, u_m, u_d, z_m, z_d;
+  };
+  std::vector<LayerSpans> ls;
+  Span xL_m, xL_d, f_m, f_d, lo, sc_m, sc_d, log_m, log_d, dlog_m, dlog_d, rowloss, losses;
+  Span dx0_m, dx0_d, dx1_m, dx1_d, dxo_m, dxo_d, dz_m, dz_d, dgu_m, dgu_d, dudf, db_m, db_d, gpart, do_m, do_d, dS_m, dS_d;
+  Span dqkv_m, dqkv_d, dqkvo_m, dqkvo_d, gqa_m, gqa_d, dl, da_m, da_d, colpart, keys, rope, cdf, gpartial, bpart, bout;
+  Span tcount;  // two int64 counters of fdh_bind_dataset
+  Span nfflag;  // non-finite flags of the input direction and the product (two int32)
+  Span wsplit;  // split-K partial products of the weight-gradient GEMMs
+  Span lz_w, lz_q, lz_qp, lz_basis, lz_alpha, lz_beta, lz_coef, lz_gram, lz_partial, lz_flag, lz_maxabs;
+  int64_t lz_ldq = 0;   // basis row stride (elements, multiple of 8)
+  int lz_dev_rows = 0;  // basis rows held in the workspace
+  // attention path: fused kernels (bf16, head dim 64 or 128, S a multiple of
+  // 128) or score/probability matrices in the workspace
+  bool fused = false;
+  int planB = 0, planS = 0, planM = 0;
+  fdh_lanczos_opts planO{};
+  size_t total = 0;     // bytes the carve needs
+};
+
+class Engine : public WsLayout {
  public:
   explicit Engine(const fdh_model_config& cfg, hipStream_t stream);
 
@@ -76,14 +103,15 @@ class Engine {
   // workspace
   char* ws = nullptr;
   size_t ws_bytes = 0;
-  int planB = 0, planS = 0, planM = 0;
-  // attention path of the current plan: fused kernels (bf16, head dim 64 or
-  // 128, S a multiple of 128) or score/probability matrices in the workspace
-  bool fused = false;
   bool force_unfused = false;   // testing: plan the unfused path even where the fused one applies
   bool force_unsplit = false;   // testing: weight-gradient GEMMs over the whole token range
-  fdh_lanczos_opts planO{};
-  size_t plan(int B, int S, int m, const fdh_lanczos_opts* o, bool carve);
+  // the carve for token batches up to [B, S] and m Lanczos steps with options
+  // o (o may be null when m == 0), written into *out; changes nothing else
+  size_t plan(int B, int S, int m, const fdh_lanczos_opts* o, WsLayout* out) const;
+  // plan, check that bytes covers it, then adopt the carve and the buffer
+  int set_workspace(void* dev, size_t bytes, int B, int S, int m, const fdh_lanczos_opts* o);
+  // order-sensitive digest of the adopted carve (testing)
+  uint64_t layout_digest() const;
 
   // operator binding for Lanczos / CG / the block-diagonal test: parameters,
   // step and the batches whose token-weighted average the operator is
@@ -100,7 +128,8 @@ class Engine {
   int hvp(const void* params, const float* v, double eps, const int32_t* tok, int B, int S, float* hv);
   int hvp_batches(const void* params, const float* v, double eps, const BatchRef* bt, int nb, double inv_n, float* hv);
   int bind_batches(const void* params, const BatchRef* bt, int nb, double eps, int reduction, int64_t* targets);
-  int hvp_bound(const float* v, float* hv);
+  int hvp_bound(const float* v, float* hv);        // checked: waits, reports NaN/Inf and bad tokens
+  int hvp_bound_async(const float* v, float* hv);  // enqueued only (Lanczos, CG, block test)
   int last_losses(double* lp, double* lm);
   int lanczos(int m, uint64_t seed, const fdh_lanczos_opts& o, double* alpha, double* beta, int* steps);
   int slq(int probes, int m, uint64_t seed, const fdh_lanczos_opts& o, double* nodes, double* weights, int* steps,
@@ -116,25 +145,13 @@ class Engine {
 
  private:
   int check_batch(const int32_t* tok, int B, int S);
+  int finish_checked(const float* hv);
   template <typename T>
   int hvp_t(const T* th, const float* v, double eps, const int32_t* tok, const int32_t* lab, int B, int S, double inv_n,
             bool acc, float* hv);
   template <typename B> int lanczos_t(int m, uint64_t seed, const fdh_lanczos_opts& o, double* alpha, double* beta, int* steps);
   template <typename T> void* wsp(const Span& s) const { return (void*)(ws + s.off); }
 
-  // workspace spans
-  struct LayerSpans {
-    Span x_in_m, x_in_d, a_m, a_d, qkv_m, qkv_d, P_m, P_d, st, o_m, o_d, xmid_m, xmid_d, b_m, b_d, u_m, u_d, z_m, z_d;
-  };
-  std::vector<LayerSpans> ls;
-  Span xL_m, xL_d, f_m, f_d, lo, sc_m, sc_d, log_m, log_d, dlog_m, dlog_d, rowloss, losses;
-  Span dx0_m, dx0_d, dx1_m, dx1_d, dxo_m, dxo_d, dz_m, dz_d, dgu_m, dgu_d, dudf, db_m, db_d, gpart, do_m, do_d, dS_m, dS_d;
-  Span dqkv_m, dqkv_d, dqkvo_m, dqkvo_d, gqa_m, gqa_d, dl, da_m, da_d, colpart, keys, rope, cdf, gpartial, bpart, bout;
-  Span tcount;  // two int64 counters of fdh_bind_dataset
-  Span wsplit;  // split-K partial products of the weight-gradient GEMMs
-  Span lz_w, lz_q, lz_qp, lz_basis, lz_alpha, lz_beta, lz_coef, lz_gram, lz_partial, lz_flag, lz_maxabs;
-  int64_t lz_ldq = 0;  // basis row stride (elements, multiple of 8)
-  int lz_dev_rows = 0;  // basis rows held in the workspace
   // basis offload: at most off_rows rows in the workspace (-1: all), the rest
   // in caller-owned pinned host memory (device-side address)
   int off_rows = -1;

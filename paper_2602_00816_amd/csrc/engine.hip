@@ -138,25 +138,26 @@ static int wgrad_splits(int M, int N, int T_) {
 // ---------------------------------------------------------------------------
 // workspace plan
 // ---------------------------------------------------------------------------
-size_t Engine::plan(int B, int S, int m, const fdh_lanczos_opts* o, bool carve) {
+size_t Engine::plan(int B, int S, int m, const fdh_lanczos_opts* o, WsLayout* out) const {
+  WsLayout W;
   size_t cur = 0;
   auto take = [&](Span& s, size_t bytes) {
     s.off = cur;
     s.bytes = bytes;
     cur += (bytes + ALIGN - 1) / ALIGN * ALIGN;
   };
-  Span dummy;
   const size_t ob = bf16 ? 2 : 4;
   if (!quad) {
     const size_t T_ = (size_t)B * S;
     const size_t td = T_ * d, tq = T_ * qkvd, ta = T_ * (size_t)Hq * dh;
     const size_t tu = T_ * (size_t)(gpt2 ? F : 2 * F), tz = T_ * F;
-    fused = bf16 && !force_unfused && flash_supported(dh, S);
+    W.fused = bf16 && !force_unfused && flash_supported(dh, S);
+    const bool fused = W.fused;
     const size_t pp = fused ? 0 : (size_t)B * Hq * S * S;   // score-shaped matrices (unfused path only)
     const size_t rows = (size_t)B * Hq * S;
-    ls.assign(L, LayerSpans{});
+    W.ls.assign(L, LayerSpans{});
     for (int l = 0; l < L; ++l) {
-      LayerSpans& s = ls[l];
+      LayerSpans& s = W.ls[l];
       take(s.x_in_m, td * 4); take(s.x_in_d, td * 4);
       take(s.a_m, td * ob); take(s.a_d, td * ob);
       take(s.qkv_m, tq * ob); take(s.qkv_d, tq * ob);
@@ -168,30 +169,30 @@ size_t Engine::plan(int B, int S, int m, const fdh_lanczos_opts* o, bool carve) 
       take(s.u_m, tu * ob); take(s.u_d, tu * ob);
       take(s.z_m, tz * ob); take(s.z_d, tz * ob);
     }
-    take(xL_m, td * 4); take(xL_d, td * 4);
-    take(f_m, td * ob); take(f_d, td * ob);
-    take(lo, (size_t)P * ob);
-    take(sc_m, pp * 4); take(sc_d, pp * 4);
-    take(log_m, T_ * V * 4); take(log_d, T_ * V * 4);
-    take(dlog_m, T_ * V * ob); take(dlog_d, T_ * V * ob);
-    take(rowloss, 2 * T_ * 8);
-    take(losses, 2 * 8);
-    take(tcount, 2 * 8);
-    take(dx0_m, td * 4); take(dx0_d, td * 4);
-    take(dx1_m, td * 4); take(dx1_d, td * 4);
-    take(dxo_m, td * ob); take(dxo_d, td * ob);
-    take(dz_m, tz * 4); take(dz_d, tz * 4);
-    take(dgu_m, tu * ob); take(dgu_d, tu * ob);
-    take(dudf, gpt2 ? tz * 4 : 0);
-    take(db_m, td * 4); take(db_d, td * 4);
-    take(gpart, std::max(td * 4, (size_t)2 * norm_bwd_groups((int)T_) * d * 8));
-    take(do_m, ta * ob); take(do_d, ta * ob);
-    take(dS_m, pp * ob); take(dS_d, pp * ob);
-    take(dqkv_m, tq * 4); take(dqkv_d, tq * 4);
-    take(dqkvo_m, tq * ob); take(dqkvo_d, tq * ob);
-    take(gqa_m, Hq != Hk && !fused ? ta * 4 : 0); take(gqa_d, Hq != Hk && !fused ? ta * 4 : 0);
-    take(dl, fused ? rows * 8 : 0);
-    take(da_m, td * 4); take(da_d, td * 4);
+    take(W.xL_m, td * 4); take(W.xL_d, td * 4);
+    take(W.f_m, td * ob); take(W.f_d, td * ob);
+    take(W.lo, (size_t)P * ob);
+    take(W.sc_m, pp * 4); take(W.sc_d, pp * 4);
+    take(W.log_m, T_ * V * 4); take(W.log_d, T_ * V * 4);
+    take(W.dlog_m, T_ * V * ob); take(W.dlog_d, T_ * V * ob);
+    take(W.rowloss, 2 * T_ * 8);
+    take(W.losses, 2 * 8);
+    take(W.tcount, 3 * 8);
+    take(W.dx0_m, td * 4); take(W.dx0_d, td * 4);
+    take(W.dx1_m, td * 4); take(W.dx1_d, td * 4);
+    take(W.dxo_m, td * ob); take(W.dxo_d, td * ob);
+    take(W.dz_m, tz * 4); take(W.dz_d, tz * 4);
+    take(W.dgu_m, tu * ob); take(W.dgu_d, tu * ob);
+    take(W.dudf, gpt2 ? tz * 4 : 0);
+    take(W.db_m, td * 4); take(W.db_d, td * 4);
+    take(W.gpart, std::max(td * 4, (size_t)2 * norm_bwd_groups((int)T_) * d * 8));
+    take(W.do_m, ta * ob); take(W.do_d, ta * ob);
+    take(W.dS_m, pp * ob); take(W.dS_d, pp * ob);
+    take(W.dqkv_m, tq * 4); take(W.dqkv_d, tq * 4);
+    take(W.dqkvo_m, tq * ob); take(W.dqkvo_d, tq * ob);
+    take(W.gqa_m, Hq != Hk && !fused ? ta * 4 : 0); take(W.gqa_d, Hq != Hk && !fused ? ta * 4 : 0);
+    take(W.dl, fused ? rows * 8 : 0);
+    take(W.da_m, td * 4); take(W.da_d, td * 4);
     {
       const int nu = gpt2 ? F : 2 * F;
       size_t mx = 0;
@@ -200,17 +201,18 @@ size_t Engine::plan(int B, int S, int m, const fdh_lanczos_opts* o, bool carve) 
         const int ns = wgrad_splits(sh[0], sh[1], (int)T_);
         if (ns > 1) mx = std::max(mx, (size_t)ns * sh[0] * sh[1] * 4);
       }
-      take(wsplit, mx);
+      take(W.wsplit, mx);
     }
     const size_t maxc = std::max<size_t>({(size_t)qkvd, (size_t)F, (size_t)d, (size_t)1});
-    take(colpart, 64 * maxc * 8);
-    take(keys, T_ * 4);
-    take(rope, (size_t)Smax * dh * 8);
-    take(cdf, (size_t)V * 8);
+    take(W.colpart, 64 * maxc * 8);
+    take(W.keys, T_ * 4);
+    take(W.rope, (size_t)Smax * dh * 8);
+    take(W.cdf, (size_t)V * 8);
   }
-  take(gpartial, 1024 * 8);
-  take(bpart, 256 * 4 * 8);
-  take(bout, (size_t)std::max(L, 1) * 4 * 8);
+  take(W.gpartial, 1024 * 8);
+  take(W.nfflag, 4 * 4);
+  take(W.bpart, 256 * 4 * 8);
+  take(W.bout, (size_t)std::max(L, 1) * 4 * 8);
   // Lanczos
   if (m > 0) {
     const int reorth = o ? o->reorth : FDH_REORTH_NONE;
@@ -218,31 +220,87 @@ size_t Engine::plan(int B, int S, int m, const fdh_lanczos_opts* o, bool carve) 
     int cap = 0;
     if (reorth == FDH_REORTH_FULL) cap = m;
     else if (reorth == FDH_REORTH_WINDOW) cap = std::min(m, o->window);
-    take(lz_w, (size_t)P * 4);
-    take(lz_q, (size_t)P * 4);
-    take(lz_qp, (size_t)P * 4);
+    take(W.lz_w, (size_t)P * 4);
+    take(W.lz_q, (size_t)P * 4);
+    take(W.lz_qp, (size_t)P * 4);
     const int64_t ldq = (P + 7) / 8 * 8;
-    if (carve) lz_ldq = ldq;
+    W.lz_ldq = ldq;
     // with the basis offload only the first off_rows rows live in the workspace
     const int ndev = off_rows >= 0 ? std::min(cap, off_rows) : cap;
-    if (carve) lz_dev_rows = ndev;
-    take(lz_basis, (size_t)ndev * ldq * (bdt == FDH_BF16 ? 2 : 4));
-    take(lz_alpha, (size_t)m * 8);
-    take(lz_beta, (size_t)m * 8);
-    take(lz_coef, 128 * 8);
-    take(lz_gram, 128 * 128 * 8);
-    take(lz_partial, (size_t)RED_BLOCKS * (2 * cap + 1) * 8);
-    take(lz_flag, 2 * 4);
-    take(lz_maxabs, 8);
+    W.lz_dev_rows = ndev;
+    take(W.lz_basis, (size_t)ndev * ldq * (bdt == FDH_BF16 ? 2 : 4));
+    take(W.lz_alpha, (size_t)m * 8);
+    take(W.lz_beta, (size_t)m * 8);
+    take(W.lz_coef, 128 * 8);
+    take(W.lz_gram, 128 * 128 * 8);
+    take(W.lz_partial, (size_t)RED_BLOCKS * (2 * cap + 1) * 8);
+    take(W.lz_flag, 2 * 4);
+    take(W.lz_maxabs, 8);
   }
-  (void)dummy;
-  if (carve) {
-    planB = B;
-    planS = S;
-    planM = m;
-    if (o) planO = *o;
-  }
+  W.planB = B;
+  W.planS = S;
+  W.planM = m;
+  if (o) W.planO = *o;
+  W.total = cur;
+  if (out) *out = std::move(W);
   return cur;
+}
+
+int Engine::set_workspace(void* dev, size_t bytes, int B, int S, int m, const fdh_lanczos_opts* o) {
+  if (!dev && bytes == 0) {  // detach: the context holds no workspace any more
+    static_cast<WsLayout&>(*this) = WsLayout{};
+    ws = nullptr;
+    ws_bytes = 0;
+    lo_for_v = nullptr;
+    return FDH_OK;
+  }
+  if (!dev || B < 0 || S < 0 || m < 0 || (m > 0 && !o)) { err = "bad workspace arguments"; return FDH_ERR_INVALID_ARG; }
+  if ((reinterpret_cast<uintptr_t>(dev) & (ALIGN - 1)) != 0) { err = "workspace must be 256-byte aligned"; return FDH_ERR_WORKSPACE; }
+  WsLayout W;
+  const size_t need = plan(B, S, m, o, &W);
+  if (bytes < need) { err = "workspace smaller than fdh_workspace_bytes"; return FDH_ERR_WORKSPACE; }
+  static_cast<WsLayout&>(*this) = std::move(W);
+  ws = (char*)dev;
+  ws_bytes = bytes;
+  // a perturbation operand written into the previous carve is not in this one
+  lo_for_v = nullptr;
+  return FDH_OK;
+}
+
+// FNV-1a over every span, the basis geometry, the attention path and the plan
+uint64_t Engine::layout_digest() const {
+  uint64_t h = 1469598103934665603ull;
+  auto mix = [&](uint64_t x) {
+    for (int i = 0; i < 8; ++i) {
+      h ^= (x >> (8 * i)) & 0xff;
+      h *= 1099511628211ull;
+    }
+  };
+  auto sp = [&](const Span& x) { mix(x.off); mix(x.bytes); };
+  for (const LayerSpans& s : ls)
+    for (const Span* x : {&s.x_in_m, &s.x_in_d, &s.a_m, &s.a_d, &s.qkv_m, &s.qkv_d, &s.P_m, &s.P_d, &s.st, &s.o_m,
+                          &s.o_d, &s.xmid_m, &s.xmid_d, &s.b_m, &s.b_d, &s.u_m, &s.u_d, &s.z_m, &s.z_d})
+      sp(*x);
+  for (const Span* x : {&xL_m, &xL_d, &f_m, &f_d, &lo, &sc_m, &sc_d, &log_m, &log_d, &dlog_m, &dlog_d, &rowloss,
+                        &losses, &dx0_m, &dx0_d, &dx1_m, &dx1_d, &dxo_m, &dxo_d, &dz_m, &dz_d, &dgu_m, &dgu_d, &dudf,
+                        &db_m, &db_d, &gpart, &do_m, &do_d, &dS_m, &dS_d, &dqkv_m, &dqkv_d, &dqkvo_m, &dqkvo_d, &gqa_m,
+                        &gqa_d, &dl, &da_m, &da_d, &colpart, &keys, &rope, &cdf, &gpartial, &bpart, &bout, &tcount,
+                        &nfflag, &wsplit, &lz_w, &lz_q, &lz_qp, &lz_basis, &lz_alpha, &lz_beta, &lz_coef, &lz_gram,
+                        &lz_partial, &lz_flag, &lz_maxabs})
+    sp(*x);
+  mix((uint64_t)lz_ldq);
+  mix((uint64_t)lz_dev_rows);
+  mix(fused ? 1 : 0);
+  mix((uint64_t)planB);
+  mix((uint64_t)planS);
+  mix((uint64_t)planM);
+  mix((uint64_t)planO.reorth);
+  mix((uint64_t)planO.window);
+  mix((uint64_t)planO.basis_dtype);
+  mix(total);
+  mix((uint64_t)(uintptr_t)ws);
+  mix(ws_bytes);
+  return h;
 }
 
 // ---------------------------------------------------------------------------
@@ -376,7 +434,8 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, c
   // batch of the same product did)
   const bool lo_ready = acc || (lo_for_v == v && lo_for_eps == eps);
   lo_for_v = nullptr;
-  if (!lo_ready) CK(launch_scale_cast<T>(lo, v, eps, P, st));
+  int* nf = (int*)(ws + nfflag.off);  // [0] v non-finite, [1] Hv non-finite, [2] token out of range
+  if (!lo_ready) CK(launch_scale_cast<T>(lo, v, eps, P, st, nf));
   if (llama) CK(launch_rope_table((double*)(ws + rope.off), S, dh, (double)cfg.rope_base, st));
 
   // ---- linear helpers ----
@@ -500,7 +559,7 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, c
   {
     PairF x0{F32(ls.empty() ? xL_m : ls[0].x_in_m), F32(ls.empty() ? xL_d : ls[0].x_in_d)};
     CK(launch_embed_fwd<T>(x0, tok, T_, S, d, V, th + wte.off, v + wte.off, gpt2 ? th + wpe.off : nullptr,
-                           gpt2 ? v + wpe.off : nullptr, eps, st));
+                           gpt2 ? v + wpe.off : nullptr, eps, nf + 2, st));
   }
   for (int l = 0; l < L; ++l) {
     const LayerRefs& R = layers[l];
@@ -797,11 +856,29 @@ int Engine::hvp(const void* params, const float* v, double eps, const int32_t* t
     else CK(launch_quad_diag_hvp<float>((const float*)params, quad_diag, v, eps, hv, P, stream));
     return FDH_OK;
   }
-  const int rc = check_batch(tok, B, S);
+  int rc = check_batch(tok, B, S);
   if (rc != FDH_OK) return rc;
   const double inv_n = 1.0 / ((double)B * (S - 1));
-  if (bf16) return hvp_t<bf16_t>((const bf16_t*)params, v, eps, tok, nullptr, B, S, inv_n, false, hv);
-  return hvp_t<float>((const float*)params, v, eps, tok, nullptr, B, S, inv_n, false, hv);
+  CK(launch_fill_f32((float*)(ws + nfflag.off), 4, 0.f, stream));
+  rc = bf16 ? hvp_t<bf16_t>((const bf16_t*)params, v, eps, tok, nullptr, B, S, inv_n, false, hv)
+            : hvp_t<float>((const float*)params, v, eps, tok, nullptr, B, S, inv_n, false, hv);
+  if (rc != FDH_OK) return rc;
+  return finish_checked(hv);
+}
+
+// After a product: scan Hv for NaN/Inf, then wait for the stream and turn the
+// flags raised on the way (non-finite direction, token out of range,
+// non-finite product) into a status.
+int Engine::finish_checked(const float* hv) {
+  int* nf = (int*)(ws + nfflag.off);
+  CK(launch_nonfinite_scan(hv, P, nf + 1, stream));
+  int h[4] = {0, 0, 0, 0};
+  CK(hipMemcpyAsync(h, nf, sizeof h, hipMemcpyDeviceToHost, stream));
+  CK(hipStreamSynchronize(stream));
+  if (h[2]) { err = "a token lies outside [0, vocab)"; return FDH_ERR_INVALID_ARG; }
+  if (h[0]) { err = "the direction v holds NaN or Inf"; return FDH_ERR_NONFINITE; }
+  if (h[1]) { err = "the product Hv holds NaN or Inf"; return FDH_ERR_NONFINITE; }
+  return FDH_OK;
 }
 
 int Engine::hvp_batches(const void* params, const float* v, double eps, const BatchRef* bt, int nb, double inv_n,
@@ -837,26 +914,23 @@ int Engine::bind_batches(const void* params, const BatchRef* bt, int nb, double 
     return FDH_OK;
   }
   if (nb < 1 || !bt) { err = "need at least one batch"; return FDH_ERR_INVALID_ARG; }
-  int64_t cnt[2] = {0, 0};
-  bool any_labels = false;
+  int64_t cnt[1] = {0};
   for (int i = 0; i < nb; ++i) {
     const int rc = check_batch(bt[i].tok, bt[i].B, bt[i].S);
     if (rc != FDH_OK) return rc;
-    if (bt[i].lab) any_labels = true;
-    else cnt[0] += (int64_t)bt[i].B * (bt[i].S - 1);
   }
-  if (any_labels) {
-    // count the kept targets and the invalid labels on the device (one small
-    // launch per labelled batch), then wait for the two integers
+  {
+    // count the kept targets, the invalid labels and the invalid tokens on
+    // the device (one small launch per batch), then wait for the three integers
     int64_t* dc = (int64_t*)(ws + tcount.off);
-    CK(launch_fill_f64((double*)dc, 2, 0.0, stream));
-    for (int i = 0; i < nb; ++i)
-      if (bt[i].lab) CK(launch_count_targets(dc, bt[i].lab, bt[i].B, bt[i].S, V, stream));
-    int64_t h[2];
+    CK(launch_fill_f64((double*)dc, 3, 0.0, stream));
+    for (int i = 0; i < nb; ++i) CK(launch_count_targets(dc, bt[i].tok, bt[i].lab, bt[i].B, bt[i].S, V, stream));
+    int64_t h[3];
     CK(hipMemcpyAsync(h, dc, sizeof h, hipMemcpyDeviceToHost, stream));
     CK(hipStreamSynchronize(stream));
+    if (h[2] != 0) { err = "tokens must be in [0, vocab)"; return FDH_ERR_INVALID_ARG; }
     if (h[1] != 0) { err = "labels must be in [0, vocab) or -100"; return FDH_ERR_INVALID_ARG; }
-    cnt[0] += h[0];
+    cnt[0] = h[0];
   }
   if (cnt[0] == 0) { err = "the batches hold no targets (every label is -100)"; return FDH_ERR_INVALID_ARG; }
   b_params = params;
@@ -869,10 +943,19 @@ int Engine::bind_batches(const void* params, const BatchRef* bt, int nb, double 
   return FDH_OK;
 }
 
-int Engine::hvp_bound(const float* v, float* hv) {
+int Engine::hvp_bound_async(const float* v, float* hv) {
   if (!bound) { err = "call fdh_bind first"; return FDH_ERR_STATE; }
   if (quad) return hvp(b_params, v, b_eps, nullptr, 0, 0, hv);
   return hvp_batches(b_params, v, b_eps, b_data.data(), (int)b_data.size(), b_inv_n, hv);
+}
+
+int Engine::hvp_bound(const float* v, float* hv) {
+  if (!bound) { err = "call fdh_bind first"; return FDH_ERR_STATE; }
+  if (quad) return hvp(b_params, v, b_eps, nullptr, 0, 0, hv);
+  CK(launch_fill_f32((float*)(ws + nfflag.off), 4, 0.f, stream));
+  const int rc = hvp_bound_async(v, hv);
+  if (rc != FDH_OK) return rc;
+  return finish_checked(hv);
 }
 
 int Engine::last_losses(double* lp, double* lm) {
@@ -940,7 +1023,7 @@ int Engine::lanczos_t(int m, uint64_t seed, const fdh_lanczos_opts& o, double* a
     if (rc_ != FDH_OK) return rc_;                             \
   } while (0)
   for (int k = 0; k < m; ++k) {
-    int rc = hvp_bound(q, w);
+    int rc = hvp_bound_async(q, w);
     if (rc != FDH_OK) return rc;
     const int nv = std::min(k + 1, cap);
     if (nv > 0) {
@@ -1275,7 +1358,7 @@ int Engine::cg_solve(const float* b, double lam, int max_iters, double rel_tol, 
   res[0] = bnorm;
   if (!std::isfinite(bnorm)) { err = "non-finite right-hand side"; return FDH_ERR_NONFINITE; }
   for (int k = 0; k < max_iters; ++k) {
-    rc = hvp_bound(p, ap);
+    rc = hvp_bound_async(p, ap);
     if (rc != FDH_OK) return rc;
     TC(12.0 * Pd, launch_cg_ap(ap, p, lam, sc, part, P, st));
     double pap = 0.0;
@@ -1313,13 +1396,13 @@ int Engine::block_diagonal(const float* v, double* out) {
   float* h = (float*)(ws + lz_w.off);
   float* vb = (float*)(ws + lz_q.off);
   float* hb = (float*)(ws + lz_qp.off);
-  int rc = hvp_bound(v, h);
+  int rc = hvp_bound_async(v, h);
   if (rc != FDH_OK) return rc;
   std::vector<int64_t> ranges = layer_ranges();
   std::vector<double> s4(4);
   for (int l = 0; l < L; ++l) {
     CK(launch_mask_range(vb, v, ranges[2 * l], ranges[2 * l + 1], P, stream));
-    rc = hvp_bound(vb, hb);
+    rc = hvp_bound_async(vb, hb);
     if (rc != FDH_OK) return rc;
     CK(launch_block_stats(h, hb, &ranges[2 * l], 1, (double*)(ws + bpart.off), (double*)(ws + bout.off), stream));
     CK(hipMemcpyAsync(s4.data(), ws + bout.off, 32, hipMemcpyDeviceToHost, stream));
@@ -1329,6 +1412,8 @@ int Engine::block_diagonal(const float* v, double* out) {
     out[4 * l + 1] = na > 0 ? dif / na : 0.0;
     out[4 * l + 2] = (na > 0 && nb > 0) ? s4[2] / (na * nb) : 0.0;
     out[4 * l + 3] = na;
+    for (int c = 0; c < 4; ++c)
+      if (!std::isfinite(s4[c])) { err = "non-finite block statistic (NaN or Inf in v or in a product)"; return FDH_ERR_NONFINITE; }
   }
   return FDH_OK;
 }

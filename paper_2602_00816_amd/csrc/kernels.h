@@ -29,7 +29,9 @@ hipError_t launch_fill_f64(double* p, int64_t n, double v, hipStream_t s);
 hipError_t launch_sum_splits(float* out, const float* part, int ns, int64_t n, bool acc, hipStream_t s);
 // lo[i] = T(eps * v[i])
 template <typename T>
-hipError_t launch_scale_cast(T* lo, const float* v, double eps, int64_t n, hipStream_t s);
+hipError_t launch_scale_cast(T* lo, const float* v, double eps, int64_t n, hipStream_t s, int* nonfinite = nullptr);
+// nonfinite[0] = 1 when some x[i], i < n, is NaN or infinite (left alone otherwise)
+hipError_t launch_nonfinite_scan(const float* x, int64_t n, int* flag, hipStream_t s);
 // QUAD_DIAG: hv = (d (theta + eps v) - d (theta - eps v)) / (2 eps), both points in fp64
 template <typename T>
 hipError_t launch_quad_diag_hvp(const T* theta, const float* d, const float* v, double eps, float* hv, int64_t n, hipStream_t s);
@@ -110,10 +112,12 @@ template <typename T> struct PairT { T* m; T* d; };
 template <typename T>
 hipError_t launch_cast_pair(PairT<T> out, const float* m, const float* d, int64_t n, hipStream_t s);
 
-// x = E[tok] (+ Pos[s]);  m = theta rows, d = eps * v rows
+// x = E[tok] (+ Pos[s]);  m = theta rows, d = eps * v rows; bad_tok[0] = 1
+// (when bad_tok is not null) if a token lies outside [0, V) (it is clamped)
 template <typename T>
 hipError_t launch_embed_fwd(PairF x, const int32_t* tok, int T_, int S, int dmodel, int V,
-                            const T* th_e, const float* v_e, const T* th_p, const float* v_p, double eps, hipStream_t s);
+                            const T* th_e, const float* v_e, const T* th_p, const float* v_p, double eps, int* bad_tok,
+                            hipStream_t s);
 
 // Norm forward at both points: y = norm(x; g +- eps vg, b +- eps vb)
 template <typename T>
@@ -209,8 +213,9 @@ hipError_t launch_ce(PairT<T> dl, double* rowloss, const float* lm, const float*
                      const int32_t* lab, int T_, int S, int V, double inv_n, hipStream_t s);
 // out2 = (or += with acc) the sums of the two rows of rowloss
 hipError_t launch_loss_sum(double* out2, const double* rowloss, int T_, bool acc, hipStream_t s);
-// out2[0] += targets of a [B, S] batch, out2[1] += labels outside [0, V) other than IGNORE_LABEL
-hipError_t launch_count_targets(int64_t* out2, const int32_t* lab, int B, int S, int V, hipStream_t s);
+// out3[0] += targets of a [B, S] batch, out3[1] += labels outside [0, V) other
+// than IGNORE_LABEL (lab may be null: next-token targets), out3[2] += tokens outside [0, V)
+hipError_t launch_count_targets(int64_t* out3, const int32_t* tok, const int32_t* lab, int B, int S, int V, hipStream_t s);
 
 // embedding backward (difference channel only): deterministic sort + segment sums
 hipError_t launch_token_sort(uint32_t* keys, const int32_t* tok, int T_, int V, hipStream_t s);

@@ -39,16 +39,20 @@ __global__ void cast_pair_kernel(PairT<T> o, const float* m, const float* d, int
 }
 
 // ---- embedding ----------------------------------------------------------------
-// token ids outside [0, V) are clamped so that no access leaves the tables
+// token ids outside [0, V) are clamped so that no access leaves the tables;
+// the embedding forward reports them (bad_tok[0] = 1) and the call that
+// launched it turns that into an invalid-argument error
 __device__ inline int clamp_tok(int t, int V) { return t < 0 ? 0 : (t >= V ? V - 1 : t); }
 
 template <typename T>
 __global__ void embed_fwd_kernel(PairF x, const int32_t* tok, int T_, int S, int dm, int V, const T* the, const float* ve,
-                                 const T* thp, const float* vp, double eps) {
+                                 const T* thp, const float* vp, double eps, int* bad_tok) {
   const int64_t n = (int64_t)T_ * dm;
   GRID_LOOP(i, n) {
     const int t = (int)(i / dm), j = (int)(i % dm);
-    const int64_t r = (int64_t)clamp_tok(tok[t], V) * dm + j;
+    const int tk = tok[t];
+    if ((tk < 0 || tk >= V) && bad_tok && j == 0) bad_tok[0] = 1;
+    const int64_t r = (int64_t)clamp_tok(tk, V) * dm + j;
     double xp = (double)ldf(the, r) + eps * (double)ve[r];
     double xm = (double)ldf(the, r) - eps * (double)ve[r];
     if (thp) {
@@ -899,12 +903,15 @@ __global__ void loss_sum_kernel(double* out2, const double* rowloss, int T_, boo
 
 // out[0] += number of targets of one [B, S] batch (positions t % S < S - 1
 // whose label at t + 1 is not IGNORE_LABEL; all of them without labels),
-// out[1] += number of labels outside [0, V) other than IGNORE_LABEL.
-__global__ void count_targets_kernel(int64_t* out, const int32_t* lab, int B, int S, int V) {
+// out[1] += number of labels outside [0, V) other than IGNORE_LABEL,
+// out[2] += number of tokens outside [0, V).
+__global__ void count_targets_kernel(int64_t* out, const int32_t* tok, const int32_t* lab, int B, int S, int V) {
   __shared__ double sh[NT / 64];
   const int64_t n = (int64_t)B * S;
-  double c = 0.0, bad = 0.0;
+  double c = 0.0, bad = 0.0, badt = 0.0;
   for (int64_t i = threadIdx.x; i < n; i += NT) {
+    const int x = tok[i];
+    if (x < 0 || x >= V) badt += 1.0;
     const int64_t t = i % S;
     if (t == S - 1) continue;
     const int y = lab ? lab[i + 1] : 0;
@@ -915,9 +922,11 @@ __global__ void count_targets_kernel(int64_t* out, const int32_t* lab, int B, in
   // counts below 2^53 are exact in fp64
   c = block_sum<NT>(c, sh);
   bad = block_sum<NT>(bad, sh);
+  badt = block_sum<NT>(badt, sh);
   if (threadIdx.x == 0) {
     out[0] += (int64_t)c;
     out[1] += (int64_t)bad;
+    out[2] += (int64_t)badt;
   }
 }
 
@@ -999,9 +1008,9 @@ hipError_t launch_cast_pair(PairT<T> out, const float* m, const float* d, int64_
 
 template <typename T>
 hipError_t launch_embed_fwd(PairF x, const int32_t* tok, int T_, int S, int dm, int V, const T* the, const float* ve,
-                            const T* thp, const float* vp, double eps, hipStream_t s) {
+                            const T* thp, const float* vp, double eps, int* bad_tok, hipStream_t s) {
   hipLaunchKernelGGL(embed_fwd_kernel<T>, dim3(grid_for((int64_t)T_ * dm)), dim3(NT), 0, s, x, tok, T_, S, dm, V, the,
-                     ve, thp, vp, eps);
+                     ve, thp, vp, eps, bad_tok);
   return hipGetLastError();
 }
 
@@ -1148,8 +1157,8 @@ hipError_t launch_loss_sum(double* out2, const double* rowloss, int T_, bool acc
   hipLaunchKernelGGL(loss_sum_kernel, dim3(1), dim3(NT), 0, s, out2, rowloss, T_, acc);
   return hipGetLastError();
 }
-hipError_t launch_count_targets(int64_t* out2, const int32_t* lab, int B, int S, int V, hipStream_t s) {
-  hipLaunchKernelGGL(count_targets_kernel, dim3(1), dim3(NT), 0, s, out2, lab, B, S, V);
+hipError_t launch_count_targets(int64_t* out3, const int32_t* tok, const int32_t* lab, int B, int S, int V, hipStream_t s) {
+  hipLaunchKernelGGL(count_targets_kernel, dim3(1), dim3(NT), 0, s, out3, tok, lab, B, S, V);
   return hipGetLastError();
 }
 
@@ -1172,7 +1181,7 @@ hipError_t launch_pos_bwd(float* hv, const float* dxd, int B, int S, int dm, dou
 #define INST_T(T)                                                                                                     \
   template hipError_t launch_cast_pair<T>(PairT<T>, const float*, const float*, int64_t, hipStream_t);                 \
   template hipError_t launch_embed_fwd<T>(PairF, const int32_t*, int, int, int, int, const T*, const float*, const T*, \
-                                          const float*, double, hipStream_t);                                          \
+                                          const float*, double, int*, hipStream_t);                                    \
   template hipError_t launch_norm_fwd<T>(PairT<T>, const float*, const float*, int, int, bool, const T*, const float*, \
                                          const T*, const float*, double, float, hipStream_t);                          \
   template hipError_t launch_norm_bwd<T>(PairF, PairT<T>, const float*, const float*, const float*, const float*,      \

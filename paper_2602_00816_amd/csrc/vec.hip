@@ -37,10 +37,15 @@ __global__ void fill_f64_kernel(double* p, int64_t n, double v) {
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) p[i] = v;
 }
 
+// lo = T(eps * v); with flag, flag[0] = 1 when some v[i] is NaN or infinite
 template <typename T>
-__global__ void scale_cast_kernel(T* lo, const float* v, double eps, int64_t n) {
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+__global__ void scale_cast_kernel(T* lo, const float* v, double eps, int64_t n, int* flag) {
+  bool bad = false;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    bad |= !isfinite(v[i]);
     stf(lo, i, (float)(eps * (double)v[i]));
+  }
+  if (flag && bad) flag[0] = 1;
 }
 
 template <typename T>
@@ -471,17 +476,42 @@ __global__ void cg_finish_kernel(double* sc, const double* partial, int mode) {
   }
 }
 
-// lo = T(eps * v), 8 elements per lane (16-byte aligned operands)
+// lo = T(eps * v), 8 elements per lane (16-byte aligned operands); with flag,
+// flag[0] = 1 when some v[i] is NaN or infinite (elements past the end load as 0)
 template <typename T>
-__global__ void scale_cast8_kernel(T* lo, const float* v, double eps, int64_t n) {
+__global__ void scale_cast8_kernel(T* lo, const float* v, double eps, int64_t n, int* flag) {
   const int64_t step = 8 * (int64_t)gridDim.x * blockDim.x;
+  bool bad = false;
   for_groups(8 * (blockIdx.x * (int64_t)blockDim.x + threadIdx.x), n, step, [&](int64_t i, int ne, auto full) {
     constexpr bool F = decltype(full)::value;
     V8 x = ldv<F>(v, i, ne);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) x.x[e] = (float)(eps * (double)x.x[e]);
+    for (int e = 0; e < 8; ++e) {
+      bad |= !isfinite(x.x[e]);
+      x.x[e] = (float)(eps * (double)x.x[e]);
+    }
     stv<F>(lo, i, x, ne);
   });
+  if (flag && bad) flag[0] = 1;
+}
+
+// flag[0] = 1 when some x[i] is NaN or infinite (one read of x)
+__global__ void nonfinite_scan8_kernel(const float* x, int64_t n, int* flag) {
+  const int64_t step = 8 * (int64_t)gridDim.x * blockDim.x;
+  bool bad = false;
+  for_groups(8 * (blockIdx.x * (int64_t)blockDim.x + threadIdx.x), n, step, [&](int64_t i, int ne, auto full) {
+    constexpr bool F = decltype(full)::value;
+    const V8 v = ldv<F>(x, i, ne);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) bad |= !isfinite(v.x[e]);
+  });
+  if (bad) flag[0] = 1;
+}
+__global__ void nonfinite_scan_kernel(const float* x, int64_t n, int* flag) {
+  bool bad = false;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    bad |= !isfinite(x[i]);
+  if (bad) flag[0] = 1;
 }
 
 // sums over [s0, s1): ||a||^2, ||b||^2, <a, b>, ||a - b||^2
@@ -584,16 +614,25 @@ hipError_t launch_fill_f64(double* p, int64_t n, double v, hipStream_t s) {
 }
 
 template <typename T>
-hipError_t launch_scale_cast(T* lo, const float* v, double eps, int64_t n, hipStream_t s) {
+hipError_t launch_scale_cast(T* lo, const float* v, double eps, int64_t n, hipStream_t s, int* nonfinite) {
   if (n <= 0) return hipSuccess;
   if ((uintptr_t)lo % 16 == 0 && (uintptr_t)v % 16 == 0)
-    hipLaunchKernelGGL(scale_cast8_kernel<T>, dim3(grid_for((n + 7) / 8)), dim3(NT), 0, s, lo, v, eps, n);
+    hipLaunchKernelGGL(scale_cast8_kernel<T>, dim3(grid_for((n + 7) / 8)), dim3(NT), 0, s, lo, v, eps, n, nonfinite);
   else
-    hipLaunchKernelGGL(scale_cast_kernel<T>, dim3(grid_for(n)), dim3(NT), 0, s, lo, v, eps, n);
+    hipLaunchKernelGGL(scale_cast_kernel<T>, dim3(grid_for(n)), dim3(NT), 0, s, lo, v, eps, n, nonfinite);
   return hipGetLastError();
 }
-template hipError_t launch_scale_cast<float>(float*, const float*, double, int64_t, hipStream_t);
-template hipError_t launch_scale_cast<bf16_t>(bf16_t*, const float*, double, int64_t, hipStream_t);
+template hipError_t launch_scale_cast<float>(float*, const float*, double, int64_t, hipStream_t, int*);
+template hipError_t launch_scale_cast<bf16_t>(bf16_t*, const float*, double, int64_t, hipStream_t, int*);
+
+hipError_t launch_nonfinite_scan(const float* x, int64_t n, int* flag, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if ((uintptr_t)x % 16 == 0)
+    hipLaunchKernelGGL(nonfinite_scan8_kernel, dim3(grid_for((n + 7) / 8)), dim3(NT), 0, s, x, n, flag);
+  else
+    hipLaunchKernelGGL(nonfinite_scan_kernel, dim3(grid_for(n)), dim3(NT), 0, s, x, n, flag);
+  return hipGetLastError();
+}
 
 template <typename T>
 hipError_t launch_quad_diag_hvp(const T* theta, const float* d, const float* v, double eps, float* hv, int64_t n, hipStream_t s) {

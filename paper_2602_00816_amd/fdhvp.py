@@ -99,6 +99,7 @@ def lib():
         "fdh_testing_timing": (i32, [vp, i32]),
         "fdh_testing_timing_read": (i32, [vp, pd]),
         "fdh_testing_copy": (i32, [vp, vp, C.c_size_t, vp]),
+        "fdh_testing_layout_digest": (i32, [vp, C.POINTER(C.c_uint64)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -116,6 +117,28 @@ def _check_tokens(t):
     import torch
     if t is not None and (t.dtype != torch.int32 or t.dim() != 2 or not t.is_cuda or not t.is_contiguous()):
         raise ValueError("tokens must be a contiguous int32 [B, S] tensor on the device")
+
+
+def _check_vec(t, n: int, what: str, dtypes=("float32",), optional=False):
+    """A parameter-sized device operand: the kernels read or write exactly n
+    elements of the given type through its pointer, so anything else (another
+    dtype, a short or strided tensor, host memory) is refused here, before any
+    launch."""
+    if t is None:
+        if optional:
+            return
+        raise ValueError(f"{what} is required")
+    if not hasattr(t, "data_ptr") or not hasattr(t, "is_cuda"):
+        raise ValueError(f"{what} must be a torch tensor on the device")
+    dt = str(t.dtype).replace("torch.", "")
+    if dt not in dtypes:
+        raise ValueError(f"{what} must have dtype {' or '.join(dtypes)}, not {dt}")
+    if not t.is_cuda:
+        raise ValueError(f"{what} must be on the device")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    if t.numel() != n:
+        raise ValueError(f"{what} must have {n} elements, not {t.numel()}")
 
 
 def _stream():
@@ -172,6 +195,15 @@ class Model:
         except Exception:
             pass
 
+    def _param_dtypes(self):
+        return ("float32",) if self.dtype == "f32" else ("bfloat16", "uint16", "int16")
+
+    def _check_params(self, p):
+        _check_vec(p, self.num_params, "params", self._param_dtypes())
+
+    def _check_vec(self, t, what, optional=False):
+        _check_vec(t, self.num_params, what, optional=optional)
+
     def _check(self, st: int, what: str) -> int:
         if st < 0:
             msg = self._L.fdh_last_error(self._h)
@@ -204,6 +236,9 @@ class Model:
     def set_workspace(self, B=0, S=0, m=0, o: LanczosOpts | None = None):
         import torch
         n = self.workspace_bytes(B, S, m, o)
+        # detach before the old buffer goes back to torch, so that the context
+        # never points at freed memory (also when the new size is refused)
+        self._check(self._L.fdh_set_workspace(self._h, None, 0, 0, 0, 0, None), "fdh_set_workspace")
         self._ws = None
         buf = torch.empty(max(n, 256) + 256, dtype=torch.uint8, device="cuda")
         base = buf.data_ptr()
@@ -222,6 +257,7 @@ class Model:
 
     def init_params(self, seed: int):
         p = self.empty_params()
+        self._check_params(p)
         self._check(self._L.fdh_init_params(self._h, _ptr(p), seed), "fdh_init_params")
         return p
 
@@ -231,13 +267,15 @@ class Model:
         self._check(self._L.fdh_make_tokens(self._h, _ptr(t), B, S, seed, TOKENS[dist]), "fdh_make_tokens")
         return t
 
-    def random_vector(self, seed: int, kind="rademacher"):
+    def random_vector(self, seed: int, kind="rademacher", out=None):
         import torch
-        v = torch.empty(self.num_params, dtype=torch.float32, device="cuda")
+        v = torch.empty(self.num_params, dtype=torch.float32, device="cuda") if out is None else out
+        self._check_vec(v, "out")
         self._check(self._L.fdh_random_vector(self._h, _ptr(v), seed, VEC[kind]), "fdh_random_vector")
         return v
 
     def set_quad_diag(self, diag):
+        self._check_vec(diag, "diag")
         self._diag = diag
         self._check(self._L.fdh_set_quad_diag(self._h, _ptr(diag)), "fdh_set_quad_diag")
 
@@ -247,6 +285,9 @@ class Model:
         import torch
         if out is None:
             out = torch.empty(self.num_params, dtype=torch.float32, device="cuda")
+        self._check_params(params)
+        self._check_vec(v, "v")
+        self._check_vec(out, "out")
         _check_tokens(tokens)
         B, S = (tokens.shape if tokens is not None else (0, 0))
         self._check(self._L.fdh_hvp(self._h, _ptr(params), _ptr(v), float(eps), _ptr(tokens), B, S, _ptr(out)),
@@ -259,6 +300,7 @@ class Model:
         return lp.value, lm.value
 
     def bind(self, params, tokens, eps: float):
+        self._check_params(params)
         _check_tokens(tokens)
         B, S = (tokens.shape if tokens is not None else (0, 0))
         self._keep = [params, tokens]
@@ -270,6 +312,7 @@ class Model:
         (labels aligned with the tokens, -100 = no target).  Returns the number
         of kept targets."""
         import torch
+        self._check_params(params)
         items = [b if isinstance(b, tuple) else (b, None) for b in batches]
         for tok, lab in items:
             for x in (tok, lab):
@@ -289,6 +332,8 @@ class Model:
         import torch
         if out is None:
             out = torch.empty(self.num_params, dtype=torch.float32, device="cuda")
+        self._check_vec(v, "v")
+        self._check_vec(out, "out")
         self._check(self._L.fdh_hvp_bound(self._h, _ptr(v), _ptr(out)), "fdh_hvp_bound")
         return out
 
@@ -325,8 +370,10 @@ class Model:
         """CG for (H + lam I) x = b on the bound operator (b: float32 [P] on device).
         Returns (x, residual norms ||r_0|| .. ||r_s||, s, status)."""
         import torch
+        self._check_vec(b, "b")
         if x is None:
             x = torch.empty_like(b)
+        self._check_vec(x, "x")
         res = np.zeros(max_iters + 1)
         s = C.c_int32()
         st = self._check(self._L.fdh_cg_solve(self._h, _ptr(b), float(lam), int(max_iters), float(rel_tol), _ptr(x),
@@ -341,6 +388,12 @@ class Model:
         """Weight-gradient GEMMs over the whole token range (testing)."""
         self._check(self._L.fdh_testing_unsplit_wgrad(self._h, int(on)), "fdh_testing_unsplit_wgrad")
 
+    def layout_digest(self) -> int:
+        """Digest of the workspace carve in use (testing; host only)."""
+        out = C.c_uint64()
+        self._check(self._L.fdh_testing_layout_digest(self._h, C.byref(out)), "fdh_testing_layout_digest")
+        return int(out.value)
+
     def timing(self, enable: bool):
         self._check(self._L.fdh_testing_timing(self._h, int(enable)), "fdh_testing_timing")
 
@@ -354,12 +407,15 @@ class Model:
 
     def block_diagonal(self, v):
         """Exp I statistics per layer: columns abs diff, relative error, cosine, ||(Hv)^(b)||."""
+        self._check_vec(v, "v")
         out = np.zeros((max(self.num_blocks, 0), 4))
         self._check(self._L.fdh_block_diagonal(self._h, _ptr(v), out.ctypes.data_as(C.POINTER(C.c_double))),
                     "fdh_block_diagonal")
         return out
 
     def block_stats(self, a, b):
+        self._check_vec(a, "a")
+        self._check_vec(b, "b")
         out = np.zeros((max(self.num_blocks, 0), 3))
         self._check(self._L.fdh_block_stats(self._h, _ptr(a), _ptr(b), out.ctypes.data_as(C.POINTER(C.c_double))),
                     "fdh_block_stats")

@@ -112,3 +112,99 @@ def test_quad_diag_context():
     m = fd.Model("quad_diag", quad_n=1000)
     assert m.num_params == 1000
     assert m.num_blocks == 0
+
+
+def _fake_workspace(lib, h, B, S, m, o, nbytes=None):
+    """Hand the context an aligned address that is never dereferenced here (no
+    kernel runs in these tests): set_workspace only plans and records it."""
+    need = C.c_size_t()
+    assert lib.fdh_workspace_bytes(h, B, S, m, C.byref(o) if o else None, C.byref(need)) == 0
+    n = need.value if nbytes is None else nbytes
+    return lib.fdh_set_workspace(h, C.c_void_p(1 << 40), n, B, S, m, C.byref(o) if o else None), need.value
+
+
+def _digest(lib, h):
+    out = C.c_uint64()
+    assert lib.fdh_testing_layout_digest(h, C.byref(out)) == 0
+    return out.value
+
+
+@pytest.mark.parametrize("name", ["llama-1.3b-bf16", "tiny-gpt2-fp32"])
+def test_workspace_queries_leave_the_carve_alone(name):
+    """fdh_workspace_bytes is a query and a rejected fdh_set_workspace keeps the
+    old buffer: neither may move the spans of the workspace in use (a query
+    with another S once switched the attention path and shrank the score
+    buffers of the live carve)."""
+    lib = fd.lib()
+    m = _model(name)
+    h = m._h
+    w = WORKLOADS[name]
+    o = fd.opts("full", 0, "bf16" if w["dtype"] == "bf16" else "f32")
+    st, need = _fake_workspace(lib, h, w["batch"], w["seq"], 2, o)
+    assert st == 0
+    d0 = _digest(lib, h)
+    for B, S, mm, oo in [(1, 1000, 0, None), (w["batch"], w["seq"] // 2, 40, o), (2 * w["batch"], 8, 1, fd.opts("window", 3))]:
+        n = C.c_size_t()
+        assert lib.fdh_workspace_bytes(h, B, S, mm, C.byref(oo) if oo else None, C.byref(n)) == 0
+        assert _digest(lib, h) == d0
+    # too small: rejected, the carve in use stays
+    st, _ = _fake_workspace(lib, h, 2 * w["batch"], w["seq"], 3, o, nbytes=need)
+    assert st == -2
+    assert _digest(lib, h) == d0
+    # unaligned: rejected as well
+    assert lib.fdh_set_workspace(h, C.c_void_p((1 << 40) + 64), need * 4, 1, 64, 0, None) == -2
+    assert _digest(lib, h) == d0
+    # an accepted plan for another shape does change it
+    st, _ = _fake_workspace(lib, h, 1, 128, 0, None)
+    assert st == 0 and _digest(lib, h) != d0
+
+
+class _FakeTensor:
+    """Stands in for a device tensor in the binding's operand checks (no memory behind it)."""
+
+    def __init__(self, dtype, n, cuda=True, contiguous=True):
+        import torch
+        self.dtype = getattr(torch, dtype)
+        self.is_cuda = cuda
+        self._n = n
+        self._c = contiguous
+
+    def numel(self):
+        return self._n
+
+    def is_contiguous(self):
+        return self._c
+
+    def data_ptr(self):
+        return 1 << 40
+
+
+def test_binding_refuses_mismatched_operands_before_any_launch():
+    pytest.importorskip("torch")
+    m = _model("tiny-gpt2-fp32")
+    P = m.num_params
+    good = _FakeTensor("float32", P)
+    tok = None
+    cases = [
+        (dict(params=_FakeTensor("bfloat16", P), v=good, out=good), "dtype"),
+        (dict(params=good, v=_FakeTensor("float16", P), out=good), "dtype"),
+        (dict(params=good, v=_FakeTensor("float32", P - 1), out=good), "elements"),
+        (dict(params=good, v=good, out=_FakeTensor("float32", P, contiguous=False)), "contiguous"),
+        (dict(params=good, v=_FakeTensor("float32", P, cuda=False), out=good), "device"),
+        (dict(params=_FakeTensor("float32", 2 * P), v=good, out=good), "elements"),
+    ]
+    for kw, word in cases:
+        with pytest.raises(ValueError, match=word):
+            m.hvp(kw["params"], kw["v"], 1e-3, tok, out=kw["out"])
+    with pytest.raises(ValueError):
+        m.hvp_bound(_FakeTensor("float64", P), out=good)
+    with pytest.raises(ValueError):
+        m.block_stats(good, _FakeTensor("float32", P + 8))
+    with pytest.raises(ValueError):
+        m.cg_solve(_FakeTensor("int32", P), 1.0, 2, x=good)
+    q = fd.Model("quad_diag", quad_n=1000)
+    with pytest.raises(ValueError):
+        q.set_quad_diag(_FakeTensor("float32", 999))
+    bm = _model("llama-1.3b-bf16")
+    with pytest.raises(ValueError, match="dtype"):
+        bm.bind(_FakeTensor("float32", bm.num_params), None, 1e-3)
