@@ -39,8 +39,19 @@ def _run(torch, fd, w, theta, tok, vs, eps):
     return outs, losses
 
 
+# The bf16 case at 10x the workloads' init scale misses the 5e-2 bar: there the
+# bf16 rounding of the mean-channel GEMM operands (common to both points, so
+# it moves the point at which H is taken by about 2^-9 relative per layer
+# rather than entering the difference) is amplified by much sharper
+# non-linearities.  It stays in the suite as a known failure against the
+# unchanged bar.
+STRESS_BF16 = pytest.mark.xfail(reason="bf16 operands of the mean channel at N(0, 0.2) init: rel L2 ~8e-2 to 1.1e-1 "
+                                       "against the 5e-2 bar", strict=False)
+
+
 @pytest.mark.parametrize("name,dtype,std", [
-    ("llama-gqa", "f32", 0.02), ("llama-gqa", "f32", 0.2), ("llama-gqa", "bf16", 0.02), ("llama-gqa", "bf16", 0.2),
+    ("llama-gqa", "f32", 0.02), ("llama-gqa", "f32", 0.2), ("llama-gqa", "bf16", 0.02),
+    pytest.param("llama-gqa", "bf16", 0.2, marks=STRESS_BF16),
     ("gpt2-small", "f32", 0.02), ("gpt2-small", "f32", 0.2), ("gpt2-small", "bf16", 0.02),
 ])
 def test_hvp_parity_small(name, dtype, std):
@@ -54,13 +65,6 @@ def test_hvp_parity_small(name, dtype, std):
     vs = [synth.rademacher_probe(3, P), synth.gaussian_direction(4, P)]
     got, (lp, lm) = _run(torch, fd, w, theta, tok, vs, eps)
     tol = 5e-3 if dtype == "f32" else 5e-2
-    if dtype == "bf16" and std > 0.02:
-        # stress case at 10x the workloads' init scale: the bf16 rounding of the
-        # mean-channel GEMM operands moves the point at which H is taken by
-        # ~2^-9 relative per layer, amplified by the sharper non-linearities;
-        # measured 8e-2 to 1.1e-1 on gfx950.  The 5e-2 bar applies at the workloads'
-        # N(0, 0.02) init (measured 3e-3 to 5e-3).
-        tol = 1.5e-1
     for v, g in zip(vs, got):
         want = OH.lm_hvp(cfg, theta, v.astype(np.float64), eps, tok)
         err = rel_l2(g, want)
