@@ -29,6 +29,9 @@ Derived variates (all computed in float64, exactly reproducible from integers):
 """
 from __future__ import annotations
 
+import concurrent.futures as cf
+import os
+
 import numpy as np
 
 GAMMA = np.uint64(0x9E3779B97F4A7C15)
@@ -79,22 +82,45 @@ def uniform(seed: int, stream: int, index) -> np.ndarray:
     return ((h >> np.uint64(11)).astype(np.float64) + 0.5) * (2.0 ** -53)
 
 
+def _threads() -> int:
+    return max(1, min(16, os.cpu_count() or 1))
+
+
+def _chunked(fn, n: int, out: np.ndarray) -> np.ndarray:
+    """Fill out[c0:c1] = fn(c0, c1) over chunks of _CHUNK elements on a thread
+    pool (numpy releases the GIL inside these element-wise kernels); every
+    element depends on its own index only, so the result does not depend on
+    the chunking or the thread count."""
+    bounds = [(c0, min(n, c0 + _CHUNK)) for c0 in range(0, n, _CHUNK)]
+    if len(bounds) <= 1:
+        for c0, c1 in bounds:
+            out[c0:c1] = fn(c0, c1)
+        return out
+
+    def work(b):
+        out[b[0]:b[1]] = fn(b[0], b[1])
+
+    with cf.ThreadPoolExecutor(_threads()) as ex:
+        list(ex.map(work, bounds))
+    return out
+
+
 def normal(seed: int, stream: int, start: int, n: int) -> np.ndarray:
     """Standard normals for elements start .. start+n-1 of (seed, stream)."""
-    out = np.empty(n, dtype=np.float64)
-    for c0 in range(0, n, _CHUNK):
-        c1 = min(n, c0 + _CHUNK)
+    def fn(c0, c1):
         i = np.arange(start + c0, start + c1, dtype=np.uint64)
         u1 = uniform(seed, stream, i * np.uint64(2))
         u2 = uniform(seed, stream, i * np.uint64(2) + np.uint64(1))
-        out[c0:c1] = np.sqrt(-2.0 * np.log(u1)) * np.cos(2.0 * np.pi * u2)
-    return out
+        return np.sqrt(-2.0 * np.log(u1)) * np.cos(2.0 * np.pi * u2)
+    return _chunked(fn, n, np.empty(n, dtype=np.float64))
 
 
 def rademacher(seed: int, n: int, stream: int = STREAM_PROBE) -> np.ndarray:
     """Signs in {-1, +1} as float64, element i from output i."""
-    h = splitmix64(seed, stream, np.arange(n, dtype=np.uint64))
-    return np.where((h >> np.uint64(63)) == np.uint64(1), -1.0, 1.0)
+    def fn(c0, c1):
+        h = splitmix64(seed, stream, np.arange(c0, c1, dtype=np.uint64))
+        return np.where((h >> np.uint64(63)) == np.uint64(1), -1.0, 1.0)
+    return _chunked(fn, n, np.empty(n, dtype=np.float64))
 
 
 def rademacher_probe(seed: int, n: int) -> np.ndarray:

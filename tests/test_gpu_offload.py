@@ -1,7 +1,9 @@
 """Krylov-basis offload (fdh_set_basis_offload): stored Lanczos rows beyond
 device_rows live in pinned host memory and are read by the same kernels over
 the host link.  The arithmetic is unchanged, so every run must reproduce the
-all-device run bit for bit:
+all-device run bit for bit, and the offloaded runs on the diagonal operator
+also meet the oracle's run (extreme Ritz values within 1e-3 relative with an
+fp32 basis):
 
 * the diagonal operator (P = 1,000,003, a ragged tail), full
   reorthogonalisation with fp32 and bf16 bases, 0 and 7 rows on the device;
@@ -16,6 +18,8 @@ import time
 import numpy as np
 import pytest
 
+import synth
+from oracle import lanczos as OL
 from synth.workloads import WORKLOADS
 from tests.gpu_util import need_gpu, say
 
@@ -59,6 +63,17 @@ def test_offload_reproduces_device_basis_bitwise(reorth, window, basis, rows):
     say(f"offload {reorth}/{basis} rows on device {rows}: steps {s1}, alpha_m {a1[-1]:.9e}")
     assert s0 == s1 == m
     assert np.array_equal(a0, a1) and np.array_equal(b0, b1)
+    # and the offloaded run against the oracle's run on the same operator and probe
+    d64 = diag.cpu().numpy().astype(np.float64)
+    q1 = synth.rademacher_probe(7, P).astype(np.float64)
+    ro = OL.FULL if reorth == "full" else OL.WINDOW
+    ao, bo, _ = OL.lanczos(lambda x: d64 * x, q1, m, ro, window)
+    lg = np.linalg.eigvalsh(OL.tridiag(a1, b1))
+    lo = np.linalg.eigvalsh(OL.tridiag(ao, bo))
+    scale = np.abs(lo).max()
+    err = max(abs(lg[-1] - lo[-1]), abs(lg[0] - lo[0])) / scale
+    say(f"  extreme Ritz values against the oracle: {err:.3e} relative")
+    assert err <= (1e-3 if basis == "f32" else 5e-3)
 
 
 def test_offload_workspace_and_host_buffer_checks():
