@@ -5,12 +5,17 @@ workload: one finite-difference HVP (two gradient passes in lockstep over a
 4 x 2048 Zipf(1.1) token batch, eps = 1e-3), the three-term recurrence and
 full classical Gram-Schmidt (twice) reorthogonalisation against the bf16
 Krylov basis.  The timed region is one fdh_lanczos call of K steps, so the
-reorthogonalisation cost is averaged over k = 1..K as in a real run.
+reorthogonalisation cost is averaged over k = 1..K as in a real run; it runs
+without per-launch instrumentation.  A second, instrumented run of the same K
+steps (HIP events around every launch on the context stream) gives the
+per-family breakdown and the GEMM roofline.  One full SLQ probe at the
+workload's own Lanczos length (m = 40 for the 1.3B workload) is timed after
+that, whatever K is.
 
 Prints one JSON line.  `value` is FD-HVPs per second through the timed
 Lanczos steps (each step performs exactly one HVP); Lanczos iterations per
-minute, HVP-only throughput, the GEMM roofline and the oracle's CPU rate are
-reported beside it.
+minute, HVP-only throughput, the SLQ probe, the GEMM roofline and the oracle's
+CPU rate are reported beside it.
 """
 from __future__ import annotations
 
@@ -90,7 +95,7 @@ def cpu_baseline(w: dict, budget_s: float = 20.0) -> dict:
     OH.lm_hvp(cfg, theta, v, 1e-3, tok)
     dt = time.perf_counter() - t0
     scale = sum(alg_flops_per_hvp(w)) / sum(alg_flops_per_hvp(sample))
-    return {"value": 1.0 / (dt * scale), "unit": "FD-HVPs/s", "cores": int(threads), "kind": "oracle",
+    return {"value": 1.0 / (dt * scale), "unit": "FD-HVPs/s", "cores": int(threads), "kind": "oracle, extrapolated",
             "sample": f"{w['family']} d={w['d_model']} with 2 of {w['n_layers']} layers, 1x1024 tokens, "
                       f"fp64 numpy HVP {dt:.2f} s, scaled x{scale:.1f} by algorithmic FLOPs to the full workload"}
 
@@ -122,7 +127,8 @@ def main():
     B, S = w["batch"], w["seq"]
     mod = fd.Model.from_workload(w)
     o = fd.opts(w["reorth"], w["window"], w["basis"])
-    m_plan = max(K, 2)
+    m_slq = int(w["m"])
+    m_plan = max(K, 2, m_slq)
     ws = mod.set_workspace(B, S, m_plan, o)
     params = mod.init_params(SEED_PARAMS)
     tok = mod.make_tokens(B, S, SEED_TOKENS, w["token_dist"])
@@ -153,16 +159,32 @@ def main():
     t_hvp = (time.perf_counter() - t0) / args.hvp_reps
     print(f"[bench] hvp {t_hvp * 1e3:.1f} ms", file=sys.stderr, flush=True)
 
-    # timed Lanczos steps, with per-launch events on the context stream
-    mod.timing(True)
+    # the timed Lanczos steps (no instrumentation)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     alpha, beta, steps, st = mod.lanczos(K, SEED_PROBE, o)
     torch.cuda.synchronize()
     t_total = time.perf_counter() - t0
+    print(f"[bench] lanczos {K} steps {t_total:.2f} s (steps_done {steps})", file=sys.stderr, flush=True)
+
+    # the same K steps again, with HIP events around every launch on the context stream
+    mod.timing(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    mod.lanczos(K, SEED_PROBE, o)
+    torch.cuda.synchronize()
+    t_instr = time.perf_counter() - t0
     tm = mod.timing_read()
     mod.timing(False)
-    print(f"[bench] lanczos {K} steps {t_total:.2f} s (steps_done {steps})", file=sys.stderr, flush=True)
+    print(f"[bench] instrumented run {K} steps {t_instr:.2f} s", file=sys.stderr, flush=True)
+
+    # one full SLQ probe at the workload's Lanczos length
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    nodes, weights, slq_steps, trace, _ = mod.slq_density(1, m_slq, SEED_PROBE, o)
+    torch.cuda.synchronize()
+    t_slq = time.perf_counter() - t0
+    print(f"[bench] slq probe m={m_slq} {t_slq:.2f} s", file=sys.stderr, flush=True)
 
     ms_step = t_total * 1e3 / K
     value = K / t_total
@@ -193,6 +215,13 @@ def main():
         "config": {"workload": args.workload, "params": mod.num_params, "global_batch": B, "seq_len": S,
                    "eps": eps, "lanczos_m": K, "reorth": w["reorth"], "basis": w["basis"], "parallelism": "none"},
         "lanczos_iters_per_min": 60.0 * value,
+        "ms_per_step_instrumented": t_instr * 1e3 / K,
+        "slq_probe": {"m": m_slq, "steps_done": int(slq_steps[0]), "seconds": t_slq,
+                      "lanczos_iters_per_min": 60.0 * int(slq_steps[0]) / t_slq,
+                      "hvp_per_s": int(slq_steps[0]) / t_slq,
+                      "ritz_max": float(nodes[0, :int(slq_steps[0])].max()),
+                      "ritz_min": float(nodes[0, :int(slq_steps[0])].min()),
+                      "trace_estimate": trace},
         "hvp_only_per_s": 1.0 / t_hvp,
         "hvp_tokens_per_s": B * S / t_hvp,
         "lanczos_overhead": (ms_step * 1e-3) / t_hvp - 1.0,
@@ -206,7 +235,7 @@ def main():
         "lanczos_vec_ms_per_step": tm["lanczos"]["ms"] / K,
         "lanczos_vec_hbm_GBps": lz_gbps,
         "lanczos_vec_hbm_frac": (lz_gbps / PEAK_HBM_GBPS) if lz_gbps else None,
-        "roofline": {"bound": "mfma", "kernel": "bf16 MFMA GEMM (all launches of one step)",
+        "roofline": {"bound": "mfma", "kernel": "bf16 MFMA GEMM (all launches of one step, instrumented run)",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
                      "traffic": committed_gemm_traffic(args.workload)},
     }
