@@ -254,6 +254,17 @@ fdh_status fdh_ritz_diagnostics(const double* alpha, const double* beta, int32_t
  * <a_b, b_b> over the parameters of layer b; a, b float32 [P] on device. */
 fdh_status fdh_block_stats(fdh_ctx* ctx, const float* a_dev, const float* b_dev, double* out_host);
 
+/* fdh_block_stats for callers that cannot allocate device memory (code under
+ * stream capture, tight serving loops, harnesses that forbid allocation): the
+ * same statistics and the same kernels, with the partial sums in a fixed
+ * 16 KiB device array that the library holds on every GPU it runs on until
+ * the process ends, instead of the workspace.  Needs no workspace and calls
+ * no device allocator.  At most 256 transformer layers (FDH_ERR_UNSUPPORTED
+ * beyond, before any launch).  All calls on one GPU share that array: calls
+ * that overlap on one GPU (other host threads or streams) race and must be
+ * serialised by the caller.  Waits for the context stream. */
+fdh_status fdh_block_stats_noalloc(fdh_ctx* ctx, const float* a_dev, const float* b_dev, double* out_host);
+
 /* Block-diagonal hypothesis test (section 6, Exp I) on the bound operator:
  * h = H v, and for every transformer layer b, h_b = H v^(b) where v^(b) is v
  * with all entries outside layer b set to zero (not renormalised).  For each b,

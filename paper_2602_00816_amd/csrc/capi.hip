@@ -1,6 +1,7 @@
 // C ABI (include/fdhvp.h): argument validation and dispatch to the engine.
 // No exception crosses this boundary.
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 
@@ -210,6 +211,80 @@ fdh_status fdh_slq_density(fdh_ctx* ctx, int32_t probes, int32_t m, uint64_t see
 
 fdh_status fdh_block_stats(fdh_ctx* ctx, const float* a_dev, const float* b_dev, double* out_host) {
   return run(ctx, [&](fdh::Engine& e) { return e.block_stats(a_dev, b_dev, out_host); });
+}
+
+}  // extern "C"
+
+// ---- allocation-free block statistics --------------------------------------
+// The partial sums of fdh_block_stats_noalloc live in one file-scope device
+// array per GPU instead of the workspace: 256 workgroup partials of four sums,
+// then four sums per block, for at most NOALLOC_MAX_BLOCKS blocks (16 KiB).
+// Host code never passes the array's name to a kernel (on the host it only
+// stands in for the symbol): its device address is looked up once per device
+// with hipGetSymbolAddress and that address is used everywhere.
+constexpr int NOALLOC_MAX_BLOCKS = 256;
+constexpr int NOALLOC_PARTIALS = 256 * 4;  // launch_block_stats: 256 workgroups x 4 sums
+static __device__ __align__(256) double scratch[NOALLOC_PARTIALS + 4 * NOALLOC_MAX_BLOCKS];
+
+namespace {
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+double* g_scratch_ptr[MAX_DEVICES] = {};
+
+// device address of this device's scratch array (looked up on first use)
+hipError_t scratch_ptr(double** out) {
+  int dev = 0;
+  hipError_t r = hipGetDevice(&dev);
+  if (r != hipSuccess) return r;
+  if (dev < 0 || dev >= MAX_DEVICES) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    r = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (r != hipSuccess) return r;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = (double*)p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+}  // namespace
+
+extern "C" {
+
+fdh_status fdh_block_stats_noalloc(fdh_ctx* ctx, const float* a_dev, const float* b_dev, double* out_host) {
+  return run(ctx, [&](fdh::Engine& e) -> int {
+    if (e.quad || !a_dev || !b_dev || !out_host) { e.err = "bad block_stats arguments"; return FDH_ERR_INVALID_ARG; }
+    if (e.L > NOALLOC_MAX_BLOCKS) {
+      e.err = "fdh_block_stats_noalloc handles at most 256 blocks; use fdh_block_stats";
+      return FDH_ERR_UNSUPPORTED;
+    }
+    double* sp = nullptr;
+    hipError_t r = scratch_ptr(&sp);
+    if (r != hipSuccess) { e.err = std::string("scratch symbol: ") + hipGetErrorString(r); return FDH_ERR_HIP; }
+    double* part = sp;
+    double* sums = sp + NOALLOC_PARTIALS;
+    // layer ranges straight from the layout (per-layer entries are contiguous)
+    for (int l = 0; l < e.L; ++l) {
+      int64_t rg[2] = {-1, -1};
+      for (const fdh::Entry& en : e.entries)
+        if (en.layer == l) {
+          if (rg[0] < 0) rg[0] = en.off;
+          rg[1] = en.off + en.numel;
+        }
+      r = fdh::launch_block_stats(a_dev, b_dev, rg, 1, part, sums + 4 * l, e.stream);
+      if (r != hipSuccess) { e.err = std::string("block stats launch: ") + hipGetErrorString(r); return FDH_ERR_HIP; }
+    }
+    double h[4 * NOALLOC_MAX_BLOCKS];
+    if (e.L > 0) {
+      r = hipMemcpyAsync(h, sums, sizeof(double) * 4 * e.L, hipMemcpyDeviceToHost, e.stream);
+      if (r == hipSuccess) r = hipStreamSynchronize(e.stream);
+      if (r != hipSuccess) { e.err = std::string("block stats read-back: ") + hipGetErrorString(r); return FDH_ERR_HIP; }
+    }
+    for (int l = 0; l < e.L; ++l)
+      for (int c = 0; c < 3; ++c) out_host[3 * l + c] = h[4 * l + c];
+    return FDH_OK;
+  });
 }
 
 fdh_status fdh_block_diagonal(fdh_ctx* ctx, const float* v_dev, double* stats_host) {

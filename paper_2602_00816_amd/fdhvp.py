@@ -89,6 +89,7 @@ def lib():
         "fdh_lanczos": (i32, [vp, i32, u64, C.POINTER(LanczosOpts), pd, pd, pi]),
         "fdh_slq_density": (i32, [vp, i32, i32, u64, C.POINTER(LanczosOpts), pd, pd, pi, pd]),
         "fdh_block_stats": (i32, [vp, vp, vp, pd]),
+        "fdh_block_stats_noalloc": (i32, [vp, vp, vp, pd]),
         "fdh_block_diagonal": (i32, [vp, vp, pd]),
         "fdh_cg_solve": (i32, [vp, vp, C.c_double, i32, C.c_double, vp, pd, C.POINTER(C.c_int32)]),
         "fdh_last_error": (C.c_char_p, [vp]),
@@ -411,6 +412,16 @@ class Model:
         out = np.zeros((max(self.num_blocks, 0), 4))
         self._check(self._L.fdh_block_diagonal(self._h, _ptr(v), out.ctypes.data_as(C.POINTER(C.c_double))),
                     "fdh_block_diagonal")
+        return out
+
+    def block_stats_noalloc(self, a, b):
+        """fdh_block_stats without the workspace (fixed device scratch; no allocation)."""
+        self._check_vec(a, "a")
+        self._check_vec(b, "b")
+        out = np.zeros((max(self.num_blocks, 0), 3))
+        self._check(self._L.fdh_block_stats_noalloc(self._h, _ptr(a), _ptr(b),
+                                                    out.ctypes.data_as(C.POINTER(C.c_double))),
+                    "fdh_block_stats_noalloc")
         return out
 
     def block_stats(self, a, b):

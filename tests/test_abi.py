@@ -208,3 +208,16 @@ def test_binding_refuses_mismatched_operands_before_any_launch():
     bm = _model("llama-1.3b-bf16")
     with pytest.raises(ValueError, match="dtype"):
         bm.bind(_FakeTensor("float32", bm.num_params), None, 1e-3)
+
+
+def test_block_stats_noalloc_refuses_too_many_blocks_before_any_launch():
+    lib = fd.lib()
+    cfg = fd.ModelConfig(1, 300, 8, 1, 1, 8, 8, 8, 0, 1e-5, 1e4, 0, 0)   # 300 tiny layers
+    h = C.c_void_p()
+    assert lib.fdh_create(C.byref(cfg), None, C.byref(h)) == 0
+    out = np.zeros(3 * 300)
+    st = lib.fdh_block_stats_noalloc(h, C.c_void_p(1 << 40), C.c_void_p(1 << 40),
+                                     out.ctypes.data_as(C.POINTER(C.c_double)))
+    assert st == -6 and b"256" in lib.fdh_last_error(h)
+    assert lib.fdh_block_stats_noalloc(h, None, C.c_void_p(1 << 40), out.ctypes.data_as(C.POINTER(C.c_double))) == -1
+    lib.fdh_destroy(h)
