@@ -109,6 +109,8 @@ def main():
     ap.add_argument("--hvp-reps", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cg-steps", type=int, default=2, help="timed CG inverse-HVP steps after the Lanczos run")
+    ap.add_argument("--slq-m", type=int, default=-1,
+                    help="Lanczos length of the timed SLQ probe (-1: the workload's m, 0: no probe)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one plain 1 GiB device copy first (reference for hardware byte counters)")
     args = ap.parse_args()
@@ -127,7 +129,7 @@ def main():
     B, S = w["batch"], w["seq"]
     mod = fd.Model.from_workload(w)
     o = fd.opts(w["reorth"], w["window"], w["basis"])
-    m_slq = int(w["m"])
+    m_slq = int(w["m"]) if args.slq_m < 0 else args.slq_m
     m_plan = max(K, 2, m_slq)
     ws = mod.set_workspace(B, S, m_plan, o)
     params = mod.init_params(SEED_PARAMS)
@@ -179,12 +181,18 @@ def main():
     print(f"[bench] instrumented run {K} steps {t_instr:.2f} s", file=sys.stderr, flush=True)
 
     # one full SLQ probe at the workload's Lanczos length
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    nodes, weights, slq_steps, trace, _ = mod.slq_density(1, m_slq, SEED_PROBE, o)
-    torch.cuda.synchronize()
-    t_slq = time.perf_counter() - t0
-    print(f"[bench] slq probe m={m_slq} {t_slq:.2f} s", file=sys.stderr, flush=True)
+    slq = None
+    if m_slq > 0:
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        nodes, weights, slq_steps, trace, _ = mod.slq_density(1, m_slq, SEED_PROBE, o)
+        torch.cuda.synchronize()
+        t_slq = time.perf_counter() - t0
+        print(f"[bench] slq probe m={m_slq} {t_slq:.2f} s", file=sys.stderr, flush=True)
+        n = int(slq_steps[0])
+        slq = {"m": m_slq, "steps_done": n, "seconds": t_slq, "lanczos_iters_per_min": 60.0 * n / t_slq,
+               "hvp_per_s": n / t_slq, "ritz_max": float(nodes[0, :n].max()), "ritz_min": float(nodes[0, :n].min()),
+               "trace_estimate": trace}
 
     ms_step = t_total * 1e3 / K
     value = K / t_total
@@ -216,12 +224,7 @@ def main():
                    "eps": eps, "lanczos_m": K, "reorth": w["reorth"], "basis": w["basis"], "parallelism": "none"},
         "lanczos_iters_per_min": 60.0 * value,
         "ms_per_step_instrumented": t_instr * 1e3 / K,
-        "slq_probe": {"m": m_slq, "steps_done": int(slq_steps[0]), "seconds": t_slq,
-                      "lanczos_iters_per_min": 60.0 * int(slq_steps[0]) / t_slq,
-                      "hvp_per_s": int(slq_steps[0]) / t_slq,
-                      "ritz_max": float(nodes[0, :int(slq_steps[0])].max()),
-                      "ritz_min": float(nodes[0, :int(slq_steps[0])].min()),
-                      "trace_estimate": trace},
+        "slq_probe": slq,
         "hvp_only_per_s": 1.0 / t_hvp,
         "hvp_tokens_per_s": B * S / t_hvp,
         "lanczos_overhead": (ms_step * 1e-3) / t_hvp - 1.0,

@@ -217,6 +217,8 @@ constexpr int STG_LD = 36;
 constexpr int STG_FLOATS = 32 * STG_LD;
 // four staging areas fit one ring stage of the DMA kernels (256 x 32 + 128 x 32 bf16 at the smallest)
 static_assert(4 * STG_FLOATS * 4 <= (256 + 128) * 32 * 2, "staging areas exceed a ring stage");
+static_assert(4 * STG_FLOATS * 4 <= (256 + 256) * 32 * 2, "four blocks of staging exceed a 256 x 256 ring stage");
+// (the eight-wavefront kernel gives each pair of wavefronts one 256 x 256 stage, two blocks each)
 
 __device__ inline void wave_lds_order() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -274,6 +276,105 @@ __device__ inline void store_block_lds(const GemmArgs& a, const f32x16_t& acc, i
     }
   }
   wave_lds_order();   // the next block's writes come after these reads
+}
+
+// LDS-staged epilogue of NB 32x32 blocks of one wavefront (blocks (rb, cb[j]),
+// j < NB) in one round: all NB are written to the wavefront's staging area
+// (NB x 32 rows x 36 floats), then every lane reads its 4 NB quads, issues
+// every global read the epilogue needs (residual, previous C) before any
+// store, and stores.  One round has the latency of one block where the
+// one-block form pays it NB times (a wavefront that is alone on its SIMD has
+// nothing else to hide it with).  Global accesses cover eight rows of
+// 128 contiguous bytes, as in store_block_lds.
+template <typename T, int NB>
+__device__ inline void store_blocks_lds(const GemmArgs& a, const f32x16_t (&acc)[NB], int64_t coff, int rb,
+                                        const int (&cb)[NB], int lane, float* stg) {
+  {
+    const int wr = lane & 31, wh = lane >> 5;
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        *reinterpret_cast<float4*>(stg + j * STG_FLOATS + wr * STG_LD + 8 * g + 4 * wh) =
+            make_float4(a.alpha * acc[j][4 * g], a.alpha * acc[j][4 * g + 1], a.alpha * acc[j][4 * g + 2],
+                        a.alpha * acc[j][4 * g + 3]);
+  }
+  wave_lds_order();
+  const int c4 = 4 * (lane & 7);
+  float4 v[NB][4];
+#pragma unroll
+  for (int j = 0; j < NB; ++j)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[j][k] = *reinterpret_cast<const float4*>(stg + j * STG_FLOATS + (8 * k + (lane >> 3)) * STG_LD + c4);
+  wave_lds_order();   // the next round's writes come after these reads
+  const size_t ob = a.out_type == OUT_F32 ? 4 : sizeof(T);
+  const bool aligned = a.ldc % 4 == 0 && coff % 4 == 0 && (uintptr_t)a.C % (4 * ob) == 0 &&
+                       (!a.resid || (uintptr_t)a.resid % 16 == 0);
+  const bool full = aligned && rb + 32 <= a.M && cb[NB - 1] + 32 <= a.N;
+  if (full && a.out_type == OUT_F32 && !a.bias_theta && !a.bias_v) {
+    // the common case of the residual stream and the weight gradients: all
+    // reads first, then all stores
+    float* C = reinterpret_cast<float*>(a.C);
+    float4 r[NB][4];
+    const bool rd = a.resid != nullptr, bt = a.beta != 0.f;
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int64_t idx = coff + (int64_t)(rb + 8 * k + (lane >> 3)) * a.ldc + cb[j] + c4;
+        float4 t = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (rd) t = *reinterpret_cast<const float4*>(a.resid + idx);
+        if (bt) {
+          const float4 c = *reinterpret_cast<const float4*>(C + idx);
+          t.x += a.beta * c.x; t.y += a.beta * c.y; t.z += a.beta * c.z; t.w += a.beta * c.w;
+        }
+        r[j][k] = t;
+      }
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int64_t idx = coff + (int64_t)(rb + 8 * k + (lane >> 3)) * a.ldc + cb[j] + c4;
+        *reinterpret_cast<float4*>(C + idx) =
+            make_float4(v[j][k].x + r[j][k].x, v[j][k].y + r[j][k].y, v[j][k].z + r[j][k].z, v[j][k].w + r[j][k].w);
+      }
+    return;
+  }
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const int col0 = cb[j] + c4;
+    float badd[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int col = min(col0 + q, a.N - 1);
+      if (a.bias_theta) badd[q] += a.bias_theta_scale * ldf(reinterpret_cast<const T*>(a.bias_theta), col);
+      if (a.bias_v) badd[q] += a.bias_v_scale * a.bias_v[col];
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int row = rb + 8 * k + (lane >> 3);
+      if (row >= a.M || col0 >= a.N) continue;
+      const float x[4] = {v[j][k].x + badd[0], v[j][k].y + badd[1], v[j][k].z + badd[2], v[j][k].w + badd[3]};
+      const int64_t base = coff + (int64_t)row * a.ldc + col0;
+      if (aligned && col0 + 3 < a.N) {
+        store_quad<T>(a, x, base);
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (col0 + q >= a.N) break;
+          float y = x[q];
+          if (a.out_type == OUT_F32) {
+            float* C = reinterpret_cast<float*>(a.C);
+            if (a.resid) y += a.resid[base + q];
+            if (a.beta != 0.f) y += a.beta * C[base + q];
+            C[base + q] = y;
+          } else {
+            stf(reinterpret_cast<T*>(a.C), base + q, y);
+          }
+        }
+      }
+    }
+  }
 }
 
 template <typename T, bool AK, bool BKM>
@@ -615,9 +716,14 @@ __device__ inline void wait_vm() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+#ifndef FDH_DMA_STAGES
+#define FDH_DMA_STAGES 4
+#endif
 template <int BN_, int WN, bool AK, bool BKM>
 __global__ __launch_bounds__(64 * 2 * WN) void gemm_bf16_dma(GemmArgs a) {
   constexpr int BM_ = 256, WM = 2, NW = WM * WN;
+  // ring depth: 4 stages, or 5 for 256-wide tiles when built with FDH_DMA_STAGES=5
+  constexpr int NS = (BN_ == 256 && FDH_DMA_STAGES == 5) ? 5 : 4;
   constexpr int WTN = BN_ / WN;                 // wavefront tile: 128 x WTN
   constexpr int IM = 4, JN = WTN / 32;
   constexpr int ASZ = BM_ * KT3, BSZ = BN_ * KT3;              // elements per stage
@@ -628,6 +734,7 @@ __global__ __launch_bounds__(64 * 2 * WN) void gemm_bf16_dma(GemmArgs a) {
   __shared__ __attribute__((aligned(1024))) bf16_t st1[ASZ + BSZ];
   __shared__ __attribute__((aligned(1024))) bf16_t st2[ASZ + BSZ];
   __shared__ __attribute__((aligned(1024))) bf16_t st3[ASZ + BSZ];
+  __shared__ __attribute__((aligned(1024))) bf16_t st4[NS == 5 ? ASZ + BSZ : 8];
 
   const int gx = gridDim.x, gy = gridDim.y;
   const int nb = gx * gy * gridDim.z;
@@ -672,7 +779,8 @@ __global__ __launch_bounds__(64 * 2 * WN) void gemm_bf16_dma(GemmArgs a) {
     if constexpr (S == 0) return st0;
     else if constexpr (S == 1) return st1;
     else if constexpr (S == 2) return st2;
-    else return st3;
+    else if constexpr (S == 3) return st3;
+    else return st4;
   };
   auto issue = [&](int t, bf16_t* st) {
     const int p = t >= nkt ? 1 : 0;
@@ -694,13 +802,14 @@ __global__ __launch_bounds__(64 * 2 * WN) void gemm_bf16_dma(GemmArgs a) {
   // the previous slice, then 2 x IM x JN MFMAs
   auto step = [&](auto s, int t) {
     constexpr int S = decltype(s)::value;
-    const int ahead = min(NS3 - 2, total - 1 - t);
-    if (ahead >= 2) wait_vm<2 * PERT>();
+    const int ahead = min(NS - 2, total - 1 - t);
+    if (ahead >= 3) wait_vm<3 * PERT>();
+    else if (ahead == 2) wait_vm<2 * PERT>();
     else if (ahead == 1) wait_vm<PERT>();
     else wait_vm<0>();
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");  // keep the stage's LDS reads after the barrier
-    if (t + NS3 - 1 < total) issue(t + NS3 - 1, stage(std::integral_constant<int, (S + NS3 - 1) % NS3>{}));
+    if (t + NS - 1 < total) issue(t + NS - 1, stage(std::integral_constant<int, (S + NS - 1) % NS>{}));
     const bf16_t* cA = stage(s);
     const bf16_t* cB = cA + ASZ;
 #pragma clang loop unroll(full)
@@ -721,24 +830,35 @@ __global__ __launch_bounds__(64 * 2 * WN) void gemm_bf16_dma(GemmArgs a) {
   if (total > 0) issue(0, st0);
   if (total > 1) issue(1, st1);
   if (total > 2) issue(2, st2);
-  for (int t0 = 0; t0 < total; t0 += NS3) {
+  if (NS == 5 && total > 3) issue(3, st3);
+  for (int t0 = 0; t0 < total; t0 += NS) {
     step(std::integral_constant<int, 0>{}, t0);
     if (t0 + 1 < total) step(std::integral_constant<int, 1>{}, t0 + 1);
     if (t0 + 2 < total) step(std::integral_constant<int, 2>{}, t0 + 2);
     if (t0 + 3 < total) step(std::integral_constant<int, 3>{}, t0 + 3);
+    if constexpr (NS == 5)
+      if (t0 + 4 < total) step(std::integral_constant<int, 4>{}, t0 + 4);
   }
 
   const int64_t coff = batch_off(z, a.inner_count, a.c_outer, a.c_inner, a.c_div);
-  // stage the output through the ring once every wavefront is done with it
+  // stage the output through the ring once every wavefront is done with it:
+  // two blocks per round, 2 x 32 x 36 floats per wavefront
   wait_vm<0>();
   __syncthreads();
   const int wv = threadIdx.x >> 6;
-  float* stg = reinterpret_cast<float*>(wv < 4 ? st0 : st1) + (wv & 3) * STG_FLOATS;
+  if constexpr (JN == 2 && NW == 8) {
+    float* stg = reinterpret_cast<float*>(wv < 2 ? st0 : wv < 4 ? st1 : wv < 6 ? st2 : st3) + (wv & 1) * 2 * STG_FLOATS;
+    const int cbs[2] = {n0 + wn * WTN, n0 + wn * WTN + 32};
 #pragma clang loop unroll(full)
-  for (int i = 0; i < IM; ++i)
+    for (int i = 0; i < IM; ++i) store_blocks_lds<bf16_t, 2>(a, acc[i], coff, m0 + wm * 128 + i * 32, cbs, lane, stg);
+  } else {
+    float* stg = reinterpret_cast<float*>(wv < 4 ? st0 : st1) + (wv & 3) * STG_FLOATS;
 #pragma clang loop unroll(full)
-    for (int j = 0; j < JN; ++j)
-      store_block_lds<bf16_t>(a, acc[i][j], coff, m0 + wm * 128 + i * 32, n0 + wn * WTN + j * 32, lane, stg);
+    for (int i = 0; i < IM; ++i)
+#pragma clang loop unroll(full)
+      for (int j = 0; j < JN; ++j)
+        store_block_lds<bf16_t>(a, acc[i][j], coff, m0 + wm * 128 + i * 32, n0 + wn * WTN + j * 32, lane, stg);
+  }
 }
 
 // ===========================================================================
@@ -915,14 +1035,14 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4(GemmArgs a) {
   }
 
   const int64_t coff = batch_off(z, a.inner_count, a.c_outer, a.c_inner, a.c_div);
-  // stage the output through the ring once every wavefront is done with it
+  // stage the output through the ring once every wavefront is done with it:
+  // wavefront w uses stage w (4 x 32 x 36 floats = 18 KB of its 32 KB)
   __syncthreads();
-  float* stg = reinterpret_cast<float*>(st0) + (threadIdx.x >> 6) * STG_FLOATS;
+  float* stg = reinterpret_cast<float*>(wave == 0 ? st0 : wave == 1 ? st1 : wave == 2 ? st2 : st3);
+  const int cbs[4] = {n0 + wn * 128, n0 + wn * 128 + 32, n0 + wn * 128 + 64, n0 + wn * 128 + 96};
 #pragma clang loop unroll(full)
   for (int i = 0; i < IM; ++i)
-#pragma clang loop unroll(full)
-    for (int j = 0; j < JN; ++j)
-      store_block_lds<bf16_t>(a, acc[i][j], coff, m0 + wm * 128 + i * 32, n0 + wn * 128 + j * 32, lane, stg);
+    store_blocks_lds<bf16_t, 4>(a, acc[i], coff, m0 + wm * 128 + i * 32, cbs, lane, stg);
 }
 
 // ===========================================================================
@@ -1213,14 +1333,14 @@ hipError_t gemm(const GemmArgs& a, hipStream_t stream) {
       const int64_t t128 = (int64_t)ceil_div(a.M, 256) * ceil_div(a.N, 128) * a.nbatch;
       const bool dma = a.K % KT3 == 0;
       // 256 x 256 tiles once there are more than 128 of them; with fewer,
-      // 256 x 128 tiles keep more of the 256 CUs busy.  With an MN-major
-      // operand the four-wavefront kernel is fastest (measured on the 1.3B
-      // layer shapes); with both operands K-major, and for short contractions
-      // that never fill its pipeline, the eight-wavefront kernel is as fast
-      // or faster, and its epilogue (fp32 output plus residual) is spread
-      // over twice as many wavefronts.
+      // 256 x 128 tiles keep more of the 256 CUs busy.  The four-wavefront
+      // kernel is the fastest for fp32 outputs on the 1.3B layer shapes (both
+      // operand layouts, one or two operand pairs); with both operands K-major
+      // and an operand-type output (q/k/v and the MLP input product), and for
+      // short contractions that never fill its pipeline, the eight-wavefront
+      // kernel is as fast or faster (measured inside the HVP).
       const bool kk = a.A[0].s_k == 1 && a.B[0].s_k == 1;
-      if (a.N > 128 && t256 > 128) tile = dma ? ((kk || a.K < 512) ? 4 : 6) : 2;
+      if (a.N > 128 && t256 > 128) tile = dma ? ((a.K < 512 || (kk && a.out_type == OUT_OP)) ? 4 : 6) : 2;
       else if (t128 >= 64) tile = dma ? 5 : 3;
     }
     if (tile == 2) { launch_big<256, 256, 2, 4>(a, stream); return hipGetLastError(); }

@@ -19,9 +19,10 @@ each case keeps a compact record of every product the parity test compares:
 Directions: ``probe`` = the Rademacher probe z/sqrt(P) of seed 3 (the SLQ
 probe q_1), ``gauss`` = the Gaussian unit direction of seed 4.
 
-Usage: python tests/golden/make_scale_fixtures.py CASE [CASE ...]
+Usage: python tests/golden/make_scale_fixtures.py [--out DIR] CASE [CASE ...]
        python tests/golden/make_scale_fixtures.py --list
-Each case is written to tests/golden/scale/<case>.npz.
+Each case is written to DIR/<case>.npz (default tests/golden/scale).  The 8B
+case needs about 90 GB of host memory.
 """
 from __future__ import annotations
 
@@ -56,7 +57,7 @@ CASES = {
     "llama3-8b-2l-1x2048": dict(workload="llama3-8b-bf16", n_layers=2, batch=1, seq=2048,
                                 dirs=("probe",), lanczos=True),
 }
-for _L in (1, 2, 4, 8):
+for _L in (1, 2, 4, 8, 16, 24):
     CASES[f"llama-1.3b-depth{_L}-1x2048"] = dict(workload="llama-1.3b-bf16", n_layers=_L, batch=1, seq=2048,
                                                  dirs=("probe",), lanczos=False)
 # the small fp32 workload's SLQ setting, one probe: m = 80 steps, full reorthogonalisation
@@ -161,6 +162,10 @@ def lanczos_case(name: str, spec: dict):
 
 
 def main(argv):
+    global OUT
+    if len(argv) >= 2 and argv[0] == "--out":
+        OUT = os.path.abspath(argv[1])
+        argv = argv[2:]
     if not argv or argv[0] == "--list":
         for k in list(CASES) + list(LANCZOS_CASES):
             print(k)

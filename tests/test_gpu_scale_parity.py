@@ -136,10 +136,11 @@ def test_hvp_parity_real_token_batch(name):
     _run_case(name)
 
 
-@pytest.mark.parametrize("depth", [1, 2, 4, 8])
+@pytest.mark.parametrize("depth", [1, 2, 4, 8, 16, 24])
 def test_hvp_error_versus_depth_1_3b(depth):
-    """The 1.3B width at 1 x 2048 tokens with 1, 2, 4 and 8 layers: the bf16
-    error of the lockstep product, recorded against depth."""
+    """The 1.3B width at 1 x 2048 tokens with 1, 2, 4, 8, 16 and 24 layers
+    (24: the whole 1.3B model): the bf16 error of the lockstep product,
+    recorded against depth."""
     out = _run_case(f"llama-1.3b-depth{depth}-1x2048")
     say(f"  depth {depth}: rel L2 (sketch) {out['probe'][0]:.3e}")
 
