@@ -90,6 +90,21 @@ def log(*a):
     print(*a, flush=True)
 
 
+def oracle_hvp(cfg, theta, v, tok, tag):
+    """oracle.hvp.lm_hvp, with a line printed after each of its two gradients
+    (one gradient of the larger cases takes minutes)."""
+    g = OH.lm_grad_fn(cfg, tok)
+    n = [0]
+
+    def grad(th):
+        t = time.time()
+        r = g(th)
+        n[0] += 1
+        log(f"  {tag}: gradient {n[0]} of 2 ({time.time() - t:.1f} s)")
+        return r
+    return OH.fd_hvp(grad, theta, v, EPS)
+
+
 def hvp_case(name: str, spec: dict):
     w = dict(WORKLOADS[spec["workload"]], n_layers=spec["n_layers"])
     t0 = time.time()
@@ -113,14 +128,14 @@ def hvp_case(name: str, spec: dict):
             cache = {}
 
             def hv_fn(x):
-                cache["hv"] = OH.lm_hvp(cfg, theta, x, EPS, tok)
+                cache["hv"] = oracle_hvp(cfg, theta, x, tok, f"{name} {kind}")
                 return cache["hv"]
             a, b, _ = OL.lanczos(hv_fn, v, 1, OL.FULL)
             hv = cache["hv"]
             rec["alpha1"] = np.float64(a[0])
             rec["beta2"] = np.float64(b[0])
         else:
-            hv = OH.lm_hvp(cfg, theta, v, EPS, tok)
+            hv = oracle_hvp(cfg, theta, v, tok, f"{name} {kind}")
         log(f"[{name}] {kind}: oracle FD-HVP {time.time() - t1:.1f} s, ||Hv|| = {np.linalg.norm(hv):.6e}")
         del v
         rec[f"{kind}_norm2"] = np.array([float(hv[e.offset:e.offset + e.numel] @ hv[e.offset:e.offset + e.numel])
@@ -129,6 +144,8 @@ def hvp_case(name: str, spec: dict):
             rec[f"{kind}_val{i}"] = hv[e.offset + rec[f"idx{i}"].astype(np.int64)]
         sk = np.zeros((NSKETCH, len(lay)))
         for j in range(NSKETCH):
+            if j % 4 == 0:
+                log(f"  {name} {kind}: sketch {j} of {NSKETCH}")
             z = synth.rademacher(SKETCH_SEED0 + j, P)
             for i, e in enumerate(lay):
                 sk[j, i] = float(hv[e.offset:e.offset + e.numel] @ z[e.offset:e.offset + e.numel])
