@@ -39,10 +39,8 @@
 //                 heads of its group), S = Q K^T tiles, dV = P^T dO, dK = dS^T Q
 // K/V (or Q/dO) tiles are streamed into a double-buffered LDS ring by direct
 // global-to-LDS loads.  LDS tiles are [rows][D] with the 16-byte chunk c of
-// row r at c ^ f(r), f a bit reversal of low row bits.  Hardware counters
-// show no bank conflicts for the 32-row 16-byte fragment reads and both kinds
-// of transposing reads; the 16-row fragment reads of flash_bwd_kv (ld_k16)
-// still conflict.
+// row r at c ^ f(r), f a bit reversal of low row bits (and, for the 16-row
+// fragment reads of flash_bwd_kv, the variant described at tswz).
 #include "common.h"
 #include "kernels.h"
 
@@ -62,11 +60,23 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 
 constexpr float NEG = -1.0e30f;   // masked logit (exp underflows to 0, no NaN)
 
-// element offset of chunk `chunk` (8 elements) of row `row` in an LDS [rows][D] tile
-template <int D>
+// element offset of chunk `chunk` (8 elements) of row `row` in an LDS [rows][D] tile.
+// SW = 0: chunk XOR the bit reversal of row & 15 (D = 128).  SW = 1 (the query
+// and output-gradient tiles of flash_bwd_kv, D = 128): chunk XOR f(row & 7)
+// with f's bits 3, 2 = bits 1, 0 of the row and bits 1, 0 both = bit 2.  A
+// 16-byte read is served for lane groups {i..i+7, i+32..i+39} (the pattern the
+// bank-conflict counters show); the 16-row reads of that kernel put rows
+// r and r ^ 4 at chunks c and c ^ 2 in one group, which needs bits 0, 2, 3 of
+// f distinct over eight consecutive rows, and its transposing reads (32 lanes
+// per clock, chunks c and c ^ 1 of eight rows) need bits 1, 2, 3 distinct:
+// this f gives both, the bit reversal only the second.
+template <int D, int SW = 0>
 __device__ inline int tswz(int row, int chunk) {
   int f;
-  if (D == 128) {
+  if (D == 128 && SW == 1) {
+    const int r = row & 7;
+    f = ((r & 3) << 2) | (((r >> 2) & 1) * 3);
+  } else if (D == 128) {
     const int r = row & 15;
     f = ((r & 1) << 3) | ((r & 2) << 1) | ((r & 4) >> 1) | ((r & 8) >> 3);
   } else {
@@ -86,11 +96,11 @@ __device__ inline bf16x8_t ld_k32(const bf16_t* t, int r0, int s, int lane) {
 // columns 32 s + 8 (lane / 16) .. + 7
 template <int D>
 __device__ inline bf16x8_t ld_k16(const bf16_t* t, int r0, int s, int lane) {
-  return *reinterpret_cast<const bf16x8_t*>(t + tswz<D>(r0 + (lane & 15), 4 * s + (lane >> 4)));
+  return *reinterpret_cast<const bf16x8_t*>(t + tswz<D, 1>(r0 + (lane & 15), 4 * s + (lane >> 4)));
 }
-template <int D>
+template <int D, int SW = 0>
 __device__ inline v4i16 tr4(const bf16_t* t, int row, int col) {
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(t + tswz<D>(row, col >> 3) + (col & 7)));
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(t + tswz<D, SW>(row, col >> 3) + (col & 7)));
 }
 __device__ inline bf16x8_t cat(v4i16 a, v4i16 b) {
   const v8i16 v = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
@@ -114,7 +124,7 @@ __device__ inline bf16x8_t ld_t16(const bf16_t* t, int kk, int n0, int lane) {
   const int g = lane >> 4, i = lane & 15;
   const int col = n0 + 4 * (i & 3);
   const int lo = kk + 4 * g + (i >> 2);
-  return cat(tr4<D>(t, lo, col), tr4<D>(t, lo + 16, col));
+  return cat(tr4<D, 1>(t, lo, col), tr4<D, 1>(t, lo + 16, col));
 }
 
 __device__ inline bf16x8_t pack8(const float* x) {
@@ -155,7 +165,7 @@ __device__ inline void coshsinh(float b, float& c, float& s) {
 // +16 l in LDS, so each lane fetches the logical chunk that the swizzle puts
 // at that position.  Completion is waited for with vmcnt before the barrier
 // that publishes the tiles.
-template <int D, int R, int NTILE>
+template <int D, int R, int NTILE, int SW = 0>
 __device__ inline void dma_tiles(bf16_t* dst, const bf16_t* const (&src)[NTILE], int64_t ld, int wave, int lane) {
   constexpr int CPR = D / 8, RPI = 64 / CPR, IPT = R / RPI, NI = NTILE * IPT;
   static_assert(IPT % 4 == 0, "each tile's loads must split evenly over four wavefronts");
@@ -164,7 +174,7 @@ __device__ inline void dma_tiles(bf16_t* dst, const bf16_t* const (&src)[NTILE],
     const int tile = 4 * u / IPT;           // compile-time: wave < 4 never crosses a tile
     const int q = 4 * u % IPT + wave;
     const int row = q * RPI + lane / CPR, pch = lane % CPR;
-    const int lch = (tswz<D>(row, pch) - row * D) >> 3;   // the swizzle is an involution on chunks
+    const int lch = (tswz<D, SW>(row, pch) - row * D) >> 3;   // the swizzle is an involution on chunks
     const bf16_t* g = src[tile] + (int64_t)row * ld + 8 * lch;
     const uint32_t la = (uint32_t)(uintptr_t)(lds_void_t*)(dst + tile * R * D + q * 512);
     asm volatile(
@@ -663,8 +673,8 @@ __global__ __launch_bounds__(256) void flash_bwd_kv_kernel(FlashArgs a) {
     // the two row strides differ: issue the Q and dO pairs separately
     const bf16_t* sq[2] = {src[0], src[1]};
     const bf16_t* so[2] = {src[2], src[3]};
-    dma_tiles<D, QB, 2>(ring[it & 1], sq, a.ld, wave, lane);
-    dma_tiles<D, QB, 2>(ring[it & 1] + 2 * TILE, so, a.ldo, wave, lane);
+    dma_tiles<D, QB, 2, 1>(ring[it & 1], sq, a.ld, wave, lane);
+    dma_tiles<D, QB, 2, 1>(ring[it & 1] + 2 * TILE, so, a.ldo, wave, lane);
   };
   // row terms of the next block: loaded into registers with its tiles, written
   // to LDS after this block's compute (the load's wait would otherwise also
