@@ -165,14 +165,14 @@ __device__ inline void coshsinh(float b, float& c, float& s) {
 // +16 l in LDS, so each lane fetches the logical chunk that the swizzle puts
 // at that position.  Completion is waited for with vmcnt before the barrier
 // that publishes the tiles.
-template <int D, int R, int NTILE, int SW = 0>
+template <int D, int R, int NTILE, int SW = 0, int NWV = 4>
 __device__ inline void dma_tiles(bf16_t* dst, const bf16_t* const (&src)[NTILE], int64_t ld, int wave, int lane) {
   constexpr int CPR = D / 8, RPI = 64 / CPR, IPT = R / RPI, NI = NTILE * IPT;
-  static_assert(IPT % 4 == 0, "each tile's loads must split evenly over four wavefronts");
+  static_assert(IPT % NWV == 0, "each tile's loads must split evenly over the wavefronts");
 #pragma unroll
-  for (int u = 0; u < NI / 4; ++u) {
-    const int tile = 4 * u / IPT;           // compile-time: wave < 4 never crosses a tile
-    const int q = 4 * u % IPT + wave;
+  for (int u = 0; u < NI / NWV; ++u) {
+    const int tile = NWV * u / IPT;         // compile-time: wave < NWV never crosses a tile
+    const int q = NWV * u % IPT + wave;
     const int row = q * RPI + lane / CPR, pch = lane % CPR;
     const int lch = (tswz<D, SW>(row, pch) - row * D) >> 3;   // the swizzle is an involution on chunks
     const bf16_t* g = src[tile] + (int64_t)row * ld + 8 * lch;
@@ -801,6 +801,223 @@ __global__ __launch_bounds__(256) void flash_bwd_kv_kernel(FlashArgs a) {
     }
 }
 
+// dK/dV with the probabilities shared through LDS (D = 128): 64 keys of one
+// key/value head per workgroup of four wavefronts.  The score phase is
+// flash_bwd_kv_kernel's: wavefront w forms S, dP, P and dS for its 16 keys and
+// the 32 queries of the block.  It then writes its P.m, P.d, dS.m, dS.d
+// fragments (16 bytes per lane, in the query order of the transposing reads)
+// to an LDS buffer of the workgroup, and after a barrier wavefront w
+// accumulates dV and dK for all 64 keys and 32 of the 128 columns (quarter
+// w): each wavefront's transposing reads of the Q and dO tiles cover a
+// quarter of them, and the P/dS operands come back as plain 16-byte reads.
+// Per block the workgroup reads 32 KB transposed instead of 128 KB.
+// P buffer: [4 operands][64 keys][4 slots of 16 bytes], slot g of key row r
+// at g ^ ((r >> 2) & 3) (16-byte accesses of 16 consecutive rows and one slot,
+// or of 8 rows and slots g and g + 2, hit 64 distinct banks).  The counters
+// still show bank conflicts in this kernel (24% of its LDS-active cycles, 34%
+// with no swizzle and 17% with 80-byte rows); the kernel time moves by 4%
+// between those layouts, so LDS conflicts do not bound it.
+constexpr int PROW = 32;   // elements per key row of the P buffer
+__device__ inline int pslot(int row, int g) { return row * PROW + ((g ^ ((row >> 2) & 3)) << 3); }   // elements
+
+template <int D>
+__global__ __launch_bounds__(256) void flash_bwd_kvp_kernel(FlashArgs a) {
+  static_assert(D == 128, "shared-probability dK/dV is for head dimension 128");
+  constexpr int QB = 32, KS = D / 32, TILE = QB * D, KEYS = 64;
+  __shared__ __attribute__((aligned(1024))) bf16_t ring[2][4 * TILE];   // Q.m Q.d dO.m dO.d
+  __shared__ __attribute__((aligned(1024))) bf16_t pbuf[4][KEYS * PROW];  // P.m P.d dS.m dS.d
+  __shared__ float4 sst[2][QB];                                         // m, u, w, D.m
+  __shared__ __attribute__((aligned(16))) float sdd[2][QB];             // D.d
+
+  int kblk, bkh;
+  work_item(gridDim.y, kblk, bkh);   // lowest keys (most queries) first
+  const int b = bkh / a.Hk, kh = bkh % a.Hk;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int k0 = kblk * KEYS, kw = k0 + 16 * wave;
+  const int64_t row0 = (int64_t)b * a.S;
+  const int kj = kw + (lane & 15);
+  const int quarter = wave;   // the dV/dK columns of this wavefront
+
+  // K and V fragments of this wavefront's 16 keys (B operands of S = Q K^T, dP = dO V^T)
+  bf16x8_t km[KS], kd[KS], vm[KS], vd[KS];
+  {
+    const int64_t r = (row0 + kj) * a.ld + kh * D + 8 * (lane >> 4);
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      km[s] = *reinterpret_cast<const bf16x8_t*>(a.qkv_m + r + a.koff + 32 * s);
+      kd[s] = *reinterpret_cast<const bf16x8_t*>(a.qkv_d + r + a.koff + 32 * s);
+      vm[s] = *reinterpret_cast<const bf16x8_t*>(a.qkv_m + r + a.voff + 32 * s);
+      vd[s] = *reinterpret_cast<const bf16x8_t*>(a.qkv_d + r + a.voff + 32 * s);
+    }
+  }
+  // accumulators (kt, dt): keys k0 + 16 kt + 4 (lane / 16) + r, columns 32 quarter + 16 dt + lane % 16
+  f32x4_t Vm_[4][2], Vd_[4][2], Km_[4][2], Kd_[4][2];
+#pragma unroll
+  for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+    for (int dt = 0; dt < 2; ++dt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) Vm_[kt][dt][r] = Vd_[kt][dt][r] = Km_[kt][dt][r] = Kd_[kt][dt][r] = 0.f;
+
+  const int nqb = (a.S - k0) / QB;   // query blocks from the first key on, per head
+  const int total = nqb * a.G;
+  auto issue = [&](int it) {
+    const int g = it / nqb, qbk = it % nqb;
+    const int h = kh * a.G + g, q0 = k0 + qbk * QB;
+    const int64_t r = row0 + q0;
+    const bf16_t* sq[2] = {a.qkv_m + r * a.ld + (int64_t)h * D, a.qkv_d + r * a.ld + (int64_t)h * D};
+    const bf16_t* so[2] = {a.do_m + r * a.ldo + (int64_t)h * D, a.do_d + r * a.ldo + (int64_t)h * D};
+    dma_tiles<D, QB, 2, 1>(ring[it & 1], sq, a.ld, wave, lane);
+    dma_tiles<D, QB, 2, 1>(ring[it & 1] + 2 * TILE, so, a.ldo, wave, lane);
+  };
+  float4 nst = make_float4(0.f, 0.f, 0.f, 0.f);
+  float ndd = 0.f;
+  auto load_rows = [&](int it) {
+    if (tid < QB) {
+      const int g = it / nqb, qbk = it % nqb;
+      const int64_t si = ((int64_t)b * a.Hq + kh * a.G + g) * a.S + k0 + qbk * QB + tid;
+      const float4 st = a.stats[si];
+      const float2 dl = a.delta[si];
+      nst = make_float4(st.x, st.y, st.z, dl.x);
+      ndd = dl.y;
+    }
+  };
+  auto store_rows = [&](int it) {
+    if (tid < QB) {
+      sst[it & 1][tid] = nst;
+      sdd[it & 1][tid] = ndd;
+    }
+  };
+  load_rows(0);
+  issue(0);
+  __builtin_amdgcn_s_waitcnt(0);
+  store_rows(0);
+  __syncthreads();
+  for (int it = 0; it < total; ++it) {
+    if (it + 1 < total) {
+      load_rows(it + 1);
+      issue(it + 1);
+    }
+    const int q0 = k0 + (it % nqb) * QB;
+    const bf16_t* Qm = ring[it & 1];
+    const bf16_t* Qd = Qm + TILE;
+    const bf16_t* Om = Qm + 2 * TILE;
+    const bf16_t* Od = Qm + 3 * TILE;
+    {   // score phase: this wavefront's 16 keys
+      f32x4_t sm[2], sd[2], pm[2], pd[2];
+#pragma unroll
+      for (int qt = 0; qt < 2; ++qt) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sm[qt][r] = sd[qt][r] = pm[qt][r] = pd[qt][r] = 0.f;
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+          const bf16x8_t qa = ld_k16<D>(Qm, 16 * qt, s, lane), qb_ = ld_k16<D>(Qd, 16 * qt, s, lane);
+          sm[qt] = mma16(qa, km[s], sm[qt]);
+          sd[qt] = mma16(qa, kd[s], sd[qt]);
+          sd[qt] = mma16(qb_, km[s], sd[qt]);
+          const bf16x8_t oa = ld_k16<D>(Om, 16 * qt, s, lane), ob = ld_k16<D>(Od, 16 * qt, s, lane);
+          pm[qt] = mma16(oa, vm[s], pm[qt]);
+          pd[qt] = mma16(oa, vd[s], pd[qt]);
+          pd[qt] = mma16(ob, vm[s], pd[qt]);
+        }
+      }
+      const bool diag = q0 < kw + 16;
+      float bmax = 0.f;
+#pragma unroll
+      for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          sm[qt][r] *= a.scale;
+          sd[qt][r] *= a.scale;
+          bmax = fmaxf(bmax, fabsf(sd[qt][r]));
+        }
+      if (diag) {
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (q0 + 16 * qt + 4 * (lane >> 4) + r < kj) sm[qt][r] = NEG;
+      }
+      float Pm[8], Pd[8], gsm[8], gsd[8];   // rows in accumulator order: (qt, r) -> 4 qt + r
+      auto terms = [&](auto ser) {
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) {
+          const float4 ddv = *reinterpret_cast<const float4*>(&sdd[it & 1][16 * qt + 4 * (lane >> 4)]);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float4 st = sst[it & 1][16 * qt + 4 * (lane >> 4) + r];
+            const float dd = r == 0 ? ddv.x : (r == 1 ? ddv.y : (r == 2 ? ddv.z : ddv.w));
+            const float e = __expf(sm[qt][r] - st.x);
+            float c, sn;
+            coshsinh<decltype(ser)::value>(sd[qt][r], c, sn);
+            const float P_m = e * (c * st.y - sn * st.z), P_d = e * (sn * st.y - c * st.z);
+            const float xm = pm[qt][r] - st.w, xd = pd[qt][r] - dd;
+            Pm[4 * qt + r] = P_m;
+            Pd[4 * qt + r] = P_d;
+            gsm[4 * qt + r] = P_m * xm + P_d * xd;
+            gsd[4 * qt + r] = P_m * xd + P_d * xm;
+          }
+        }
+      };
+      if (!__any(bmax >= SERIES_MAX)) terms(std::true_type{});
+      else terms(std::false_type{});
+      // lane (g, i) holds queries 4g..4g+3 and 16+4g..+3 of key 16 wave + i: slot g of that key row
+      const int prow = 16 * wave + (lane & 15), g = lane >> 4;
+      *reinterpret_cast<bf16x8_t*>(&pbuf[0][pslot(prow, g)]) = pack8(Pm);
+      *reinterpret_cast<bf16x8_t*>(&pbuf[1][pslot(prow, g)]) = pack8(Pd);
+      *reinterpret_cast<bf16x8_t*>(&pbuf[2][pslot(prow, g)]) = pack8(gsm);
+      *reinterpret_cast<bf16x8_t*>(&pbuf[3][pslot(prow, g)]) = pack8(gsd);
+    }
+    __syncthreads();   // every wavefront's P and dS are in the buffer
+    {   // dV, dK phase: all 64 keys, columns 32 quarter .. + 31
+      bf16x8_t om[2], od[2], qa[2], qb_[2];
+#pragma unroll
+      for (int dt = 0; dt < 2; ++dt) {
+        const int n0 = 32 * quarter + 16 * dt;
+        om[dt] = ld_t16<D>(Om, 0, n0, lane);
+        od[dt] = ld_t16<D>(Od, 0, n0, lane);
+        qa[dt] = ld_t16<D>(Qm, 0, n0, lane);
+        qb_[dt] = ld_t16<D>(Qd, 0, n0, lane);
+      }
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt) {
+        const int prow = 16 * kt + (lane & 15), g = lane >> 4;
+        const bf16x8_t apm = *reinterpret_cast<const bf16x8_t*>(&pbuf[0][pslot(prow, g)]);
+        const bf16x8_t apd = *reinterpret_cast<const bf16x8_t*>(&pbuf[1][pslot(prow, g)]);
+        const bf16x8_t asm_ = *reinterpret_cast<const bf16x8_t*>(&pbuf[2][pslot(prow, g)]);
+        const bf16x8_t asd = *reinterpret_cast<const bf16x8_t*>(&pbuf[3][pslot(prow, g)]);
+#pragma unroll
+        for (int dt = 0; dt < 2; ++dt) {
+          Vm_[kt][dt] = mma16(apm, om[dt], Vm_[kt][dt]);
+          Vd_[kt][dt] = mma16(apm, od[dt], Vd_[kt][dt]);
+          Vd_[kt][dt] = mma16(apd, om[dt], Vd_[kt][dt]);
+          Km_[kt][dt] = mma16(asm_, qa[dt], Km_[kt][dt]);
+          Kd_[kt][dt] = mma16(asm_, qb_[dt], Kd_[kt][dt]);
+          Kd_[kt][dt] = mma16(asd, qa[dt], Kd_[kt][dt]);
+        }
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    if (it + 1 < total) store_rows(it + 1);
+    __syncthreads();   // the ring stage and the P buffer are free again
+  }
+
+#pragma unroll
+  for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+    for (int dt = 0; dt < 2; ++dt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int key = k0 + 16 * kt + 4 * (lane >> 4) + r;
+        const int64_t o = (row0 + key) * a.ldg + kh * D + 32 * quarter + 16 * dt + (lane & 15);
+        a.g_m[o + a.koff] = Km_[kt][dt][r] * a.scale;
+        a.g_d[o + a.koff] = Kd_[kt][dt][r] * a.scale;
+        a.g_m[o + a.voff] = Vm_[kt][dt][r];
+        a.g_d[o + a.voff] = Vd_[kt][dt][r];
+      }
+}
+
 }  // namespace
 
 bool flash_supported(int dh, int S) { return (dh == 64 || dh == 128) && S % 128 == 0; }
@@ -831,8 +1048,10 @@ hipError_t launch_flash_bwd(const FlashArgs& a0, int B, hipStream_t s) {
   dim3 gq(a.S / 128, B * a.Hq);
   if (a.D == 128) hipLaunchKernelGGL(flash_bwd_q_kernel<128>, gq, dim3(256), 0, s, a);
   else hipLaunchKernelGGL(flash_bwd_q_kernel<64>, gq, dim3(256), 0, s, a);
+  // dK/dV: 64 keys per workgroup; for D = 128 the probabilities are shared
+  // through LDS between the four wavefronts
   dim3 gk(a.S / 64, B * a.Hk);
-  if (a.D == 128) hipLaunchKernelGGL(flash_bwd_kv_kernel<128>, gk, dim3(256), 0, s, a);
+  if (a.D == 128) hipLaunchKernelGGL(flash_bwd_kvp_kernel<128>, gk, dim3(256), 0, s, a);
   else hipLaunchKernelGGL(flash_bwd_kv_kernel<64>, gk, dim3(256), 0, s, a);
   return hipGetLastError();
 }
