@@ -127,6 +127,12 @@ __device__ inline bf16x8_t ld_t16(const bf16_t* t, int kk, int n0, int lane) {
   return cat(tr4<D, 1>(t, lo, col), tr4<D, 1>(t, lo + 16, col));
 }
 
+__device__ inline v4i16 pack4(const float* x) {
+  v4i16 v;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) v[j] = __builtin_bit_cast(short, (__bf16)x[j]);
+  return v;
+}
 __device__ inline bf16x8_t pack8(const float* x) {
   bf16x8_t v;
 #pragma unroll
@@ -802,42 +808,39 @@ __global__ __launch_bounds__(256) void flash_bwd_kv_kernel(FlashArgs a) {
 }
 
 // dK/dV with the probabilities shared through LDS (D = 128): 64 keys of one
-// key/value head per workgroup of four wavefronts.  The score phase is
-// flash_bwd_kv_kernel's: wavefront w forms S, dP, P and dS for its 16 keys and
-// the 32 queries of the block.  It then writes its P.m, P.d, dS.m, dS.d
-// fragments (16 bytes per lane, in the query order of the transposing reads)
-// to an LDS buffer of the workgroup, and after a barrier wavefront w
-// accumulates dV and dK for all 64 keys and 32 of the 128 columns (quarter
-// w): each wavefront's transposing reads of the Q and dO tiles cover a
-// quarter of them, and the P/dS operands come back as plain 16-byte reads.
-// Per block the workgroup reads 32 KB transposed instead of 128 KB.
-// P buffer: [4 operands][64 keys][4 slots of 16 bytes], slot g of key row r
-// at g ^ ((r >> 2) & 3) (16-byte accesses of 16 consecutive rows and one slot,
-// or of 8 rows and slots g and g + 2, hit 64 distinct banks).  The counters
-// still show bank conflicts in this kernel (24% of its LDS-active cycles, 34%
-// with no swizzle and 17% with 80-byte rows); the kernel time moves by 4%
-// between those layouts, so LDS conflicts do not bound it.
+// key/value head per workgroup of eight wavefronts, two per SIMD (about 220
+// registers each), where the one-workgroup-of-four form runs one wavefront
+// per SIMD and hides nothing.  Score phase: wavefront w forms S, dP, P and dS
+// for 16 keys (group w / 2) and 16 of the 32 queries of the block (half
+// w % 2), as flash_bwd_kv_kernel does for both halves; it writes its P.m, P.d,
+// dS.m, dS.d fragments (8 bytes per lane, in the query order of the
+// transposing reads) to an LDS buffer of the workgroup.  After a barrier
+// wavefront w accumulates dV and dK for all 64 keys on 16 of the 128 columns
+// (16 w .. 16 w + 15): its transposing reads of the Q and dO tiles cover an
+// eighth of them, and the P/dS operands come back as 16-byte reads.
+// P buffer: [4 operands][64 keys][4 slots of 16 bytes]; slot g of key row r
+// (queries 4g..4g+3 then 16+4g..+3) sits at g ^ ((r >> 2) & 3).
 constexpr int PROW = 32;   // elements per key row of the P buffer
 __device__ inline int pslot(int row, int g) { return row * PROW + ((g ^ ((row >> 2) & 3)) << 3); }   // elements
 
 template <int D>
-__global__ __launch_bounds__(256) void flash_bwd_kvp_kernel(FlashArgs a) {
-  static_assert(D == 128, "shared-probability dK/dV is for head dimension 128");
+__global__ __launch_bounds__(512, 1) void flash_bwd_kv8_kernel(FlashArgs a) {
+  static_assert(D == 128, "eight-wavefront dK/dV is for head dimension 128");
   constexpr int QB = 32, KS = D / 32, TILE = QB * D, KEYS = 64;
-  __shared__ __attribute__((aligned(1024))) bf16_t ring[2][4 * TILE];   // Q.m Q.d dO.m dO.d
+  __shared__ __attribute__((aligned(1024))) bf16_t ring[2][4 * TILE];     // Q.m Q.d dO.m dO.d
   __shared__ __attribute__((aligned(1024))) bf16_t pbuf[4][KEYS * PROW];  // P.m P.d dS.m dS.d
-  __shared__ float4 sst[2][QB];                                         // m, u, w, D.m
-  __shared__ __attribute__((aligned(16))) float sdd[2][QB];             // D.d
+  __shared__ float4 sst[2][QB];                                           // m, u, w, D.m
+  __shared__ __attribute__((aligned(16))) float sdd[2][QB];               // D.d
 
   int kblk, bkh;
   work_item(gridDim.y, kblk, bkh);   // lowest keys (most queries) first
   const int b = bkh / a.Hk, kh = bkh % a.Hk;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int k0 = kblk * KEYS, kw = k0 + 16 * wave;
+  const int kg = wave >> 1, qt = wave & 1;   // score phase: key group and query half
+  const int k0 = kblk * KEYS, kw = k0 + 16 * kg;
   const int64_t row0 = (int64_t)b * a.S;
   const int kj = kw + (lane & 15);
-  const int quarter = wave;   // the dV/dK columns of this wavefront
 
   // K and V fragments of this wavefront's 16 keys (B operands of S = Q K^T, dP = dO V^T)
   bf16x8_t km[KS], kd[KS], vm[KS], vd[KS];
@@ -851,14 +854,12 @@ __global__ __launch_bounds__(256) void flash_bwd_kvp_kernel(FlashArgs a) {
       vd[s] = *reinterpret_cast<const bf16x8_t*>(a.qkv_d + r + a.voff + 32 * s);
     }
   }
-  // accumulators (kt, dt): keys k0 + 16 kt + 4 (lane / 16) + r, columns 32 quarter + 16 dt + lane % 16
-  f32x4_t Vm_[4][2], Vd_[4][2], Km_[4][2], Kd_[4][2];
+  // accumulators kt: keys k0 + 16 kt + 4 (lane / 16) + r, columns 16 wave + lane % 16
+  f32x4_t Vm_[4], Vd_[4], Km_[4], Kd_[4];
 #pragma unroll
   for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-    for (int dt = 0; dt < 2; ++dt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) Vm_[kt][dt][r] = Vd_[kt][dt][r] = Km_[kt][dt][r] = Kd_[kt][dt][r] = 0.f;
+    for (int r = 0; r < 4; ++r) Vm_[kt][r] = Vd_[kt][r] = Km_[kt][r] = Kd_[kt][r] = 0.f;
 
   const int nqb = (a.S - k0) / QB;   // query blocks from the first key on, per head
   const int total = nqb * a.G;
@@ -868,8 +869,8 @@ __global__ __launch_bounds__(256) void flash_bwd_kvp_kernel(FlashArgs a) {
     const int64_t r = row0 + q0;
     const bf16_t* sq[2] = {a.qkv_m + r * a.ld + (int64_t)h * D, a.qkv_d + r * a.ld + (int64_t)h * D};
     const bf16_t* so[2] = {a.do_m + r * a.ldo + (int64_t)h * D, a.do_d + r * a.ldo + (int64_t)h * D};
-    dma_tiles<D, QB, 2, 1>(ring[it & 1], sq, a.ld, wave, lane);
-    dma_tiles<D, QB, 2, 1>(ring[it & 1] + 2 * TILE, so, a.ldo, wave, lane);
+    dma_tiles<D, QB, 2, 1, 8>(ring[it & 1], sq, a.ld, wave, lane);
+    dma_tiles<D, QB, 2, 1, 8>(ring[it & 1] + 2 * TILE, so, a.ldo, wave, lane);
   };
   float4 nst = make_float4(0.f, 0.f, 0.f, 0.f);
   float ndd = 0.f;
@@ -904,82 +905,65 @@ __global__ __launch_bounds__(256) void flash_bwd_kvp_kernel(FlashArgs a) {
     const bf16_t* Qd = Qm + TILE;
     const bf16_t* Om = Qm + 2 * TILE;
     const bf16_t* Od = Qm + 3 * TILE;
-    {   // score phase: this wavefront's 16 keys
-      f32x4_t sm[2], sd[2], pm[2], pd[2];
+    {   // score phase: keys kw .. kw + 15, queries q0 + 16 qt .. + 15
+      f32x4_t sm, sd, pm, pd;
 #pragma unroll
-      for (int qt = 0; qt < 2; ++qt) {
+      for (int r = 0; r < 4; ++r) sm[r] = sd[r] = pm[r] = pd[r] = 0.f;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) sm[qt][r] = sd[qt][r] = pm[qt][r] = pd[qt][r] = 0.f;
-#pragma unroll
-        for (int s = 0; s < KS; ++s) {
-          const bf16x8_t qa = ld_k16<D>(Qm, 16 * qt, s, lane), qb_ = ld_k16<D>(Qd, 16 * qt, s, lane);
-          sm[qt] = mma16(qa, km[s], sm[qt]);
-          sd[qt] = mma16(qa, kd[s], sd[qt]);
-          sd[qt] = mma16(qb_, km[s], sd[qt]);
-          const bf16x8_t oa = ld_k16<D>(Om, 16 * qt, s, lane), ob = ld_k16<D>(Od, 16 * qt, s, lane);
-          pm[qt] = mma16(oa, vm[s], pm[qt]);
-          pd[qt] = mma16(oa, vd[s], pd[qt]);
-          pd[qt] = mma16(ob, vm[s], pd[qt]);
-        }
+      for (int s = 0; s < KS; ++s) {
+        const bf16x8_t qa = ld_k16<D>(Qm, 16 * qt, s, lane), qb_ = ld_k16<D>(Qd, 16 * qt, s, lane);
+        sm = mma16(qa, km[s], sm);
+        sd = mma16(qa, kd[s], sd);
+        sd = mma16(qb_, km[s], sd);
+        const bf16x8_t oa = ld_k16<D>(Om, 16 * qt, s, lane), ob = ld_k16<D>(Od, 16 * qt, s, lane);
+        pm = mma16(oa, vm[s], pm);
+        pd = mma16(oa, vd[s], pd);
+        pd = mma16(ob, vm[s], pd);
       }
-      const bool diag = q0 < kw + 16;
       float bmax = 0.f;
 #pragma unroll
-      for (int qt = 0; qt < 2; ++qt)
+      for (int r = 0; r < 4; ++r) {
+        sm[r] *= a.scale;
+        sd[r] *= a.scale;
+        bmax = fmaxf(bmax, fabsf(sd[r]));
+      }
+      if (q0 + 16 * qt < kw + 16) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (q0 + 16 * qt + 4 * (lane >> 4) + r < kj) sm[r] = NEG;
+      }
+      float Pm[4], Pd[4], gsm[4], gsd[4];
+      auto terms = [&](auto ser) {
+        const float4 ddv = *reinterpret_cast<const float4*>(&sdd[it & 1][16 * qt + 4 * (lane >> 4)]);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          sm[qt][r] *= a.scale;
-          sd[qt][r] *= a.scale;
-          bmax = fmaxf(bmax, fabsf(sd[qt][r]));
-        }
-      if (diag) {
-#pragma unroll
-        for (int qt = 0; qt < 2; ++qt)
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (q0 + 16 * qt + 4 * (lane >> 4) + r < kj) sm[qt][r] = NEG;
-      }
-      float Pm[8], Pd[8], gsm[8], gsd[8];   // rows in accumulator order: (qt, r) -> 4 qt + r
-      auto terms = [&](auto ser) {
-#pragma unroll
-        for (int qt = 0; qt < 2; ++qt) {
-          const float4 ddv = *reinterpret_cast<const float4*>(&sdd[it & 1][16 * qt + 4 * (lane >> 4)]);
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float4 st = sst[it & 1][16 * qt + 4 * (lane >> 4) + r];
-            const float dd = r == 0 ? ddv.x : (r == 1 ? ddv.y : (r == 2 ? ddv.z : ddv.w));
-            const float e = __expf(sm[qt][r] - st.x);
-            float c, sn;
-            coshsinh<decltype(ser)::value>(sd[qt][r], c, sn);
-            const float P_m = e * (c * st.y - sn * st.z), P_d = e * (sn * st.y - c * st.z);
-            const float xm = pm[qt][r] - st.w, xd = pd[qt][r] - dd;
-            Pm[4 * qt + r] = P_m;
-            Pd[4 * qt + r] = P_d;
-            gsm[4 * qt + r] = P_m * xm + P_d * xd;
-            gsd[4 * qt + r] = P_m * xd + P_d * xm;
-          }
+          const float4 st = sst[it & 1][16 * qt + 4 * (lane >> 4) + r];
+          const float dd = r == 0 ? ddv.x : (r == 1 ? ddv.y : (r == 2 ? ddv.z : ddv.w));
+          const float e = __expf(sm[r] - st.x);
+          float c, sn;
+          coshsinh<decltype(ser)::value>(sd[r], c, sn);
+          const float P_m = e * (c * st.y - sn * st.z), P_d = e * (sn * st.y - c * st.z);
+          const float xm = pm[r] - st.w, xd = pd[r] - dd;
+          Pm[r] = P_m;
+          Pd[r] = P_d;
+          gsm[r] = P_m * xm + P_d * xd;
+          gsd[r] = P_m * xd + P_d * xm;
         }
       };
       if (!__any(bmax >= SERIES_MAX)) terms(std::true_type{});
       else terms(std::false_type{});
-      // lane (g, i) holds queries 4g..4g+3 and 16+4g..+3 of key 16 wave + i: slot g of that key row
-      const int prow = 16 * wave + (lane & 15), g = lane >> 4;
-      *reinterpret_cast<bf16x8_t*>(&pbuf[0][pslot(prow, g)]) = pack8(Pm);
-      *reinterpret_cast<bf16x8_t*>(&pbuf[1][pslot(prow, g)]) = pack8(Pd);
-      *reinterpret_cast<bf16x8_t*>(&pbuf[2][pslot(prow, g)]) = pack8(gsm);
-      *reinterpret_cast<bf16x8_t*>(&pbuf[3][pslot(prow, g)]) = pack8(gsd);
+      // lane (g, i) holds queries 16 qt + 4g .. + 3 of key 16 kg + i: half qt of slot g of that key row
+      const int prow = 16 * kg + (lane & 15), g = lane >> 4, o = pslot(prow, g) + 4 * qt;
+      *reinterpret_cast<v4i16*>(&pbuf[0][o]) = pack4(Pm);
+      *reinterpret_cast<v4i16*>(&pbuf[1][o]) = pack4(Pd);
+      *reinterpret_cast<v4i16*>(&pbuf[2][o]) = pack4(gsm);
+      *reinterpret_cast<v4i16*>(&pbuf[3][o]) = pack4(gsd);
     }
     __syncthreads();   // every wavefront's P and dS are in the buffer
-    {   // dV, dK phase: all 64 keys, columns 32 quarter .. + 31
-      bf16x8_t om[2], od[2], qa[2], qb_[2];
-#pragma unroll
-      for (int dt = 0; dt < 2; ++dt) {
-        const int n0 = 32 * quarter + 16 * dt;
-        om[dt] = ld_t16<D>(Om, 0, n0, lane);
-        od[dt] = ld_t16<D>(Od, 0, n0, lane);
-        qa[dt] = ld_t16<D>(Qm, 0, n0, lane);
-        qb_[dt] = ld_t16<D>(Qd, 0, n0, lane);
-      }
+    {   // dV, dK phase: all 64 keys, columns 16 wave .. + 15
+      const int n0 = 16 * wave;
+      const bf16x8_t om = ld_t16<D>(Om, 0, n0, lane), od = ld_t16<D>(Od, 0, n0, lane);
+      const bf16x8_t qa = ld_t16<D>(Qm, 0, n0, lane), qb_ = ld_t16<D>(Qd, 0, n0, lane);
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt) {
         const int prow = 16 * kt + (lane & 15), g = lane >> 4;
@@ -987,15 +971,12 @@ __global__ __launch_bounds__(256) void flash_bwd_kvp_kernel(FlashArgs a) {
         const bf16x8_t apd = *reinterpret_cast<const bf16x8_t*>(&pbuf[1][pslot(prow, g)]);
         const bf16x8_t asm_ = *reinterpret_cast<const bf16x8_t*>(&pbuf[2][pslot(prow, g)]);
         const bf16x8_t asd = *reinterpret_cast<const bf16x8_t*>(&pbuf[3][pslot(prow, g)]);
-#pragma unroll
-        for (int dt = 0; dt < 2; ++dt) {
-          Vm_[kt][dt] = mma16(apm, om[dt], Vm_[kt][dt]);
-          Vd_[kt][dt] = mma16(apm, od[dt], Vd_[kt][dt]);
-          Vd_[kt][dt] = mma16(apd, om[dt], Vd_[kt][dt]);
-          Km_[kt][dt] = mma16(asm_, qa[dt], Km_[kt][dt]);
-          Kd_[kt][dt] = mma16(asm_, qb_[dt], Kd_[kt][dt]);
-          Kd_[kt][dt] = mma16(asd, qa[dt], Kd_[kt][dt]);
-        }
+        Vm_[kt] = mma16(apm, om, Vm_[kt]);
+        Vd_[kt] = mma16(apm, od, Vd_[kt]);
+        Vd_[kt] = mma16(apd, om, Vd_[kt]);
+        Km_[kt] = mma16(asm_, qa, Km_[kt]);
+        Kd_[kt] = mma16(asm_, qb_, Kd_[kt]);
+        Kd_[kt] = mma16(asd, qa, Kd_[kt]);
       }
     }
     __builtin_amdgcn_s_waitcnt(0);
@@ -1006,16 +987,14 @@ __global__ __launch_bounds__(256) void flash_bwd_kvp_kernel(FlashArgs a) {
 #pragma unroll
   for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-    for (int dt = 0; dt < 2; ++dt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int key = k0 + 16 * kt + 4 * (lane >> 4) + r;
-        const int64_t o = (row0 + key) * a.ldg + kh * D + 32 * quarter + 16 * dt + (lane & 15);
-        a.g_m[o + a.koff] = Km_[kt][dt][r] * a.scale;
-        a.g_d[o + a.koff] = Kd_[kt][dt][r] * a.scale;
-        a.g_m[o + a.voff] = Vm_[kt][dt][r];
-        a.g_d[o + a.voff] = Vd_[kt][dt][r];
-      }
+    for (int r = 0; r < 4; ++r) {
+      const int key = k0 + 16 * kt + 4 * (lane >> 4) + r;
+      const int64_t o = (row0 + key) * a.ldg + kh * D + 16 * wave + (lane & 15);
+      a.g_m[o + a.koff] = Km_[kt][r] * a.scale;
+      a.g_d[o + a.koff] = Kd_[kt][r] * a.scale;
+      a.g_m[o + a.voff] = Vm_[kt][r];
+      a.g_d[o + a.voff] = Vd_[kt][r];
+    }
 }
 
 }  // namespace
@@ -1048,10 +1027,10 @@ hipError_t launch_flash_bwd(const FlashArgs& a0, int B, hipStream_t s) {
   dim3 gq(a.S / 128, B * a.Hq);
   if (a.D == 128) hipLaunchKernelGGL(flash_bwd_q_kernel<128>, gq, dim3(256), 0, s, a);
   else hipLaunchKernelGGL(flash_bwd_q_kernel<64>, gq, dim3(256), 0, s, a);
-  // dK/dV: 64 keys per workgroup; for D = 128 the probabilities are shared
-  // through LDS between the four wavefronts
+  // dK/dV: 64 keys per workgroup; for D = 128 eight wavefronts share the
+  // probabilities through LDS
   dim3 gk(a.S / 64, B * a.Hk);
-  if (a.D == 128) hipLaunchKernelGGL(flash_bwd_kvp_kernel<128>, gk, dim3(256), 0, s, a);
+  if (a.D == 128) hipLaunchKernelGGL(flash_bwd_kv8_kernel<128>, gk, dim3(512), 0, s, a);
   else hipLaunchKernelGGL(flash_bwd_kv_kernel<64>, gk, dim3(256), 0, s, a);
   return hipGetLastError();
 }
