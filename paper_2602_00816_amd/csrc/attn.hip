@@ -476,6 +476,180 @@ __global__ __launch_bounds__(256) void flash_fwd_kernel(FlashArgs a) {
   if (lane < 32) a.stats[(int64_t)bh * a.S + qi] = make_float4(mrun, u, w, 0.f);
 }
 
+// Forward with 16 queries per wavefront (D = 128): NW wavefronts, 16 NW
+// queries of one head per workgroup, K and V blocks of 32 keys through a
+// two-stage DMA ring.  Each wavefront forms S^T for the 32 keys and its 16
+// queries (two 16-key halves); lane 16 g + i then holds keys 4g .. 4g + 3 and
+// 16 + 4g .. + 3 of query i, which is the B operand of O^T = V^T P^T in the
+// key order of the transposing V reads.  The output accumulators are O^T, so
+// every lane holds its own query's columns (16 t + 4 g + r) and the lazy
+// rescale by the running maximum stays lane-local; the maximum and the row
+// sums are combined over the four lanes of a query with two shuffles.  Key
+// blocks wholly above a wavefront's queries are skipped.  At under 256
+// registers and 64 KB of LDS two workgroups share a CU.
+template <int D, int NW>
+__global__ __launch_bounds__(64 * NW, 2) void flash_fwd16_kernel(FlashArgs a) {
+  static_assert(D == 128, "16-query forward is for head dimension 128");
+  constexpr int KB = 32, KS = D / 32, TILE = KB * D, QS = 16 * NW, NT = D / 16;
+  __shared__ __attribute__((aligned(1024))) bf16_t ring[2][4 * TILE];   // K.m K.d V.m V.d
+
+  int qb, bh;
+  work_item(gridDim.y, qb, bh);
+  qb = gridDim.x - 1 - qb;   // longest rows first
+  const int b = bh / a.Hq, h = bh % a.Hq, kh = h / a.G;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int q0 = qb * QS, qw = q0 + 16 * wave;
+  const int64_t row0 = (int64_t)b * a.S;
+  const int qi = qw + (lane & 15);
+
+  bf16x8_t qm[KS], qd[KS];   // B operands of S^T = K Q^T
+  {
+    const int64_t off = (row0 + qi) * a.ld + (int64_t)h * D + 8 * (lane >> 4);
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      qm[s] = *reinterpret_cast<const bf16x8_t*>(a.qkv_m + off + 32 * s);
+      qd[s] = *reinterpret_cast<const bf16x8_t*>(a.qkv_d + off + 32 * s);
+    }
+  }
+  // Ac = sum e^a cosh b V.m;  X = sum e^a (sinh b V.m + cosh b V.d), as O^T
+  f32x4_t Ac[NT], X[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) Ac[t][r] = X[t][r] = 0.f;
+  float zc = 0.f, zs = 0.f;
+  constexpr float LOG2E = 1.4426950408889634f;
+  float mrun = NEG;   // reference maximum of the scaled logits, moved lazily (see flash_fwd_kernel)
+
+  const int nkb = (q0 + QS) / KB;
+  const int lastw = (qw + 15) / KB;   // this wavefront's last key block
+  auto issue = [&](int kb) {
+    const int64_t r = row0 + (int64_t)kb * KB;
+    const bf16_t* src[4] = {a.qkv_m + r * a.ld + a.koff + kh * D, a.qkv_d + r * a.ld + a.koff + kh * D,
+                            a.qkv_m + r * a.ld + a.voff + kh * D, a.qkv_d + r * a.ld + a.voff + kh * D};
+    dma_tiles<D, KB, 4, 1, NW>(ring[kb & 1], src, a.ld, wave, lane);
+  };
+  issue(0);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  for (int kb = 0; kb < nkb; ++kb) {
+    if (kb + 1 < nkb) issue(kb + 1);
+    if (kb <= lastw) {
+      const bf16_t* Km = ring[kb & 1];
+      const bf16_t* Kd = Km + TILE;
+      const bf16_t* Vm = Km + 2 * TILE;
+      const bf16_t* Vd = Km + 3 * TILE;
+      f32x4_t sm[2], sd[2];   // raw scores: sm = K.m q.m, sd = K.m q.d + K.d q.m
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sm[hf][r] = sd[hf][r] = 0.f;
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+          const bf16x8_t km = ld_k16<D>(Km, 16 * hf, s, lane), kd = ld_k16<D>(Kd, 16 * hf, s, lane);
+          sm[hf] = mma16(km, qm[s], sm[hf]);
+          sd[hf] = mma16(km, qd[s], sd[hf]);
+          sd[hf] = mma16(kd, qm[s], sd[hf]);
+        }
+        if (kb * KB + 16 * hf + 15 > qw) {
+          const int key0 = kb * KB + 16 * hf + 4 * (lane >> 4);
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (key0 + r > qi) sm[hf][r] = NEG;
+        }
+      }
+      float amax = NEG, bmax = 0.f;
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          amax = fmaxf(amax, sm[hf][r]);
+          bmax = fmaxf(bmax, fabsf(sd[hf][r]));
+        }
+      amax *= a.scale;
+      amax = fmaxf(amax, __shfl_xor(amax, 16, 64));
+      amax = fmaxf(amax, __shfl_xor(amax, 32, 64));
+      if (__any(amax > mrun + 8.f)) {
+        const float mnew = fmaxf(mrun, amax);
+        const float alpha = __expf(mrun - mnew);
+        mrun = mnew;
+        zc *= alpha;
+        zs *= alpha;
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            Ac[t][r] *= alpha;
+            X[t][r] *= alpha;
+          }
+      }
+      const float moff = -mrun * LOG2E;
+      float pc[2][4], ps[2][4];
+      if (!__any(bmax * a.scale >= SERIES_MAX)) {
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float e = __builtin_amdgcn_exp2f(fmaf(sm[hf][r], a.c_exp, moff));
+            const float q2 = sd[hf][r] * sd[hf][r];
+            pc[hf][r] = e * fmaf(q2, a.c_cosh, 1.f);                  // e^a cosh b
+            ps[hf][r] = e * (sd[hf][r] * fmaf(q2, a.c_sinh, a.scale));  // e^a sinh b
+          }
+      } else {
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float e = __builtin_amdgcn_exp2f(fmaf(sm[hf][r], a.c_exp, moff));
+            float c, sn;
+            coshsinh<false>(sd[hf][r] * a.scale, c, sn);
+            pc[hf][r] = e * c;
+            ps[hf][r] = e * sn;
+          }
+      }
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          zc += pc[hf][r];
+          zs += ps[hf][r];
+        }
+      const bf16x8_t bc = cat(pack4(pc[0]), pack4(pc[1])), bs = cat(pack4(ps[0]), pack4(ps[1]));
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const bf16x8_t vmt = ld_t16<D>(Vm, 0, 16 * t, lane), vdt = ld_t16<D>(Vd, 0, 16 * t, lane);
+        Ac[t] = mma16(vmt, bc, Ac[t]);
+        X[t] = mma16(vmt, bs, X[t]);
+        X[t] = mma16(vdt, bc, X[t]);
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();   // the ring stage is free again
+  }
+
+  zc += __shfl_xor(zc, 16, 64);
+  zs += __shfl_xor(zs, 16, 64);
+  zc += __shfl_xor(zc, 32, 64);
+  zs += __shfl_xor(zs, 32, 64);
+  const float den = (zc - zs) * (zc + zs);
+  const float u = zc / den, w = zs / den;
+  const int64_t orow = (row0 + qi) * a.ldo + (int64_t)h * D + 4 * (lane >> 4);
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    uint16_t om[4], od[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      om[r] = f32_to_bf16(u * Ac[t][r]);
+      od[r] = f32_to_bf16(u * X[t][r] - w * Ac[t][r]);
+    }
+    const int64_t o = orow + 16 * t;
+    *reinterpret_cast<uint2*>(a.o_m + o) = make_uint2(om[0] | ((uint32_t)om[1] << 16), om[2] | ((uint32_t)om[3] << 16));
+    *reinterpret_cast<uint2*>(a.o_d + o) = make_uint2(od[0] | ((uint32_t)od[1] << 16), od[2] | ((uint32_t)od[3] << 16));
+  }
+  if (lane < 16) a.stats[(int64_t)bh * a.S + qi] = make_float4(mrun, u, w, 0.f);
+}
+
 // ---------------------------------------------------------------------------
 // backward: row terms D.m, D.d
 // ---------------------------------------------------------------------------
@@ -1154,9 +1328,13 @@ static FlashArgs with_constants(const FlashArgs& a0) {
 
 hipError_t launch_flash_fwd(const FlashArgs& a0, int B, hipStream_t s) {
   const FlashArgs a = with_constants(a0);
-  dim3 g(a.S / 128, B * a.Hq);
-  if (a.D == 128) hipLaunchKernelGGL(flash_fwd_kernel<128>, g, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(flash_fwd_kernel<64>, g, dim3(256), 0, s, a);
+  if (a.D == 128) {
+    dim3 g(a.S / 64, B * a.Hq);
+    hipLaunchKernelGGL((flash_fwd16_kernel<128, 4>), g, dim3(256), 0, s, a);
+  } else {
+    dim3 g(a.S / 128, B * a.Hq);
+    hipLaunchKernelGGL(flash_fwd_kernel<64>, g, dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 
