@@ -1133,7 +1133,15 @@ __global__ __launch_bounds__(256) void flash_bwd_kv_kernel(FlashArgs a) {
 // wavefront w accumulates dV and dK for all 64 keys on 16 of the 128 columns
 // (16 w .. 16 w + 15): its transposing reads of the Q and dO tiles cover an
 // eighth of them, and the P/dS operands come back as 16-byte reads.
-// P buffer: one [64 keys][128] bf16 tile with the SW = 2 swizzle, operand o
+// One barrier per query block: the Q/dO tiles go through a three-stage ring
+// (the block after the next is loaded only once every wavefront has passed
+// the barrier that follows its last reads of that stage) and the P buffer is
+// doubled, so a wavefront may start the score phase of the next block while
+// others still accumulate this one; each wavefront waits for its own loads of
+// the next block before the barrier, which then publishes them.  With a
+// second barrier at the end of every block (two stages, one buffer) the
+// kernel took 5% longer.
+// P buffer (each of the two): one [64 keys][128] bf16 tile with the SW = 2 swizzle, operand o
 // (P.m, P.d, dS.m, dS.d) in chunks 4o .. 4o + 3, chunk 4o + g of key row r
 // holding queries 4g .. 4g + 3 and 16 + 4g .. + 3, in that order when g has
 // even parity and swapped when odd (the B operands are read with the same
@@ -1146,8 +1154,8 @@ template <int D>
 __global__ __launch_bounds__(512, 1) void flash_bwd_kv8_kernel(FlashArgs a) {
   static_assert(D == 128, "eight-wavefront dK/dV is for head dimension 128");
   constexpr int QB = 32, KS = D / 32, TILE = QB * D, KEYS = 64;
-  __shared__ __attribute__((aligned(1024))) bf16_t ring[2][4 * TILE];     // Q.m Q.d dO.m dO.d
-  __shared__ __attribute__((aligned(1024))) bf16_t pbuf[KEYS * D];        // P.m P.d dS.m dS.d
+  __shared__ __attribute__((aligned(1024))) bf16_t ring[3][4 * TILE];     // Q.m Q.d dO.m dO.d
+  __shared__ __attribute__((aligned(1024))) bf16_t pbufs[2][KEYS * D];    // P.m P.d dS.m dS.d
   __shared__ float4 sst[2][QB];                                           // m, u, w, D.m
   __shared__ __attribute__((aligned(16))) float sdd[2][QB];               // D.d
 
@@ -1188,8 +1196,8 @@ __global__ __launch_bounds__(512, 1) void flash_bwd_kv8_kernel(FlashArgs a) {
     const int64_t r = row0 + q0;
     const bf16_t* sq[2] = {a.qkv_m + r * a.ld + (int64_t)h * D, a.qkv_d + r * a.ld + (int64_t)h * D};
     const bf16_t* so[2] = {a.do_m + r * a.ldo + (int64_t)h * D, a.do_d + r * a.ldo + (int64_t)h * D};
-    dma_tiles<D, QB, 2, 1, 8>(ring[it & 1], sq, a.ld, wave, lane);
-    dma_tiles<D, QB, 2, 1, 8>(ring[it & 1] + 2 * TILE, so, a.ldo, wave, lane);
+    dma_tiles<D, QB, 2, 1, 8>(ring[it % 3], sq, a.ld, wave, lane);
+    dma_tiles<D, QB, 2, 1, 8>(ring[it % 3] + 2 * TILE, so, a.ldo, wave, lane);
   };
   float4 nst = make_float4(0.f, 0.f, 0.f, 0.f);
   float ndd = 0.f;
@@ -1220,7 +1228,8 @@ __global__ __launch_bounds__(512, 1) void flash_bwd_kv8_kernel(FlashArgs a) {
       issue(it + 1);
     }
     const int q0 = k0 + (it % nqb) * QB;
-    const bf16_t* Qm = ring[it & 1];
+    const bf16_t* Qm = ring[it % 3];
+    bf16_t* pbuf = pbufs[it & 1];
     const bf16_t* Qd = Qm + TILE;
     const bf16_t* Om = Qm + 2 * TILE;
     const bf16_t* Od = Qm + 3 * TILE;
@@ -1278,7 +1287,9 @@ __global__ __launch_bounds__(512, 1) void flash_bwd_kv8_kernel(FlashArgs a) {
       *reinterpret_cast<v4i16*>(&pbuf[tswz<D, 2>(prow, 8 + g) + hf]) = pack4(gsm);
       *reinterpret_cast<v4i16*>(&pbuf[tswz<D, 2>(prow, 12 + g) + hf]) = pack4(gsd);
     }
-    __syncthreads();   // every wavefront's P and dS are in the buffer
+    __builtin_amdgcn_s_waitcnt(0);   // own loads of the next block
+    if (it + 1 < total) store_rows(it + 1);
+    __syncthreads();   // every wavefront's P and dS are in the buffer, the next block is in the ring
     {   // dV, dK phase: all 64 keys, columns 16 wave .. + 15
       const int n0 = 16 * wave;
       const bf16x8_t om = ld_t16<D, true>(Om, 0, n0, lane), od = ld_t16<D, true>(Od, 0, n0, lane);
@@ -1295,9 +1306,6 @@ __global__ __launch_bounds__(512, 1) void flash_bwd_kv8_kernel(FlashArgs a) {
         Kd_[kt] = mma16(asd, qa, Kd_[kt]);
       }
     }
-    __builtin_amdgcn_s_waitcnt(0);
-    if (it + 1 < total) store_rows(it + 1);
-    __syncthreads();   // the ring stage and the P buffer are free again
   }
 
 #pragma unroll
