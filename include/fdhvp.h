@@ -142,6 +142,19 @@ fdh_status fdh_workspace_bytes(const fdh_ctx* ctx, int32_t B, int32_t S, int32_t
 fdh_status fdh_set_workspace(fdh_ctx* ctx, void* dev, size_t bytes, int32_t B, int32_t S,
                              int32_t m, const fdh_lanczos_opts* o);
 
+/* Activation recomputation (gradient checkpointing, an option of the
+ * fine-tuning runs of section 6): with on != 0 the workspace keeps, per
+ * decoder layer, only the fp32 input pair of the layer (mean and
+ * half-difference channels) plus one set of the layer's other activations
+ * that all layers share.  Before each layer's backward the HVP runs that
+ * layer's forward again from its stored input, up to the MLP activation, so
+ * one HVP executes every decoder layer but the last one's forward twice (about
+ * a quarter more GEMM work) and needs L - 1 fewer activation sets.  Results are the
+ * same bits as without.  Takes effect for the following fdh_workspace_bytes /
+ * fdh_set_workspace; the carve in use keeps its mode until then.  Off by
+ * default; no effect for QUAD_DIAG. */
+fdh_status fdh_set_recompute(fdh_ctx* ctx, int32_t on);
+
 /* Synthetic inputs (the SplitMix64 counter generator of Steele, Lea and Flood,
  * OOPSLA 2014, in counter form): theta with N(0, 0.02) matrices, unit gains, zero biases (bf16 by
  * round-to-nearest-even); tokens uniform or Zipf(1.1); unit vectors. */

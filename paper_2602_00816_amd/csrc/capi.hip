@@ -126,6 +126,13 @@ fdh_status fdh_set_workspace(fdh_ctx* ctx, void* dev, size_t bytes, int32_t B, i
   return run(ctx, [&](fdh::Engine& e) { return e.set_workspace(dev, bytes, B, S, m, o); });
 }
 
+fdh_status fdh_set_recompute(fdh_ctx* ctx, int32_t on) {
+  return run(ctx, [&](fdh::Engine& e) -> int {
+    e.recompute = on != 0;
+    return FDH_OK;
+  });
+}
+
 fdh_status fdh_init_params(fdh_ctx* ctx, void* params_dev, uint64_t seed) {
   return run(ctx, [&](fdh::Engine& e) { return e.init_params(params_dev, seed); });
 }

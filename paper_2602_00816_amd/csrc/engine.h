@@ -80,6 +80,10 @@ struct WsLayout {
   // attention path: fused kernels (bf16, head dim 64 or 128, S a multiple of
   // 128) or score/probability matrices in the workspace
   bool fused = false;
+  // activation recomputation: only each layer's input pair x_in is kept; the
+  // other spans of every layer alias one shared set, which the backward refills
+  // by running that layer's forward again (x_in -> z) just before its backward
+  bool rc = false;
   int planB = 0, planS = 0, planM = 0;
   fdh_lanczos_opts planO{};
   size_t total = 0;     // bytes the carve needs
@@ -105,6 +109,7 @@ class Engine : public WsLayout {
   size_t ws_bytes = 0;
   bool force_unfused = false;   // testing: plan the unfused path even where the fused one applies
   bool force_unsplit = false;   // testing: weight-gradient GEMMs over the whole token range
+  bool recompute = false;       // plan (and run) with activation recomputation
   // the carve for token batches up to [B, S] and m Lanczos steps with options
   // o (o may be null when m == 0), written into *out; changes nothing else
   size_t plan(int B, int S, int m, const fdh_lanczos_opts* o, WsLayout* out) const;

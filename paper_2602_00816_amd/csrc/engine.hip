@@ -156,9 +156,9 @@ size_t Engine::plan(int B, int S, int m, const fdh_lanczos_opts* o, WsLayout* ou
     const size_t pp = fused ? 0 : (size_t)B * Hq * S * S;   // score-shaped matrices (unfused path only)
     const size_t rows = (size_t)B * Hq * S;
     W.ls.assign(L, LayerSpans{});
-    for (int l = 0; l < L; ++l) {
-      LayerSpans& s = W.ls[l];
-      take(s.x_in_m, td * 4); take(s.x_in_d, td * 4);
+    W.rc = recompute;
+    // the activations a layer's backward reads (everything but its input pair)
+    auto take_acts = [&](LayerSpans& s) {
       take(s.a_m, td * ob); take(s.a_d, td * ob);
       take(s.qkv_m, tq * ob); take(s.qkv_d, tq * ob);
       take(s.P_m, pp * ob); take(s.P_d, pp * ob);
@@ -168,6 +168,20 @@ size_t Engine::plan(int B, int S, int m, const fdh_lanczos_opts* o, WsLayout* ou
       take(s.b_m, td * ob); take(s.b_d, td * ob);
       take(s.u_m, tu * ob); take(s.u_d, tu * ob);
       take(s.z_m, tz * ob); take(s.z_d, tz * ob);
+    };
+    for (int l = 0; l < L; ++l) {
+      LayerSpans& s = W.ls[l];
+      take(s.x_in_m, td * 4); take(s.x_in_d, td * 4);
+      if (!W.rc) take_acts(s);
+    }
+    if (W.rc && L > 0) {
+      LayerSpans shared;
+      take_acts(shared);
+      for (LayerSpans& s : W.ls) {
+        const Span xm = s.x_in_m, xd = s.x_in_d;
+        s = shared;
+        s.x_in_m = xm; s.x_in_d = xd;
+      }
     }
     take(W.xL_m, td * 4); take(W.xL_d, td * 4);
     take(W.f_m, td * ob); take(W.f_d, td * ob);
@@ -291,6 +305,7 @@ uint64_t Engine::layout_digest() const {
   mix((uint64_t)lz_ldq);
   mix((uint64_t)lz_dev_rows);
   mix(fused ? 1 : 0);
+  mix(rc ? 1 : 0);
   mix((uint64_t)planB);
   mix((uint64_t)planS);
   mix((uint64_t)planM);
@@ -561,7 +576,10 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, c
     CK(launch_embed_fwd<T>(x0, tok, T_, S, d, V, th + wte.off, v + wte.off, gpt2 ? th + wpe.off : nullptr,
                            gpt2 ? v + wpe.off : nullptr, eps, nf + 2, st));
   }
-  for (int l = 0; l < L; ++l) {
+  // one decoder layer's forward from its stored input pair x_in: norm 1, qkv,
+  // attention, output projection + residual, norm 2, MLP and, with
+  // write_next, the down projection into the next layer's input
+  auto layer_fwd = [&](int l, bool write_next) -> int {
     const LayerRefs& R = layers[l];
     LayerSpans& s = ls[l];
     const float* xm = F32(s.x_in_m);
@@ -639,10 +657,15 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, c
     RC(lin_fwd(OP(s.b_m), OP(s.b_d), d, R.w1, R.b1, OP(s.u_m), OP(s.u_d), nullptr, nullptr, nu, OUT_OP));
     if (gpt2) CK(launch_gelu_fwd<T>(PairT<T>{OP(s.z_m), OP(s.z_d)}, OP(s.u_m), OP(s.u_d), (int64_t)T_ * F, st));
     else CK(launch_swiglu_fwd<T>(PairT<T>{OP(s.z_m), OP(s.z_d)}, OP(s.u_m), OP(s.u_d), T_, F, st));
+    // the down projection (+ residual) writes the next layer's input; a
+    // recompute stops before it, the stored input is already there
+    if (!write_next) return FDH_OK;
     float* nxm = (l + 1 < L) ? F32(ls[l + 1].x_in_m) : F32(xL_m);
     float* nxd = (l + 1 < L) ? F32(ls[l + 1].x_in_d) : F32(xL_d);
     RC(lin_fwd(OP(s.z_m), OP(s.z_d), F, R.w2, R.b2, nxm, nxd, F32(s.xmid_m), F32(s.xmid_d), d, OUT_F32));
-  }
+    return FDH_OK;
+  };
+  for (int l = 0; l < L; ++l) RC(layer_fwd(l, true));
   // final norm + head + cross-entropy
   CK(launch_norm_fwd<T>(PairT<T>{OP(f_m), OP(f_d)}, F32(xL_m), F32(xL_d), T_, d, ln, th + nfg.off, v + nfg.off,
                         ln ? th + nfb.off : nullptr, ln ? v + nfb.off : nullptr, eps, neps, st));
@@ -664,6 +687,9 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, c
   for (int l = L - 1; l >= 0; --l) {
     const LayerRefs& R = layers[l];
     LayerSpans& s = ls[l];
+    // with recomputation the shared activation set still holds the last
+    // layer's forward; every earlier layer refills it from its stored input
+    if (rc && l < L - 1) RC(layer_fwd(l, false));
     // ---- MLP ----  (dx = gradient w.r.t. layer output)
     T *gom, *god;
     RC(as_op(dxm, dxd, dxo_m, dxo_d, (int64_t)T_ * d, &gom, &god));

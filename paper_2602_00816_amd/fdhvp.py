@@ -76,6 +76,7 @@ def lib():
         "fdh_param_layout": (i32, [vp, C.POINTER(Block), i32, pi]),
         "fdh_workspace_bytes": (i32, [vp, i32, i32, i32, C.POINTER(LanczosOpts), C.POINTER(C.c_size_t)]),
         "fdh_set_workspace": (i32, [vp, vp, C.c_size_t, i32, i32, i32, C.POINTER(LanczosOpts)]),
+        "fdh_set_recompute": (i32, [vp, i32]),
         "fdh_init_params": (i32, [vp, vp, u64]),
         "fdh_make_tokens": (i32, [vp, vp, i32, i32, u64, i32]),
         "fdh_random_vector": (i32, [vp, vp, u64, i32]),
@@ -232,6 +233,12 @@ class Model:
         self._check(self._L.fdh_workspace_bytes(self._h, B, S, m, C.byref(o) if o else None, C.byref(out)),
                     "fdh_workspace_bytes")
         return int(out.value)
+
+    def set_recompute(self, on: bool = True):
+        """Activation recomputation for the following workspace_bytes /
+        set_workspace: keep only each layer's input pair and rerun the layer's
+        forward before its backward (same results, less memory)."""
+        self._check(self._L.fdh_set_recompute(self._h, 1 if on else 0), "fdh_set_recompute")
 
     # ---- memory ----
     def set_workspace(self, B=0, S=0, m=0, o: LanczosOpts | None = None):

@@ -5,7 +5,7 @@
 
 Runs the SLQ estimate of section 4 with the workload's own settings (probe
 count, Lanczos length, reorthogonalisation mode and window, basis precision,
-finite-difference step) on its synthetic inputs: random-init weights and a
+finite-difference step, activation recomputation) on its synthetic inputs: random-init weights and a
 Zipf(1.1) token batch from the workload seeds.  Every probe is a Rademacher
 vector; each Lanczos step is one FD-HVP (section 3.1) through the library.
 
@@ -75,6 +75,7 @@ def main(argv=None):
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
     mod = fd.Model.from_workload(w)
+    mod.set_recompute(w.get("recompute", False))
     ws = mod.set_workspace(B, S, m, o)
     params = mod.init_params(SEED_PARAMS)
     tok = mod.make_tokens(B, S, SEED_TOKENS, w["token_dist"])
@@ -82,7 +83,7 @@ def main(argv=None):
     torch.cuda.synchronize()
     say(f"{args.workload}: P = {mod.num_params}, {B}x{S} tokens, eps {eps:g}, {probes} probes x m = {m}, "
         f"reorth {w['reorth']}{' ' + str(w['window']) if w['reorth'] == 'window' else ''}, {w['basis']} basis, "
-        f"workspace {ws / 1e9:.1f} GB")
+        f"workspace {ws / 1e9:.1f} GB{' (activation recomputation)' if w.get('recompute') else ''}")
 
     t0 = time.perf_counter()
     nodes, weights, steps, trace, st = mod.slq_density(probes, m, args.seed, o)

@@ -41,7 +41,7 @@ WORKLOADS = {
         family="llama", n_layers=32, d_model=4096, n_heads=32, n_kv_heads=8, d_ff=14336,
         vocab=128256, max_seq=2048, rope_base=500000.0, dtype="bf16",
         batch=1, seq=2048, token_dist="zipf",
-        probes=2, m=30, reorth="window", window=8, basis="bf16", eps=[1e-3]),
+        probes=2, m=30, reorth="window", window=8, basis="bf16", eps=[1e-3], recompute=True),
 }
 
 MODEL_KEYS = ("family", "n_layers", "d_model", "n_heads", "n_kv_heads", "d_ff",

@@ -159,6 +159,50 @@ def test_workspace_queries_leave_the_carve_alone(name):
     assert st == 0 and _digest(lib, h) != d0
 
 
+def _activation_set_bytes(w, B, S, fused):
+    """Bytes of one layer's activations other than its input pair, written out
+    from the model shapes: the pairs (mean, half-difference) of the norm-1
+    output, q/k/v, scores (unfused attention only), attention output, fp32
+    mid-layer residual, norm-2 output, MLP input product and MLP activation,
+    plus the fused attention's per-row statistics."""
+    T, d, F = B * S, w["d_model"], w["d_ff"]
+    H, Hk = w["n_heads"], w["n_kv_heads"]
+    dh = d // H
+    ob = 2 if w["dtype"] == "bf16" else 4
+    nu = F if w["family"] == "gpt2" else 2 * F
+    elems_op = T * d + T * (H + 2 * Hk) * dh + T * H * dh + T * d + T * nu + T * F
+    if not fused:
+        elems_op += B * H * S * S
+    return 2 * elems_op * ob + 2 * T * d * 4 + (B * H * S * 16 if fused else 0)
+
+
+@pytest.mark.parametrize("name", ["llama3-8b-bf16", "tiny-gpt2-fp32", "gpt2-medium-bf16"])
+def test_recompute_plan_keeps_one_activation_set(name):
+    """fdh_set_recompute: the plan keeps each layer's input pair and one shared
+    activation set, so the workspace shrinks by exactly L - 1 sets; the mode
+    is taken at the next fdh_set_workspace, not before."""
+    lib = fd.lib()
+    w = WORKLOADS[name]
+    m = _model(name)
+    h = m._h
+    B, S = w["batch"], w["seq"]
+    fused = w["dtype"] == "bf16" and S % 128 == 0
+    n0 = m.workspace_bytes(B, S)
+    st, _ = _fake_workspace(lib, h, B, S, 0, None)
+    assert st == 0
+    d0 = _digest(lib, h)
+    m.set_recompute(True)
+    n1 = m.workspace_bytes(B, S)
+    assert _digest(lib, h) == d0          # the carve in use keeps its mode
+    assert n0 - n1 == (w["n_layers"] - 1) * _activation_set_bytes(w, B, S, fused)
+    st, _ = _fake_workspace(lib, h, B, S, 0, None)
+    assert st == 0 and _digest(lib, h) != d0
+    m.set_recompute(False)
+    assert m.workspace_bytes(B, S) == n0
+    st, _ = _fake_workspace(lib, h, B, S, 0, None)
+    assert st == 0 and _digest(lib, h) == d0
+
+
 class _FakeTensor:
     """Stands in for a device tensor in the binding's operand checks (no memory behind it)."""
 
