@@ -869,10 +869,14 @@ __global__ __launch_bounds__(64 * 2 * WN) void gemm_bf16_dma(GemmArgs a) {
 // single wavefront per SIMD nothing else hides LDS latency, so each wavefront
 // keeps two fragment register sets and its instruction order is fixed by
 // scheduling barriers: a K slice is two half slices of 16 k; while the 16
-// MFMAs of one half run, the fragments of the next half are read and, after
-// the ring barrier, the refill of the freed stage is issued.  Refills past the
-// last slice reload the last slice into the free stage (never read), so every
-// slice issues the same number of loads and the vmcnt waits are constants.
+// MFMAs of one half run, the fragments of the next half are read.  The loads
+// of a slice are spread over two half slices, one load per two MFMAs: A's
+// into the stage freed at the ring barrier (three slices ahead), B's during
+// the next half slice (then two and a half slices ahead), which keeps the
+// load queue shorter than issuing all eight at once (measured 1.5-3% faster
+// on the 1.3B layer shapes, same bits).  Loads past the last slice reload the
+// last slice into the free stage (never read), so every slice issues the same
+// number of loads and the vmcnt waits are constants.
 // ===========================================================================
 template <bool AK, bool BKM>
 __global__ __launch_bounds__(256) void gemm_bf16_w4(GemmArgs a) {
@@ -987,25 +991,30 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4(GemmArgs a) {
   auto step = [&](auto s, int t) {
     constexpr int S = decltype(s)::value;
     const bf16_t* cur = stage(s);
-    // half slice 0 on f0 (read during the previous slice); read half 1 into f1
+    bf16_t* fill2 = stage(std::integral_constant<int, S + 2>{});
+    // half slice 0 on f0 (read during the previous slice); read half 1 into
+    // f1; issue B's loads of slice t + 2 into the stage freed at the previous
+    // barrier (A's went out during the previous half slice)
 #pragma clang loop unroll(full)
     for (int x = 0; x < IM + JN; ++x) {
       rd(f1[x], cur, x, 16);
+      if (x & 1) dma(fill2, t + 2, NU + x / 2);
       mma(f0, 2 * x);
       mma(f0, 2 * x + 1);
       __builtin_amdgcn_sched_barrier(0);
     }
-    // own loads of slice t + 1 done, then everyone's; stage S - 1 is free
+    // own loads of slice t + 1 done (the 8 issued since are slice t + 2's),
+    // then everyone's; stage S - 1 is free
     wait_vm<PERT>();
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
     __builtin_amdgcn_sched_barrier(0);
     bf16_t* nxt_fill = stage(std::integral_constant<int, S + 3>{});
     const bf16_t* nxt = stage(std::integral_constant<int, S + 1>{});
-    // half slice 1 on f1; refill stage S - 1 with slice t + 3; read half 0 of slice t + 1 into f0
+    // half slice 1 on f1; A's loads of slice t + 3 into stage S - 1; read half 0 of slice t + 1 into f0
 #pragma clang loop unroll(full)
     for (int x = 0; x < IM + JN; ++x) {
-      dma(nxt_fill, t + 3, x);
+      if (x & 1) dma(nxt_fill, t + 3, x / 2);
       rd(f0[x], nxt, x, 0);
       mma(f1, 2 * x);
       mma(f1, 2 * x + 1);
@@ -1014,13 +1023,14 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4(GemmArgs a) {
   };
 
   if (total > 0) {
+    // slices 0 and 1, and A's loads of slice 2 (B's go out in the first step)
 #pragma clang loop unroll(full)
     for (int u = 0; u < 2 * NU; ++u) dma(st0, 0, u);
 #pragma clang loop unroll(full)
     for (int u = 0; u < 2 * NU; ++u) dma(st1, 1, u);
 #pragma clang loop unroll(full)
-    for (int u = 0; u < 2 * NU; ++u) dma(st2, 2, u);
-    wait_vm<2 * PERT>();
+    for (int u = 0; u < NU; ++u) dma(st2, 2, u);
+    wait_vm<PERT + NU>();
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
 #pragma clang loop unroll(full)
