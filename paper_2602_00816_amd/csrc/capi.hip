@@ -322,7 +322,7 @@ extern "C" fdh_status fdh_testing_gemm(int32_t dtype, int32_t M, int32_t N, int3
                                        int32_t b_kmajor, const void* A, const void* B, const void* A2, const void* B2,
                                        float* C, int32_t causal, float alpha, int32_t tile, void* hip_stream) {
   if (!A || !B || !C || (!A2) != (!B2) || M < 0 || N < 0 || K < 0 || batch < 1 || causal < 0 || causal > 3 ||
-      tile < 0 || tile > 7)
+      tile < 0 || tile > 8)
     return FDH_ERR_INVALID_ARG;
   fdh::GemmArgs g;
   g.tile = tile;

@@ -863,10 +863,12 @@ __global__ __launch_bounds__(64 * 2 * WN) void gemm_bf16_dma(GemmArgs a) {
 
 // ===========================================================================
 // bf16 GEMM, 256 x 256 block tile, four wavefronts of 128 x 128 each (one per
-// SIMD), on the same DMA-fed LDS ring and LDS layouts as gemm_bf16_dma.  With
-// 128 x 128 per wavefront every fragment read from LDS feeds four MFMAs
-// instead of two or three, which halves LDS read traffic per FLOP.  With a
-// single wavefront per SIMD nothing else hides LDS latency, so each wavefront
+// SIMD; WN = 2), on the same DMA-fed LDS ring and LDS layouts as
+// gemm_bf16_dma.  With 128 x 128 per wavefront every fragment read from LDS
+// feeds four MFMAs instead of two or three, which halves LDS read traffic per
+// FLOP.  WN = 4 runs the same schedule on eight wavefronts of 128 x 64 (two
+// per SIMD, 220 registers), which trades LDS reads for a second wavefront to
+// hide latency and a shorter prologue and epilogue per tile.  A wavefront
 // keeps two fragment register sets and its instruction order is fixed by
 // scheduling barriers: a K slice is two half slices of 16 k; while the 16
 // MFMAs of one half run, the fragments of the next half are read.  The loads
@@ -878,9 +880,10 @@ __global__ __launch_bounds__(64 * 2 * WN) void gemm_bf16_dma(GemmArgs a) {
 // last slice into the free stage (never read), so every slice issues the same
 // number of loads and the vmcnt waits are constants.
 // ===========================================================================
-template <bool AK, bool BKM>
-__global__ __launch_bounds__(256) void gemm_bf16_w4(GemmArgs a) {
-  constexpr int BM_ = 256, BN_ = 256, NW = 4, IM = 4, JN = 4;
+template <bool AK, bool BKM, int WN = 2>
+__global__ __launch_bounds__(64 * 2 * WN) void gemm_bf16_w4(GemmArgs a) {
+  // WN = 2: four wavefronts of 128 x 128; WN = 4: eight of 128 x 64
+  constexpr int BM_ = 256, BN_ = 256, NW = 2 * WN, IM = 4, JN = 8 / WN, WTN = BN_ / WN;
   constexpr int ASZ = BM_ * KT3, BSZ = BN_ * KT3;
   constexpr int NU = BM_ * KT3 * 2 / 1024 / NW;   // 1 KB loads per operand per wavefront per slice
   constexpr int PERT = 2 * NU;                    // loads per wavefront per slice
@@ -908,7 +911,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4(GemmArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN, wn = wave % WN;
 
   int kmin = 0, kmax = a.K;
   if (a.causal == CAUSAL_K_LE_M) kmax = min(a.K, m0 + BM_);
@@ -981,7 +984,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4(GemmArgs a) {
   bf16x8_t f0[IM + JN], f1[IM + JN];   // fragments of half slices (k 0..15, k 16..31)
   auto rd = [&](bf16x8_t& f, const bf16_t* st, int x, int kk) {
     if (x < IM) f = frag<BM_, AK>(st, wm * 128 + x * 32, kk, lane);
-    else f = frag<BN_, BKM>(st + ASZ, wn * 128 + (x - IM) * 32, kk, lane);
+    else f = frag<BN_, BKM>(st + ASZ, wn * WTN + (x - IM) * 32, kk, lane);
   };
   auto mma = [&](const bf16x8_t (&f)[IM + JN], int e) {
     const int i = e / JN, j = e % JN;
@@ -998,9 +1001,9 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4(GemmArgs a) {
 #pragma clang loop unroll(full)
     for (int x = 0; x < IM + JN; ++x) {
       rd(f1[x], cur, x, 16);
-      if (x & 1) dma(fill2, t + 2, NU + x / 2);
-      mma(f0, 2 * x);
-      mma(f0, 2 * x + 1);
+      if ((x & 1) && x / 2 < NU) dma(fill2, t + 2, NU + x / 2);
+#pragma clang loop unroll(full)
+      for (int e = x * IM * JN / (IM + JN); e < (x + 1) * IM * JN / (IM + JN); ++e) mma(f0, e);
       __builtin_amdgcn_sched_barrier(0);
     }
     // own loads of slice t + 1 done (the 8 issued since are slice t + 2's),
@@ -1014,10 +1017,10 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4(GemmArgs a) {
     // half slice 1 on f1; A's loads of slice t + 3 into stage S - 1; read half 0 of slice t + 1 into f0
 #pragma clang loop unroll(full)
     for (int x = 0; x < IM + JN; ++x) {
-      if (x & 1) dma(nxt_fill, t + 3, x / 2);
+      if ((x & 1) && x / 2 < NU) dma(nxt_fill, t + 3, x / 2);
       rd(f0[x], nxt, x, 0);
-      mma(f1, 2 * x);
-      mma(f1, 2 * x + 1);
+#pragma clang loop unroll(full)
+      for (int e = x * IM * JN / (IM + JN); e < (x + 1) * IM * JN / (IM + JN); ++e) mma(f1, e);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -1046,13 +1049,23 @@ __global__ __launch_bounds__(256) void gemm_bf16_w4(GemmArgs a) {
 
   const int64_t coff = batch_off(z, a.inner_count, a.c_outer, a.c_inner, a.c_div);
   // stage the output through the ring once every wavefront is done with it:
-  // wavefront w uses stage w (4 x 32 x 36 floats = 18 KB of its 32 KB)
+  // four wavefronts: wavefront w uses stage w (4 x 32 x 36 floats = 18 KB of
+  // its 32 KB); eight: wavefronts 2s and 2s + 1 share stage s, 2 blocks each
   __syncthreads();
-  float* stg = reinterpret_cast<float*>(wave == 0 ? st0 : wave == 1 ? st1 : wave == 2 ? st2 : st3);
-  const int cbs[4] = {n0 + wn * 128, n0 + wn * 128 + 32, n0 + wn * 128 + 64, n0 + wn * 128 + 96};
+  if constexpr (WN == 2) {
+    float* stg = reinterpret_cast<float*>(wave == 0 ? st0 : wave == 1 ? st1 : wave == 2 ? st2 : st3);
+    const int cbs[4] = {n0 + wn * 128, n0 + wn * 128 + 32, n0 + wn * 128 + 64, n0 + wn * 128 + 96};
 #pragma clang loop unroll(full)
-  for (int i = 0; i < IM; ++i)
-    store_blocks_lds<bf16_t, 4>(a, acc[i], coff, m0 + wm * 128 + i * 32, cbs, lane, stg);
+    for (int i = 0; i < IM; ++i)
+      store_blocks_lds<bf16_t, 4>(a, acc[i], coff, m0 + wm * 128 + i * 32, cbs, lane, stg);
+  } else {
+    float* stg = reinterpret_cast<float*>(wave < 2 ? st0 : wave < 4 ? st1 : wave < 6 ? st2 : st3) +
+                 (wave & 1) * 2 * STG_FLOATS;
+    const int cbs[2] = {n0 + wn * WTN, n0 + wn * WTN + 32};
+#pragma clang loop unroll(full)
+    for (int i = 0; i < IM; ++i)
+      store_blocks_lds<bf16_t, 2>(a, acc[i], coff, m0 + wm * 128 + i * 32, cbs, lane, stg);
+  }
 }
 
 // ===========================================================================
@@ -1255,17 +1268,18 @@ void launch_w4k64(const GemmArgs& a, hipStream_t stream) {
   else launch_w4k64_t<false, false>(a, stream);
 }
 
-template <bool AK, bool BKM>
+template <bool AK, bool BKM, int WN>
 void launch_w4_t(const GemmArgs& a, hipStream_t stream) {
   dim3 grid(ceil_div(a.N, 256), ceil_div(a.M, 256), a.nbatch);
-  hipLaunchKernelGGL((gemm_bf16_w4<AK, BKM>), grid, dim3(256), 0, stream, a);
+  hipLaunchKernelGGL((gemm_bf16_w4<AK, BKM, WN>), grid, dim3(128 * WN), 0, stream, a);
 }
+template <int WN>
 void launch_w4(const GemmArgs& a, hipStream_t stream) {
   const bool ak = a.A[0].s_k == 1, bk = a.B[0].s_k == 1;
-  if (ak && bk) launch_w4_t<true, true>(a, stream);
-  else if (ak && !bk) launch_w4_t<true, false>(a, stream);
-  else if (!ak && bk) launch_w4_t<false, true>(a, stream);
-  else launch_w4_t<false, false>(a, stream);
+  if (ak && bk) launch_w4_t<true, true, WN>(a, stream);
+  else if (ak && !bk) launch_w4_t<true, false, WN>(a, stream);
+  else if (!ak && bk) launch_w4_t<false, true, WN>(a, stream);
+  else launch_w4_t<false, false, WN>(a, stream);
 }
 
 template <int BN_, int WN>
@@ -1323,10 +1337,10 @@ const char* gemm_check(const GemmArgs& a) {
     }
   }
   if (a.causal == CAUSAL_SKIP_UPPER && a.M > a.N) return "gemm: causal skip needs M <= N";
-  if (a.tile < 0 || a.tile > 7) return "gemm: bad tile";
+  if (a.tile < 0 || a.tile > 8) return "gemm: bad tile";
   if (a.tile >= 4 && (a.K % 32 || a.M < 8 || a.N < 8)) return "gemm: the DMA kernel needs K % 32 == 0";
-  if (a.tile >= 7 && a.K % 64) return "gemm: the 64-deep kernels need K % 64 == 0";
-  if (a.tile >= 7 && a.npairs == 2 &&
+  if (a.tile == 7 && a.K % 64) return "gemm: the 64-deep kernels need K % 64 == 0";
+  if (a.tile == 7 && a.npairs == 2 &&
       (a.A[1].s_row != a.A[0].s_row || a.A[1].s_k != a.A[0].s_k || a.B[1].s_row != a.B[0].s_row ||
        a.B[1].s_k != a.B[0].s_k))
     return "gemm: the 64-deep kernels need equal operand strides in both pairs";
@@ -1343,21 +1357,22 @@ hipError_t gemm(const GemmArgs& a, hipStream_t stream) {
       const int64_t t128 = (int64_t)ceil_div(a.M, 256) * ceil_div(a.N, 128) * a.nbatch;
       const bool dma = a.K % KT3 == 0;
       // 256 x 256 tiles once there are more than 128 of them; with fewer,
-      // 256 x 128 tiles keep more of the 256 CUs busy.  The four-wavefront
-      // kernel is the fastest for fp32 outputs on the 1.3B layer shapes (both
-      // operand layouts, one or two operand pairs); with both operands K-major
-      // and an operand-type output (q/k/v and the MLP input product), and for
-      // short contractions that never fill its pipeline, the eight-wavefront
-      // kernel is as fast or faster (measured inside the HVP).
-      const bool kk = a.A[0].s_k == 1 && a.B[0].s_k == 1;
-      if (a.N > 128 && t256 > 128) tile = dma ? ((a.K < 512 || (kk && a.out_type == OUT_OP)) ? 4 : 6) : 2;
+      // 256 x 128 tiles keep more of the 256 CUs busy.  Contractions up to
+      // 4096 deep (the forward projections and the input gradients of
+      // 2048-wide layers) run on eight wavefronts of 128 x 64, two per SIMD,
+      // whose tiles spend less of their time in the prologue and the staged
+      // epilogue; longer ones (the weight gradients, the input gradients of the
+      // MLP and q/k/v) on four wavefronts of 128 x 128 (measured on the 1.3B
+      // layer shapes, one and two operand pairs).
+      if (a.N > 128 && t256 > 128) tile = dma ? (a.K <= 4096 ? 8 : 6) : 2;
       else if (t128 >= 64) tile = dma ? 5 : 3;
     }
     if (tile == 2) { launch_big<256, 256, 2, 4>(a, stream); return hipGetLastError(); }
     if (tile == 3) { launch_big<256, 128, 2, 2>(a, stream); return hipGetLastError(); }
     if (tile == 4) { launch_dma<256, 4>(a, stream); return hipGetLastError(); }
     if (tile == 5) { launch_dma<128, 2>(a, stream); return hipGetLastError(); }
-    if (tile == 6) { launch_w4(a, stream); return hipGetLastError(); }
+    if (tile == 6) { launch_w4<2>(a, stream); return hipGetLastError(); }
+    if (tile == 8) { launch_w4<4>(a, stream); return hipGetLastError(); }
     if (tile == 7) { launch_w4k64(a, stream); return hipGetLastError(); }
   }
   dim3 grid(ceil_div(a.N, BN), ceil_div(a.M, BM), a.nbatch);

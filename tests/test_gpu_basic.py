@@ -18,7 +18,7 @@ def _bf16_np(x):
     return synth.bf16_round(x.astype(np.float32))
 
 
-@pytest.mark.parametrize("dtype,tile", [("bf16", 1), ("bf16", 2), ("bf16", 3), ("bf16", 4), ("bf16", 5), ("bf16", 6), ("bf16", 7), ("f32", 0)])
+@pytest.mark.parametrize("dtype,tile", [("bf16", 1), ("bf16", 2), ("bf16", 3), ("bf16", 4), ("bf16", 5), ("bf16", 6), ("bf16", 7), ("bf16", 8), ("f32", 0)])
 @pytest.mark.parametrize("ak,bk", [(1, 1), (1, 0), (0, 1), (0, 0)])
 def test_gemm_layouts_pairs_batches(dtype, tile, ak, bk):
     torch = need_gpu()
@@ -47,7 +47,7 @@ def test_gemm_layouts_pairs_batches(dtype, tile, ak, bk):
     assert err < 2e-6, err
 
 
-@pytest.mark.parametrize("tile", [1, 2, 3, 4, 5, 6, 7])
+@pytest.mark.parametrize("tile", [1, 2, 3, 4, 5, 6, 7, 8])
 @pytest.mark.parametrize("causal", [1, 2, 3])
 def test_gemm_causal_modes(causal, tile):
     torch = need_gpu()
