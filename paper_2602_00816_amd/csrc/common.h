@@ -18,15 +18,9 @@ __host__ __device__ inline float bf16_to_f32(bf16_t h) {
   return c.f;
 }
 
-// round-to-nearest-even float32 -> bfloat16 (NaN kept quiet)
-__host__ __device__ inline bf16_t f32_to_bf16(float f) {
-  union { uint32_t u; float f; } c;
-  c.f = f;
-  uint32_t u = c.u;
-  if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu)) return (bf16_t)((u >> 16) | 0x40);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
-}
+// round-to-nearest-even float32 -> bfloat16 (NaN kept quiet): the compiler's
+// conversion, one v_cvt_pk_bf16_f32 per pair of values on gfx950
+__host__ __device__ inline bf16_t f32_to_bf16(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
 
 template <typename T> struct OpType;
 template <> struct OpType<float> {
