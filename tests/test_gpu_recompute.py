@@ -103,3 +103,35 @@ def test_recompute_full_8b_and_window_lanczos():
     assert s == steps and np.all(np.isfinite(al)) and np.all(np.isfinite(be))
     assert abs(al[0] - vhv) <= 1e-4 * abs(vhv) + 1e-12
     assert abs(al[0] ** 2 + be[0] ** 2 - nhv2) <= 1e-4 * nhv2
+
+
+def test_recompute_dataset_operator_same_bits():
+    """The token-weighted dataset operator (three batches of different shapes,
+    one with ignored targets) and a short Lanczos run on it: with
+    recomputation the products and the Lanczos coefficients are the same bits."""
+    torch = need_gpu()
+    from paper_2602_00816_amd import fdhvp as fd
+    w = dict(WORKLOADS["llama-1.3b-bf16"], n_layers=3)
+    cfg, theta, _ = workload_inputs(w, batch=1, seq=128)
+    shapes = [(1, 256), (2, 128), (1, 128)]
+    toks = [synth.tokens(10 + i, B, S, w["vocab"], "zipf") for i, (B, S) in enumerate(shapes)]
+    lab = toks[1].copy()
+    lab[:, :40] = -100
+    out = {}
+    for rc in (False, True):
+        mod = fd.Model.from_workload(w)
+        mod.set_recompute(rc)
+        o = fd.opts("full", 0, "bf16")
+        mod.set_workspace(2, 256, 4, o)
+        th = upload_params(torch, theta, "bf16")
+        db = [torch.from_numpy(toks[0]).cuda(), (torch.from_numpy(toks[1]).cuda(), torch.from_numpy(lab).cuda()),
+              torch.from_numpy(toks[2]).cuda()]
+        n = mod.bind_dataset(th, db, 1e-3)
+        v = torch.from_numpy(synth.rademacher_probe(3, theta.size)).cuda()
+        hv = mod.hvp_bound(v).cpu().numpy()
+        al, be, s, st = mod.lanczos(4, 5, o)
+        out[rc] = (n, hv, al, be)
+        say(f"recompute={rc}: {n} targets, alpha {al}")
+    assert out[False][0] == out[True][0]
+    assert np.array_equal(out[False][1], out[True][1])
+    assert np.array_equal(out[False][2], out[True][2]) and np.array_equal(out[False][3], out[True][3])
