@@ -204,8 +204,14 @@ def test_lanczos_quad_diag_matches_oracle(reorth, window, basis):
     lam_g = np.sort(np.linalg.eigvalsh(OL.tridiag(a, b)))
     lam_o = np.sort(np.linalg.eigvalsh(OL.tridiag(ao, bo)))
     scale = np.abs(lam_o).max()
-    # extreme Ritz values within 1e-3 relative (fp32); the bf16 basis is reported looser
-    tol = 1e-3 if basis == "f32" else 5e-2
+    say(f"  extreme Ritz errors {abs(lam_g[-1] - lam_o[-1]) / scale:.3e}, {abs(lam_g[0] - lam_o[0]) / scale:.3e}; "
+        f"alpha_1 {abs(a[0] - ao[0]) / scale:.3e}")
+    # extreme Ritz values within 1e-3 relative (fp32).  A bf16 basis stores every
+    # row with a relative rounding of at most 2^-9, so the reorthogonalisation
+    # removes the stored directions only to that accuracy and the Ritz values
+    # of the perturbed recurrence move by about 2^-9 of the spectral scale at
+    # first order: the bar is 2^-8 (measured 1.0e-4 and 8.8e-4 at m = 16)
+    tol = 1e-3 if basis == "f32" else 2.0 ** -8
     assert abs(lam_g[-1] - lam_o[-1]) <= tol * scale
     assert abs(lam_g[0] - lam_o[0]) <= tol * scale
     assert abs(a[0] - ao[0]) <= 1e-5 * scale
@@ -229,6 +235,9 @@ def test_lanczos_long_runs_match_oracle(m, basis):
     lam_g = np.sort(np.linalg.eigvalsh(OL.tridiag(a, b)))
     lam_o = np.sort(np.linalg.eigvalsh(OL.tridiag(ao, bo)))
     scale = np.abs(lam_o).max()
+    # the five largest of this spectrum are well separated and converged after
+    # 24 steps, which damps the basis rounding well below its 2^-9 first-order
+    # size: 5e-4 holds for the bf16 basis here
     tol = 1e-5 if basis == "f32" else 5e-4
     assert np.abs(lam_g[-5:] - lam_o[-5:]).max() <= tol * scale
     assert abs(lam_g[0] - lam_o[0]) <= tol * scale
