@@ -781,6 +781,34 @@ __device__ inline void swiglu_pair(float gm, float gd, float um, float ud, float
   od = S * ud + D * um;
 }
 
+// SwiGLU backward at both points in the same channel form: for the upstream
+// gradient z = zm +- zd, the gate gradient z v s'(g) and the up gradient
+// z s(g), with s'(x) = sig(x) (1 + x sig(-x)).  Every factor is split into its
+// half sum and half difference and a product of two split factors is formed as
+// (xm ym + xd yd, xm yd + xd ym), which is exact before rounding.  The half
+// difference of s' is (sig(a) - sig(b) + h(a) - h(b)) / 2 with
+// h(x) = x sig'(x), sig' = sig(x) sig(-x), and
+//   h(a) - h(b) = gd (sig'(a) + sig'(b)) + gm (sig'(a) - sig'(b)),
+//   sig'(a) - sig'(b) = (sig(a) - sig(b)) (1 - sig(a) - sig(b)),
+// so no term subtracts two values of the full size of s'.
+__device__ inline void swiglu_bwd_pair(float gm, float gd, float um, float ud, float zm, float zd, float& am,
+                                       float& ad, float& bm, float& bd) {
+  const float a = gm + gd, b = gm - gd;
+  const float ea = expf(-a), eb = expf(-b);
+  const float sa = 1.f / (1.f + ea), sb = 1.f / (1.f + eb);
+  const float sna = a < 0.f ? 1.f - sa : ea * sa, snb = b < 0.f ? 1.f - sb : eb * sb;
+  const float dsig = sa * snb * -expm1f(-2.f * gd);
+  const float pa = sa * sna, pb = sb * snb;   // sig'(a), sig'(b)
+  const float S1 = 0.5f * (sa * (1.f + a * sna) + sb * (1.f + b * snb));
+  const float D1 = 0.5f * (dsig + gd * (pa + pb) + gm * dsig * (1.f - sa - sb));
+  const float S0 = 0.5f * (a * sa + b * sb), D0 = 0.5f * (gd * (sa + sb) + gm * dsig);
+  const float xm = zm * um + zd * ud, xd = zm * ud + zd * um;   // z v
+  am = xm * S1 + xd * D1;
+  ad = xm * D1 + xd * S1;
+  bm = zm * S0 + zd * D0;
+  bd = zm * D0 + zd * S0;
+}
+
 template <typename T>
 __global__ void gelu_fwd_kernel(PairT<T> z, const T* um, const T* ud, int64_t n) {
   GRID_LOOP(i, n) {
@@ -829,18 +857,8 @@ __global__ void swiglu_bwd4_kernel(PairT<T> dgu, const T* gum, const T* gud, con
   const float4 zm = *reinterpret_cast<const float4*>(dzm + io), zd = *reinterpret_cast<const float4*>(dzd + io);
   float am[4], ad[4], bm[4], bd[4];
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const double gp = (double)f4e(gm, e) + (double)f4e(gd, e), gn = (double)f4e(gm, e) - (double)f4e(gd, e);
-    const double vp = (double)f4e(um, e) + (double)f4e(ud, e), vn = (double)f4e(um, e) - (double)f4e(ud, e);
-    const double zp = (double)f4e(zm, e) + (double)f4e(zd, e), zn = (double)f4e(zm, e) - (double)f4e(zd, e);
-    const double sp = sigm(gp), sn = sigm(gn);
-    const double ap = zp * vp * sp * (1.0 + gp * (1.0 - sp)), an = zn * vn * sn * (1.0 + gn * (1.0 - sn));
-    const double bp = zp * gp * sp, bn = zn * gn * sn;
-    am[e] = (float)(0.5 * (ap + an));
-    ad[e] = (float)(0.5 * (ap - an));
-    bm[e] = (float)(0.5 * (bp + bn));
-    bd[e] = (float)(0.5 * (bp - bn));
-  }
+  for (int e = 0; e < 4; ++e)
+    swiglu_bwd_pair(f4e(gm, e), f4e(gd, e), f4e(um, e), f4e(ud, e), f4e(zm, e), f4e(zd, e), am[e], ad[e], bm[e], bd[e]);
   st4f(dgu.m, ig, am[0], am[1], am[2], am[3]);
   st4f(dgu.d, ig, ad[0], ad[1], ad[2], ad[3]);
   st4f(dgu.m, iu, bm[0], bm[1], bm[2], bm[3]);
@@ -866,12 +884,12 @@ __global__ void swiglu_bwd_kernel(PairT<T> dgu, const T* gum, const T* gud, cons
   GRID_LOOP(i, n) {
     const int64_t t = i / F, c = i % F;
     const int64_t ig = t * 2 * F + c, iu = ig + F;
-    const double gp = (double)ldf(gum, ig) + (double)ldf(gud, ig), gn = (double)ldf(gum, ig) - (double)ldf(gud, ig);
-    const double vp = (double)ldf(gum, iu) + (double)ldf(gud, iu), vn = (double)ldf(gum, iu) - (double)ldf(gud, iu);
-    const double zp = (double)dzm[i] + (double)dzd[i], zn = (double)dzm[i] - (double)dzd[i];
-    const double sp = sigm(gp), sn = sigm(gn);
-    put_pair(dgu, ig, zp * vp * sp * (1.0 + gp * (1.0 - sp)), zn * vn * sn * (1.0 + gn * (1.0 - sn)));
-    put_pair(dgu, iu, zp * gp * sp, zn * gn * sn);
+    float am, ad, bm, bd;
+    swiglu_bwd_pair(ldf(gum, ig), ldf(gud, ig), ldf(gum, iu), ldf(gud, iu), dzm[i], dzd[i], am, ad, bm, bd);
+    stf(dgu.m, ig, am);
+    stf(dgu.d, ig, ad);
+    stf(dgu.m, iu, bm);
+    stf(dgu.d, iu, bd);
   }
 }
 
