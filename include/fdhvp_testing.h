@@ -32,6 +32,19 @@ fdh_status fdh_testing_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, int3
                             int32_t b_kmajor, const void* A, const void* B, const void* A2, const void* B2,
                             float* C, int32_t causal, float alpha, int32_t tile, void* hip_stream);
 
+/* Two independent bf16 products in one launch of the 256 x 256 kernel given
+ * by tile (6 or 8, as for fdh_testing_gemm), the way the weight gradients of
+ * the attention output and q/k/v projections share a launch in an HVP.
+ * Product p is C_p[M_p][N_p] = alpha (A_p B_p^T + A2_p B2_p^T), operands laid
+ * out as for fdh_testing_gemm with batch 1, both products with the same
+ * a_kmajor / b_kmajor; A2_p, B2_p may be NULL together.  K_p % 32 == 0, M_p and
+ * N_p >= 8.  FDH_ERR_UNSUPPORTED when a product does not fit the kernel.
+ * Enqueued on hip_stream; returns without waiting. */
+fdh_status fdh_testing_gemm_pair(int32_t M0, int32_t N0, int32_t K0, int32_t M1, int32_t N1, int32_t K1,
+                                 int32_t a_kmajor, int32_t b_kmajor, const void* A0, const void* B0, const void* A20,
+                                 const void* B20, float* C0, const void* A1, const void* B1, const void* A21,
+                                 const void* B21, float* C1, float alpha, int32_t tile, void* hip_stream);
+
 /* on != 0 makes the next fdh_set_workspace plan the unfused attention path
  * (score, probability and score-gradient matrices in the workspace, MFMA
  * GEMMs and row kernels) even where the fused kernels apply (bf16 operands,
@@ -39,10 +52,14 @@ fdh_status fdh_testing_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, int3
  * be compared on one model. */
 fdh_status fdh_testing_unfused_attention(fdh_ctx* ctx, int32_t on);
 
-/* on != 0 makes the weight-gradient GEMMs contract over the whole token range
- * in one pass, where by default small output grids are cut into token slices
- * whose fp32 partial products are added afterwards (fp64 sums in slice
- * order), so that the two can be compared.  Takes effect at the next HVP. */
+/* Weight-gradient launch forms, so that they can be compared.  By default
+ * (on = 0) small output grids are cut into token slices whose fp32 partial
+ * products are added afterwards (fp64 sums in slice order), and with fused
+ * attention the attention output projection's weight gradient shares one
+ * launch with the q/k/v one when its tiles fit into that grid's last wave.
+ * on = 1: every weight gradient contracts over the whole token range in a
+ * launch of its own; on = 2: token slices as by default, no shared launch.
+ * Other values: FDH_ERR_INVALID_ARG.  Takes effect at the next HVP. */
 fdh_status fdh_testing_unsplit_wgrad(fdh_ctx* ctx, int32_t on);
 
 /* Per-launch timing with HIP events recorded on the context stream around every

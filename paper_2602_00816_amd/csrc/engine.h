@@ -109,6 +109,7 @@ class Engine : public WsLayout {
   size_t ws_bytes = 0;
   bool force_unfused = false;   // testing: plan the unfused path even where the fused one applies
   bool force_unsplit = false;   // testing: weight-gradient GEMMs over the whole token range
+  bool force_unpaired = false;  // testing: no weight-gradient GEMMs paired in one launch
   bool recompute = false;       // plan (and run) with activation recomputation
   // the carve for token batches up to [B, S] and m Lanczos steps with options
   // o (o may be null when m == 0), written into *out; changes nothing else

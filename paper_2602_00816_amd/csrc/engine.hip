@@ -135,6 +135,18 @@ static int wgrad_splits(int M, int N, int T_) {
   return best;
 }
 
+// The weight gradient of the attention output projection (Mo x No) runs in
+// the same launch as the q/k/v one (Mq x Nq) when the q/k/v grid is not cut
+// along the tokens and the output projection's tiles fit into the idle part
+// of its last wave of 256 tiles (the 2048-wide layer: 192 + 64 tiles).  Its
+// tiles then cost no extra time, where on their own they would be cut into
+// token slices and summed.
+static bool pair_wgrads(int Mq, int Nq, int Mo, int No, int T_) {
+  const int64_t tq = (int64_t)((Mq + 255) / 256) * ((Nq + 255) / 256);
+  const int64_t to = (int64_t)((Mo + 255) / 256) * ((No + 255) / 256);
+  return wgrad_splits(Mq, Nq, T_) == 1 && tq % 256 != 0 && tq % 256 + to <= 256;
+}
+
 // ---------------------------------------------------------------------------
 // workspace plan
 // ---------------------------------------------------------------------------
@@ -406,6 +418,32 @@ static int run_gemm(Engine& e, GemmArgs& g) {
   return FDH_OK;
 }
 
+template <typename T>
+static int run_gemm_pair(Engine& e, GemmArgs& g0, GemmArgs& g1) {
+  for (const GemmArgs* g : {&g0, &g1}) {
+    const char* msg = gemm_check<T>(*g);
+    if (msg) {
+      e.err = msg;
+      return FDH_ERR_UNSUPPORTED;
+    }
+  }
+  int e0 = 0;
+  if (e.timing.on) {
+    hipError_t r = e.timing.begin(e.stream, &e0);
+    if (r != hipSuccess) { e.err = "timing event"; return FDH_ERR_HIP; }
+  }
+  hipError_t r = gemm_pair<T>(g0, g1, e.stream);
+  if (r != hipSuccess) {
+    e.err = std::string("gemm launch: ") + hipGetErrorString(r);
+    return FDH_ERR_HIP;
+  }
+  if (e.timing.on) {
+    r = e.timing.end(e.stream, 0, e0, gemm_flops(g0) + gemm_flops(g1), 0.0);
+    if (r != hipSuccess) { e.err = "timing event"; return FDH_ERR_HIP; }
+  }
+  return FDH_OK;
+}
+
 #define RG(T, g)                       \
   do {                                 \
     int rc_ = run_gemm<T>(*this, g);   \
@@ -466,7 +504,6 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, c
     g.C = Ym; g.ldc = N; g.out_type = out;
     g.resid = Rm;
     if (bias.valid()) g.bias_theta = th + bias.off;
-    RG(T, g);
     GemmArgs h;
     h.M = T_; h.N = N; h.K = K; h.npairs = 2;
     h.A[0] = kmaj(Xd, K); h.B[0] = kmaj(th + W.off, K);
@@ -474,6 +511,7 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, c
     h.C = Yd; h.ldc = N; h.out_type = out;
     h.resid = Rd;
     if (bias.valid()) { h.bias_v = v + bias.off; h.bias_v_scale = feps; }
+    RG(T, g);
     RG(T, h);
     return FDH_OK;
   };
@@ -484,24 +522,33 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, c
     g.A[0] = kmaj(dYm, N);
     g.B[0] = mnmaj(th + W.off, K);
     g.C = dXm; g.ldc = K; g.out_type = out;
-    RG(T, g);
     GemmArgs h;
     h.M = T_; h.N = K; h.K = N; h.npairs = 2;
     h.A[0] = kmaj(dYd, N); h.B[0] = mnmaj(th + W.off, K);
     h.A[1] = kmaj(dYm, N); h.B[1] = mnmaj(lo + W.off, K);
     h.C = dXd; h.ldc = K; h.out_type = out;
+    RG(T, g);
     RG(T, h);
     return FDH_OK;
   };
   // Hv_W = (dY.m^T X.d + dY.d^T X.m) / eps
   // (with ns > 1 the token range is cut into ns slices, one GEMM batch entry
   // each, into fp32 partial products that a second pass adds in slice order)
-  auto lin_wgrad = [&](const T* dYm, const T* dYd, int N, const T* Xm, const T* Xd, int K, const ParamRef& W) -> int {
+  auto wgrad_args = [&](const T* dYm, const T* dYd, int N, const T* Xm, const T* Xd, int K, const ParamRef& W) {
     GemmArgs g;
     g.M = N; g.N = K; g.K = T_; g.npairs = 2;
     g.A[0] = mnmaj(dYm, N); g.B[0] = mnmaj(Xd, K);
     g.A[1] = mnmaj(dYd, N); g.B[1] = mnmaj(Xm, K);
     g.C = hv + W.off; g.ldc = K; g.alpha = inv_eps;
+    return g;
+  };
+  // two weight gradients over the whole token range in one launch
+  auto lin_wgrad_pair = [&](GemmArgs g0, GemmArgs g1) -> int {
+    if (acc) g0.beta = g1.beta = 1.f;
+    return run_gemm_pair<T>(*this, g0, g1);
+  };
+  auto lin_wgrad = [&](const T* dYm, const T* dYd, int N, const T* Xm, const T* Xd, int K, const ParamRef& W) -> int {
+    GemmArgs g = wgrad_args(dYm, dYd, N, Xm, Xd, K, W);
     const int ns = wgrad_splits(N, K, T_);
     if (ns == 1 || force_unsplit || wsplit.bytes < (size_t)ns * N * K * 4) {
       if (acc) g.beta = 1.f;
@@ -713,7 +760,11 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, c
     // ---- attention ----  (dx = gradient w.r.t. x_mid)
     RC(as_op(dxm, dxd, dxo_m, dxo_d, (int64_t)T_ * d, &gom, &god));
     if (gpt2) RC(colsum_hv(dxd, d, d, R.bo));
-    RC(lin_wgrad(gom, god, d, OP(s.o_m), OP(s.o_d), Hq * dh, R.wo));
+    // (paired with the q/k/v weight gradient below: gom, god and o stay intact
+    // through the fused attention backward)
+    const bool pair_o = std::is_same<T, bf16_t>::value && fused && !force_unsplit && !force_unpaired &&
+                        pair_wgrads(qkvd, d, d, Hq * dh, T_);
+    if (!pair_o) RC(lin_wgrad(gom, god, d, OP(s.o_m), OP(s.o_d), Hq * dh, R.wo));
     RC(lin_dgrad(gom, god, d, R.wo, Hq * dh, OP(do_m), OP(do_d), OUT_OP));
     const T* qm = OP(s.qkv_m);
     const T* qd = OP(s.qkv_d);
@@ -840,7 +891,11 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, c
       CK(launch_qkv_bwd_post<T>(PairT<T>{OP(dqkvo_m), OP(dqkvo_d)}, gm, gd, T_, S, Hq, Hk, dh,
                                 (const double*)(ws + rope.off), llama, st));
     }
-    RC(lin_wgrad(OP(dqkvo_m), OP(dqkvo_d), qkvd, OP(s.a_m), OP(s.a_d), d, R.wqkv));
+    if (pair_o)
+      RC(lin_wgrad_pair(wgrad_args(OP(dqkvo_m), OP(dqkvo_d), qkvd, OP(s.a_m), OP(s.a_d), d, R.wqkv),
+                        wgrad_args(gom, god, d, OP(s.o_m), OP(s.o_d), Hq * dh, R.wo)));
+    else
+      RC(lin_wgrad(OP(dqkvo_m), OP(dqkvo_d), qkvd, OP(s.a_m), OP(s.a_d), d, R.wqkv));
     RC(lin_dgrad(OP(dqkvo_m), OP(dqkvo_d), qkvd, R.wqkv, d, F32(da_m), F32(da_d), OUT_F32));
     RC(norm_back(dym, dyd, dxm, dxd, F32(s.x_in_m), F32(s.x_in_d), F32(da_m), F32(da_d), R.n1g, R.n1b));
     std::swap(dxm, dym);

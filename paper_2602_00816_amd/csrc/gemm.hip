@@ -880,8 +880,10 @@ __global__ __launch_bounds__(64 * 2 * WN) void gemm_bf16_dma(GemmArgs a) {
 // last slice into the free stage (never read), so every slice issues the same
 // number of loads and the vmcnt waits are constants.
 // ===========================================================================
-template <bool AK, bool BKM, int WN = 2>
-__global__ __launch_bounds__(64 * 2 * WN) void gemm_bf16_w4(GemmArgs a) {
+// One 256 x 256 output tile of the product a: tile lin of a gx x gy tile grid
+// (times a.nbatch).
+template <bool AK, bool BKM, int WN>
+__device__ __forceinline__ void w4_tile(const GemmArgs& a, int gx, int gy, int lin) {
   // WN = 2: four wavefronts of 128 x 128; WN = 4: eight of 128 x 64
   constexpr int BM_ = 256, BN_ = 256, NW = 2 * WN, IM = 4, JN = 8 / WN, WTN = BN_ / WN;
   constexpr int ASZ = BM_ * KT3, BSZ = BN_ * KT3;
@@ -892,11 +894,6 @@ __global__ __launch_bounds__(64 * 2 * WN) void gemm_bf16_w4(GemmArgs a) {
   __shared__ __attribute__((aligned(1024))) bf16_t st2[ASZ + BSZ];
   __shared__ __attribute__((aligned(1024))) bf16_t st3[ASZ + BSZ];
 
-  const int gx = gridDim.x, gy = gridDim.y;
-  const int nb = gx * gy * gridDim.z;
-  int lin = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
-  const int per = nb / 8;
-  if (lin < per * 8) lin = (lin % 8) * per + lin / 8;
   const int tiles = gx * gy;
   const int z = lin / tiles;
   const int tl = lin % tiles;
@@ -1066,6 +1063,32 @@ __global__ __launch_bounds__(64 * 2 * WN) void gemm_bf16_w4(GemmArgs a) {
     for (int i = 0; i < IM; ++i)
       store_blocks_lds<bf16_t, 2>(a, acc[i], coff, m0 + wm * 128 + i * 32, cbs, lane, stg);
   }
+}
+
+// Workgroup ids are dealt to the 8 XCDs in turn; renumber them so that each
+// XCD takes a contiguous run of tiles (neighbouring tiles share operand rows
+// and columns in that XCD's L2).
+__device__ inline int xcd_order(int lin, int nb) {
+  const int per = nb / 8;
+  return lin < per * 8 ? (lin % 8) * per + lin / 8 : lin;
+}
+
+template <bool AK, bool BKM, int WN = 2>
+__global__ __launch_bounds__(64 * 2 * WN) void gemm_bf16_w4(GemmArgs a) {
+  const int gx = gridDim.x, gy = gridDim.y;
+  w4_tile<AK, BKM, WN>(a, gx, gy, xcd_order(blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z), gx * gy * gridDim.z));
+}
+
+// Two independent products in one grid (one-dimensional, n0 tiles of a0
+// then those of a1): the tiles of a1 take the compute units that a grid of
+// a0 alone would leave idle in its last wave.  Each product is renumbered on
+// its own, so that every XCD takes an eighth of each (renumbering the joint
+// grid would give a0 to some XCDs and a1 to the others).
+template <bool AK, bool BKM, int WN = 2>
+__global__ __launch_bounds__(64 * 2 * WN) void gemm_bf16_w4_pair(GemmArgs a0, GemmArgs a1, int n0) {
+  const int b = blockIdx.x;
+  if (b < n0) w4_tile<AK, BKM, WN>(a0, (a0.N + 255) / 256, (a0.M + 255) / 256, xcd_order(b, n0));
+  else w4_tile<AK, BKM, WN>(a1, (a1.N + 255) / 256, (a1.M + 255) / 256, xcd_order(b - n0, gridDim.x - n0));
 }
 
 // ===========================================================================
@@ -1347,26 +1370,32 @@ const char* gemm_check(const GemmArgs& a) {
   return nullptr;
 }
 
+// The bf16 kernel a product runs on (the tile values of GemmArgs::tile).
+static int bf16_tile(const GemmArgs& a) {
+  int tile = a.tile;
+  if (tile == 0 && a.M >= 256) {
+    const int64_t t256 = (int64_t)ceil_div(a.M, 256) * ceil_div(a.N, 256) * a.nbatch;
+    const int64_t t128 = (int64_t)ceil_div(a.M, 256) * ceil_div(a.N, 128) * a.nbatch;
+    const bool dma = a.K % KT3 == 0;
+    // 256 x 256 tiles once there are more than 128 of them; with fewer,
+    // 256 x 128 tiles keep more of the 256 CUs busy.  Contractions up to
+    // 4096 deep (the forward projections and the input gradients of
+    // 2048-wide layers) run on eight wavefronts of 128 x 64, two per SIMD,
+    // whose tiles spend less of their time in the prologue and the staged
+    // epilogue; longer ones (the weight gradients, the input gradients of the
+    // MLP and q/k/v) on four wavefronts of 128 x 128 (measured on the 1.3B
+    // layer shapes, one and two operand pairs).
+    if (a.N > 128 && t256 > 128) tile = dma ? (a.K <= 4096 ? 8 : 6) : 2;
+    else if (t128 >= 64) tile = dma ? 5 : 3;
+  }
+  return tile;
+}
+
 template <typename T>
 hipError_t gemm(const GemmArgs& a, hipStream_t stream) {
   if (a.M == 0 || a.N == 0) return hipSuccess;
   if constexpr (sizeof(T) == 2) {
-    int tile = a.tile;
-    if (tile == 0 && a.M >= 256) {
-      const int64_t t256 = (int64_t)ceil_div(a.M, 256) * ceil_div(a.N, 256) * a.nbatch;
-      const int64_t t128 = (int64_t)ceil_div(a.M, 256) * ceil_div(a.N, 128) * a.nbatch;
-      const bool dma = a.K % KT3 == 0;
-      // 256 x 256 tiles once there are more than 128 of them; with fewer,
-      // 256 x 128 tiles keep more of the 256 CUs busy.  Contractions up to
-      // 4096 deep (the forward projections and the input gradients of
-      // 2048-wide layers) run on eight wavefronts of 128 x 64, two per SIMD,
-      // whose tiles spend less of their time in the prologue and the staged
-      // epilogue; longer ones (the weight gradients, the input gradients of the
-      // MLP and q/k/v) on four wavefronts of 128 x 128 (measured on the 1.3B
-      // layer shapes, one and two operand pairs).
-      if (a.N > 128 && t256 > 128) tile = dma ? (a.K <= 4096 ? 8 : 6) : 2;
-      else if (t128 >= 64) tile = dma ? 5 : 3;
-    }
+    const int tile = bf16_tile(a);
     if (tile == 2) { launch_big<256, 256, 2, 4>(a, stream); return hipGetLastError(); }
     if (tile == 3) { launch_big<256, 128, 2, 2>(a, stream); return hipGetLastError(); }
     if (tile == 4) { launch_dma<256, 4>(a, stream); return hipGetLastError(); }
@@ -1384,8 +1413,44 @@ hipError_t gemm(const GemmArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
+template <bool AK, bool BKM, int WN>
+static void launch_w4_pair_t(const GemmArgs& a0, const GemmArgs& a1, int n0, int n1, hipStream_t stream) {
+  hipLaunchKernelGGL((gemm_bf16_w4_pair<AK, BKM, WN>), dim3(n0 + n1), dim3(128 * WN), 0, stream, a0, a1, n0);
+}
+template <int WN>
+static void launch_w4_pair(const GemmArgs& a0, const GemmArgs& a1, int n0, int n1, hipStream_t stream) {
+  const bool ak = a0.A[0].s_k == 1, bk = a0.B[0].s_k == 1;
+  if (ak && bk) launch_w4_pair_t<true, true, WN>(a0, a1, n0, n1, stream);
+  else if (ak && !bk) launch_w4_pair_t<true, false, WN>(a0, a1, n0, n1, stream);
+  else if (!ak && bk) launch_w4_pair_t<false, true, WN>(a0, a1, n0, n1, stream);
+  else launch_w4_pair_t<false, false, WN>(a0, a1, n0, n1, stream);
+}
+
+template <typename T>
+hipError_t gemm_pair(const GemmArgs& a0, const GemmArgs& a1, hipStream_t stream) {
+  if constexpr (sizeof(T) == 2) {
+    GemmArgs b = a1;
+    b.tile = bf16_tile(a0);
+    const bool one = (b.tile == 6 || b.tile == 8) && a0.M > 0 && a0.N > 0 && a1.M > 0 && a1.N > 0 &&
+                     a0.nbatch == 1 && a1.nbatch == 1 && a0.causal == CAUSAL_NONE && a1.causal == CAUSAL_NONE &&
+                     (a0.A[0].s_k == 1) == (a1.A[0].s_k == 1) && (a0.B[0].s_k == 1) == (a1.B[0].s_k == 1) &&
+                     gemm_check<T>(b) == nullptr;
+    if (one) {
+      const int n0 = (int)(ceil_div(a0.M, 256) * ceil_div(a0.N, 256));
+      const int n1 = (int)(ceil_div(a1.M, 256) * ceil_div(a1.N, 256));
+      if (b.tile == 6) launch_w4_pair<2>(a0, b, n0, n1, stream);
+      else launch_w4_pair<4>(a0, b, n0, n1, stream);
+      return hipGetLastError();
+    }
+  }
+  const hipError_t r = gemm<T>(a0, stream);
+  return r != hipSuccess ? r : gemm<T>(a1, stream);
+}
+
 template hipError_t gemm<float>(const GemmArgs&, hipStream_t);
 template hipError_t gemm<bf16_t>(const GemmArgs&, hipStream_t);
+template hipError_t gemm_pair<float>(const GemmArgs&, const GemmArgs&, hipStream_t);
+template hipError_t gemm_pair<bf16_t>(const GemmArgs&, const GemmArgs&, hipStream_t);
 template const char* gemm_check<float>(const GemmArgs&);
 template const char* gemm_check<bf16_t>(const GemmArgs&);
 

@@ -74,18 +74,20 @@ def test_fused_rejects_unaligned_sequence():
 
 
 def test_wgrad_token_slices_match_whole_range():
-    """Weight gradients summed over token slices (the 2048 x 2048 output of wo
-    of the 1.3B layer at 4096 tokens: four slices) against one GEMM over all
-    tokens: only the order of the fp32 partial sums differs."""
+    """The three launch forms of the weight gradients on the 1.3B layer at
+    4096 tokens: by default the 2048 x 2048 output of wo shares one launch with
+    the 6144 x 2048 q/k/v one (192 + 64 tiles); without that it is summed over
+    four token slices; the reference is one launch per weight over all tokens.
+    Only the order of the fp32 partial sums may differ."""
     torch = need_gpu()
     from paper_2602_00816_amd import fdhvp as fd
     w = dict(WORKLOADS["llama-1.3b-bf16"], n_layers=1)
-    say("wgrad token slices vs whole range: llama-1.3b, 1 layer, 2x2048")
+    say("wgrad launch forms (shared launch, token slices, whole range): llama-1.3b, 1 layer, 2x2048")
     out = []
-    for unsplit in (False, True):
+    for mode in (0, 2, 1):
         mod = fd.Model.from_workload(w)
         mod.set_workspace(2, 2048)
-        mod.unsplit_wgrad(unsplit)
+        mod.unsplit_wgrad(mode)
         th = mod.init_params(1)
         tok = mod.make_tokens(2, 2048, 2, "zipf")
         v = mod.random_vector(3, "rademacher")
@@ -93,10 +95,21 @@ def test_wgrad_token_slices_match_whole_range():
         del mod
         torch.cuda.synchronize()
     layout = M.layout(micro.cfg_of(w, bf16=True))
-    err = rel_l2(out[0], out[1])
-    say(f"  rel_l2 {err:.3e}")
-    assert err <= 1e-4
-    for e in layout:
-        ref = out[1][e.offset:e.offset + e.numel]
-        if np.linalg.norm(ref) > 1e-3 * np.linalg.norm(out[1]):
-            assert rel_l2(out[0][e.offset:e.offset + e.numel], ref) <= 1e-4, e.name
+    ref = out[2]
+    for name, got in (("shared launch", out[0]), ("token slices", out[1])):
+        err = rel_l2(got, ref)
+        say(f"  {name}: rel_l2 {err:.3e}, identical {bool(np.array_equal(got, ref))}")
+        assert err <= 1e-4
+        for e in layout:
+            r = ref[e.offset:e.offset + e.numel]
+            if np.linalg.norm(r) > 1e-3 * np.linalg.norm(ref):
+                assert rel_l2(got[e.offset:e.offset + e.numel], r) <= 1e-4, (name, e.name)
+    # the forms differ only in the wo block (and not at all for q/k/v and the rest)
+    wo = [e for e in layout if e.name.endswith("wo")]
+    assert wo
+    mask = np.ones(ref.size, bool)
+    for e in wo:
+        mask[e.offset:e.offset + e.numel] = False
+    assert np.array_equal(out[1][mask], ref[mask])
+    with pytest.raises(fd.FdhError):
+        fd.Model.from_workload(w).unsplit_wgrad(3)
