@@ -14,6 +14,9 @@
 #include "engine.h"
 
 #include <algorithm>
+#include <functional>
+#include <queue>
+#include <vector>
 #include <type_traits>
 #include <cmath>
 #include <cstring>
@@ -147,6 +150,51 @@ static bool pair_wgrads(int Mq, int Nq, int Mo, int No, int T_) {
   return wgrad_splits(Mq, Nq, T_) == 1 && tq % 256 != 0 && tq % 256 + to <= 256;
 }
 
+// The MLP's two weight gradients (gate/up: Ma x Na, down: Mb x Nb) in one
+// launch, the down one cut into s token slices: returns s, or 0 for two
+// launches of their own.  Tiles of the same depth take one time unit (a wave
+// of 256 takes one), and the dispatcher hands the next tile of the grid to the
+// first free compute unit; the estimate adds the slice sums (s partial
+// products written and read at about 5 TB/s, against a 256 x 256 tile of two
+// operand pairs at about 4.7 TFLOP/s per compute unit).  The 2048-wide layer
+// at 8192 tokens: 352 + 176 tiles take 3 units in two launches, 2.25 in one
+// with the down gradient in 4 slices.
+static int mlp_wgrad_split(int Ma, int Na, int Mb, int Nb, int T_) {
+  const int64_t ta = (int64_t)((Ma + 255) / 256) * ((Na + 255) / 256);
+  const int64_t tb = (int64_t)((Mb + 255) / 256) * ((Nb + 255) / 256);
+  if (wgrad_splits(Ma, Na, T_) != 1 || wgrad_splits(Mb, Nb, T_) != 1) return 0;
+  auto makespan = [&](int s) {
+    std::priority_queue<double, std::vector<double>, std::greater<double>> cu;
+    for (int i = 0; i < 256; ++i) cu.push(0.0);
+    auto take = [&](double len) {
+      const double t = cu.top();
+      cu.pop();
+      cu.push(t + len);
+    };
+    for (int64_t i = 0; i < ta; ++i) take(1.0);
+    for (int64_t i = 0; i < tb * s; ++i) take(1.0 / s);
+    double end = 0.0;
+    while (!cu.empty()) {
+      end = std::max(end, cu.top());
+      cu.pop();
+    }
+    return end;
+  };
+  const double apart = (double)((ta + 255) / 256 + (tb + 255) / 256);
+  double best = apart - 0.25;
+  int pick = 0;
+  for (int s : {1, 2, 4}) {
+    if (T_ % (64 * s) != 0 || T_ / s < 1024) continue;
+    const double sums = s > 1 ? (double)s * Mb * Nb * 8.0 / (2.8e5 * T_) : 0.0;
+    const double t = makespan(s) + sums;
+    if (t < best) {
+      best = t;
+      pick = s;
+    }
+  }
+  return pick;
+}
+
 // ---------------------------------------------------------------------------
 // workspace plan
 // ---------------------------------------------------------------------------
@@ -227,6 +275,9 @@ size_t Engine::plan(int B, int S, int m, const fdh_lanczos_opts* o, WsLayout* ou
         const int ns = wgrad_splits(sh[0], sh[1], (int)T_);
         if (ns > 1) mx = std::max(mx, (size_t)ns * sh[0] * sh[1] * 4);
       }
+      // the down projection's slices when the MLP weight gradients share a launch
+      const int nm = bf16 && !gpt2 ? mlp_wgrad_split(nu, d, d, F, (int)T_) : 0;
+      if (nm > 1) mx = std::max(mx, (size_t)nm * d * F * 4);
       take(W.wsplit, mx);
     }
     const size_t maxc = std::max<size_t>({(size_t)qkvd, (size_t)F, (size_t)d, (size_t)1});
@@ -542,10 +593,30 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, c
     g.C = hv + W.off; g.ldc = K; g.alpha = inv_eps;
     return g;
   };
-  // two weight gradients over the whole token range in one launch
-  auto lin_wgrad_pair = [&](GemmArgs g0, GemmArgs g1) -> int {
-    if (acc) g0.beta = g1.beta = 1.f;
-    return run_gemm_pair<T>(*this, g0, g1);
+  // two weight gradients in one launch, the first over the whole token range,
+  // the second (parameter block W1) over ns token slices into fp32 partial
+  // products that a second pass adds in slice order
+  auto lin_wgrad_pair = [&](GemmArgs g0, GemmArgs g1, int ns, const ParamRef& W1) -> int {
+    if (acc) g0.beta = 1.f;
+    if (ns <= 1) {
+      if (acc) g1.beta = 1.f;
+      return run_gemm_pair<T>(*this, g0, g1);
+    }
+    const int kc = T_ / ns;
+    g1.K = kc;
+    g1.nbatch = ns;
+    for (int p = 0; p < 2; ++p) {
+      g1.A[p].s_outer = (int64_t)kc * g1.M;
+      g1.B[p].s_outer = (int64_t)kc * g1.N;
+    }
+    g1.C = F32(wsplit); g1.c_outer = (int64_t)g1.M * g1.N;
+    const int rc = run_gemm_pair<T>(*this, g0, g1);
+    if (rc != FDH_OK) return rc;
+    int e0 = 0;
+    if (timing.on) CK(timing.begin(st, &e0));
+    CK(launch_sum_splits(hv + W1.off, F32(wsplit), ns, (int64_t)g1.M * g1.N, acc, st));
+    if (timing.on) CK(timing.end(st, 0, e0, 0.0, 0.0));
+    return FDH_OK;
   };
   auto lin_wgrad = [&](const T* dYm, const T* dYd, int N, const T* Xm, const T* Xd, int K, const ParamRef& W) -> int {
     GemmArgs g = wgrad_args(dYm, dYd, N, Xm, Xd, K, W);
@@ -731,6 +802,13 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, c
   float* dyd = F32(dx1_d);
   RC(norm_back(dxm, dxd, nullptr, nullptr, F32(xL_m), F32(xL_d), F32(db_m), F32(db_d), nfg, nfb));
 
+  // token slices of the down projection's weight gradient when the MLP's two
+  // weight gradients share a launch (0: two launches)
+  int mlp_split = 0;
+  if (std::is_same<T, bf16_t>::value && !gpt2 && !force_unsplit && !force_unpaired) {
+    mlp_split = mlp_wgrad_split(2 * F, d, d, F, T_);
+    if (mlp_split > 1 && wsplit.bytes < (size_t)mlp_split * d * F * 4) mlp_split = 0;
+  }
   for (int l = L - 1; l >= 0; --l) {
     const LayerRefs& R = layers[l];
     LayerSpans& s = ls[l];
@@ -741,7 +819,9 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, c
     T *gom, *god;
     RC(as_op(dxm, dxd, dxo_m, dxo_d, (int64_t)T_ * d, &gom, &god));
     if (gpt2) RC(colsum_hv(dxd, d, d, R.b2));
-    RC(lin_wgrad(gom, god, d, OP(s.z_m), OP(s.z_d), F, R.w2));
+    // (with mlp_split > 0 the down projection's weight gradient shares the
+    // gate/up one's launch below: gom, god and z stay intact until then)
+    if (!mlp_split) RC(lin_wgrad(gom, god, d, OP(s.z_m), OP(s.z_d), F, R.w2));
     RC(lin_dgrad(gom, god, d, R.w2, F, F32(dz_m), F32(dz_d), OUT_F32));
     const int nu = gpt2 ? F : 2 * F;
     if (gpt2) {
@@ -751,7 +831,12 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, c
     } else {
       CK(launch_swiglu_bwd<T>(PairT<T>{OP(dgu_m), OP(dgu_d)}, OP(s.u_m), OP(s.u_d), F32(dz_m), F32(dz_d), T_, F, st));
     }
-    RC(lin_wgrad(OP(dgu_m), OP(dgu_d), nu, OP(s.b_m), OP(s.b_d), d, R.w1));
+    if (mlp_split) {
+      RC(lin_wgrad_pair(wgrad_args(OP(dgu_m), OP(dgu_d), nu, OP(s.b_m), OP(s.b_d), d, R.w1),
+                        wgrad_args(gom, god, d, OP(s.z_m), OP(s.z_d), F, R.w2), mlp_split, R.w2));
+    } else {
+      RC(lin_wgrad(OP(dgu_m), OP(dgu_d), nu, OP(s.b_m), OP(s.b_d), d, R.w1));
+    }
     RC(lin_dgrad(OP(dgu_m), OP(dgu_d), nu, R.w1, d, F32(db_m), F32(db_d), OUT_F32));
     // norm 2 backward, residual: dy = dx + norm2'(db)
     RC(norm_back(dym, dyd, dxm, dxd, F32(s.xmid_m), F32(s.xmid_d), F32(db_m), F32(db_d), R.n2g, R.n2b));
@@ -893,7 +978,7 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, c
     }
     if (pair_o)
       RC(lin_wgrad_pair(wgrad_args(OP(dqkvo_m), OP(dqkvo_d), qkvd, OP(s.a_m), OP(s.a_d), d, R.wqkv),
-                        wgrad_args(gom, god, d, OP(s.o_m), OP(s.o_d), Hq * dh, R.wo)));
+                        wgrad_args(gom, god, d, OP(s.o_m), OP(s.o_d), Hq * dh, R.wo), 1, R.wo));
     else
       RC(lin_wgrad(OP(dqkvo_m), OP(dqkvo_d), qkvd, OP(s.a_m), OP(s.a_d), d, R.wqkv));
     RC(lin_dgrad(OP(dqkvo_m), OP(dqkvo_d), qkvd, R.wqkv, d, F32(da_m), F32(da_d), OUT_F32));

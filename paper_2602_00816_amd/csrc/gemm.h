@@ -45,8 +45,8 @@ struct GemmArgs {
 template <typename T>
 hipError_t gemm(const GemmArgs& a, hipStream_t stream);
 
-// Two independent products (no batches, no causal limits) in one launch of
-// the 256 x 256 kernel that a0 runs on, when a1 can run on it too; else one
+// Two independent products (batched or not, no causal limits) in one launch
+// of the 256 x 256 kernel that a0 runs on, when a1 can run on it too; else one
 // launch each.  Each output gets the same arithmetic as in a launch of its own
 // on that kernel.
 template <typename T>

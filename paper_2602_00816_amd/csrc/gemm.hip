@@ -1079,9 +1079,9 @@ __global__ __launch_bounds__(64 * 2 * WN) void gemm_bf16_w4(GemmArgs a) {
   w4_tile<AK, BKM, WN>(a, gx, gy, xcd_order(blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z), gx * gy * gridDim.z));
 }
 
-// Two independent products in one grid (one-dimensional, n0 tiles of a0
-// then those of a1): the tiles of a1 take the compute units that a grid of
-// a0 alone would leave idle in its last wave.  Each product is renumbered on
+// Two independent products in one grid (one-dimensional, the n0 tiles of a0,
+// batch entries included, then those of a1): the tiles of a1 take the compute
+// units that a grid of a0 alone would leave idle in its last wave.  Each product is renumbered on
 // its own, so that every XCD takes an eighth of each (renumbering the joint
 // grid would give a0 to some XCDs and a1 to the others).
 template <bool AK, bool BKM, int WN = 2>
@@ -1432,12 +1432,12 @@ hipError_t gemm_pair(const GemmArgs& a0, const GemmArgs& a1, hipStream_t stream)
     GemmArgs b = a1;
     b.tile = bf16_tile(a0);
     const bool one = (b.tile == 6 || b.tile == 8) && a0.M > 0 && a0.N > 0 && a1.M > 0 && a1.N > 0 &&
-                     a0.nbatch == 1 && a1.nbatch == 1 && a0.causal == CAUSAL_NONE && a1.causal == CAUSAL_NONE &&
+                     a0.causal == CAUSAL_NONE && a1.causal == CAUSAL_NONE &&
                      (a0.A[0].s_k == 1) == (a1.A[0].s_k == 1) && (a0.B[0].s_k == 1) == (a1.B[0].s_k == 1) &&
                      gemm_check<T>(b) == nullptr;
     if (one) {
-      const int n0 = (int)(ceil_div(a0.M, 256) * ceil_div(a0.N, 256));
-      const int n1 = (int)(ceil_div(a1.M, 256) * ceil_div(a1.N, 256));
+      const int n0 = (int)(ceil_div(a0.M, 256) * ceil_div(a0.N, 256)) * a0.nbatch;
+      const int n1 = (int)(ceil_div(a1.M, 256) * ceil_div(a1.N, 256)) * a1.nbatch;
       if (b.tile == 6) launch_w4_pair<2>(a0, b, n0, n1, stream);
       else launch_w4_pair<4>(a0, b, n0, n1, stream);
       return hipGetLastError();
