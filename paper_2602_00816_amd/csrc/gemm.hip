@@ -897,7 +897,10 @@ __device__ __forceinline__ void w4_tile(const GemmArgs& a, int gx, int gy, int l
   const int tiles = gx * gy;
   const int z = lin / tiles;
   const int tl = lin % tiles;
-  constexpr int GM = 8;
+  // tiles run down GM tile rows before the next column (with the XCD
+  // renumbering, each XCD's 32 concurrent tiles then share 4 A and 8 B
+  // operand blocks); 4 measured 0.35% faster per HVP than 8 and 16 slower
+  constexpr int GM = 4;
   const int gsize = GM * gx;
   const int first_m = (tl / gsize) * GM;
   const int gm_rows = min(gy - first_m, GM);
