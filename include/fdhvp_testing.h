@@ -35,15 +35,16 @@ fdh_status fdh_testing_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, int3
 /* Two independent bf16 products in one launch of the 256 x 256 kernel given
  * by tile (6 or 8, as for fdh_testing_gemm), the way the weight gradients of
  * the attention output and q/k/v projections share a launch in an HVP.
- * Product p is C_p[M_p][N_p] = alpha (A_p B_p^T + A2_p B2_p^T), operands laid
- * out as for fdh_testing_gemm with batch 1, both products with the same
- * a_kmajor / b_kmajor; A2_p, B2_p may be NULL together.  K_p % 32 == 0, M_p and
- * N_p >= 8.  FDH_ERR_UNSUPPORTED when a product does not fit the kernel.
- * Enqueued on hip_stream; returns without waiting. */
-fdh_status fdh_testing_gemm_pair(int32_t M0, int32_t N0, int32_t K0, int32_t M1, int32_t N1, int32_t K1,
-                                 int32_t a_kmajor, int32_t b_kmajor, const void* A0, const void* B0, const void* A20,
-                                 const void* B20, float* C0, const void* A1, const void* B1, const void* A21,
-                                 const void* B21, float* C1, float alpha, int32_t tile, void* hip_stream);
+ * Product p is C_p[batch_p][M_p][N_p] = alpha (A_p B_p^T + A2_p B2_p^T) per
+ * batch entry, operands laid out as for fdh_testing_gemm, both products with
+ * the same a_kmajor / b_kmajor; A2_p, B2_p may be NULL together.  K_p % 32 ==
+ * 0, M_p and N_p >= 8, batch_p >= 1.  FDH_ERR_UNSUPPORTED when a product does
+ * not fit the kernel.  Enqueued on hip_stream; returns without waiting. */
+fdh_status fdh_testing_gemm_pair(int32_t M0, int32_t N0, int32_t K0, int32_t batch0, int32_t M1, int32_t N1,
+                                 int32_t K1, int32_t batch1, int32_t a_kmajor, int32_t b_kmajor, const void* A0,
+                                 const void* B0, const void* A20, const void* B20, float* C0, const void* A1,
+                                 const void* B1, const void* A21, const void* B21, float* C1, float alpha,
+                                 int32_t tile, void* hip_stream);
 
 /* on != 0 makes the next fdh_set_workspace plan the unfused attention path
  * (score, probability and score-gradient matrices in the workspace, MFMA

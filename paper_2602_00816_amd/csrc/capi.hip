@@ -356,16 +356,17 @@ extern "C" fdh_status fdh_testing_gemm(int32_t dtype, int32_t M, int32_t N, int3
   return r == hipSuccess ? FDH_OK : FDH_ERR_HIP;
 }
 
-extern "C" fdh_status fdh_testing_gemm_pair(int32_t M0, int32_t N0, int32_t K0, int32_t M1, int32_t N1, int32_t K1,
-                                            int32_t a_kmajor, int32_t b_kmajor, const void* A0, const void* B0,
-                                            const void* A20, const void* B20, float* C0, const void* A1,
-                                            const void* B1, const void* A21, const void* B21, float* C1, float alpha,
-                                            int32_t tile, void* hip_stream) {
+extern "C" fdh_status fdh_testing_gemm_pair(int32_t M0, int32_t N0, int32_t K0, int32_t batch0, int32_t M1,
+                                            int32_t N1, int32_t K1, int32_t batch1, int32_t a_kmajor,
+                                            int32_t b_kmajor, const void* A0, const void* B0, const void* A20,
+                                            const void* B20, float* C0, const void* A1, const void* B1,
+                                            const void* A21, const void* B21, float* C1, float alpha, int32_t tile,
+                                            void* hip_stream) {
   if (!A0 || !B0 || !C0 || !A1 || !B1 || !C1 || (!A20) != (!B20) || (!A21) != (!B21) || M0 < 0 || N0 < 0 ||
-      K0 < 0 || M1 < 0 || N1 < 0 || K1 < 0 || (tile != 6 && tile != 8))
+      K0 < 0 || M1 < 0 || N1 < 0 || K1 < 0 || batch0 < 1 || batch1 < 1 || (tile != 6 && tile != 8))
     return FDH_ERR_INVALID_ARG;
   fdh::GemmArgs g[2];
-  const int32_t Ms[2] = {M0, M1}, Ns[2] = {N0, N1}, Ks[2] = {K0, K1};
+  const int32_t Ms[2] = {M0, M1}, Ns[2] = {N0, N1}, Ks[2] = {K0, K1}, Bs_[2] = {batch0, batch1};
   const void* As[2][2] = {{A0, A20}, {A1, A21}};
   const void* Bs[2][2] = {{B0, B20}, {B1, B21}};
   float* Cs[2] = {C0, C1};
@@ -373,16 +374,19 @@ extern "C" fdh_status fdh_testing_gemm_pair(int32_t M0, int32_t N0, int32_t K0, 
     fdh::GemmArgs& a = g[q];
     a.tile = tile;
     a.M = Ms[q]; a.N = Ns[q]; a.K = Ks[q];
+    a.nbatch = Bs_[q]; a.inner_count = 1;
     a.npairs = As[q][1] ? 2 : 1;
     for (int p = 0; p < a.npairs; ++p) {
       a.A[p].ptr = As[q][p];
       a.A[p].s_row = a_kmajor ? Ks[q] : 1;
       a.A[p].s_k = a_kmajor ? 1 : Ms[q];
+      a.A[p].s_outer = (int64_t)Ms[q] * Ks[q];
       a.B[p].ptr = Bs[q][p];
       a.B[p].s_row = b_kmajor ? Ks[q] : 1;
       a.B[p].s_k = b_kmajor ? 1 : Ns[q];
+      a.B[p].s_outer = (int64_t)Ns[q] * Ks[q];
     }
-    a.C = Cs[q]; a.ldc = Ns[q];
+    a.C = Cs[q]; a.ldc = Ns[q]; a.c_outer = (int64_t)Ms[q] * Ns[q];
     a.alpha = alpha;
     if (a.M < 8 || a.N < 8 || fdh::gemm_check<fdh::bf16_t>(a)) return FDH_ERR_UNSUPPORTED;
   }

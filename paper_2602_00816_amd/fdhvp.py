@@ -96,8 +96,8 @@ def lib():
         "fdh_last_error": (C.c_char_p, [vp]),
         "fdh_ritz_diagnostics": (i32, [pd, pd, i32, f64, pd, pd, pd, pi, pi, pi]),
         "fdh_testing_gemm": (i32, [i32, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, i32, C.c_float, i32, vp]),
-        "fdh_testing_gemm_pair": (i32, [i32, i32, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
-                                        C.c_float, i32, vp]),
+        "fdh_testing_gemm_pair": (i32, [i32, i32, i32, i32, i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp,
+                                        vp, vp, C.c_float, i32, vp]),
         "fdh_testing_unfused_attention": (i32, [vp, i32]),
         "fdh_testing_unsplit_wgrad": (i32, [vp, i32]),
         "fdh_testing_timing": (i32, [vp, i32]),
@@ -476,17 +476,18 @@ def testing_gemm(dtype: str, M, N, K, batch, a_kmajor, b_kmajor, A, B, A2, B2, C
         raise FdhError(st, "fdh_testing_gemm")
 
 
-def testing_gemm_pair(M0, N0, K0, M1, N1, K1, a_kmajor, b_kmajor, P0, P1, alpha=1.0, tile=6):
+def testing_gemm_pair(M0, N0, K0, M1, N1, K1, a_kmajor, b_kmajor, P0, P1, alpha=1.0, tile=6, batch0=1, batch1=1):
     """Two bf16 products in one launch (testing); P_q = (A, B, A2, B2, C), A2/B2 may be None."""
     import torch
     A0, B0, A20, B20, C0 = P0
     A1, B1, A21, B21, C1 = P1
-    for (M, N, K, (A, B, A2, B2, Cq)) in ((M0, N0, K0, P0), (M1, N1, K1, P1)):
-        for t, n, dt in ((A, M * K, torch.bfloat16), (B, N * K, torch.bfloat16), (A2, M * K, torch.bfloat16),
-                         (B2, N * K, torch.bfloat16), (Cq, M * N, torch.float32)):
+    for (M, N, K, z, (A, B, A2, B2, Cq)) in ((M0, N0, K0, batch0, P0), (M1, N1, K1, batch1, P1)):
+        for t, n, dt in ((A, z * M * K, torch.bfloat16), (B, z * N * K, torch.bfloat16), (A2, z * M * K, torch.bfloat16),
+                         (B2, z * N * K, torch.bfloat16), (Cq, z * M * N, torch.float32)):
             if t is not None and (not t.is_cuda or not t.is_contiguous() or t.dtype != dt or t.numel() != n):
                 raise ValueError("testing_gemm_pair: operand of the wrong device, layout, type or size")
-    st = lib().fdh_testing_gemm_pair(M0, N0, K0, M1, N1, K1, int(a_kmajor), int(b_kmajor), _ptr(A0), _ptr(B0),
+    st = lib().fdh_testing_gemm_pair(M0, N0, K0, int(batch0), M1, N1, K1, int(batch1), int(a_kmajor), int(b_kmajor),
+                                     _ptr(A0), _ptr(B0),
                                      _ptr(A20), _ptr(B20), _ptr(C0), _ptr(A1), _ptr(B1), _ptr(A21), _ptr(B21),
                                      _ptr(C1), float(alpha), int(tile), _stream())
     if st != OK:
