@@ -555,6 +555,7 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, c
     g.C = Ym; g.ldc = N; g.out_type = out;
     g.resid = Rm;
     if (bias.valid()) g.bias_theta = th + bias.off;
+    RG(T, g);
     GemmArgs h;
     h.M = T_; h.N = N; h.K = K; h.npairs = 2;
     h.A[0] = kmaj(Xd, K); h.B[0] = kmaj(th + W.off, K);
@@ -562,7 +563,6 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, c
     h.C = Yd; h.ldc = N; h.out_type = out;
     h.resid = Rd;
     if (bias.valid()) { h.bias_v = v + bias.off; h.bias_v_scale = feps; }
-    RG(T, g);
     RG(T, h);
     return FDH_OK;
   };
@@ -573,12 +573,12 @@ int Engine::hvp_t(const T* th, const float* v, double eps, const int32_t* tok, c
     g.A[0] = kmaj(dYm, N);
     g.B[0] = mnmaj(th + W.off, K);
     g.C = dXm; g.ldc = K; g.out_type = out;
+    RG(T, g);
     GemmArgs h;
     h.M = T_; h.N = K; h.K = N; h.npairs = 2;
     h.A[0] = kmaj(dYd, N); h.B[0] = mnmaj(th + W.off, K);
     h.A[1] = kmaj(dYm, N); h.B[1] = mnmaj(lo + W.off, K);
     h.C = dXd; h.ldc = K; h.out_type = out;
-    RG(T, g);
     RG(T, h);
     return FDH_OK;
   };
