@@ -897,6 +897,22 @@ __global__ void swiglu_bwd_kernel(PairT<T> dgu, const T* gum, const T* gud, cons
 // The logits of position t predict the label of position t + 1: the next token,
 // or lab[t + 1] when labels are given; a label of IGNORE_LABEL (padding,
 // masked prompt) leaves the row out.  inv_n scales every kept row.
+// e^b and e^-b as c + s and c - s with c = cosh b and s = sinh b: for
+// |b| < 1/16 their Taylor series to b^8 and b^9 (the first omitted terms are
+// below 2^-40 / 10! of the sum), otherwise from exp.
+__device__ inline void exp_pm(double b, double& ep, double& en) {
+  if (fabs(b) < 0.0625) {
+    const double b2 = b * b;
+    const double c = 1.0 + b2 * (1.0 / 2 + b2 * (1.0 / 24 + b2 * (1.0 / 720 + b2 * (1.0 / 40320))));
+    const double sn = b * (1.0 + b2 * (1.0 / 6 + b2 * (1.0 / 120 + b2 * (1.0 / 5040 + b2 * (1.0 / 362880)))));
+    ep = c + sn;
+    en = c - sn;
+  } else {
+    ep = exp(b);
+    en = exp(-b);
+  }
+}
+
 template <typename T>
 __global__ __launch_bounds__(NT) void ce_kernel(PairT<T> dl, double* rowloss, const float* lm, const float* ld,
                                                 const int32_t* tok, const int32_t* lab, int T_, int S, int V,
@@ -915,18 +931,38 @@ __global__ __launch_bounds__(NT) void ce_kernel(PairT<T> dl, double* rowloss, co
   double mx = -1e300;
   for (int j = threadIdx.x; j < V; j += NT) mx = fmax(mx, (double)lm[o + j]);
   mx = block_max<NT>(mx, sh);
+  // exp(a +- b) = E e^+-b with E = exp(a) shared by both points.  For bf16
+  // models E is taken in fp32 (a common factor of the two channels, so its
+  // rounding never cancels in their half difference) and e^+-b from exp_pm;
+  // fp32 models keep both exponentials in fp64.
+  auto both = [&](double a, double b, double& xp, double& xn) {
+    if constexpr (sizeof(T) == 2) {
+      const double E = (double)__expf((float)a);
+      double ep, en;
+      exp_pm(b, ep, en);
+      xp = E * ep;
+      xn = E * en;
+    } else {
+      xp = exp(a + b);
+      xn = exp(a - b);
+    }
+  };
   double zp = 0.0, zm = 0.0;
   for (int j = threadIdx.x; j < V; j += NT) {
     const double a = (double)lm[o + j] - mx, b = (double)ld[o + j];
-    zp += exp(a + b);
-    zm += exp(a - b);
+    double xp, xn;
+    both(a, b, xp, xn);
+    zp += xp;
+    zm += xn;
   }
   zp = block_sum<NT>(zp, sh);
   zm = block_sum<NT>(zm, sh);
   const double izp = 1.0 / zp, izm = 1.0 / zm;
   for (int j = threadIdx.x; j < V; j += NT) {
     const double a = (double)lm[o + j] - mx, b = (double)ld[o + j];
-    double pp = exp(a + b) * izp, pn = exp(a - b) * izm;
+    double xp, xn;
+    both(a, b, xp, xn);
+    double pp = xp * izp, pn = xn * izm;
     if (j == y) { pp -= 1.0; pn -= 1.0; }
     put_pair(dl, o + j, pp * inv_n, pn * inv_n);
   }
