@@ -928,9 +928,6 @@ __global__ __launch_bounds__(NT) void ce_kernel(PairT<T> dl, double* rowloss, co
     return;
   }
   const int y = clamp_tok(raw, V);
-  double mx = -1e300;
-  for (int j = threadIdx.x; j < V; j += NT) mx = fmax(mx, (double)lm[o + j]);
-  mx = block_max<NT>(mx, sh);
   // exp(a +- b) = E e^+-b with E = exp(a) shared by both points.  For bf16
   // models E is taken in fp32 (a common factor of the two channels, so its
   // rounding never cancels in their half difference) and e^+-b from exp_pm;
@@ -947,16 +944,32 @@ __global__ __launch_bounds__(NT) void ce_kernel(PairT<T> dl, double* rowloss, co
       xn = exp(a - b);
     }
   };
-  double zp = 0.0, zm = 0.0;
+  // one pass for the row maximum and the sums: each thread keeps its sums
+  // relative to its own running maximum mt, rescaled by exp(old mt - new mt)
+  // when mt rises, then relative to the row maximum mx.  The rescale factors
+  // are common to both points (taken in fp32 for bf16 models, like E).
+  auto rescale = [&](double d) {
+    if constexpr (sizeof(T) == 2) return (double)__expf((float)d);
+    else return exp(d);
+  };
+  double mt = -1e300, zp = 0.0, zm = 0.0;
   for (int j = threadIdx.x; j < V; j += NT) {
-    const double a = (double)lm[o + j] - mx, b = (double)ld[o + j];
+    const double av = (double)lm[o + j], b = (double)ld[o + j];
+    if (av > mt) {
+      const double f = mt > -1e300 ? rescale(mt - av) : 0.0;
+      zp *= f;
+      zm *= f;
+      mt = av;
+    }
     double xp, xn;
-    both(a, b, xp, xn);
+    both(av - mt, b, xp, xn);
     zp += xp;
     zm += xn;
   }
-  zp = block_sum<NT>(zp, sh);
-  zm = block_sum<NT>(zm, sh);
+  const double mx = block_max<NT>(mt, sh);
+  const double fr = mt > -1e300 ? rescale(mt - mx) : 0.0;
+  zp = block_sum<NT>(zp * fr, sh);
+  zm = block_sum<NT>(zm * fr, sh);
   const double izp = 1.0 / zp, izm = 1.0 / zm;
   for (int j = threadIdx.x; j < V; j += NT) {
     const double a = (double)lm[o + j] - mx, b = (double)ld[o + j];
