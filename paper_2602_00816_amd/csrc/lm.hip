@@ -339,11 +339,14 @@ __global__ __launch_bounds__(NT) void norm_bwd_wave_kernel(PairF dx, PairT<T> dx
     if (row >= rows) break;
     const int64_t o = (int64_t)row * DM + 4 * lane;
     double mup = 0.0, mum = 0.0;
+    float4 xac[CPL], xbc[CPL];   // the row of x, kept in registers for the later passes
     if (ln) {
       double sp = 0.0, sm = 0.0;
-#pragma unroll 2
+#pragma unroll
       for (int c = 0; c < CPL; ++c) {
         const float4 xa = ld(xm, o + 256 * c), xb = ld(xd, o + 256 * c);
+        xac[c] = xa;
+        xbc[c] = xb;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           sp += (double)f4e(xa, e) + (double)f4e(xb, e);
@@ -354,7 +357,6 @@ __global__ __launch_bounds__(NT) void norm_bwd_wave_kernel(PairF dx, PairT<T> dx
       mum = wave_sum(sm) / DM;
     }
     double rp, rmi, a1p = 0.0, a1m = 0.0, a2p, a2m;
-    float4 xac[CPL], xbc[CPL];   // RMSNorm: the row of x, kept for the last pass
     if (!ln) {
       // RMSNorm (no mean): sum x^2 and sum dxhat * x in one pass over x and
       // dy; mean(dxhat * xhat) = r * mean(dxhat * x)
@@ -383,50 +385,42 @@ __global__ __launch_bounds__(NT) void norm_bwd_wave_kernel(PairF dx, PairT<T> dx
       a2p = rp * (wave_sum(tp) / DM);
       a2m = rmi * (wave_sum(tm) / DM);
     } else {
-      double qp = 0.0, qm = 0.0;
-#pragma unroll 2
-      for (int c = 0; c < CPL; ++c) {
-        const float4 xa = ld(xm, o + 256 * c), xb = ld(xd, o + 256 * c);
+      // LayerNorm: the variance, sum dxhat and sum dxhat * (x - mu) in one
+      // pass over dy, x from the registers; mean(dxhat * xhat) =
+      // r * mean(dxhat * (x - mu))
+      double qp = 0.0, qm = 0.0, s1p = 0.0, s1m = 0.0, tp = 0.0, tm = 0.0;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const double p = (double)f4e(xa, e) + (double)f4e(xb, e) - mup;
-          const double q = (double)f4e(xa, e) - (double)f4e(xb, e) - mum;
-          qp += p * p;
-          qm += q * q;
-        }
-      }
-      rp = 1.0 / sqrt(wave_sum(qp) / DM + neps);
-      rmi = 1.0 / sqrt(wave_sum(qm) / DM + neps);
-      // means of dxhat and dxhat * xhat at both points
-      double s1p = 0.0, s1m = 0.0, s2p = 0.0, s2m = 0.0;
-#pragma unroll 2
       for (int c = 0; c < CPL; ++c) {
         const int col = 256 * c + 4 * lane;
-        const float4 xa = ld(xm, o + 256 * c), xb = ld(xd, o + 256 * c);
+        const float4 xa = xac[c], xb = xbc[c];
         const float4 ya = ld(dym, o + 256 * c), yb = ld(dyd, o + 256 * c);
         const float4 g4 = ld4f(thg, col), v4 = ld(vg, col);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const double g = f4e(g4, e), dg = eps * (double)f4e(v4, e);
-          const double xhp = ((double)f4e(xa, e) + (double)f4e(xb, e) - mup) * rp;
-          const double xhm = ((double)f4e(xa, e) - (double)f4e(xb, e) - mum) * rmi;
+          const double p = (double)f4e(xa, e) + (double)f4e(xb, e) - mup;
+          const double q = (double)f4e(xa, e) - (double)f4e(xb, e) - mum;
           const double dhp = ((double)f4e(ya, e) + (double)f4e(yb, e)) * (g + dg);
           const double dhm = ((double)f4e(ya, e) - (double)f4e(yb, e)) * (g - dg);
+          qp += p * p;
+          qm += q * q;
           s1p += dhp;
           s1m += dhm;
-          s2p += dhp * xhp;
-          s2m += dhm * xhm;
+          tp += dhp * p;
+          tm += dhm * q;
         }
       }
+      rp = 1.0 / sqrt(wave_sum(qp) / DM + neps);
+      rmi = 1.0 / sqrt(wave_sum(qm) / DM + neps);
       a1p = wave_sum(s1p) / DM;
       a1m = wave_sum(s1m) / DM;
-      a2p = wave_sum(s2p) / DM;
-      a2m = wave_sum(s2m) / DM;
+      a2p = rp * (wave_sum(tp) / DM);
+      a2m = rmi * (wave_sum(tm) / DM);
     }
 #pragma unroll
     for (int c = 0; c < CPL; ++c) {
       const int col = 256 * c + 4 * lane;
-      const float4 xa = ln ? ld(xm, o + 256 * c) : xac[c], xb = ln ? ld(xd, o + 256 * c) : xbc[c];
+      const float4 xa = xac[c], xb = xbc[c];
       const float4 ya = ld(dym, o + 256 * c), yb = ld(dyd, o + 256 * c);
       const float4 g4 = ld4f(thg, col), v4 = ld(vg, col);
       const float4 ra = dresm ? ld(dresm, o + 256 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
