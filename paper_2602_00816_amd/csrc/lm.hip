@@ -1222,8 +1222,11 @@ hipError_t launch_gelu_bwd(PairT<T> du, float* dudf, const T* um, const T* ud, c
 }
 template <typename T>
 hipError_t launch_swiglu_fwd(PairT<T> z, const T* gum, const T* gud, int rows, int F, hipStream_t s) {
-  if (F % 4 == 0 && rows <= 65535)
-    hipLaunchKernelGGL(swiglu_fwd4_kernel<T>, dim3(ceil_div(F / 4, NT), rows), dim3(NT), 0, s, z, gum, gud, F);
+  if (F % 4 == 0 && rows <= 65535) {
+    // workgroups of 128 threads divide the 1.3B row (1408 groups of 4) exactly
+    const int nt = (F / 4) % 128 == 0 ? 128 : NT;
+    hipLaunchKernelGGL(swiglu_fwd4_kernel<T>, dim3(ceil_div(F / 4, nt), rows), dim3(nt), 0, s, z, gum, gud, F);
+  }
   else
     hipLaunchKernelGGL(swiglu_fwd_kernel<T>, dim3(grid_for((int64_t)rows * F)), dim3(NT), 0, s, z, gum, gud, rows, F);
   return hipGetLastError();
@@ -1231,8 +1234,10 @@ hipError_t launch_swiglu_fwd(PairT<T> z, const T* gum, const T* gud, int rows, i
 template <typename T>
 hipError_t launch_swiglu_bwd(PairT<T> dgu, const T* gum, const T* gud, const float* dzm, const float* dzd, int rows,
                              int F, hipStream_t s) {
-  if (F % 4 == 0 && rows <= 65535)
-    hipLaunchKernelGGL(swiglu_bwd4_kernel<T>, dim3(ceil_div(F / 4, NT), rows), dim3(NT), 0, s, dgu, gum, gud, dzm, dzd, F);
+  if (F % 4 == 0 && rows <= 65535) {
+    const int nt = (F / 4) % 128 == 0 ? 128 : NT;
+    hipLaunchKernelGGL(swiglu_bwd4_kernel<T>, dim3(ceil_div(F / 4, nt), rows), dim3(nt), 0, s, dgu, gum, gud, dzm, dzd, F);
+  }
   else
     hipLaunchKernelGGL(swiglu_bwd_kernel<T>, dim3(grid_for((int64_t)rows * F)), dim3(NT), 0, s, dgu, gum, gud, dzm, dzd, rows,
                        F);
