@@ -224,7 +224,7 @@ __device__ inline float f4e(const float4& v, int e) { return e == 0 ? v.x : (e =
 // at columns 256 c + 4 l), NORM_FWD_ROWS rows per workgroup: wavefront
 // reductions, x reread from the caches between the passes.  Same arithmetic
 // as norm_fwd_kernel.
-constexpr int NORM_FWD_ROWS = 8;
+constexpr int NORM_FWD_ROWS = 4;
 // An empty statement that claims to modify the cached row values, so that the
 // compiler recomputes their fp64 conversions in each pass instead of keeping
 // them live (twice the registers) from the previous one.  No instruction.
